@@ -1,0 +1,281 @@
+"""CPU oracle, part 2: one lookahead step of constrained decoding with
+speculative lookaheads (CDSL), computed from the definitions in float64.
+
+TEST INFRASTRUCTURE ONLY (see ``oracle/decoder.py``).
+
+One step for one prompt, in the paper's order (Sec. 3.2, Alg. 1; the beam
+heads and the reward selection follow CDLH, Alg. 2 and Sec. 2.1):
+
+a1  beam heads: c_1..c_k = top-k of s_t = log_softmax(M_p(pfx)) (Alg. 2,
+    the top-k selection; Step-2 of Sec. 3.2.3); head_lp_i = s_t[c_i].
+a2  draft rollout: x_{i,j} = argmax q_j, q_j = M_q(pfx + c_i + x_{i,<j}),
+    j = 1..d, greedy (Alg. 1, drafting loop; Sec. 3.2.1).
+a3  verification: p_j = M_p(pfx + c_i + x_{i,<j}), j = 1..d, all k*d rows
+    in one pass (Alg. 1, parallel verification; Sec. 3.2.2).
+a4  l_{i,j} = log p_j(x_{i,j}); y_{i,j} = argmax p_j.
+a5  hard rejection: n_i = number of leading j with y_{i,j} = x_{i,j}
+    (Alg. 1, rejection loop); a_i = n_i / d; score_i = head_lp_i + sum_j l_{i,j}.
+a6  reward r_i over generated-so-far + c_i + x_{i,1..d} (Sec. 3.2.2,
+    validation by R; lexical rewards of Sec. 4.1).
+a7  select i* = argmax_i (score_i + alpha * r_i); alpha = inf means the
+    reward alone, ties to the lowest index (Alg. 2's strict ">" update).
+a8  commit: emit O = [c_i*, x_i*,1..n_i*] (S1 action, no bonus token from
+    M_p; Sec. 3.2.3), pfx <- pfx + O, and s_{t+1} = log_softmax(M_p(pfx)).
+
+Readings where the paper is silent or garbled are listed in the design doc and
+restated next to the code that takes them.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+from typing import Callable, List, Optional, Sequence
+
+import numpy as np
+
+from .decoder import Decoder, KVCache
+
+
+# ----------------------------------------------------------------------------
+# row operations on one distribution
+# ----------------------------------------------------------------------------
+def log_softmax(z: np.ndarray) -> np.ndarray:
+    z = np.asarray(z, dtype=np.float64)
+    m = np.max(z, axis=-1, keepdims=True)
+    return z - (m + np.log(np.sum(np.exp(z - m), axis=-1, keepdims=True)))
+
+
+def argmax_lowest(z: np.ndarray) -> int:
+    """argmax; equal maxima resolve to the lowest token id."""
+    return int(np.argmax(z))
+
+
+def topk_ids(z: np.ndarray, k: int) -> np.ndarray:
+    """The k largest entries: value descending, then token id ascending."""
+    z = np.asarray(z)
+    order = np.lexsort((np.arange(z.shape[-1]), -z))
+    return order[:k].astype(np.int64)
+
+
+def top2_margin(z: np.ndarray) -> float:
+    """Gap between the largest and the second-largest entry."""
+    s = np.sort(np.asarray(z, dtype=np.float64))
+    return float(s[-1] - s[-2])
+
+
+def leading_matches(y: Sequence[int], x: Sequence[int]) -> int:
+    """Hard rejection: count positions before the first y_j != x_j."""
+    n = 0
+    for yj, xj in zip(y, x):
+        if yj != xj:
+            break
+        n += 1
+    return n
+
+
+# ----------------------------------------------------------------------------
+# rewards (stand-ins; see module docstring of cdsl_inputs)
+# ----------------------------------------------------------------------------
+def keyword_hits(window: Sequence[int], kws: Sequence[int]) -> int:
+    """Number of distinct keywords that occur in ``window``."""
+    present = set(int(t) for t in window)
+    return sum(1 for kw in set(int(k) for k in kws) if kw in present)
+
+
+def keyword_coverage(window: Sequence[int], kws: Sequence[int]) -> float:
+    """Fraction of the keyword set covered (concept counting, Sec. 4.1)."""
+    kws = list(set(int(k) for k in kws))
+    return keyword_hits(window, kws) / len(kws)
+
+
+def select_beam(scores: np.ndarray, reward: np.ndarray, alpha: float) -> int:
+    """argmax_i (score_i + alpha r_i), lowest i on ties; alpha = inf: reward only."""
+    scores = np.asarray(scores, np.float64)
+    reward = np.asarray(reward, np.float64)
+    if math.isinf(alpha) and alpha > 0:
+        comb = reward
+    else:
+        comb = scores + alpha * reward
+    return int(np.argmax(comb))
+
+
+# ----------------------------------------------------------------------------
+# per-prompt state and the step
+# ----------------------------------------------------------------------------
+@dataclass
+class PromptState:
+    tokens: List[int]          # prompt + everything emitted so far
+    n_prompt: int
+    draft_cache: KVCache
+    target_cache: KVCache
+    s: np.ndarray              # log_softmax of M_p at the end of the prefix
+    s_logits: np.ndarray       # the raw target logits of that row
+
+    @property
+    def generated(self) -> List[int]:
+        return self.tokens[self.n_prompt:]
+
+    @property
+    def length(self) -> int:
+        return len(self.tokens)
+
+
+def prefill(draft: Decoder, target: Decoder, prompt: Sequence[int]) -> PromptState:
+    prompt = [int(t) for t in prompt]
+    _, dc = draft.extend(draft.empty_cache(), prompt)
+    out, tc = target.extend(target.empty_cache(), prompt)
+    z = out.logits[-1]
+    return PromptState(list(prompt), len(prompt), dc, tc, log_softmax(z), z)
+
+
+@dataclass
+class Rollout:
+    x: np.ndarray              # [k, d] lookahead tokens
+    margin: np.ndarray         # [k, d] top-2 margin of the draft logits at each draw
+
+
+def rollout(draft: Decoder, st: PromptState, heads: Sequence[int], d: int) -> Rollout:
+    """a2: greedy lookahead of d tokens from each head, one token at a time,
+    each beam on its own copy of the prefix cache."""
+    k = len(heads)
+    x = np.zeros((k, d), np.int64)
+    mg = np.zeros((k, d))
+    for i, c in enumerate(heads):
+        cache = st.draft_cache
+        fed = int(c)
+        for j in range(d):
+            out, cache = draft.extend(cache, [fed])
+            z = out.logits[0]
+            x[i, j] = argmax_lowest(z)
+            mg[i, j] = top2_margin(z)
+            fed = int(x[i, j])
+    return Rollout(x, mg)
+
+
+@dataclass
+class Verify:
+    logits: np.ndarray         # [k, d, V] target logits of the fed rows
+    hidden: np.ndarray         # [k, d, D] final-normed hidden states
+    logprobs: np.ndarray       # [k, d]  l_{i,j} = log p_j(x_{i,j})
+    y: np.ndarray              # [k, d]  argmax p_j
+    margin: np.ndarray         # [k, d]  top-2 margin of p_j logits
+    n: np.ndarray              # [k]     leading matches
+    scores: np.ndarray         # [k]     head_lp + sum_j l
+    row_topk: np.ndarray       # [k, d, k] top-k ids of every fed row
+    row_topk_lp: np.ndarray    # [k, d, k]
+
+
+def verify_rows_tree(target: Decoder, st: PromptState, heads, x) -> tuple:
+    """a3 as one pass: rows (i, j) feed [c_i, x_{i,1..d-1}] at positions
+    L + j; row (i, j) sees the whole prefix and rows (i, 0..j) of its beam."""
+    k, d = x.shape
+    L = st.length
+    fed = np.concatenate([np.asarray(heads, np.int64)[:, None], x[:, :d - 1]], 1)  # [k, d]
+    toks = fed.reshape(-1)
+    pos = np.tile(L + np.arange(d), k)
+    beam_of = np.repeat(np.arange(k), d)
+    j_of = np.tile(np.arange(d), k)
+    tree = (beam_of[:, None] == beam_of[None, :]) & (j_of[None, :] <= j_of[:, None])
+    allowed = np.concatenate([np.ones((k * d, L), bool), tree], 1)
+    out = target.forward(toks, pos, st.target_cache, allowed)
+    return out.logits.reshape(k, d, -1), out.hidden.reshape(k, d, -1)
+
+
+def verify_rows_per_beam(target: Decoder, st: PromptState, heads, x) -> tuple:
+    """a3 with one causal pass per beam on a duplicated prefix cache."""
+    k, d = x.shape
+    lg, hd = [], []
+    for i in range(k):
+        fed = [int(heads[i])] + [int(t) for t in x[i, :d - 1]]
+        out, _ = target.extend(st.target_cache.copy(), fed)
+        lg.append(out.logits)
+        hd.append(out.hidden)
+    return np.stack(lg), np.stack(hd)
+
+
+def verify(target: Decoder, st: PromptState, heads, head_lp, x, tree: bool = True) -> Verify:
+    x = np.asarray(x, np.int64)
+    k, d = x.shape
+    logits, hidden = (verify_rows_tree if tree else verify_rows_per_beam)(target, st, heads, x)
+    lp = np.zeros((k, d))
+    y = np.zeros((k, d), np.int64)
+    mg = np.zeros((k, d))
+    rtk = np.zeros((k, d, k), np.int64)
+    rtl = np.zeros((k, d, k))
+    for i in range(k):
+        for j in range(d):
+            z = logits[i, j]
+            ls = log_softmax(z)
+            lp[i, j] = ls[x[i, j]]
+            y[i, j] = argmax_lowest(z)
+            mg[i, j] = top2_margin(z)
+            ids = topk_ids(z, k)
+            rtk[i, j] = ids
+            rtl[i, j] = ls[ids]
+    n = np.array([leading_matches(y[i], x[i]) for i in range(k)], np.int64)
+    scores = np.asarray(head_lp, np.float64) + lp.sum(1)
+    return Verify(logits, hidden, lp, y, mg, n, scores, rtk, rtl)
+
+
+def reward_for(kind: str, generated: Sequence[int], heads, x, hidden, kws=None, w=None) -> np.ndarray:
+    """a6: one reward per beam.  Keyword rewards look at generated-so-far
+    + c_i + x_{i,1..d} (the prompt is excluded: prompts carry the concepts);
+    the linear reward reads the final-normed hidden state of row (i, d-1)."""
+    k, d = np.asarray(x).shape
+    r = np.zeros(k)
+    for i in range(k):
+        window = list(generated) + [int(heads[i])] + [int(t) for t in x[i]]
+        if kind == "keyword_count":
+            r[i] = keyword_hits(window, kws)
+        elif kind == "keyword_coverage":
+            r[i] = keyword_coverage(window, kws)
+        elif kind == "linear":
+            r[i] = float(np.dot(np.asarray(hidden[i, d - 1], np.float64), np.asarray(w, np.float64)))
+        else:
+            raise ValueError(kind)
+    return r
+
+
+def commit(draft: Decoder, target: Decoder, st: PromptState, emitted: Sequence[int]) -> PromptState:
+    """a8: pfx <- pfx + O; both caches are extended by feeding O, and the
+    next head distribution is read at the last emitted token."""
+    emitted = [int(t) for t in emitted]
+    _, dc = draft.extend(st.draft_cache, emitted)
+    out, tc = target.extend(st.target_cache, emitted)
+    z = out.logits[-1]
+    return PromptState(st.tokens + emitted, st.n_prompt, dc, tc, log_softmax(z), z)
+
+
+@dataclass
+class StepResult:
+    heads: np.ndarray          # [k]
+    head_lp: np.ndarray        # [k]
+    head_margins: np.ndarray   # [k] gap between consecutive top-(k+1) values of s_t
+    roll: Rollout
+    ver: Verify
+    reward: np.ndarray         # [k]
+    combined: np.ndarray       # [k]
+    beam: int
+    emitted: List[int]
+    state: PromptState         # state after the commit
+
+
+def beam_heads(st: PromptState, k: int):
+    """a1: top-k of s_t (value descending, id ascending) and their log-probs."""
+    ids = topk_ids(st.s_logits, k)
+    srt = np.sort(st.s_logits)[::-1][:k + 1]
+    return ids, st.s[ids], -np.diff(srt)
+
+
+def step(draft: Decoder, target: Decoder, st: PromptState, k: int, d: int, alpha: float,
+         reward_kind: str, kws=None, w=None, tree: bool = True) -> StepResult:
+    heads, head_lp, hm = beam_heads(st, k)
+    ro = rollout(draft, st, heads, d)
+    ve = verify(target, st, heads, head_lp, ro.x, tree=tree)
+    r = reward_for(reward_kind, st.generated, heads, ro.x, ve.hidden, kws, w)
+    comb = r if (math.isinf(alpha) and alpha > 0) else ve.scores + alpha * r
+    b = select_beam(ve.scores, r, alpha)
+    n = int(ve.n[b])
+    emitted = [int(heads[b])] + [int(t) for t in ro.x[b, :n]]
+    nst = commit(draft, target, st, emitted)
+    return StepResult(heads, head_lp, hm, ro, ve, r, comb, b, emitted, nst)

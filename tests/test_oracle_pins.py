@@ -1,0 +1,292 @@
+"""Pins for the CPU oracle: every check compares it with something other than
+itself (an independent library decoder, brute force, closed forms, the
+paper's worked example, algebraic invariants of the method)."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import cdsl_inputs as ci
+import oracle
+from oracle import decoder as odec
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+GQA = ci.ModelShape(2, 32, 4, 2, 48, 64)      # G = 2
+MHA = ci.ModelShape(3, 48, 3, 3, 64, 64)      # hd = 16
+
+
+def _weights(shape, model_id, gains=True, seed=7):
+    w = ci.model_weights(shape, seed, model_id, "f32", threads=1)
+    # scale so the random model has sharp distributions, and random gains so a
+    # dropped norm gain cannot go unnoticed
+    rng = np.random.default_rng([seed, 99, model_id])
+    for lw in w["layers"]:
+        for nm in ci.LAYER_MATS:
+            lw[nm] = lw[nm] * 10.0
+        if gains:
+            lw["attn_norm"] = rng.uniform(0.5, 1.5, shape.d_model)
+            lw["mlp_norm"] = rng.uniform(0.5, 1.5, shape.d_model)
+    w["tok_emb"] = w["tok_emb"] * 10.0
+    w["lm_head"] = w["lm_head"] * 10.0
+    if gains:
+        w["final_norm"] = rng.uniform(0.5, 1.5, shape.d_model)
+    return w
+
+
+@pytest.fixture(scope="module")
+def models():
+    from hf_ref import hf_llama
+    out = {}
+    for nm, shape, mid in (("gqa", GQA, 0), ("mha", MHA, 1)):
+        w = _weights(shape, mid)
+        out[nm] = (shape, w, odec.Decoder(shape, w), hf_llama(shape, w))
+    return out
+
+
+def _prompt(n, V, seed=3):
+    return np.random.default_rng(seed).integers(0, V, n)
+
+
+# ---------------------------------------------------------------------------
+# the decoder against an independent implementation
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("which", ["gqa", "mha"])
+def test_decoder_matches_library_llama(models, which):
+    from hf_ref import hf_logits
+    shape, w, dec, hf = models[which]
+    toks = _prompt(21, shape.vocab)
+    ours = dec.full(toks).logits
+    ref = hf_logits(hf, toks)
+    # the library evaluates the rotary angles in float32 (its only non-fp64
+    # step), hence 2e-5 rather than 1e-12; planted mistakes below give > 1e-3
+    assert np.max(np.abs(ours - ref)) < 2e-5 * max(1.0, np.max(np.abs(ref)))
+
+
+def test_plausible_mistakes_fail_the_library_pin(models, monkeypatch):
+    """Planted oracle mistakes (in the oracle, on the CPU) are caught."""
+    from hf_ref import hf_logits
+    shape, w, dec, hf = models["gqa"]
+    toks = _prompt(12, shape.vocab)
+    ref = hf_logits(hf, toks)
+
+    def wrong_rope(x, pos, theta):  # interleaved pairing instead of rotate-half
+        hd = x.shape[-1]
+        inv = theta ** (-(np.arange(hd // 2) * 2.0) / hd)
+        ang = np.asarray(pos, float)[:, None] * inv[None, :]
+        c, s = np.cos(ang)[:, None, :], np.sin(ang)[:, None, :]
+        x1, x2 = x[..., 0::2], x[..., 1::2]
+        o = np.empty_like(x)
+        o[..., 0::2] = x1 * c - x2 * s
+        o[..., 1::2] = x2 * c + x1 * s
+        return o
+
+    def no_gain_norm(x, g, eps):
+        return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps)
+
+    for name, fn in (("rope", wrong_rope), ("rms_norm", no_gain_norm)):
+        with monkeypatch.context() as m:
+            m.setattr(odec, name, fn)
+            bad = dec.full(toks).logits
+        assert np.max(np.abs(bad - ref)) > 1e-3, name
+
+
+# ---------------------------------------------------------------------------
+# caching and verification invariants
+# ---------------------------------------------------------------------------
+def test_incremental_equals_full_recompute(models):
+    shape, w, dec, _ = models["gqa"]
+    toks = _prompt(17, shape.vocab)
+    full = dec.full(toks).logits
+    cache = dec.empty_cache()
+    rows = []
+    for t in toks:
+        out, cache = dec.extend(cache, [t])
+        rows.append(out.logits[0])
+    assert np.max(np.abs(np.stack(rows) - full)) < 1e-10
+
+
+def _state(models, which_d="gqa", which_t="mha", n=9):
+    sd, wd, dd, _ = models[which_d]
+    st_, wt, dt, _ = models[which_t]
+    return dd, dt, oracle.prefill(dd, dt, _prompt(n, sd.vocab, seed=11))
+
+
+def test_tree_verify_equals_per_beam_and_full(models):
+    draft, target, st = _state(models)
+    k, d = 3, 4
+    heads = oracle.topk_ids(st.s_logits, k)
+    x = oracle.rollout(draft, st, heads, d).x
+    lt, ht = oracle.verify_rows_tree(target, st, heads, x)
+    lb, hb = oracle.verify_rows_per_beam(target, st, heads, x)
+    assert np.max(np.abs(lt - lb)) < 1e-10 and np.max(np.abs(ht - hb)) < 1e-10
+    for i in range(k):
+        seq = st.tokens + [int(heads[i])] + [int(t) for t in x[i, :d - 1]]
+        full = target.full(seq).logits[-d:]
+        assert np.max(np.abs(full - lt[i])) < 1e-10
+
+
+def test_shared_prefix_equals_duplicated_prefix(models):
+    """Rollout of every beam from one shared prefix cache equals rollouts
+    from independent full recomputes (no state leaks between beams)."""
+    draft, target, st = _state(models)
+    heads = oracle.topk_ids(st.s_logits, 4)
+    ro = oracle.rollout(draft, st, heads, 3)
+    for i, c in enumerate(heads):
+        seq = list(st.tokens) + [int(c)]
+        for j in range(3):
+            z = draft.full(seq).logits[-1]
+            assert ro.x[i, j] == int(np.argmax(z))
+            seq.append(int(ro.x[i, j]))
+
+
+def test_rollout_is_argmax_of_library_forward(models):
+    from hf_ref import hf_logits
+    sd, wd, dd, hf_d = models["gqa"]
+    _, _, dt, _ = models["mha"]
+    st = oracle.prefill(dd, dt, _prompt(8, sd.vocab, seed=5))
+    heads = oracle.topk_ids(st.s_logits, 3)
+    ro = oracle.rollout(dd, st, heads, 4)
+    for i, c in enumerate(heads):
+        seq = list(st.tokens) + [int(c)]
+        for j in range(4):
+            assert ro.x[i, j] == int(np.argmax(hf_logits(hf_d, seq)[-1]))
+            seq.append(int(ro.x[i, j]))
+
+
+# ---------------------------------------------------------------------------
+# special cases of the whole step
+# ---------------------------------------------------------------------------
+def test_k1_reduces_to_greedy_decoding_of_target(models):
+    """With one beam the emitted tokens are exactly the target's greedy
+    continuation (greedy speculative decoding is lossless), for any draft."""
+    from hf_ref import hf_greedy
+    draft, target, st0 = _state(models, n=7)
+    hf_t = models["mha"][3]
+    st = st0
+    out = []
+    for _ in range(5):
+        r = oracle.step(draft, target, st, 1, 3, 1.0, "keyword_count", kws=[1, 2, 3])
+        out += r.emitted
+        st = r.state
+    assert out == hf_greedy(hf_t, st0.tokens, len(out))
+
+
+def test_draft_equal_to_target_accepts_every_token(models):
+    _, _, dt, _ = models["mha"]
+    st = oracle.prefill(dt, dt, _prompt(6, 64, seed=2))
+    k, d = 3, 4
+    r = oracle.step(dt, dt, st, k, d, 1.0, "keyword_count", kws=[5, 6, 7])
+    assert list(r.ver.n) == [d] * k
+    for i in range(k):
+        for j in range(d):
+            z = r.ver.logits[i, j]
+            assert abs(r.ver.logprobs[i, j] - oracle.log_softmax(z).max()) < 1e-12
+    # n = d: all d+1 tokens are emitted and the next head distribution is the
+    # target's distribution after x_d
+    assert len(r.emitted) == d + 1
+    full = dt.full(r.state.tokens).logits[-1]
+    assert np.max(np.abs(r.state.s - oracle.log_softmax(full))) < 1e-10
+
+
+TINY = ci.ModelShape(1, 16, 2, 1, 32, 16)
+
+
+def test_select_matches_brute_force_enumeration():
+    """k = V: every possible head is a beam.  Enumerate all heads, roll out
+    and score by full recompute, and check the step's choice."""
+    wt = _weights(TINY, 1, seed=21)
+    wd = _weights(TINY, 0, seed=22)
+    T, Dm = odec.Decoder(TINY, wt), odec.Decoder(TINY, wd)
+    V = TINY.vocab
+    prompt = [3, 9, 1, 14]
+    st = oracle.prefill(Dm, T, prompt)
+    kws = [2, 5, 11]
+    for d in (1, 2, 3):
+        for alpha in (0.0, 0.7, math.inf):
+            r = oracle.step(Dm, T, st, V, d, alpha, "keyword_count", kws=kws)
+            best, best_val, rows = None, -math.inf, []
+            s0 = oracle.log_softmax(T.full(prompt).logits[-1])
+            for c in range(V):
+                seq = prompt + [c]
+                for _ in range(d):
+                    seq.append(int(np.argmax(Dm.full(seq).logits[-1])))
+                ls = oracle.log_softmax(T.full(seq[:-1]).logits[-d:])
+                x = seq[len(prompt) + 1:]
+                score = s0[c] + sum(ls[j, x[j]] for j in range(d))
+                rew = oracle.keyword_hits([c] + x, kws)
+                val = rew if math.isinf(alpha) else score + alpha * rew
+                rows.append((c, val))
+            ordered = sorted(rows, key=lambda cv: (-cv[1], [h for h in r.heads].index(cv[0])))
+            assert int(r.heads[r.beam]) == ordered[0][0]
+            assert abs(r.combined[r.beam] - ordered[0][1]) < 1e-9
+
+
+def test_alpha_infinity_is_the_lookahead_heuristic_rule():
+    """alpha = inf keeps the first beam with the strictly largest reward."""
+    scores = np.array([-1.0, -9.0, -2.0, -0.5])
+    reward = np.array([0.25, 0.75, 0.75, 0.5])
+    best, best_r = None, -math.inf
+    for i, r in enumerate(reward):   # the CDLH update, written out
+        if r > best_r:
+            best, best_r = i, r
+    assert oracle.select_beam(scores, reward, math.inf) == best == 1
+    assert oracle.select_beam(scores, reward, 0.0) == 3
+
+
+# ---------------------------------------------------------------------------
+# reward, rows, rejection
+# ---------------------------------------------------------------------------
+def test_reward_worked_example_from_the_paper():
+    g = json.load(open(os.path.join(GOLDEN, "reward_worked_example.json")))
+    concepts = list(range(100, 100 + g["concepts"]))
+    window = [7, concepts[0], 8, concepts[3], concepts[3], 9]
+    assert oracle.keyword_hits(window, concepts) == g["covered"]
+    assert abs(oracle.keyword_coverage(window, concepts) - g["reward"]) < 1e-15
+
+
+def test_log_softmax_and_topk_rows():
+    rng = np.random.default_rng(0)
+    z = rng.standard_normal(50) * 3
+    ls = oracle.log_softmax(z)
+    assert abs(np.sum(np.exp(ls)) - 1.0) < 1e-13
+    assert np.allclose(ls - ls[0], z - z[0], atol=1e-12)
+    # forced ties: equal values resolve to the lower id
+    z = np.array([1.0, 3.0, 2.0, 3.0, 2.0, -1.0, 3.0])
+    assert list(oracle.topk_ids(z, 5)) == [1, 3, 6, 2, 4]
+    assert oracle.argmax_lowest(z) == 1
+    brute = sorted(range(len(z)), key=lambda i: (-z[i], i))
+    assert list(oracle.topk_ids(z, 7)) == brute
+
+
+def test_hard_rejection_counts_leading_matches():
+    assert oracle.leading_matches([1, 2, 3], [1, 2, 3]) == 3
+    assert oracle.leading_matches([1, 2, 3], [1, 5, 3]) == 1
+    assert oracle.leading_matches([4, 2, 3], [1, 2, 3]) == 0
+
+
+# ---------------------------------------------------------------------------
+# resume and batch independence
+# ---------------------------------------------------------------------------
+def test_resume_by_reprefill_equals_uninterrupted_run(models):
+    draft, target, st = _state(models, n=6)
+    a = st
+    for _ in range(4):
+        a = oracle.step(draft, target, a, 3, 2, 1.0, "keyword_count", kws=[1, 2]).state
+    b = oracle.prefill(draft, target, a.tokens)
+    b.n_prompt = st.n_prompt
+    for _ in range(3):
+        a = oracle.step(draft, target, a, 3, 2, 1.0, "keyword_count", kws=[1, 2]).state
+        b = oracle.step(draft, target, b, 3, 2, 1.0, "keyword_count", kws=[1, 2]).state
+    assert a.tokens == b.tokens
+
+
+def test_inputs_do_not_depend_on_batch_size():
+    a = ci.prompts(0, 5, 9, 1000)
+    b = ci.prompts(0, 2, 9, 1000, first=3)
+    assert np.array_equal(a[3:], b)
+    ka = ci.keywords(0, 4, 3, 1000)
+    assert all(len(set(r)) == 3 for r in ka)
+    assert np.array_equal(ka[2:], ci.keywords(0, 2, 3, 1000, first=2))
