@@ -1,0 +1,225 @@
+/*
+ * cdsl.h -- C ABI of the CDSL lookahead-step library for MI355X (gfx950).
+ *
+ * One lookahead step of constrained decoding with speculative lookaheads
+ * (Nakshatri et al., "Constrained Decoding with Speculative Lookaheads"):
+ *
+ *   cdsl_prefill   prompt forward of both decoders, first beam heads
+ *   cdsl_rollout   the draft model extends each of the k beam heads by d
+ *                  greedy tokens (Sec. 3.2.1; Alg. 1, drafting loop)
+ *   cdsl_verify    the target model scores all k*d lookahead tokens in one
+ *                  tree-masked forward pass; per-token log-probs, target
+ *                  argmax, hard-rejection counts and beam scores
+ *                  (Sec. 3.2.2; Alg. 1, verification and rejection loops)
+ *   cdsl_reward_*  the task reward R per beam (Sec. 3.2.2, validation by R;
+ *                  Sec. 4.1 concept counting; a linear head stands in for the
+ *                  semantic reward model)
+ *   cdsl_select    the beam maximising score + alpha * reward (Alg. 2, the
+ *                  reward argmax; alpha = +inf is exactly that rule)
+ *   cdsl_commit    emits the selected beam's head plus its accepted tokens
+ *                  (S1 action of Sec. 3.2.3, no bonus token), makes them part
+ *                  of the shared prefix and produces the next beam heads
+ *
+ * Conventions
+ *   - Every call returns CDSL_OK (0) or a negative CDSL_E* code; the message
+ *     of the last failure is available from cdsl_last_error(ctx).  No C++
+ *     exception crosses this boundary.  Arguments are checked on the host
+ *     before anything is launched; a failed call has launched nothing.
+ *   - Pointer arguments are DEVICE pointers unless the name ends in _host.
+ *     They are owned by the caller and only read/written during the call
+ *     (device work is ordered on the context's stream).
+ *   - Calls are asynchronous on the stream given to cdsl_init, except
+ *     cdsl_commit, which synchronises that stream once (it must learn how
+ *     many tokens each prompt emitted to manage the KV blocks).
+ *   - Shapes are row-major, innermost last.  Token ids are int32 in [0, V).
+ *   - Nothing is allocated after cdsl_init except by cdsl_prefill (the
+ *     prefix handle's bookkeeping; KV blocks come from the pool sized at
+ *     init).  A context is not thread-safe.
+ */
+#ifndef CDSL_H
+#define CDSL_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  CDSL_OK = 0,
+  CDSL_EINVAL = -1,   /* bad argument (shape, pointer, value)            */
+  CDSL_ERANGE = -2,   /* beyond the limits given at init                 */
+  CDSL_ENOMEM = -3,   /* device memory or KV pool exhausted              */
+  CDSL_EDEVICE = -4,  /* a HIP runtime call failed                       */
+  CDSL_ESTATE = -5    /* call out of order (e.g. verify before rollout)  */
+};
+
+enum { CDSL_F32 = 0, CDSL_BF16 = 1 };
+
+/* Shape of one Llama-style decoder: pre-norm RMSNorm, rotary embedding
+ * (rotate-half pairing, 0-based positions), grouped-query attention,
+ * SwiGLU MLP, no biases, untied LM head.  head_dim = d_model / n_heads and
+ * must be 32, 64 or 128. */
+typedef struct cdsl_model_config {
+  int32_t n_layers;
+  int32_t d_model;
+  int32_t n_heads;
+  int32_t n_kv_heads;
+  int32_t ffn_dim;
+  int32_t vocab;
+  float rope_theta;
+  float rms_eps;
+  int32_t dtype;      /* CDSL_F32 or CDSL_BF16: weights, activations, KV */
+} cdsl_model_config;
+
+/* Weights of one decoder, device pointers in the dtype of cfg (norm gains
+ * are always fp32).  Matrices are [out_features, in_features] row-major.
+ * layer_ptrs points to a HOST array of n_layers * 9 device pointers, per
+ * layer in this order:
+ *   attn_norm[D], wq[H*hd, D], wk[Hkv*hd, D], wv[Hkv*hd, D], wo[D, H*hd],
+ *   mlp_norm[D], w_gate[F, D], w_up[F, D], w_down[D, F]
+ * cdsl_init copies (and re-packs) everything into library-owned memory; the
+ * caller's buffers are not referenced after cdsl_init returns. */
+typedef struct cdsl_model {
+  cdsl_model_config cfg;
+  const void* tok_emb;              /* [V, D]   */
+  const void* final_norm;           /* [D] fp32 */
+  const void* lm_head;              /* [V, D]   */
+  const void* const* layer_ptrs;    /* host array, n_layers * 9 entries */
+} cdsl_model;
+
+/* Capacity limits; every later call is checked against them. */
+typedef struct cdsl_limits {
+  int32_t max_batch;     /* prompts per prefix handle                    */
+  int32_t max_ctx;       /* prompt + generated tokens per prompt         */
+  int32_t max_k;         /* beams (<= 16)                                */
+  int32_t max_d;         /* lookahead depth (<= 32)                      */
+  int32_t max_prompt;    /* longest prompt passed to cdsl_prefill        */
+  int32_t max_prefixes;  /* prefix handles alive at once                 */
+} cdsl_limits;
+
+typedef struct cdsl_ctx cdsl_ctx;
+typedef struct cdsl_prefix cdsl_prefix;
+
+/* Create a context for a draft/target pair (same vocabulary and dtype, as
+ * speculative decoding requires models of one family, Sec. 4.2).  stream is
+ * a hipStream_t (NULL = the default stream).  Allocates the weights copy,
+ * the paged KV pools of both models, the rotary tables and all workspaces.
+ * Errors: EINVAL (shapes, vocab or dtype mismatch), ENOMEM, EDEVICE. */
+int cdsl_init(const cdsl_model* draft, const cdsl_model* target,
+              const cdsl_limits* limits, void* stream, cdsl_ctx** out);
+
+/* Prompt forward of both models over tokens[B, L] (device int32), writing
+ * the shared-prefix KV blocks of a new prefix handle (*out, library-owned,
+ * released by cdsl_free_prefix).  Writes the first beam heads: beams[B, k]
+ * = the k most likely next tokens of the target (log-prob descending, token
+ * id ascending on ties) and head_lp[B, k] their log-probs (fp32).
+ * Errors: EINVAL, ERANGE (B, L or k beyond limits), ENOMEM (KV pool). */
+int cdsl_prefill(cdsl_ctx* ctx, const int32_t* tokens, int32_t B, int32_t L,
+                 int32_t k, cdsl_prefix** out, int32_t* beams, float* head_lp);
+
+/* Draft rollout.  For every prompt b and beam i, feeds the head
+ * beams[b, i] and then its own greedy outputs to the draft model for d
+ * steps: lookaheads[b, i, 0] = beams[b, i] and lookaheads[b, i, j] =
+ * argmax of the draft at step j (lowest id on ties), j = 1..d.
+ * lookaheads is [B, k, d+1] int32.  All beams of a prompt read that
+ * prompt's prefix KV blocks once; each beam writes its own suffix blocks.
+ * Errors: EINVAL, ERANGE (k, d). */
+int cdsl_rollout(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* beams,
+                 int32_t k, int32_t d, int32_t* lookaheads);
+
+/* Target verification of lookaheads[B, k, d+1] (any values, not only those
+ * of the last rollout: the call depends on its arguments and the prefix
+ * only).  Feeds rows (i, j) = lookaheads[b, i, j], j = 0..d-1, at positions
+ * L_b + j in ONE forward pass; row (i, j) attends to the whole prefix and to
+ * rows (i, 0..j) of its own beam.  Outputs (device):
+ *   logprobs[B,k,d]       log p_j(x_{i,j}) where p_j is row (i, j-1)'s
+ *                         distribution and x_{i,j} = lookaheads[b, i, j]
+ *   target_argmax[B,k,d]  argmax of row (i, j-1) (lowest id on ties)
+ *   n_accept[B,k]         leading j with target_argmax == x (hard rejection)
+ *   scores[B,k]           head_lp[b, i] + sum_j logprobs[b, i, j]
+ *   row_topk_ids[B,k,d,k], row_topk_lp[B,k,d,k]  top-k of every fed row
+ *   hidden[B,k,D]         fp32 final-normed hidden state of row (i, d-1),
+ *                         or NULL if not wanted
+ * Errors: EINVAL, ERANGE. */
+int cdsl_verify(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookaheads,
+                int32_t k, int32_t d, const float* head_lp, float* logprobs,
+                int32_t* target_argmax, int32_t* n_accept, float* scores,
+                int32_t* row_topk_ids, float* row_topk_lp, float* hidden);
+
+/* Keyword reward: for every beam, the number of distinct keywords of
+ * keywords[b, 0..n_kw) that occur in generated-so-far + lookaheads[b, i,
+ * 0..d] (the prompt is not searched).  With normalize != 0 the count is
+ * divided by the number of distinct keywords (concept coverage, Sec. 4.1).
+ * reward is [B, k] fp32.  Errors: EINVAL. */
+int cdsl_reward_keywords(cdsl_ctx* ctx, cdsl_prefix* prefix,
+                         const int32_t* lookaheads, int32_t k, int32_t d,
+                         const int32_t* keywords, int32_t n_kw, int32_t normalize,
+                         float* reward);
+
+/* Linear reward head: reward[b, i] = dot(w, hidden[b, i, :]), hidden as
+ * written by cdsl_verify, w [D] fp32.  Errors: EINVAL. */
+int cdsl_reward_linear(cdsl_ctx* ctx, const float* hidden, const float* w,
+                       int32_t B, int32_t k, int32_t D, float* reward);
+
+/* beam[b] = argmax_i (scores[b, i] + alpha * reward[b, i]), lowest i on
+ * ties; alpha = +INFINITY selects on the reward alone.  A NaN score or
+ * reward makes beam[b] = -1, which cdsl_commit reports as EINVAL. */
+int cdsl_select(cdsl_ctx* ctx, const float* scores, const float* reward,
+                float alpha, int32_t B, int32_t k, int32_t* beam);
+
+/* Commit the selected beams.  Emits, per prompt, O = [c_i*, x_i*,1..n]
+ * with n = n_accept[b, i*]: emitted_host[b, 0..n] and n_emit_host[b] = n+1
+ * (host buffers, [B, d+1] and [B]).  The beam's KV for those tokens becomes
+ * part of the prefix (both models); if n == d the last token is fed through
+ * both models so the prefix is complete.  next_beams[B, k] / next_head_lp
+ * receive the next beam heads (top-k of the target after O).  Synchronises
+ * the context stream once.  Errors: EINVAL (beam -1 / out of range),
+ * ERANGE (max_ctx exceeded), ENOMEM, ESTATE (no verify since the last
+ * commit). */
+int cdsl_commit(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookaheads,
+                const int32_t* beam, const int32_t* n_accept,
+                const int32_t* row_topk_ids, const float* row_topk_lp,
+                int32_t k, int32_t d, int32_t* emitted_host,
+                int32_t* n_emit_host, int32_t* next_beams, float* next_head_lp);
+
+/* Current length (prompt + emitted) of every prompt: lengths_host[B]. */
+int cdsl_prefix_lengths(cdsl_ctx* ctx, const cdsl_prefix* prefix,
+                        int32_t* lengths_host);
+
+/* Per-kernel-class timing, for measurement.  While enabled, every launch
+ * is bracketed by a pair of HIP events on the context stream and its
+ * algorithmic work is added to its class: flops (2*M*N*K for a projection,
+ * 4*hd per visible (query, key) pair for attention) and bytes (each operand
+ * read once, each output written once; for attention the prefix KV of a
+ * prompt counts once for all its beams).  cdsl_profile_enable(ctx, 1)
+ * resets the totals; cdsl_profile_read synchronises the stream and returns
+ * the totals since then.  Disabled (the default), no events are recorded. */
+enum {
+  CDSL_K_GEMM_DENSE = 0,   /* bf16 MFMA projection, > 128 rows          */
+  CDSL_K_GEMM_SKINNY = 1,  /* bf16 MFMA projection, <= 128 rows (decode) */
+  CDSL_K_ATTENTION = 2,    /* paged shared-prefix / tree attention       */
+  CDSL_K_ATTN_COMBINE = 3, /* merge of key-split partials                */
+  CDSL_K_LOGIT_ROWS = 4,   /* log-softmax + gather + argmax + top-k      */
+  CDSL_K_ROWWISE = 5,      /* embedding, RMSNorm, rotary + KV write      */
+  CDSL_K_STEP = 6,         /* scores, rewards, select, commit, promote   */
+  CDSL_K_GEMM_F32 = 7,     /* fp32 projection                            */
+  CDSL_K_CLASSES = 8
+};
+typedef struct cdsl_kernel_stats {
+  int64_t launches[CDSL_K_CLASSES];
+  double ms[CDSL_K_CLASSES];
+  double flops[CDSL_K_CLASSES];
+  double bytes[CDSL_K_CLASSES];
+} cdsl_kernel_stats;
+int cdsl_profile_enable(cdsl_ctx* ctx, int32_t enable);
+int cdsl_profile_read(cdsl_ctx* ctx, cdsl_kernel_stats* out);
+
+int cdsl_free_prefix(cdsl_ctx* ctx, cdsl_prefix* prefix);
+int cdsl_destroy(cdsl_ctx* ctx);          /* NULL is accepted */
+const char* cdsl_last_error(const cdsl_ctx* ctx);   /* never NULL */
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CDSL_H */

@@ -1,0 +1,59 @@
+/*
+ * cdsl_ops.h -- kernel-level entry points of the CDSL library, exported so
+ * that single kernels can be checked in isolation.  They run exactly the
+ * kernels that cdsl_rollout / cdsl_verify launch, on caller buffers.
+ * All pointers are device pointers owned by the caller; calls are
+ * asynchronous on `stream` (a hipStream_t, NULL = default stream) and return
+ * CDSL_OK or a negative CDSL_E* code (see cdsl.h).  No call allocates.
+ */
+#ifndef CDSL_OPS_H
+#define CDSL_OPS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  CDSL_EPI_STORE = 0,     /* C[M,N] (fp32)  = A * B^T                 */
+  CDSL_EPI_RESIDUAL = 1   /* C[M,N] (fp32) += A * B^T  (residual add)   */
+};
+
+/* Bytes of workspace cdsl_op_gemm needs for this shape (split-K partial
+ * tiles and their arrival counters); 0 if none. */
+size_t cdsl_op_gemm_workspace(int32_t M, int32_t N, int32_t K, int32_t dtype);
+
+/* Dense projection C = A[M,K] * B[N,K]^T with fp32 accumulation: the
+ * contraction of every linear layer of the decoders (q/k/v/o, gate/up/down,
+ * LM head).  A (activations) is fp32; B (weights) is bf16 (dtype
+ * CDSL_BF16: A is split into bf16 hi + lo halves, two MFMA products, so the
+ * result keeps fp32-level accuracy) or fp32 (CDSL_F32); C is fp32.  K must
+ * be a multiple of 32 for bf16 (16 for fp32).  The workspace
+ * must hold cdsl_op_gemm_workspace(M, N, K, dtype) bytes and be zeroed once
+ * before first use (its counters return to zero after every call).
+ * Errors: EINVAL. */
+int cdsl_op_gemm(const void* A, const void* B, float* C, int32_t M, int32_t N,
+                 int32_t K, int32_t dtype, int32_t epilogue, void* workspace,
+                 size_t workspace_bytes, void* stream);
+
+/* Row statistics of logits[M, V] (fp32), one pass per row, never writing
+ * probabilities: for row m,
+ *   lp[m]        = logits[m, gather[m]] - logsumexp(logits[m, :])
+ *                  (skipped, lp untouched, if gather is NULL)
+ *   amax[m]      = argmax (lowest id on ties)
+ *   topk_ids[m, 0..kk), topk_lp[m, 0..kk): the kk largest entries, value
+ *                  descending then id ascending, as log-probs
+ *                  (skipped if kk == 0; kk <= 16)
+ * This is the log-softmax + gather + argmax + top-k step of verification.
+ * Errors: EINVAL. */
+int cdsl_op_logit_rows(const float* logits, int32_t M, int32_t V,
+                       const int32_t* gather, int32_t kk, float* lp,
+                       int32_t* amax, int32_t* topk_ids, float* topk_lp,
+                       void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CDSL_OPS_H */

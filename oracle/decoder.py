@@ -94,6 +94,15 @@ class Decoder:
     def __init__(self, shape, weights):
         self.shape = shape
         self.w = weights
+        self._f64 = {}
+
+    def mat(self, layer, name):
+        """Weight as float64, converted once and kept."""
+        key = (layer, name)
+        if key not in self._f64:
+            src = self.w[name] if layer is None else self.w["layers"][layer][name]
+            self._f64[key] = _f64(src)
+        return self._f64[key]
 
     @property
     def n_layers(self):
@@ -121,9 +130,9 @@ class Decoder:
         new_k, new_v = [], []
         for l, lw in enumerate(self.w["layers"]):
             u = rms_norm(h, lw["attn_norm"], s.rms_eps)
-            q = (u @ _f64(lw["wq"]).T).reshape(T, H, hd)
-            k = (u @ _f64(lw["wk"]).T).reshape(T, Hkv, hd)
-            v = (u @ _f64(lw["wv"]).T).reshape(T, Hkv, hd)
+            q = (u @ self.mat(l, "wq").T).reshape(T, H, hd)
+            k = (u @ self.mat(l, "wk").T).reshape(T, Hkv, hd)
+            v = (u @ self.mat(l, "wv").T).reshape(T, Hkv, hd)
             q = rope(q, positions, s.rope_theta)
             k = rope(k, positions, s.rope_theta)
             new_k.append(k)
@@ -136,12 +145,12 @@ class Decoder:
                 sc = (q[:, hq, :] @ K[:, kv, :].T) / np.sqrt(hd)
                 sc = np.where(allowed, sc, -np.inf)
                 o[:, hq, :] = softmax_rows(sc) @ V[:, kv, :]
-            h = h + o.reshape(T, H * hd) @ _f64(lw["wo"]).T
+            h = h + o.reshape(T, H * hd) @ self.mat(l, "wo").T
             u = rms_norm(h, lw["mlp_norm"], s.rms_eps)
-            a = silu(u @ _f64(lw["w_gate"]).T) * (u @ _f64(lw["w_up"]).T)
-            h = h + a @ _f64(lw["w_down"]).T
+            a = silu(u @ self.mat(l, "w_gate").T) * (u @ self.mat(l, "w_up").T)
+            h = h + a @ self.mat(l, "w_down").T
         hf = rms_norm(h, self.w["final_norm"], s.rms_eps)
-        logits = hf @ _f64(self.w["lm_head"]).T
+        logits = hf @ self.mat(None, "lm_head").T
         return ForwardOut(logits, hf, new_k, new_v)
 
     # -- convenience wrappers -------------------------------------------------

@@ -1,0 +1,349 @@
+"""ctypes binding of libcdsl.so: the calls of include/cdsl.h and
+include/cdsl_ops.h with the same names, marshalling torch device tensors to
+plain pointers.  Every step of the computation runs in the HIP library; if
+the library is missing, loading fails loudly (there is no fallback)."""
+from __future__ import annotations
+
+import ctypes as C
+import math
+import os
+from typing import Dict, List, Optional, Sequence
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "_lib", "libcdsl.so")
+
+CDSL_OK, CDSL_EINVAL, CDSL_ERANGE, CDSL_ENOMEM, CDSL_EDEVICE, CDSL_ESTATE = 0, -1, -2, -3, -4, -5
+CDSL_F32, CDSL_BF16 = 0, 1
+CDSL_EPI_STORE, CDSL_EPI_RESIDUAL = 0, 1
+ERR_NAMES = {0: "OK", -1: "EINVAL", -2: "ERANGE", -3: "ENOMEM", -4: "EDEVICE", -5: "ESTATE"}
+
+EXPORTS = [
+    "cdsl_init", "cdsl_prefill", "cdsl_rollout", "cdsl_verify", "cdsl_reward_keywords",
+    "cdsl_reward_linear", "cdsl_select", "cdsl_commit", "cdsl_prefix_lengths",
+    "cdsl_free_prefix", "cdsl_destroy", "cdsl_last_error", "cdsl_profile_enable", "cdsl_profile_read",
+    "cdsl_op_gemm_workspace", "cdsl_op_gemm", "cdsl_op_logit_rows",
+]
+
+
+class CDSLError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{ERR_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+class ModelConfig(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("ffn_dim", C.c_int32), ("vocab", C.c_int32),
+                ("rope_theta", C.c_float), ("rms_eps", C.c_float), ("dtype", C.c_int32)]
+
+
+class Model(C.Structure):
+    _fields_ = [("cfg", ModelConfig), ("tok_emb", C.c_void_p), ("final_norm", C.c_void_p),
+                ("lm_head", C.c_void_p), ("layer_ptrs", C.POINTER(C.c_void_p))]
+
+
+KERNEL_CLASSES = ["gemm_dense", "gemm_skinny", "attention", "attn_combine", "logit_rows", "rowwise", "step",
+                  "gemm_f32"]
+
+
+class KernelStats(C.Structure):
+    _fields_ = [("launches", C.c_int64 * 8), ("ms", C.c_double * 8), ("flops", C.c_double * 8),
+                ("bytes", C.c_double * 8)]
+
+
+class Limits(C.Structure):
+    _fields_ = [("max_batch", C.c_int32), ("max_ctx", C.c_int32), ("max_k", C.c_int32),
+                ("max_d", C.c_int32), ("max_prompt", C.c_int32), ("max_prefixes", C.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libcdsl.so (built in-tree by ``paper_2412_10418_amd.build``)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2412_10418_amd.build` (no CPU fallback exists)")
+    L = C.CDLL(LIB_PATH)
+    vp, i32, f32 = C.c_void_p, C.c_int32, C.c_float
+    sig = {
+        "cdsl_init": ([C.POINTER(Model), C.POINTER(Model), C.POINTER(Limits), vp, C.POINTER(vp)], i32),
+        "cdsl_prefill": ([vp, vp, i32, i32, i32, C.POINTER(vp), vp, vp], i32),
+        "cdsl_rollout": ([vp, vp, vp, i32, i32, vp], i32),
+        "cdsl_verify": ([vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp], i32),
+        "cdsl_reward_keywords": ([vp, vp, vp, i32, i32, vp, i32, i32, vp], i32),
+        "cdsl_reward_linear": ([vp, vp, vp, i32, i32, i32, vp], i32),
+        "cdsl_select": ([vp, vp, vp, f32, i32, i32, vp], i32),
+        "cdsl_commit": ([vp, vp, vp, vp, vp, vp, vp, i32, i32, vp, vp, vp, vp], i32),
+        "cdsl_prefix_lengths": ([vp, vp, vp], i32),
+        "cdsl_free_prefix": ([vp, vp], i32),
+        "cdsl_destroy": ([vp], i32),
+        "cdsl_last_error": ([vp], C.c_char_p),
+        "cdsl_profile_enable": ([vp, i32], i32),
+        "cdsl_profile_read": ([vp, C.POINTER(KernelStats)], i32),
+        "cdsl_op_gemm_workspace": ([i32, i32, i32, i32], C.c_size_t),
+        "cdsl_op_gemm": ([vp, vp, vp, i32, i32, i32, i32, i32, vp, C.c_size_t, vp], i32),
+        "cdsl_op_logit_rows": ([vp, i32, i32, vp, i32, vp, vp, vp, vp, vp], i32),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = L
+    return L
+
+
+def _ptr(t: Optional[torch.Tensor], dtype=None, name="tensor"):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _check(rc, ctx=None):
+    if rc != CDSL_OK:
+        msg = lib().cdsl_last_error(ctx)
+        raise CDSLError(rc, msg.decode() if msg else "")
+
+
+# ---------------------------------------------------------------------------
+# kernel-level entry points
+# ---------------------------------------------------------------------------
+_GEMM_WS = {}
+
+
+def cdsl_op_gemm(A: torch.Tensor, B: torch.Tensor, C_out: Optional[torch.Tensor] = None,
+                 residual: bool = False) -> torch.Tensor:
+    M, K = A.shape
+    N = B.shape[0]
+    dt = CDSL_BF16 if B.dtype == torch.bfloat16 else CDSL_F32
+    if C_out is None:
+        C_out = torch.zeros((M, N), dtype=torch.float32, device=A.device)
+    need = lib().cdsl_op_gemm_workspace(M, N, K, dt)
+    ws = _GEMM_WS.get(A.device)
+    if ws is None or ws.numel() < need:
+        ws = torch.zeros(max(need, 256), dtype=torch.uint8, device=A.device)
+        _GEMM_WS[A.device] = ws
+    rc = lib().cdsl_op_gemm(_ptr(A, torch.float32, "A"), _ptr(B, B.dtype, "B"), _ptr(C_out, torch.float32, "C"),
+                            M, N, K, dt, CDSL_EPI_RESIDUAL if residual else CDSL_EPI_STORE,
+                            ws.data_ptr(), ws.numel(), _stream())
+    _check(rc)
+    return C_out
+
+
+def cdsl_op_logit_rows(logits: torch.Tensor, gather: Optional[torch.Tensor], kk: int):
+    M, V = logits.shape
+    dev = logits.device
+    lp = torch.zeros(M, dtype=torch.float32, device=dev)
+    amax = torch.zeros(M, dtype=torch.int32, device=dev)
+    tk = torch.zeros((M, max(kk, 1)), dtype=torch.int32, device=dev)
+    tl = torch.zeros((M, max(kk, 1)), dtype=torch.float32, device=dev)
+    rc = lib().cdsl_op_logit_rows(_ptr(logits, torch.float32, "logits"), M, V,
+                                  _ptr(gather, torch.int32, "gather"), kk, lp.data_ptr(),
+                                  amax.data_ptr(), tk.data_ptr(), tl.data_ptr(), _stream())
+    _check(rc)
+    return lp, amax, tk[:, :kk], tl[:, :kk]
+
+
+# ---------------------------------------------------------------------------
+# context
+# ---------------------------------------------------------------------------
+def _model_struct(shape, dtype_code, tensors: Dict[str, object]):
+    cfg = ModelConfig(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads, shape.ffn_dim,
+                      shape.vocab, shape.rope_theta, shape.rms_eps, dtype_code)
+    order = ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "w_gate", "w_up", "w_down")
+    ptrs = []
+    for lw in tensors["layers"]:
+        for nm in order:
+            ptrs.append(_ptr(lw[nm], None, nm))
+    arr = (C.c_void_p * len(ptrs))(*ptrs)
+    m = Model(cfg, _ptr(tensors["tok_emb"], None, "tok_emb"), _ptr(tensors["final_norm"], torch.float32, "final_norm"),
+              _ptr(tensors["lm_head"], None, "lm_head"), C.cast(arr, C.POINTER(C.c_void_p)))
+    return m, arr
+
+
+class Prefix:
+    def __init__(self, ctx: "Context", handle, B: int):
+        self.ctx, self.handle, self.B = ctx, handle, B
+
+    def lengths(self) -> List[int]:
+        out = (C.c_int32 * self.B)()
+        _check(lib().cdsl_prefix_lengths(self.ctx.handle, self.handle, out), self.ctx.handle)
+        return list(out)
+
+    def free(self):
+        if self.handle:
+            _check(lib().cdsl_free_prefix(self.ctx.handle, self.handle), self.ctx.handle)
+            self.handle = None
+
+
+class Context:
+    """One draft/target pair behind cdsl_init.  Weights are dicts of device
+    tensors laid out like ``cdsl_inputs.model_weights`` (matrices
+    [out, in] in the model dtype, norm gains fp32)."""
+
+    def __init__(self, draft_shape, draft_w, target_shape, target_w, dtype: str, limits: Dict[str, int]):
+        code = CDSL_BF16 if dtype == "bf16" else CDSL_F32
+        dm, dkeep = _model_struct(draft_shape, code, draft_w)
+        tm, tkeep = _model_struct(target_shape, code, target_w)
+        lim = Limits(limits["max_batch"], limits["max_ctx"], limits["max_k"], limits["max_d"],
+                     limits["max_prompt"], limits.get("max_prefixes", 1))
+        h = C.c_void_p()
+        rc = lib().cdsl_init(C.byref(dm), C.byref(tm), C.byref(lim), _stream(), C.byref(h))
+        _check(rc)
+        self.handle = h
+        self.draft_shape, self.target_shape = draft_shape, target_shape
+        self.dtype = dtype
+        del dkeep, tkeep
+
+    def close(self):
+        if self.handle:
+            lib().cdsl_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- measurement -----------------------------------------------------------
+    def profile_enable(self, on: bool = True):
+        _check(lib().cdsl_profile_enable(self.handle, 1 if on else 0), self.handle)
+
+    def profile_read(self) -> Dict[str, dict]:
+        st = KernelStats()
+        _check(lib().cdsl_profile_read(self.handle, C.byref(st)), self.handle)
+        return {nm: {"launches": int(st.launches[i]), "ms": float(st.ms[i]), "flops": float(st.flops[i]),
+                     "bytes": float(st.bytes[i])} for i, nm in enumerate(KERNEL_CLASSES)}
+
+    # -- the step ------------------------------------------------------------
+    def cdsl_prefill(self, tokens: torch.Tensor, k: int):
+        B, L = tokens.shape
+        dev = tokens.device
+        beams = torch.empty((B, k), dtype=torch.int32, device=dev)
+        head_lp = torch.empty((B, k), dtype=torch.float32, device=dev)
+        h = C.c_void_p()
+        rc = lib().cdsl_prefill(self.handle, _ptr(tokens, torch.int32, "tokens"), B, L, k, C.byref(h),
+                                beams.data_ptr(), head_lp.data_ptr())
+        _check(rc, self.handle)
+        return Prefix(self, h, B), beams, head_lp
+
+    def cdsl_rollout(self, prefix: Prefix, beams: torch.Tensor, k: int, d: int,
+                     lookaheads: Optional[torch.Tensor] = None) -> torch.Tensor:
+        if lookaheads is None:
+            lookaheads = torch.empty((prefix.B, k, d + 1), dtype=torch.int32, device=beams.device)
+        rc = lib().cdsl_rollout(self.handle, prefix.handle, _ptr(beams, torch.int32, "beams"), k, d,
+                                _ptr(lookaheads, torch.int32, "lookaheads"))
+        _check(rc, self.handle)
+        return lookaheads
+
+    def cdsl_verify(self, prefix: Prefix, lookaheads: torch.Tensor, k: int, d: int, head_lp: torch.Tensor,
+                    want_hidden: bool = False, out: Optional[dict] = None) -> dict:
+        B = prefix.B
+        dev = lookaheads.device
+        if out is None:
+            out = {
+                "logprobs": torch.empty((B, k, d), dtype=torch.float32, device=dev),
+                "target_argmax": torch.empty((B, k, d), dtype=torch.int32, device=dev),
+                "n_accept": torch.empty((B, k), dtype=torch.int32, device=dev),
+                "scores": torch.empty((B, k), dtype=torch.float32, device=dev),
+                "row_topk_ids": torch.empty((B, k, d, k), dtype=torch.int32, device=dev),
+                "row_topk_lp": torch.empty((B, k, d, k), dtype=torch.float32, device=dev),
+                "hidden": (torch.empty((B, k, self.target_shape.d_model), dtype=torch.float32, device=dev)
+                           if want_hidden else None),
+            }
+        rc = lib().cdsl_verify(self.handle, prefix.handle, _ptr(lookaheads, torch.int32, "lookaheads"), k, d,
+                               _ptr(head_lp, torch.float32, "head_lp"), out["logprobs"].data_ptr(),
+                               out["target_argmax"].data_ptr(), out["n_accept"].data_ptr(),
+                               out["scores"].data_ptr(), out["row_topk_ids"].data_ptr(),
+                               out["row_topk_lp"].data_ptr(),
+                               out["hidden"].data_ptr() if out.get("hidden") is not None else None)
+        _check(rc, self.handle)
+        return out
+
+    def cdsl_reward_keywords(self, prefix: Prefix, lookaheads, k, d, keywords, normalize: bool,
+                             reward: Optional[torch.Tensor] = None):
+        if reward is None:
+            reward = torch.empty((prefix.B, k), dtype=torch.float32, device=lookaheads.device)
+        rc = lib().cdsl_reward_keywords(self.handle, prefix.handle, _ptr(lookaheads, torch.int32, "lookaheads"),
+                                        k, d, _ptr(keywords, torch.int32, "keywords"), keywords.shape[1],
+                                        1 if normalize else 0, reward.data_ptr())
+        _check(rc, self.handle)
+        return reward
+
+    def cdsl_reward_linear(self, hidden: torch.Tensor, w: torch.Tensor, reward: Optional[torch.Tensor] = None):
+        B, k, D = hidden.shape
+        if reward is None:
+            reward = torch.empty((B, k), dtype=torch.float32, device=hidden.device)
+        rc = lib().cdsl_reward_linear(self.handle, _ptr(hidden, torch.float32, "hidden"),
+                                      _ptr(w, torch.float32, "w"), B, k, D, reward.data_ptr())
+        _check(rc, self.handle)
+        return reward
+
+    def cdsl_select(self, scores: torch.Tensor, reward: torch.Tensor, alpha: float,
+                    beam: Optional[torch.Tensor] = None) -> torch.Tensor:
+        B, k = scores.shape
+        if beam is None:
+            beam = torch.empty(B, dtype=torch.int32, device=scores.device)
+        rc = lib().cdsl_select(self.handle, _ptr(scores, torch.float32, "scores"),
+                               _ptr(reward, torch.float32, "reward"), float(alpha), B, k, beam.data_ptr())
+        _check(rc, self.handle)
+        return beam
+
+    def cdsl_commit(self, prefix: Prefix, lookaheads, beam, n_accept, row_topk_ids, row_topk_lp, k, d,
+                    next_beams: Optional[torch.Tensor] = None, next_head_lp: Optional[torch.Tensor] = None):
+        B = prefix.B
+        dev = lookaheads.device
+        if next_beams is None:
+            next_beams = torch.empty((B, k), dtype=torch.int32, device=dev)
+        if next_head_lp is None:
+            next_head_lp = torch.empty((B, k), dtype=torch.float32, device=dev)
+        emitted = (C.c_int32 * (B * (d + 1)))()
+        n_emit = (C.c_int32 * B)()
+        rc = lib().cdsl_commit(self.handle, prefix.handle, _ptr(lookaheads, torch.int32, "lookaheads"),
+                               _ptr(beam, torch.int32, "beam"), _ptr(n_accept, torch.int32, "n_accept"),
+                               _ptr(row_topk_ids, torch.int32, "row_topk_ids"),
+                               _ptr(row_topk_lp, torch.float32, "row_topk_lp"), k, d, emitted, n_emit,
+                               next_beams.data_ptr(), next_head_lp.data_ptr())
+        _check(rc, self.handle)
+        em = [[emitted[b * (d + 1) + t] for t in range(n_emit[b])] for b in range(B)]
+        return em, next_beams, next_head_lp
+
+
+# ---------------------------------------------------------------------------
+# weight upload (marshalling of the seeded host arrays)
+# ---------------------------------------------------------------------------
+def upload_weights(w: Dict[str, object], dtype: str, device="cuda") -> Dict[str, object]:
+    """Host float32 arrays (bf16-representable for bf16) -> device tensors."""
+    import numpy as np
+    from cdsl_inputs import f32_to_bf16_bits
+
+    def mat(a):
+        if dtype == "bf16":
+            bits = torch.from_numpy(f32_to_bf16_bits(a).view(np.int16))
+            return bits.to(device).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device)
+
+    def vec(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device)
+
+    out = {"tok_emb": mat(w["tok_emb"]), "lm_head": mat(w["lm_head"]), "final_norm": vec(w["final_norm"]),
+           "layers": []}
+    for lw in w["layers"]:
+        out["layers"].append({nm: (vec(v) if nm.endswith("norm") else mat(v)) for nm, v in lw.items()})
+    return out

@@ -1,0 +1,32 @@
+// Internal interface of the attention kernels (attention.hip).
+#pragma once
+#include "common.h"
+
+namespace cdsl {
+
+struct AttnArgs {
+  PassDesc p;
+  const void* Q;          // [M][H][hd] (model dtype), rotary already applied
+  void* O;                // [M][H][hd] (model dtype)
+  KVPool pool;
+  int layer;
+  int H, Hkv, G;
+  long long rows_total;   // M * H
+  float scale_log2;       // log2(e) / sqrt(hd)
+  float* part_o;          // [nsplit][M*H][hd]
+  float* part_ml;         // [nsplit][M*H][2]  (running max in log2 units, sum)
+  int nsplit, blocks_per_split;
+};
+
+struct AttnPlan {
+  int row_tiles, row_groups, threads;
+  int nsplit, blocks_per_split;
+};
+
+// max_prefix_len: the longest prefix of the prompts in the pass (host copy).
+AttnPlan attn_plan(const PassDesc& p, int H, int Hkv, int hd, int dtype, int max_prefix_len, int max_splits);
+hipError_t attn_launch(const AttnArgs& a, const AttnPlan& pl, int hd, int dtype, hipStream_t st);
+// the merge of split partials (a no-op when pl.nsplit == 1)
+hipError_t attn_combine_launch(const AttnArgs& a, const AttnPlan& pl, int hd, hipStream_t st);
+
+}  // namespace cdsl

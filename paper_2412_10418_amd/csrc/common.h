@@ -1,0 +1,96 @@
+// Shared device/host definitions of the CDSL library (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cdsl {
+
+typedef __bf16 bf16;
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+
+constexpr int kBlock = 16;        // tokens per KV block (= one MFMA key tile)
+constexpr int kMaxK = 16;         // beams
+constexpr int kMaxD = 32;         // lookahead depth
+constexpr int kWave = 64;
+
+// --------------------------------------------------------------------------
+// One forward pass of a decoder over a set of rows.
+//
+// Rows are grouped by prompt: row m = (bi * kp + i) * R + j for prompt slot
+// bi < nb (batch index b = prompt_ids ? prompt_ids[bi] : bi), beam i < kp and
+// row j < R of that beam.
+//   mode kAppend: the rows extend the prefix (prompt prefill, catch-up).
+//                 Row j sits at position Lp[b] + j, writes its K/V into the
+//                 prefix blocks and attends causally to prefix [0, pos].
+//   mode kSuffix: the rows are beam continuations (rollout, verification).
+//                 Row (i, j) sits at position Lp[b] + j0 + j, writes its K/V
+//                 into slot j0 + j of beam i's suffix blocks and attends to
+//                 the prefix [0, Lp[b]) plus its beam's slots [0, j0 + j].
+// --------------------------------------------------------------------------
+enum PassMode { kAppend = 0, kSuffix = 1 };
+
+struct PassDesc {
+  int mode;
+  int nb, kp, R, j0;
+  const int* prompt_ids;   // [nb] or null (identity)
+  const int* Lp;           // [B] prefix length before this pass
+  const int* ptable;       // [B][ptable_stride] prefix block ids
+  int ptable_stride;
+  const int* stable;       // [Bmax][kmax][sblocks] suffix block ids
+  int s_stride_b, s_stride_i, sblocks;
+  // token of row m: tok[(b * kp + i) * tok_stride + tok_off + j]
+  const int* tok;
+  int tok_stride, tok_off;
+  int M() const { return nb * kp * R; }
+};
+
+__host__ __device__ inline int pass_batch(const PassDesc& p, int bi) {
+  return p.prompt_ids ? p.prompt_ids[bi] : bi;
+}
+
+// KV pool of one model: per layer, per block, per KV head:
+//   K: [16 tokens][hd]            (key-major, hd contiguous)
+//   V: [hd][16 tokens]            (transposed: token contiguous)
+// so that both MFMA operands of attention read 8/16-byte runs.
+struct KVPool {
+  void* k;                 // base of layer 0
+  void* v;
+  long long layer_elems;   // elements per layer = nblocks * Hkv * 16 * hd
+  int Hkv, hd;
+};
+
+template <typename T>
+__device__ __forceinline__ float to_f32(T x);
+template <>
+__device__ __forceinline__ float to_f32<float>(float x) { return x; }
+template <>
+__device__ __forceinline__ float to_f32<bf16>(bf16 x) { return (float)x; }
+
+template <typename T>
+__device__ __forceinline__ T from_f32(float x);
+template <>
+__device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <>
+__device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// (value, id) ordering used by every argmax / top-k: larger value first,
+// then smaller id.
+__device__ __forceinline__ bool vi_better(float a, int ia, float b, int ib) {
+  return a > b || (a == b && ia < ib);
+}
+
+}  // namespace cdsl

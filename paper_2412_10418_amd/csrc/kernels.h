@@ -1,0 +1,65 @@
+// Internal interface of the row-wise kernels (kernels.hip).
+#pragma once
+#include "common.h"
+
+namespace cdsl {
+
+// Index of row m of a pass into a [B][kp][stride] token array:
+// (b * kp + i) * stride + off + j.  Disabled: index = m.
+struct RowMap {
+  int enabled;
+  PassDesc p;
+  int stride, off;
+};
+
+struct LogitArgs {
+  const float* logits;     // [M][V]
+  int V;
+  int want_lse;            // 0: argmax only
+  int kk;                  // top-k per row (0..16)
+  int* amax;               // argmax destination (RowMap or [M])
+  RowMap amax_map;
+  float* lp;               // [M] gathered log-prob, or null
+  const int* gather_tok;   // token array read through gather_map
+  RowMap gather_map;
+  int* topk_ids;           // [rows][kk]
+  float* topk_lp;
+  const int* topk_rows;    // destination row of row m (null: m)
+};
+
+__host__ __device__ inline long long rowmap_index(const RowMap& r, int m) {
+  if (!r.enabled) return m;
+  const int j = m % r.p.R;
+  const int t = m / r.p.R;
+  const int i = t % r.p.kp;
+  const int bi = t / r.p.kp;
+  const int b = r.p.prompt_ids ? r.p.prompt_ids[bi] : bi;
+  return (long long)(b * r.p.kp + i) * r.stride + r.off + j;
+}
+
+hipError_t embed_launch(const PassDesc& p, const void* emb, float* h, int D, int V, int dtype, hipStream_t st);
+hipError_t rmsnorm_launch(const float* x, const float* g, void* out, int rows, int D, float eps, int last_only, int R,
+                          float* hid, int dtype, hipStream_t st);
+hipError_t rope_kv_launch(const PassDesc& p, const float* qkv, void* qout, const KVPool& pool, int layer,
+                          const float* cos_t, const float* sin_t, int H, int Hkv, int hd, int dtype, hipStream_t st);
+hipError_t logit_rows_launch(const LogitArgs& a, int M, hipStream_t st);
+hipError_t beam_scores_launch(int BK, int d, const int* look, const int* y, const float* lp, const float* head_lp,
+                              int* n_accept, float* scores, hipStream_t st);
+hipError_t select_launch(int B, int k, const float* scores, const float* reward, float alpha, int reward_only,
+                         int* beam, hipStream_t st);
+hipError_t reward_keywords_launch(int B, int k, int d, const int* gen, int gen_stride, const int* gen_len,
+                                  const int* look, const int* kws, int n_kw, int normalize, float* reward,
+                                  hipStream_t st);
+hipError_t reward_linear_launch(int BK, const float* hidden, const float* w, int D, float* reward, hipStream_t st);
+hipError_t commit_launch(int B, int k, int d, const int* look, const int* beam, const int* n_accept,
+                         const int* rtk_ids, const float* rtk_lp, int* next_beams, float* next_head_lp, int* stage,
+                         int stage_stride, int* gen, int gen_stride, int* gen_len, int* catch_tok, hipStream_t st);
+hipError_t promote_launch(int B, int k, const KVPool& pool, int n_layers, const int* stage, int stage_stride, int dlim,
+                          const int* Lp, const int* ptable, int ptable_stride, const int* stable, int s_stride_b,
+                          int s_stride_i, int dtype, hipStream_t st);
+hipError_t advance_launch(int B, const int* stage, int stage_stride, int dlim, int* Lp, hipStream_t st);
+hipError_t add_launch(int n, const int* ids, int* v, int delta, hipStream_t st);
+hipError_t fill_int_launch(int* p, int v, long long n, hipStream_t st);
+hipError_t heads_to_lookaheads_launch(int BK, int d, const int* beams, int* look, hipStream_t st);
+
+}  // namespace cdsl

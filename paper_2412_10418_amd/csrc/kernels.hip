@@ -1,0 +1,579 @@
+// Row-wise kernels of the CDSL step: embedding gather, RMSNorm, rotary
+// embedding + KV write, the fused log-softmax / gather / argmax / top-k of a
+// logits row, hard rejection and beam scores, rewards, beam selection, and
+// the commit (emit, next beams, prefix promotion).
+#include <float.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace cdsl {
+
+namespace {
+
+__device__ __forceinline__ void row_decode(const PassDesc& p, int m, int& bi, int& b, int& i, int& j) {
+  j = m % p.R;
+  int t = m / p.R;
+  i = t % p.kp;
+  bi = t / p.kp;
+  b = pass_batch(p, bi);
+}
+
+template <int NW>
+__device__ __forceinline__ float block_sum(float v, float* sh) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  __syncthreads();
+  if (lane == 0) sh[w] = v;
+  __syncthreads();
+  float t = 0.f;
+#pragma unroll
+  for (int u = 0; u < NW; ++u) t += sh[u];
+  return t;
+}
+
+// ---------------------------------------------------------------------------
+// Token ids outside [0, V) are clamped: a bad id gives a wrong row, never
+// an out-of-bounds read.
+template <typename T>
+__global__ __launch_bounds__(256) void embed_rows(PassDesc p, const T* __restrict__ emb, float* __restrict__ h,
+                                                  int D, int V) {
+  const int m = blockIdx.x;
+  int bi, b, i, j;
+  row_decode(p, m, bi, b, i, j);
+  const int tok = min(max(p.tok[(long long)(b * p.kp + i) * p.tok_stride + p.tok_off + j], 0), V - 1);
+  const T* e = emb + (long long)tok * D;
+  float* o = h + (long long)m * D;
+  for (int c = threadIdx.x; c < D; c += 256) o[c] = to_f32<T>(e[c]);
+}
+
+// out[r] = x[src(r)] / sqrt(mean(x^2) + eps) * g.  src(r) = r, or the last
+// row of beam r when last_only (prompt prefill: only the last position needs
+// logits).  hid (fp32) additionally receives the normed row of every beam's
+// last row (the reward reads it).
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_rows(const float* __restrict__ x, const float* __restrict__ g,
+                                                    T* __restrict__ out, int D, float eps, int last_only, int R,
+                                                    float* __restrict__ hid) {
+  __shared__ float sh[4];
+  const int r = blockIdx.x;
+  const int src = last_only ? r * R + (R - 1) : r;
+  const float* xr = x + (long long)src * D;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < D; c += 256) ss = fmaf(xr[c], xr[c], ss);
+  ss = block_sum<4>(ss, sh);
+  const float inv = rsqrtf(ss / (float)D + eps);
+  T* o = out + (long long)r * D;
+  const bool want_hid = hid && (last_only || (r % R) == R - 1);
+  float* hr = want_hid ? hid + (long long)(last_only ? r : r / R) * D : nullptr;
+  for (int c = threadIdx.x; c < D; c += 256) {
+    float v = xr[c] * inv * g[c];
+    o[c] = from_f32<T>(v);
+    if (hr) hr[c] = v;
+  }
+}
+
+// Rotary embedding of q and k (rotate-half pairs (d, d + hd/2), angle
+// pos * theta^(-2d/hd) from the host-built tables), then q -> Q buffer and
+// k, v -> the row's KV slot: prefix block for kAppend, the beam's suffix
+// block for kSuffix.
+template <typename T>
+__global__ __launch_bounds__(256) void rope_kv_write(PassDesc p, const float* __restrict__ qkv, T* __restrict__ qout,
+                                                     KVPool pool, int layer, const float* __restrict__ cos_t,
+                                                     const float* __restrict__ sin_t, int H, int Hkv, int hd) {
+  const int m = blockIdx.x;
+  int bi, b, i, j;
+  row_decode(p, m, bi, b, i, j);
+  const int Lp = p.Lp[b];
+  int pos, blk, slot;
+  if (p.mode == kSuffix) {
+    const int s = p.j0 + j;
+    pos = Lp + s;
+    blk = p.stable[(long long)b * p.s_stride_b + i * p.s_stride_i + s / kBlock];
+    slot = s % kBlock;
+  } else {
+    pos = Lp + j;
+    blk = p.ptable[(long long)b * p.ptable_stride + pos / kBlock];
+    slot = pos % kBlock;
+  }
+  const int half = hd / 2;
+  const float* row = qkv + (long long)m * (H + 2 * Hkv) * hd;
+  const float* ct = cos_t + (long long)pos * half;
+  const float* stt = sin_t + (long long)pos * half;
+  T* kb = (T*)pool.k + (long long)layer * pool.layer_elems + ((long long)blk * Hkv) * kBlock * hd;
+  T* vb = (T*)pool.v + (long long)layer * pool.layer_elems + ((long long)blk * Hkv) * kBlock * hd;
+  // q and k heads: pairs
+  const int npairs = (H + Hkv) * half;
+  for (int u = threadIdx.x; u < npairs; u += 256) {
+    const int hh = u / half, d = u % half;
+    const float x1 = row[hh * hd + d], x2 = row[hh * hd + d + half];
+    const float c = ct[d], s = stt[d];
+    const float y1 = x1 * c - x2 * s, y2 = x2 * c + x1 * s;
+    if (hh < H) {
+      T* q = qout + ((long long)m * H + hh) * hd;
+      q[d] = from_f32<T>(y1);
+      q[d + half] = from_f32<T>(y2);
+    } else {
+      T* kr = kb + ((long long)(hh - H) * kBlock + slot) * hd;
+      kr[d] = from_f32<T>(y1);
+      kr[d + half] = from_f32<T>(y2);
+    }
+  }
+  // v: transposed [hd][16] per block and head
+  const float* vrow = row + (long long)(H + Hkv) * hd;
+  for (int u = threadIdx.x; u < Hkv * hd; u += 256) {
+    const int hh = u / hd, d = u % hd;
+    vb[((long long)hh * hd + d) * kBlock + slot] = from_f32<T>(vrow[u]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Logits row statistics, one workgroup per row, one read of the row:
+// online logsumexp, argmax, thread-local top-KK lists merged by KK rounds of
+// block argmax.  Ordering: value descending, then id ascending.
+template <int KKMAX>
+__global__ __launch_bounds__(256) void logit_rows_kernel(LogitArgs a) {
+  __shared__ float shv[4];
+  __shared__ int shi[4];
+  __shared__ float shs[4];
+  const int m = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const float* z = a.logits + (long long)m * a.V;
+
+  float mloc = -INFINITY, sloc = 0.f;
+  float bv = -INFINITY;
+  int bid = 0x7fffffff;
+  float lv[KKMAX > 0 ? KKMAX : 1];
+  int li[KKMAX > 0 ? KKMAX : 1];
+#pragma unroll
+  for (int s = 0; s < (KKMAX > 0 ? KKMAX : 1); ++s) {
+    lv[s] = -INFINITY;
+    li[s] = 0x7fffffff;
+  }
+  auto visit = [&](float v, int id) {
+    if (a.want_lse) {
+      if (v > mloc) {
+        sloc = sloc * __expf(mloc - v) + 1.f;
+        mloc = v;
+      } else {
+        sloc += __expf(v - mloc);
+      }
+    }
+    if (vi_better(v, id, bv, bid)) {
+      bv = v;
+      bid = id;
+    }
+    // keep the best KKMAX (>= kk) so every list index is static
+    if (KKMAX > 0 && vi_better(v, id, lv[(KKMAX > 0 ? KKMAX : 1) - 1], li[(KKMAX > 0 ? KKMAX : 1) - 1])) {
+      float cv = v;
+      int ci = id;
+#pragma unroll
+      for (int s = 0; s < KKMAX; ++s) {
+        if (vi_better(cv, ci, lv[s], li[s])) {
+          float tv = lv[s];
+          int ti = li[s];
+          lv[s] = cv;
+          li[s] = ci;
+          cv = tv;
+          ci = ti;
+        }
+      }
+    }
+  };
+  const int V4 = (a.V & 3) == 0 ? a.V / 4 : 0;
+  const float4* z4 = (const float4*)z;
+  for (int c = tid; c < V4; c += 256) {
+    float4 v = z4[c];
+    visit(v.x, 4 * c);
+    visit(v.y, 4 * c + 1);
+    visit(v.z, 4 * c + 2);
+    visit(v.w, 4 * c + 3);
+  }
+  for (int c = 4 * V4 + tid; c < a.V; c += 256) visit(z[c], c);
+
+  // argmax
+  {
+    float v = bv;
+    int id = bid;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      float ov = __shfl_xor(v, o, 64);
+      int oi = __shfl_xor(id, o, 64);
+      if (vi_better(ov, oi, v, id)) {
+        v = ov;
+        id = oi;
+      }
+    }
+    if (lane == 0) {
+      shv[w] = v;
+      shi[w] = id;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      float fv = shv[0];
+      int fi = shi[0];
+      for (int u = 1; u < 4; ++u)
+        if (vi_better(shv[u], shi[u], fv, fi)) {
+          fv = shv[u];
+          fi = shi[u];
+        }
+      shi[0] = fi;
+      shv[0] = fv;
+    }
+    __syncthreads();
+    if (tid == 0 && a.amax) a.amax[rowmap_index(a.amax_map, m)] = shi[0];
+    __syncthreads();
+  }
+  if (!a.want_lse) return;
+  // logsumexp
+  float lse;
+  {
+    float mm = wave_max(mloc);
+    if (lane == 0) shv[w] = mm;
+    __syncthreads();
+    const float M = fmaxf(fmaxf(shv[0], shv[1]), fmaxf(shv[2], shv[3]));
+    float sv = mloc == -INFINITY ? 0.f : sloc * __expf(mloc - M);
+    sv = wave_sum(sv);
+    if (lane == 0) shs[w] = sv;
+    __syncthreads();
+    lse = M + __logf(shs[0] + shs[1] + shs[2] + shs[3]);
+    __syncthreads();
+  }
+  if (a.lp && tid == 0) {
+    const int tok = min(max(a.gather_tok[rowmap_index(a.gather_map, m)], 0), a.V - 1);
+    a.lp[m] = z[tok] - lse;
+  }
+  if (KKMAX == 0 || a.kk == 0) return;
+  const int dst = a.topk_rows ? a.topk_rows[m] : m;
+  for (int r = 0; r < a.kk; ++r) {
+    float v = lv[0];
+    int id = li[0];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      float ov = __shfl_xor(v, o, 64);
+      int oi = __shfl_xor(id, o, 64);
+      if (vi_better(ov, oi, v, id)) {
+        v = ov;
+        id = oi;
+      }
+    }
+    if (lane == 0) {
+      shv[w] = v;
+      shi[w] = id;
+    }
+    __syncthreads();
+    float fv = shv[0];
+    int fi = shi[0];
+    for (int u = 1; u < 4; ++u)
+      if (vi_better(shv[u], shi[u], fv, fi)) {
+        fv = shv[u];
+        fi = shi[u];
+      }
+    if (tid == 0) {
+      a.topk_ids[(long long)dst * a.kk + r] = fi;
+      a.topk_lp[(long long)dst * a.kk + r] = fv - lse;
+    }
+    if (li[0] == fi) {   // ids are unique: exactly one thread pops
+#pragma unroll
+      for (int s = 0; s + 1 < (KKMAX > 0 ? KKMAX : 1); ++s) {
+        lv[s] = lv[s + 1];
+        li[s] = li[s + 1];
+      }
+      lv[(KKMAX > 0 ? KKMAX : 1) - 1] = -INFINITY;
+      li[(KKMAX > 0 ? KKMAX : 1) - 1] = 0x7fffffff;
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Hard rejection (leading matches of target argmax and lookahead) and beam
+// scores, one thread per (b, i).
+__global__ void beam_scores_kernel(int BK, int d, const int* __restrict__ look, const int* __restrict__ y,
+                                   const float* __restrict__ lp, const float* __restrict__ head_lp,
+                                   int* __restrict__ n_accept, float* __restrict__ scores) {
+  const int bk = blockIdx.x * blockDim.x + threadIdx.x;
+  if (bk >= BK) return;
+  int n = 0;
+  bool run = true;
+  float s = head_lp[bk];
+  for (int j = 0; j < d; ++j) {
+    const int x = look[(long long)bk * (d + 1) + j + 1];
+    if (run && y[(long long)bk * d + j] == x) ++n;
+    else run = false;
+    s += lp[(long long)bk * d + j];
+  }
+  n_accept[bk] = n;
+  scores[bk] = s;
+}
+
+__global__ void select_kernel(int B, int k, const float* __restrict__ scores, const float* __restrict__ reward,
+                              float alpha, int reward_only, int* __restrict__ beam) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  int best = -1;
+  float bv = -INFINITY;
+  bool bad = false;
+  for (int i = 0; i < k; ++i) {
+    const float sc = scores[b * k + i], r = reward[b * k + i];
+    if (isnan(sc) || isnan(r)) bad = true;
+    const float v = reward_only ? r : sc + alpha * r;
+    if (best < 0 || v > bv) {
+      best = i;
+      bv = v;
+    }
+  }
+  beam[b] = bad ? -1 : best;
+}
+
+// Keyword reward, one workgroup per (b, i): distinct keywords present in
+// generated-so-far + lookahead row.
+__global__ __launch_bounds__(256) void reward_keywords_kernel(int k, int d, const int* __restrict__ gen,
+                                                              int gen_stride, const int* __restrict__ gen_len,
+                                                              const int* __restrict__ look,
+                                                              const int* __restrict__ kws, int n_kw, int normalize,
+                                                              float* __restrict__ reward) {
+  __shared__ int hit[64];
+  __shared__ int uniq[64];
+  const int bk = blockIdx.x;
+  const int b = bk / k;
+  for (int u = threadIdx.x; u < 64; u += 256) hit[u] = 0;
+  __syncthreads();
+  const int* kw = kws + (long long)b * n_kw;
+  const int gl = gen_len[b];
+  const int total = gl + d + 1;
+  for (int t = threadIdx.x; t < total; t += 256) {
+    const int tok = t < gl ? gen[(long long)b * gen_stride + t] : look[(long long)bk * (d + 1) + (t - gl)];
+    for (int u = 0; u < n_kw; ++u)
+      if (kw[u] == tok) atomicOr(&hit[u], 1);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int cnt = 0, nd = 0;
+    for (int u = 0; u < n_kw; ++u) {
+      bool dup = false;
+      for (int v = 0; v < u; ++v) dup |= kw[v] == kw[u];
+      if (dup) continue;
+      ++nd;
+      cnt += hit[u];
+    }
+    reward[bk] = normalize ? (float)cnt / (float)(nd > 0 ? nd : 1) : (float)cnt;
+  }
+}
+
+__global__ __launch_bounds__(256) void reward_linear_kernel(const float* __restrict__ hidden,
+                                                            const float* __restrict__ w, int D,
+                                                            float* __restrict__ reward) {
+  __shared__ float sh[4];
+  const int bk = blockIdx.x;
+  const float* h = hidden + (long long)bk * D;
+  float s = 0.f;
+  for (int c = threadIdx.x; c < D; c += 256) s = fmaf(h[c], w[c], s);
+  s = block_sum<4>(s, sh);
+  if (threadIdx.x == 0) reward[bk] = s;
+}
+
+// Commit, one thread per prompt.  stage[b] = {n_emit, catch_up, tokens...}.
+__global__ void commit_kernel(int B, int k, int d, const int* __restrict__ look, const int* __restrict__ beam,
+                              const int* __restrict__ n_accept, const int* __restrict__ rtk_ids,
+                              const float* __restrict__ rtk_lp, int* __restrict__ next_beams,
+                              float* __restrict__ next_head_lp, int* __restrict__ stage, int stage_stride,
+                              int* __restrict__ gen, int gen_stride, int* __restrict__ gen_len,
+                              int* __restrict__ catch_tok) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  int* st = stage + (long long)b * stage_stride;
+  const int i = beam[b];
+  if (i < 0 || i >= k) {
+    st[0] = -1;
+    return;
+  }
+  const int bk = b * k + i;
+  const int n = n_accept[bk];
+  const int* row = look + (long long)bk * (d + 1);
+  st[0] = n + 1;
+  st[1] = n == d;
+  st[2] = i;
+  const int gl = gen_len[b];
+  for (int t = 0; t <= n; ++t) {
+    st[3 + t] = row[t];
+    gen[(long long)b * gen_stride + gl + t] = row[t];
+  }
+  gen_len[b] = gl + n + 1;
+  if (n < d) {
+    const long long r = ((long long)bk * d + n) * k;
+    for (int u = 0; u < k; ++u) {
+      next_beams[b * k + u] = rtk_ids[r + u];
+      next_head_lp[b * k + u] = rtk_lp[r + u];
+    }
+  } else {
+    catch_tok[b] = row[d];
+  }
+}
+
+// Copy the selected beam's first cnt suffix slots into the prefix at
+// positions Lp[b] .. Lp[b] + cnt - 1, for every layer and KV head.
+template <typename T>
+__global__ __launch_bounds__(256) void promote_kernel(int k, KVPool pool, int n_layers, const int* __restrict__ stage,
+                                                      int stage_stride, int dlim, const int* __restrict__ Lp,
+                                                      const int* __restrict__ ptable, int ptable_stride,
+                                                      const int* __restrict__ stable, int s_stride_b,
+                                                      int s_stride_i) {
+  const int b = blockIdx.x;
+  const int layer = blockIdx.y;
+  const int* st = stage + (long long)b * stage_stride;
+  const int ne = st[0];
+  if (ne <= 0) return;
+  const int cnt = min(ne, dlim);
+  const int i = st[2];
+  const int L0 = Lp[b];
+  const int hd = pool.hd, Hkv = pool.Hkv;
+  T* kl = (T*)pool.k + (long long)layer * pool.layer_elems;
+  T* vl = (T*)pool.v + (long long)layer * pool.layer_elems;
+  const int per_tok = Hkv * hd;
+  for (int u = threadIdx.x; u < cnt * per_tok; u += 256) {
+    const int t = u / per_tok, rem = u % per_tok;
+    const int hh = rem / hd, dd = rem % hd;
+    const int sblk = stable[(long long)b * s_stride_b + i * s_stride_i + t / kBlock];
+    const int sslot = t % kBlock;
+    const int pos = L0 + t;
+    const int pblk = ptable[(long long)b * ptable_stride + pos / kBlock];
+    const int pslot = pos % kBlock;
+    kl[(((long long)pblk * Hkv + hh) * kBlock + pslot) * hd + dd] =
+        kl[(((long long)sblk * Hkv + hh) * kBlock + sslot) * hd + dd];
+    vl[(((long long)pblk * Hkv + hh) * hd + dd) * kBlock + pslot] =
+        vl[(((long long)sblk * Hkv + hh) * hd + dd) * kBlock + sslot];
+  }
+}
+
+__global__ void advance_kernel(int B, const int* __restrict__ stage, int stage_stride, int dlim,
+                               int* __restrict__ Lp) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const int ne = stage[(long long)b * stage_stride];
+  if (ne > 0) Lp[b] += min(ne, dlim);
+}
+
+__global__ void add_kernel(int n, const int* __restrict__ ids, int* __restrict__ v, int delta) {
+  const int u = blockIdx.x * blockDim.x + threadIdx.x;
+  if (u < n) v[ids ? ids[u] : u] += delta;
+}
+
+__global__ void fill_int_kernel(int* __restrict__ p, int v, long long n) {
+  long long u = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (u < n) p[u] = v;
+}
+
+__global__ void heads_to_lookaheads(int BK, int d, const int* __restrict__ beams, int* __restrict__ look) {
+  const int u = blockIdx.x * blockDim.x + threadIdx.x;
+  if (u < BK) look[(long long)u * (d + 1)] = beams[u];
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+hipError_t embed_launch(const PassDesc& p, const void* emb, float* h, int D, int V, int dtype, hipStream_t st) {
+  const int M = p.M();
+  if (M == 0) return hipSuccess;
+  if (dtype == 1) embed_rows<bf16><<<M, 256, 0, st>>>(p, (const bf16*)emb, h, D, V);
+  else embed_rows<float><<<M, 256, 0, st>>>(p, (const float*)emb, h, D, V);
+  return hipGetLastError();
+}
+
+hipError_t rmsnorm_launch(const float* x, const float* g, void* out, int rows, int D, float eps, int last_only, int R,
+                          float* hid, int dtype, hipStream_t st) {
+  if (rows == 0) return hipSuccess;
+  (void)dtype;   // activations are fp32 for every weight dtype
+  rmsnorm_rows<float><<<rows, 256, 0, st>>>(x, g, (float*)out, D, eps, last_only, R, hid);
+  return hipGetLastError();
+}
+
+hipError_t rope_kv_launch(const PassDesc& p, const float* qkv, void* qout, const KVPool& pool, int layer,
+                          const float* cos_t, const float* sin_t, int H, int Hkv, int hd, int dtype, hipStream_t st) {
+  const int M = p.M();
+  if (M == 0) return hipSuccess;
+  (void)dtype;   // q and the KV cache are fp32 for every weight dtype
+  rope_kv_write<float><<<M, 256, 0, st>>>(p, qkv, (float*)qout, pool, layer, cos_t, sin_t, H, Hkv, hd);
+  return hipGetLastError();
+}
+
+hipError_t logit_rows_launch(const LogitArgs& a, int M, hipStream_t st) {
+  if (M == 0) return hipSuccess;
+  if (a.kk > 16 || a.kk < 0) return hipErrorInvalidValue;
+  if (a.kk == 0) logit_rows_kernel<0><<<M, 256, 0, st>>>(a);
+  else if (a.kk <= 4) logit_rows_kernel<4><<<M, 256, 0, st>>>(a);
+  else if (a.kk <= 8) logit_rows_kernel<8><<<M, 256, 0, st>>>(a);
+  else logit_rows_kernel<16><<<M, 256, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t beam_scores_launch(int BK, int d, const int* look, const int* y, const float* lp, const float* head_lp,
+                              int* n_accept, float* scores, hipStream_t st) {
+  if (BK == 0) return hipSuccess;
+  beam_scores_kernel<<<(BK + 127) / 128, 128, 0, st>>>(BK, d, look, y, lp, head_lp, n_accept, scores);
+  return hipGetLastError();
+}
+
+hipError_t select_launch(int B, int k, const float* scores, const float* reward, float alpha, int reward_only,
+                         int* beam, hipStream_t st) {
+  if (B == 0) return hipSuccess;
+  select_kernel<<<(B + 127) / 128, 128, 0, st>>>(B, k, scores, reward, alpha, reward_only, beam);
+  return hipGetLastError();
+}
+
+hipError_t reward_keywords_launch(int B, int k, int d, const int* gen, int gen_stride, const int* gen_len,
+                                  const int* look, const int* kws, int n_kw, int normalize, float* reward,
+                                  hipStream_t st) {
+  if (B * k == 0) return hipSuccess;
+  reward_keywords_kernel<<<B * k, 256, 0, st>>>(k, d, gen, gen_stride, gen_len, look, kws, n_kw, normalize, reward);
+  return hipGetLastError();
+}
+
+hipError_t reward_linear_launch(int BK, const float* hidden, const float* w, int D, float* reward, hipStream_t st) {
+  if (BK == 0) return hipSuccess;
+  reward_linear_kernel<<<BK, 256, 0, st>>>(hidden, w, D, reward);
+  return hipGetLastError();
+}
+
+hipError_t commit_launch(int B, int k, int d, const int* look, const int* beam, const int* n_accept,
+                         const int* rtk_ids, const float* rtk_lp, int* next_beams, float* next_head_lp, int* stage,
+                         int stage_stride, int* gen, int gen_stride, int* gen_len, int* catch_tok, hipStream_t st) {
+  commit_kernel<<<(B + 63) / 64, 64, 0, st>>>(B, k, d, look, beam, n_accept, rtk_ids, rtk_lp, next_beams,
+                                              next_head_lp, stage, stage_stride, gen, gen_stride, gen_len, catch_tok);
+  return hipGetLastError();
+}
+
+hipError_t promote_launch(int B, int k, const KVPool& pool, int n_layers, const int* stage, int stage_stride, int dlim,
+                          const int* Lp, const int* ptable, int ptable_stride, const int* stable, int s_stride_b,
+                          int s_stride_i, int dtype, hipStream_t st) {
+  dim3 grid(B, n_layers);
+  (void)dtype;
+  promote_kernel<float><<<grid, 256, 0, st>>>(k, pool, n_layers, stage, stage_stride, dlim, Lp, ptable,
+                                              ptable_stride, stable, s_stride_b, s_stride_i);
+  return hipGetLastError();
+}
+
+hipError_t advance_launch(int B, const int* stage, int stage_stride, int dlim, int* Lp, hipStream_t st) {
+  advance_kernel<<<(B + 127) / 128, 128, 0, st>>>(B, stage, stage_stride, dlim, Lp);
+  return hipGetLastError();
+}
+
+hipError_t add_launch(int n, const int* ids, int* v, int delta, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  add_kernel<<<(n + 127) / 128, 128, 0, st>>>(n, ids, v, delta);
+  return hipGetLastError();
+}
+
+hipError_t fill_int_launch(int* p, int v, long long n, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  fill_int_kernel<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(p, v, n);
+  return hipGetLastError();
+}
+
+hipError_t heads_to_lookaheads_launch(int BK, int d, const int* beams, int* look, hipStream_t st) {
+  if (BK == 0) return hipSuccess;
+  heads_to_lookaheads<<<(BK + 127) / 128, 128, 0, st>>>(BK, d, beams, look);
+  return hipGetLastError();
+}
+
+}  // namespace cdsl

@@ -1,0 +1,1001 @@
+// Host runtime and C ABI of the CDSL library: weight packing, the paged KV
+// pool and its block allocator, the per-pass model runner, and the entry
+// points declared in include/cdsl.h and include/cdsl_ops.h.
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/cdsl.h"
+#include "../../include/cdsl_ops.h"
+#include "attention.h"
+#include "common.h"
+#include "gemm.h"
+#include "kernels.h"
+
+using namespace cdsl;
+
+namespace {
+
+constexpr int kMaxSplits = 16;
+
+struct Fail {
+  int code;
+};
+
+struct Model {
+  cdsl_model_config c{};
+  int hd = 0, G = 0, qkv_n = 0;
+  size_t esz = 0;
+  void* emb = nullptr;
+  void* lm = nullptr;
+  float* gf = nullptr;
+  std::vector<void*> wqkv, wo, wgu, wd;
+  std::vector<float*> g1, g2;
+  KVPool pool{};
+  float* cos_t = nullptr;
+  float* sin_t = nullptr;
+};
+
+struct Workspace {
+  int Mmax = 0, Mlog = 0;
+  float* h = nullptr;
+  void* u = nullptr;
+  float* qkv = nullptr;
+  void* q = nullptr;
+  void* o = nullptr;
+  void* act = nullptr;
+  float* gu32 = nullptr;
+  float* logits = nullptr;
+  float* part_o = nullptr;
+  float* part_ml = nullptr;
+  size_t part_rows = 0;     // capacity in (row, head) units for one split
+  void* gemm_ws = nullptr;
+  size_t gemm_ws_bytes = 0;
+};
+
+}  // namespace
+
+struct cdsl_prefix {
+  int B = 0;
+  std::vector<int> len;        // host copy of prefix lengths
+  std::vector<int> table;      // [B][pstride] prefix block ids
+  std::vector<int> owned;      // blocks to return on free
+  int* Lp = nullptr;           // device [B]
+  int* table_dev = nullptr;    // device [B][pstride]
+  int* gen = nullptr;          // device [B][gen_stride] emitted tokens
+  int* gen_len = nullptr;      // device [B]
+  int rolled_k = 0, rolled_d = 0;
+  int verified_k = 0, verified_d = 0;
+};
+
+struct cdsl_ctx {
+  hipStream_t st = nullptr;
+  cdsl_limits lim{};
+  Model m[2];                  // 0 draft, 1 target
+  int dtype = 0;
+  Workspace ws;
+  int nblocks = 0;
+  int pstride = 0;             // prefix blocks per prompt
+  int sblocks = 0;             // suffix blocks per beam
+  std::vector<int> free_blocks;
+  int* stable = nullptr;       // device [max_B][max_k][sblocks]
+  int* iota = nullptr;         // device [max_B] = 0..max_B-1
+  int* stage = nullptr;        // device [max_B][stage_stride]
+  int stage_stride = 0;
+  int* stage_host = nullptr;   // pinned
+  int* table_host = nullptr;   // pinned [max_B][pstride]
+  int* ids_host = nullptr;     // pinned [max_B]
+  int* ids_dev = nullptr;      // device [max_B]
+  int* catch_tok = nullptr;    // device [max_B]
+  int live_prefixes = 0;
+  std::vector<void*> allocs;
+  std::string err;
+  // per-kernel-class timing (cdsl_profile_*)
+  bool prof = false;
+  cdsl_kernel_stats acc{};
+  std::vector<hipEvent_t> ev_free;
+  struct Pending {
+    hipEvent_t a, b;
+    int cls;
+  };
+  std::vector<Pending> pend;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(cdsl_ctx* c, int code, const std::string& msg) {
+  if (c) c->err = msg;
+  g_err = msg;
+  return code;
+}
+
+#define CK(call)                                                                             \
+  do {                                                                                       \
+    hipError_t e_ = (call);                                                                  \
+    if (e_ != hipSuccess) {                                                                  \
+      throw_dev(#call, e_);                                                                  \
+    }                                                                                        \
+  } while (0)
+
+[[noreturn]] void throw_dev(const char* what, hipError_t e) {
+  g_err = std::string(what) + ": " + hipGetErrorString(e);
+  throw Fail{CDSL_EDEVICE};
+}
+
+template <typename T>
+T* dev_alloc(cdsl_ctx* c, size_t count) {
+  if (count == 0) count = 1;
+  void* p = nullptr;
+  hipError_t e = hipMalloc(&p, count * sizeof(T));
+  if (e != hipSuccess) {
+    g_err = "hipMalloc of " + std::to_string(count * sizeof(T)) + " bytes failed";
+    throw Fail{CDSL_ENOMEM};
+  }
+  c->allocs.push_back(p);
+  return (T*)p;
+}
+
+void* dev_alloc_bytes(cdsl_ctx* c, size_t bytes) { return dev_alloc<char>(c, bytes); }
+
+// ---------------------------------------------------------------------------
+// profiling: a pair of events around a launch, harvested after a sync
+// ---------------------------------------------------------------------------
+hipEvent_t take_event(cdsl_ctx* c) {
+  if (!c->ev_free.empty()) {
+    hipEvent_t e = c->ev_free.back();
+    c->ev_free.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) {
+    g_err = "hipEventCreate failed";
+    throw Fail{CDSL_EDEVICE};
+  }
+  return e;
+}
+
+void harvest(cdsl_ctx* c) {
+  for (auto& p : c->pend) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) c->acc.ms[p.cls] += ms;
+    c->ev_free.push_back(p.a);
+    c->ev_free.push_back(p.b);
+  }
+  c->pend.clear();
+}
+
+struct Span {
+  cdsl_ctx* c;
+  int cls;
+  hipEvent_t a = nullptr;
+  Span(cdsl_ctx* cc, int k, double flops, double bytes) : c(cc), cls(k) {
+    if (!c->prof) return;
+    a = take_event(c);
+    (void)hipEventRecord(a, c->st);
+    c->acc.launches[cls] += 1;
+    c->acc.flops[cls] += flops;
+    c->acc.bytes[cls] += bytes;
+  }
+  ~Span() {
+    if (!a) return;
+    hipEvent_t b = nullptr;
+    if (!c->ev_free.empty()) {
+      b = c->ev_free.back();
+      c->ev_free.pop_back();
+    } else if (hipEventCreate(&b) != hipSuccess) {
+      c->ev_free.push_back(a);
+      return;
+    }
+    (void)hipEventRecord(b, c->st);
+    c->pend.push_back({a, b, cls});
+  }
+};
+
+bool cfg_ok(const cdsl_model_config& c, std::string& why) {
+  if (c.n_layers <= 0 || c.d_model <= 0 || c.n_heads <= 0 || c.n_kv_heads <= 0 || c.ffn_dim <= 0 || c.vocab <= 0) {
+    why = "non-positive model dimension";
+    return false;
+  }
+  if (c.d_model % c.n_heads != 0 || c.n_heads % c.n_kv_heads != 0) {
+    why = "d_model % n_heads or n_heads % n_kv_heads != 0";
+    return false;
+  }
+  int hd = c.d_model / c.n_heads;
+  if (hd != 32 && hd != 64 && hd != 128) {
+    why = "head_dim must be 32, 64 or 128";
+    return false;
+  }
+  if (c.dtype != CDSL_F32 && c.dtype != CDSL_BF16) {
+    why = "dtype must be CDSL_F32 or CDSL_BF16";
+    return false;
+  }
+  if (c.ffn_dim % 16 != 0) {
+    why = "ffn_dim must be a multiple of 16";
+    return false;
+  }
+  int kmul = c.dtype == CDSL_BF16 ? 64 : 16;
+  if (c.d_model % kmul != 0 || c.ffn_dim % kmul != 0) {
+    why = "d_model and ffn_dim must be multiples of 64 (bf16) or 16 (fp32)";
+    return false;
+  }
+  if (c.dtype == CDSL_BF16 && c.ffn_dim % 32 != 0) {
+    why = "bf16 ffn_dim must be a multiple of 32";
+    return false;
+  }
+  if (!(c.rms_eps > 0.f) || !(c.rope_theta > 0.f)) {
+    why = "rms_eps and rope_theta must be positive";
+    return false;
+  }
+  return true;
+}
+
+void load_model(cdsl_ctx* c, Model& md, const cdsl_model& src, int max_pos) {
+  md.c = src.cfg;
+  const auto& k = md.c;
+  md.hd = k.d_model / k.n_heads;
+  md.G = k.n_heads / k.n_kv_heads;
+  md.qkv_n = (k.n_heads + 2 * k.n_kv_heads) * md.hd;
+  md.esz = k.dtype == CDSL_BF16 ? 2 : 4;
+  const size_t D = k.d_model, F = k.ffn_dim, V = k.vocab, hd = md.hd;
+  const size_t Hq = k.n_heads * hd, Hk = k.n_kv_heads * hd;
+  const size_t es = md.esz;
+  hipStream_t st = c->st;
+  if (!src.tok_emb || !src.lm_head || !src.final_norm || !src.layer_ptrs) {
+    g_err = "null weight pointer";
+    throw Fail{CDSL_EINVAL};
+  }
+  md.emb = dev_alloc_bytes(c, V * D * es);
+  CK(hipMemcpyAsync(md.emb, src.tok_emb, V * D * es, hipMemcpyDeviceToDevice, st));
+  md.lm = dev_alloc_bytes(c, V * D * es);
+  CK(hipMemcpyAsync(md.lm, src.lm_head, V * D * es, hipMemcpyDeviceToDevice, st));
+  md.gf = dev_alloc<float>(c, D);
+  CK(hipMemcpyAsync(md.gf, src.final_norm, D * 4, hipMemcpyDeviceToDevice, st));
+  for (int l = 0; l < k.n_layers; ++l) {
+    const void* const* lp = src.layer_ptrs + 9 * l;
+    for (int u = 0; u < 9; ++u)
+      if (!lp[u]) {
+        g_err = "null layer weight pointer";
+        throw Fail{CDSL_EINVAL};
+      }
+    float* g1 = dev_alloc<float>(c, D);
+    float* g2 = dev_alloc<float>(c, D);
+    CK(hipMemcpyAsync(g1, lp[0], D * 4, hipMemcpyDeviceToDevice, st));
+    CK(hipMemcpyAsync(g2, lp[5], D * 4, hipMemcpyDeviceToDevice, st));
+    md.g1.push_back(g1);
+    md.g2.push_back(g2);
+    char* qkv = (char*)dev_alloc_bytes(c, (Hq + 2 * Hk) * D * es);
+    CK(hipMemcpyAsync(qkv, lp[1], Hq * D * es, hipMemcpyDeviceToDevice, st));
+    CK(hipMemcpyAsync(qkv + Hq * D * es, lp[2], Hk * D * es, hipMemcpyDeviceToDevice, st));
+    CK(hipMemcpyAsync(qkv + (Hq + Hk) * D * es, lp[3], Hk * D * es, hipMemcpyDeviceToDevice, st));
+    md.wqkv.push_back(qkv);
+    void* wo = dev_alloc_bytes(c, D * Hq * es);
+    CK(hipMemcpyAsync(wo, lp[4], D * Hq * es, hipMemcpyDeviceToDevice, st));
+    md.wo.push_back(wo);
+    // gate/up interleaved in groups of 16 rows: [g0..g15, u0..u15, g16..]
+    char* gu = (char*)dev_alloc_bytes(c, 2 * F * D * es);
+    CK(hipMemcpy2DAsync(gu, 32 * D * es, lp[6], 16 * D * es, 16 * D * es, F / 16, hipMemcpyDeviceToDevice, st));
+    CK(hipMemcpy2DAsync(gu + 16 * D * es, 32 * D * es, lp[7], 16 * D * es, 16 * D * es, F / 16,
+                        hipMemcpyDeviceToDevice, st));
+    md.wgu.push_back(gu);
+    void* wd = dev_alloc_bytes(c, D * F * es);
+    CK(hipMemcpyAsync(wd, lp[8], D * F * es, hipMemcpyDeviceToDevice, st));
+    md.wd.push_back(wd);
+  }
+  // rotary tables in double precision, stored fp32: [max_pos][hd/2]
+  const int half = md.hd / 2;
+  std::vector<float> ct((size_t)max_pos * half), stt((size_t)max_pos * half);
+  for (int p = 0; p < max_pos; ++p)
+    for (int d = 0; d < half; ++d) {
+      double inv = pow((double)k.rope_theta, -2.0 * d / (double)md.hd);
+      double ang = (double)p * inv;
+      ct[(size_t)p * half + d] = (float)cos(ang);
+      stt[(size_t)p * half + d] = (float)sin(ang);
+    }
+  md.cos_t = dev_alloc<float>(c, ct.size());
+  md.sin_t = dev_alloc<float>(c, stt.size());
+  CK(hipMemcpy(md.cos_t, ct.data(), ct.size() * 4, hipMemcpyHostToDevice));
+  CK(hipMemcpy(md.sin_t, stt.data(), stt.size() * 4, hipMemcpyHostToDevice));
+}
+
+void alloc_pool(cdsl_ctx* c, Model& md) {
+  const long long per_layer = (long long)c->nblocks * md.c.n_kv_heads * kBlock * md.hd;
+  md.pool.Hkv = md.c.n_kv_heads;
+  md.pool.hd = md.hd;
+  md.pool.layer_elems = per_layer;
+  const size_t bytes = (size_t)per_layer * md.c.n_layers * sizeof(float);   // fp32 KV
+  md.pool.k = dev_alloc_bytes(c, bytes);
+  md.pool.v = dev_alloc_bytes(c, bytes);
+  // zero once: stale slots are then always finite (masked weights are 0)
+  CK(hipMemsetAsync(md.pool.k, 0, bytes, c->st));
+  CK(hipMemsetAsync(md.pool.v, 0, bytes, c->st));
+}
+
+int prefill_chunk_prompts(const cdsl_limits& l) {
+  int per = std::max(1, 8192 / std::max(1, l.max_prompt));
+  return std::min(per, l.max_batch);
+}
+
+void alloc_workspace(cdsl_ctx* c) {
+  const cdsl_limits& l = c->lim;
+  const int verify_rows = l.max_batch * l.max_k * l.max_d;
+  const int roll_rows = l.max_batch * l.max_k;
+  const int pre_rows = prefill_chunk_prompts(l) * l.max_prompt;
+  Workspace& w = c->ws;
+  w.Mmax = std::max({verify_rows, roll_rows, pre_rows, l.max_batch});
+  w.Mlog = std::max({verify_rows, roll_rows, l.max_batch});
+  size_t Dm = 0, QKVm = 0, HQm = 0, Fm = 0, Vm = 0, Hm = 0, HDm = 0;
+  for (auto& md : c->m) {
+    Dm = std::max<size_t>(Dm, md.c.d_model);
+    QKVm = std::max<size_t>(QKVm, md.qkv_n);
+    HQm = std::max<size_t>(HQm, (size_t)md.c.n_heads * md.hd);
+    Fm = std::max<size_t>(Fm, md.c.ffn_dim);
+    Vm = std::max<size_t>(Vm, md.c.vocab);
+    Hm = std::max<size_t>(Hm, md.c.n_heads);
+    HDm = std::max<size_t>(HDm, md.hd);
+  }
+  const size_t es = 4;   // activations are fp32 for every weight dtype
+  const size_t M = w.Mmax;
+  w.h = dev_alloc<float>(c, M * Dm);
+  w.u = dev_alloc_bytes(c, M * Dm * es);
+  w.qkv = dev_alloc<float>(c, M * QKVm);
+  w.q = dev_alloc_bytes(c, M * HQm * es);
+  w.o = dev_alloc_bytes(c, M * HQm * es);
+  w.act = dev_alloc_bytes(c, M * Fm * es);
+  if (c->dtype == CDSL_F32) w.gu32 = dev_alloc<float>(c, M * 2 * Fm);
+  w.logits = dev_alloc<float>(c, (size_t)w.Mlog * Vm);
+  // attention split partials sized for the verification / rollout passes
+  w.part_rows = (size_t)std::max(verify_rows, roll_rows) * Hm;
+  if (c->dtype == CDSL_BF16) {
+    w.part_o = dev_alloc<float>(c, kMaxSplits * w.part_rows * HDm);
+    w.part_ml = dev_alloc<float>(c, kMaxSplits * w.part_rows * 2);
+  }
+  // GEMM split-K workspace: the largest need over every shape and row count
+  size_t need = 0;
+  for (auto& md : c->m) {
+    const int D = md.c.d_model, F = md.c.ffn_dim, V = md.c.vocab, HQ = md.c.n_heads * md.hd;
+    const int shapes[5][2] = {{md.qkv_n, D}, {D, HQ}, {2 * F, D}, {D, F}, {V, D}};
+    for (int mm = 1; mm <= w.Mmax; ++mm)
+      for (auto& s : shapes) need = std::max(need, gemm_workspace_bytes(mm, s[0], s[1], c->dtype));
+  }
+  w.gemm_ws_bytes = need;
+  if (need) {
+    w.gemm_ws = dev_alloc_bytes(c, need);
+    CK(hipMemsetAsync(w.gemm_ws, 0, need, c->st));
+  }
+}
+
+// ---------------------------------------------------------------------------
+// model runner
+// ---------------------------------------------------------------------------
+void gemm(cdsl_ctx* c, const void* A, const void* B, void* C, int M, int N, int K, int ldc, int epi) {
+  const double wes = c->dtype == CDSL_BF16 ? 2.0 : 4.0;   // weight element size
+  double out = epi == kEpiSwiGLU ? (double)M * (N / 2) * 4.0
+                                 : (double)M * N * 4.0 * (epi == kEpiResidual ? 2.0 : 1.0);
+  const int kind = gemm_kind(M, N, K, c->dtype);
+  const int cls = kind == 0 ? CDSL_K_GEMM_DENSE : kind == 1 ? CDSL_K_GEMM_SKINNY : CDSL_K_GEMM_F32;
+  Span sp(c, cls, 2.0 * M * N * (double)K, (double)M * K * 4.0 + (double)N * K * wes + out);
+  CK(gemm_launch(A, B, C, M, N, K, ldc, c->dtype, epi, c->ws.gemm_ws, c->ws.gemm_ws_bytes, c->st));
+}
+
+// Forward pass of one model over the rows of p.  With want_logits, the
+// final-normed rows (all, or the last row of each beam with last_only) go
+// through the LM head into ws.logits; hid receives fp32 final-normed rows of
+// every beam's last row when non-null.
+void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, long long sum_prefix_len,
+              bool want_logits, bool last_only, float* hid) {
+  Workspace& w = c->ws;
+  const auto& k = md.c;
+  const int M = p.M();
+  const int D = k.d_model, F = k.ffn_dim, H = k.n_heads, Hkv = k.n_kv_heads, hd = md.hd;
+  const int dt = k.dtype;
+  if (M > w.Mmax) {
+    g_err = "pass rows exceed the workspace";
+    throw Fail{CDSL_ERANGE};
+  }
+  const double es = 4.0;   // fp32 activations and KV
+  {
+    Span sp(c, CDSL_K_ROWWISE, 0.0, (double)M * D * ((dt == CDSL_BF16 ? 2.0 : 4.0) + 4.0));
+    CK(embed_launch(p, md.emb, w.h, D, k.vocab, dt, c->st));
+  }
+  // algorithmic attention work of this pass: the prefix KV of a prompt is
+  // read once for all its rows; every query head sees its visible keys
+  const double kvtok = (double)Hkv * hd * 2.0 * es;
+  const double R = p.R, kp = p.kp;
+  const double pre_tok = p.mode == kSuffix ? (double)sum_prefix_len : (double)sum_prefix_len + p.nb * R;
+  const double suf_tok = p.mode == kSuffix ? (double)p.nb * kp * (p.j0 + R) : 0.0;
+  const double attn_bytes = (pre_tok + suf_tok) * kvtok + 2.0 * M * (double)H * hd * es;
+  const double vis = p.mode == kSuffix
+                         ? kp * (R * ((double)sum_prefix_len + p.nb * (double)p.j0) + p.nb * R * (R + 1) / 2)
+                         : R * (double)sum_prefix_len + p.nb * R * (R + 1) / 2;
+  const double attn_flops = 4.0 * hd * (double)H * vis;
+  AttnPlan pl = attn_plan(p, H, Hkv, hd, dt, max_prefix_len, kMaxSplits);
+  if (pl.nsplit > 1 && (size_t)M * H > w.part_rows) {
+    pl = attn_plan(p, H, Hkv, hd, dt, max_prefix_len, 1);
+  }
+  AttnArgs aa{};
+  aa.p = p;
+  aa.Q = w.q;
+  aa.O = w.o;
+  aa.pool = md.pool;
+  aa.H = H;
+  aa.Hkv = Hkv;
+  aa.G = md.G;
+  aa.rows_total = (long long)M * H;
+  aa.scale_log2 = (float)(1.4426950408889634 / sqrt((double)hd));
+  aa.part_o = w.part_o;
+  aa.part_ml = w.part_ml;
+  const double norm_bytes = (double)M * D * (4.0 + es);
+  const double rope_bytes = (double)M * md.qkv_n * (4.0 + es);
+  const double comb_bytes = (double)pl.nsplit * M * H * (hd + 2) * 4.0 + (double)M * H * hd * es;
+  for (int l = 0; l < k.n_layers; ++l) {
+    {
+      Span sp(c, CDSL_K_ROWWISE, 0.0, norm_bytes);
+      CK(rmsnorm_launch(w.h, md.g1[l], w.u, M, D, k.rms_eps, 0, 1, nullptr, dt, c->st));
+    }
+    gemm(c, w.u, md.wqkv[l], w.qkv, M, md.qkv_n, D, md.qkv_n, kEpiStore);
+    {
+      Span sp(c, CDSL_K_ROWWISE, 0.0, rope_bytes);
+      CK(rope_kv_launch(p, w.qkv, w.q, md.pool, l, md.cos_t, md.sin_t, H, Hkv, hd, dt, c->st));
+    }
+    aa.layer = l;
+    {
+      Span sp(c, CDSL_K_ATTENTION, attn_flops, attn_bytes);
+      CK(attn_launch(aa, pl, hd, dt, c->st));
+    }
+    if (pl.nsplit > 1) {
+      Span sp(c, CDSL_K_ATTN_COMBINE, 0.0, comb_bytes);
+      CK(attn_combine_launch(aa, pl, hd, c->st));
+    }
+    gemm(c, w.o, md.wo[l], w.h, M, D, H * hd, D, kEpiResidual);
+    {
+      Span sp(c, CDSL_K_ROWWISE, 0.0, norm_bytes);
+      CK(rmsnorm_launch(w.h, md.g2[l], w.u, M, D, k.rms_eps, 0, 1, nullptr, dt, c->st));
+    }
+    if (dt == CDSL_BF16) {
+      gemm(c, w.u, md.wgu[l], w.act, M, 2 * F, D, F, kEpiSwiGLU);
+    } else {
+      gemm(c, w.u, md.wgu[l], w.gu32, M, 2 * F, D, 2 * F, kEpiStore);
+      Span sp(c, CDSL_K_ROWWISE, 0.0, (double)M * F * 12.0);
+      CK(swiglu_f32_launch(w.gu32, (float*)w.act, M, F, c->st));
+    }
+    gemm(c, w.act, md.wd[l], w.h, M, D, F, D, kEpiResidual);
+  }
+  if (!want_logits) return;
+  const int rows = last_only ? p.nb * p.kp : M;
+  {
+    Span sp(c, CDSL_K_ROWWISE, 0.0, (double)rows * D * (4.0 + es));
+    CK(rmsnorm_launch(w.h, md.gf, w.u, rows, D, k.rms_eps, last_only ? 1 : 0, p.R, hid, dt, c->st));
+  }
+  gemm(c, w.u, md.lm, w.logits, rows, k.vocab, D, k.vocab, kEpiStore);
+}
+
+void logit_rows(cdsl_ctx* c, const LogitArgs& la, int M) {
+  Span sp(c, CDSL_K_LOGIT_ROWS, 0.0, (double)M * la.V * 4.0);
+  CK(logit_rows_launch(la, M, c->st));
+}
+
+long long sum_len(const cdsl_prefix* px) {
+  long long s = 0;
+  for (int v : px->len) s += v;
+  return s;
+}
+
+PassDesc base_pass(cdsl_ctx* c, cdsl_prefix* px) {
+  PassDesc p{};
+  p.Lp = px->Lp;
+  p.ptable = px->table_dev;
+  p.ptable_stride = c->pstride;
+  p.stable = c->stable;
+  p.sblocks = c->sblocks;
+  p.s_stride_i = c->sblocks;
+  p.s_stride_b = c->lim.max_k * c->sblocks;
+  return p;
+}
+
+int max_len(const cdsl_prefix* px) {
+  int m = 0;
+  for (int v : px->len) m = std::max(m, v);
+  return m;
+}
+
+// make sure prompt b owns blocks for positions [0, new_len)
+void ensure_blocks(cdsl_ctx* c, cdsl_prefix* px, int b, int new_len) {
+  const int need = (new_len + kBlock - 1) / kBlock;
+  if (need > c->pstride) {
+    g_err = "prompt " + std::to_string(b) + " exceeds max_ctx";
+    throw Fail{CDSL_ERANGE};
+  }
+  for (int q = 0; q < need; ++q) {
+    int& slot = px->table[(size_t)b * c->pstride + q];
+    if (slot >= 0) continue;
+    if (c->free_blocks.empty()) {
+      g_err = "KV pool exhausted";
+      throw Fail{CDSL_ENOMEM};
+    }
+    slot = c->free_blocks.back();
+    c->free_blocks.pop_back();
+    px->owned.push_back(slot);
+  }
+}
+
+void upload_table(cdsl_ctx* c, cdsl_prefix* px) {
+  const size_t n = (size_t)px->B * c->pstride;
+  for (size_t u = 0; u < n; ++u) c->table_host[u] = px->table[u] < 0 ? 0 : px->table[u];
+  CK(hipMemcpyAsync(px->table_dev, c->table_host, n * sizeof(int), hipMemcpyHostToDevice, c->st));
+}
+
+template <typename F>
+int guarded(cdsl_ctx* c, F&& f) {
+  try {
+    return f();
+  } catch (const Fail& e) {
+    if (c) c->err = g_err;
+    return e.code;
+  } catch (const std::bad_alloc&) {
+    return fail(c, CDSL_ENOMEM, "host allocation failed");
+  } catch (...) {
+    return fail(c, CDSL_EDEVICE, "unexpected exception");
+  }
+}
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+extern "C" {
+
+int cdsl_init(const cdsl_model* draft, const cdsl_model* target, const cdsl_limits* limits, void* stream,
+              cdsl_ctx** out) {
+  if (!draft || !target || !limits || !out) return fail(nullptr, CDSL_EINVAL, "null argument");
+  *out = nullptr;
+  std::string why;
+  if (!cfg_ok(draft->cfg, why)) return fail(nullptr, CDSL_EINVAL, "draft: " + why);
+  if (!cfg_ok(target->cfg, why)) return fail(nullptr, CDSL_EINVAL, "target: " + why);
+  if (draft->cfg.vocab != target->cfg.vocab)
+    return fail(nullptr, CDSL_EINVAL, "draft and target vocabularies differ");
+  if (draft->cfg.dtype != target->cfg.dtype) return fail(nullptr, CDSL_EINVAL, "draft and target dtypes differ");
+  const cdsl_limits& l = *limits;
+  if (l.max_batch <= 0 || l.max_ctx <= 0 || l.max_k <= 0 || l.max_k > kMaxK || l.max_d <= 0 || l.max_d > kMaxD ||
+      l.max_prompt <= 0 || l.max_prompt > l.max_ctx || l.max_prefixes <= 0)
+    return fail(nullptr, CDSL_EINVAL, "invalid limits (max_k <= 16, max_d <= 32, max_prompt <= max_ctx)");
+  cdsl_ctx* c = new (std::nothrow) cdsl_ctx();
+  if (!c) return fail(nullptr, CDSL_ENOMEM, "host allocation failed");
+  c->st = (hipStream_t)stream;
+  c->lim = l;
+  c->dtype = draft->cfg.dtype;
+  int rc = guarded(c, [&]() {
+    const int max_pos = l.max_ctx + l.max_d + 2;
+    load_model(c, c->m[0], *draft, max_pos);
+    load_model(c, c->m[1], *target, max_pos);
+    c->pstride = (l.max_ctx + l.max_d + 2 + kBlock - 1) / kBlock;
+    c->sblocks = (l.max_d + kBlock - 1) / kBlock;
+    const int suffix_blocks = l.max_batch * l.max_k * c->sblocks;
+    const int prefix_blocks = l.max_prefixes * l.max_batch * c->pstride;
+    c->nblocks = suffix_blocks + prefix_blocks;
+    alloc_pool(c, c->m[0]);
+    alloc_pool(c, c->m[1]);
+    std::vector<int> st_ids(suffix_blocks);
+    for (int u = 0; u < suffix_blocks; ++u) st_ids[u] = u;
+    c->stable = dev_alloc<int>(c, suffix_blocks);
+    CK(hipMemcpy(c->stable, st_ids.data(), suffix_blocks * sizeof(int), hipMemcpyHostToDevice));
+    c->free_blocks.reserve(prefix_blocks);
+    for (int u = c->nblocks - 1; u >= suffix_blocks; --u) c->free_blocks.push_back(u);
+    std::vector<int> io(l.max_batch);
+    for (int u = 0; u < l.max_batch; ++u) io[u] = u;
+    c->iota = dev_alloc<int>(c, l.max_batch);
+    CK(hipMemcpy(c->iota, io.data(), io.size() * sizeof(int), hipMemcpyHostToDevice));
+    c->stage_stride = 3 + l.max_d + 1;
+    c->stage = dev_alloc<int>(c, (size_t)l.max_batch * c->stage_stride);
+    c->ids_dev = dev_alloc<int>(c, l.max_batch);
+    c->catch_tok = dev_alloc<int>(c, l.max_batch);
+    CK(hipHostMalloc((void**)&c->stage_host, (size_t)l.max_batch * c->stage_stride * sizeof(int), 0));
+    CK(hipHostMalloc((void**)&c->table_host, (size_t)l.max_batch * c->pstride * sizeof(int), 0));
+    CK(hipHostMalloc((void**)&c->ids_host, (size_t)l.max_batch * sizeof(int), 0));
+    alloc_workspace(c);
+    CK(hipStreamSynchronize(c->st));
+    return CDSL_OK;
+  });
+  if (rc != CDSL_OK) {
+    std::string msg = c->err;
+    cdsl_destroy(c);
+    return fail(nullptr, rc, msg);
+  }
+  *out = c;
+  return CDSL_OK;
+}
+
+int cdsl_destroy(cdsl_ctx* c) {
+  if (!c) return CDSL_OK;
+  if (c->st) (void)hipStreamSynchronize(c->st);
+  else (void)hipDeviceSynchronize();
+  for (auto& p : c->pend) {
+    (void)hipEventDestroy(p.a);
+    (void)hipEventDestroy(p.b);
+  }
+  for (hipEvent_t e : c->ev_free) (void)hipEventDestroy(e);
+  for (void* p : c->allocs) (void)hipFree(p);
+  if (c->stage_host) (void)hipHostFree(c->stage_host);
+  if (c->table_host) (void)hipHostFree(c->table_host);
+  if (c->ids_host) (void)hipHostFree(c->ids_host);
+  delete c;
+  return CDSL_OK;
+}
+
+const char* cdsl_last_error(const cdsl_ctx* c) {
+  if (c) return c->err.c_str();
+  return g_err.c_str();
+}
+
+int cdsl_prefill(cdsl_ctx* c, const int32_t* tokens, int32_t B, int32_t L, int32_t k, cdsl_prefix** out,
+                 int32_t* beams, float* head_lp) {
+  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  if (!tokens || !out || !beams || !head_lp) return fail(c, CDSL_EINVAL, "null argument");
+  if (B <= 0 || L <= 0 || k <= 0) return fail(c, CDSL_EINVAL, "B, L and k must be positive");
+  if (B > c->lim.max_batch || L > c->lim.max_prompt || k > c->lim.max_k)
+    return fail(c, CDSL_ERANGE, "B, L or k beyond the limits");
+  if (k > c->m[1].c.vocab) return fail(c, CDSL_EINVAL, "k exceeds the vocabulary");
+  if (c->live_prefixes >= c->lim.max_prefixes) return fail(c, CDSL_ERANGE, "too many live prefixes");
+  *out = nullptr;
+  cdsl_prefix* px = new (std::nothrow) cdsl_prefix();
+  if (!px) return fail(c, CDSL_ENOMEM, "host allocation failed");
+  int rc = guarded(c, [&]() {
+    px->B = B;
+    px->len.assign(B, 0);
+    px->table.assign((size_t)B * c->pstride, -1);
+    // per-handle device state (lengths, block table, emitted tokens)
+    px->Lp = dev_alloc<int>(c, B);
+    px->table_dev = dev_alloc<int>(c, (size_t)B * c->pstride);
+    px->gen = dev_alloc<int>(c, (size_t)B * c->lim.max_ctx);
+    px->gen_len = dev_alloc<int>(c, B);
+    for (int b = 0; b < B; ++b) ensure_blocks(c, px, b, L);
+    upload_table(c, px);
+    CK(fill_int_launch(px->Lp, 0, B, c->st));
+    CK(fill_int_launch(px->gen_len, 0, B, c->st));
+    const int chunk = prefill_chunk_prompts(c->lim);
+    for (int b0 = 0; b0 < B; b0 += chunk) {
+      const int nb = std::min(chunk, B - b0);
+      PassDesc p = base_pass(c, px);
+      p.mode = kAppend;
+      p.nb = nb;
+      p.kp = 1;
+      p.R = L;
+      p.j0 = 0;
+      p.prompt_ids = c->iota + b0;
+      p.tok = tokens;
+      p.tok_stride = L;
+      p.tok_off = 0;
+      run_pass(c, c->m[0], p, 0, 0, false, false, nullptr);
+      run_pass(c, c->m[1], p, 0, 0, true, true, nullptr);
+      LogitArgs la{};
+      la.logits = c->ws.logits;
+      la.V = c->m[1].c.vocab;
+      la.want_lse = 1;
+      la.kk = k;
+      la.topk_ids = beams;
+      la.topk_lp = head_lp;
+      la.topk_rows = c->iota + b0;
+      logit_rows(c, la, nb);
+    }
+    CK(add_launch(B, nullptr, px->Lp, L, c->st));
+    for (int b = 0; b < B; ++b) px->len[b] = L;
+    CK(hipStreamSynchronize(c->st));
+    return CDSL_OK;
+  });
+  if (rc != CDSL_OK) {
+    for (int blk : px->owned) c->free_blocks.push_back(blk);
+    delete px;
+    return rc;
+  }
+  c->live_prefixes++;
+  *out = px;
+  return CDSL_OK;
+}
+
+int cdsl_rollout(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, int32_t d, int32_t* lookaheads) {
+  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  if (!px || !beams || !lookaheads) return fail(c, CDSL_EINVAL, "null argument");
+  if (k <= 0 || d <= 0) return fail(c, CDSL_EINVAL, "k and d must be positive");
+  if (k > c->lim.max_k || d > c->lim.max_d) return fail(c, CDSL_ERANGE, "k or d beyond the limits");
+  if (max_len(px) + d + 1 > c->lim.max_ctx) return fail(c, CDSL_ERANGE, "context would exceed max_ctx");
+  return guarded(c, [&]() {
+    const int B = px->B;
+    CK(heads_to_lookaheads_launch(B * k, d, beams, lookaheads, c->st));
+    const int Lmax = max_len(px);
+    for (int j0 = 0; j0 < d; ++j0) {
+      PassDesc p = base_pass(c, px);
+      p.mode = kSuffix;
+      p.nb = B;
+      p.kp = k;
+      p.R = 1;
+      p.j0 = j0;
+      p.tok = lookaheads;
+      p.tok_stride = d + 1;
+      p.tok_off = j0;
+      run_pass(c, c->m[0], p, Lmax, sum_len(px), true, false, nullptr);
+      LogitArgs la{};
+      la.logits = c->ws.logits;
+      la.V = c->m[0].c.vocab;
+      la.want_lse = 0;
+      la.kk = 0;
+      la.amax = lookaheads;
+      la.amax_map.enabled = 1;
+      la.amax_map.p = p;
+      la.amax_map.stride = d + 1;
+      la.amax_map.off = j0 + 1;
+      logit_rows(c, la, p.M());
+    }
+    px->rolled_k = k;
+    px->rolled_d = d;
+    px->verified_k = px->verified_d = 0;
+    return CDSL_OK;
+  });
+}
+
+int cdsl_verify(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d, const float* head_lp,
+                float* logprobs, int32_t* target_argmax, int32_t* n_accept, float* scores, int32_t* row_topk_ids,
+                float* row_topk_lp, float* hidden) {
+  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  if (!px || !look || !head_lp || !logprobs || !target_argmax || !n_accept || !scores || !row_topk_ids ||
+      !row_topk_lp)
+    return fail(c, CDSL_EINVAL, "null argument");
+  if (k <= 0 || d <= 0) return fail(c, CDSL_EINVAL, "k and d must be positive");
+  if (k > c->lim.max_k || d > c->lim.max_d) return fail(c, CDSL_ERANGE, "k or d beyond the limits");
+  if (max_len(px) + d + 1 > c->lim.max_ctx) return fail(c, CDSL_ERANGE, "context would exceed max_ctx");
+  return guarded(c, [&]() {
+    const int B = px->B;
+    PassDesc p = base_pass(c, px);
+    p.mode = kSuffix;
+    p.nb = B;
+    p.kp = k;
+    p.R = d;
+    p.j0 = 0;
+    p.tok = look;
+    p.tok_stride = d + 1;
+    p.tok_off = 0;
+    run_pass(c, c->m[1], p, max_len(px), sum_len(px), true, false, hidden);
+    LogitArgs la{};
+    la.logits = c->ws.logits;
+    la.V = c->m[1].c.vocab;
+    la.want_lse = 1;
+    la.kk = k;
+    la.amax = target_argmax;
+    la.lp = logprobs;
+    la.gather_tok = look;
+    la.gather_map.enabled = 1;
+    la.gather_map.p = p;
+    la.gather_map.stride = d + 1;
+    la.gather_map.off = 1;
+    la.topk_ids = row_topk_ids;
+    la.topk_lp = row_topk_lp;
+    logit_rows(c, la, p.M());
+    {
+      Span sp(c, CDSL_K_STEP, 0.0, (double)B * k * d * 12.0);
+      CK(beam_scores_launch(B * k, d, look, target_argmax, logprobs, head_lp, n_accept, scores, c->st));
+    }
+    px->verified_k = k;
+    px->verified_d = d;
+    return CDSL_OK;
+  });
+}
+
+int cdsl_reward_keywords(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d,
+                         const int32_t* keywords, int32_t n_kw, int32_t normalize, float* reward) {
+  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  if (!px || !look || !keywords || !reward) return fail(c, CDSL_EINVAL, "null argument");
+  if (k <= 0 || d <= 0 || n_kw <= 0 || n_kw > 64) return fail(c, CDSL_EINVAL, "bad k, d or n_kw (1..64)");
+  return guarded(c, [&]() {
+    Span sp(c, CDSL_K_STEP, 0.0, (double)px->B * k * (d + 1) * 4.0);
+    CK(reward_keywords_launch(px->B, k, d, px->gen, c->lim.max_ctx, px->gen_len, look, keywords, n_kw, normalize,
+                              reward, c->st));
+    return CDSL_OK;
+  });
+}
+
+int cdsl_reward_linear(cdsl_ctx* c, const float* hidden, const float* w, int32_t B, int32_t k, int32_t D,
+                       float* reward) {
+  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  if (!hidden || !w || !reward || B <= 0 || k <= 0 || D <= 0) return fail(c, CDSL_EINVAL, "bad argument");
+  return guarded(c, [&]() {
+    Span sp(c, CDSL_K_STEP, 2.0 * B * k * D, (double)B * k * D * 4.0);
+    CK(reward_linear_launch(B * k, hidden, w, D, reward, c->st));
+    return CDSL_OK;
+  });
+}
+
+int cdsl_select(cdsl_ctx* c, const float* scores, const float* reward, float alpha, int32_t B, int32_t k,
+                int32_t* beam) {
+  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  if (!scores || !reward || !beam || B <= 0 || k <= 0) return fail(c, CDSL_EINVAL, "bad argument");
+  if (isnan(alpha) || (isinf(alpha) && alpha < 0)) return fail(c, CDSL_EINVAL, "alpha must be finite or +inf");
+  return guarded(c, [&]() {
+    const int reward_only = isinf(alpha) ? 1 : 0;
+    Span sp(c, CDSL_K_STEP, 0.0, (double)B * k * 8.0);
+    CK(select_launch(B, k, scores, reward, reward_only ? 0.f : alpha, reward_only, beam, c->st));
+    return CDSL_OK;
+  });
+}
+
+int cdsl_commit(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, const int32_t* n_accept,
+                const int32_t* rtk_ids, const float* rtk_lp, int32_t k, int32_t d, int32_t* emitted_host,
+                int32_t* n_emit_host, int32_t* next_beams, float* next_head_lp) {
+  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  if (!px || !look || !beam || !n_accept || !rtk_ids || !rtk_lp || !emitted_host || !n_emit_host || !next_beams ||
+      !next_head_lp)
+    return fail(c, CDSL_EINVAL, "null argument");
+  if (px->rolled_k != k || px->rolled_d != d || px->verified_k != k || px->verified_d != d)
+    return fail(c, CDSL_ESTATE, "commit needs a rollout and a verify with the same k and d");
+  return guarded(c, [&]() {
+    const int B = px->B;
+    {
+      Span sp(c, CDSL_K_STEP, 0.0, (double)B * (d + 1 + 2 * k) * 4.0);
+      CK(commit_launch(B, k, d, look, beam, n_accept, rtk_ids, rtk_lp, next_beams, next_head_lp, c->stage,
+                       c->stage_stride, px->gen, c->lim.max_ctx, px->gen_len, c->catch_tok, c->st));
+    }
+    CK(hipMemcpyAsync(c->stage_host, c->stage, (size_t)B * c->stage_stride * sizeof(int), hipMemcpyDeviceToHost,
+                      c->st));
+    CK(hipStreamSynchronize(c->st));
+    if (c->prof) harvest(c);
+    for (int b = 0; b < B; ++b)
+      if (c->stage_host[(size_t)b * c->stage_stride] < 0) {
+        g_err = "invalid beam index (NaN score or reward?) for prompt " + std::to_string(b);
+        throw Fail{CDSL_EINVAL};
+      }
+    int ncatch = 0;
+    for (int b = 0; b < B; ++b) {
+      const int* stg = c->stage_host + (size_t)b * c->stage_stride;
+      const int ne = stg[0];
+      const int cnt = std::min(ne, d);
+      const int newlen = px->len[b] + ne;
+      if (newlen > c->lim.max_ctx) {
+        g_err = "prompt " + std::to_string(b) + " exceeds max_ctx";
+        throw Fail{CDSL_ERANGE};
+      }
+      ensure_blocks(c, px, b, newlen);
+      (void)cnt;
+      if (stg[1]) c->ids_host[ncatch++] = b;
+    }
+    upload_table(c, px);
+    for (int mi = 0; mi < 2; ++mi) {
+      Model& md = c->m[mi];
+      Span sp(c, CDSL_K_STEP, 0.0, 0.0);
+      CK(promote_launch(B, k, md.pool, md.c.n_layers, c->stage, c->stage_stride, d, px->Lp, px->table_dev,
+                        c->pstride, c->stable, c->lim.max_k * c->sblocks, c->sblocks, md.c.dtype, c->st));
+    }
+    CK(advance_launch(B, c->stage, c->stage_stride, d, px->Lp, c->st));
+    for (int b = 0; b < B; ++b) px->len[b] += std::min(c->stage_host[(size_t)b * c->stage_stride], d);
+    if (ncatch > 0) {
+      CK(hipMemcpyAsync(c->ids_dev, c->ids_host, ncatch * sizeof(int), hipMemcpyHostToDevice, c->st));
+      PassDesc p = base_pass(c, px);
+      p.mode = kAppend;
+      p.nb = ncatch;
+      p.kp = 1;
+      p.R = 1;
+      p.j0 = 0;
+      p.prompt_ids = c->ids_dev;
+      p.tok = c->catch_tok;
+      p.tok_stride = 1;
+      p.tok_off = 0;
+      const int Lmax = max_len(px);
+      long long sl = 0;
+      for (int u = 0; u < ncatch; ++u) sl += px->len[c->ids_host[u]];
+      run_pass(c, c->m[0], p, Lmax, sl, false, false, nullptr);
+      run_pass(c, c->m[1], p, Lmax, sl, true, false, nullptr);
+      LogitArgs la{};
+      la.logits = c->ws.logits;
+      la.V = c->m[1].c.vocab;
+      la.want_lse = 1;
+      la.kk = k;
+      la.topk_ids = next_beams;
+      la.topk_lp = next_head_lp;
+      la.topk_rows = c->ids_dev;
+      logit_rows(c, la, ncatch);
+      CK(add_launch(ncatch, c->ids_dev, px->Lp, 1, c->st));
+      for (int u = 0; u < ncatch; ++u) px->len[c->ids_host[u]] += 1;
+    }
+    for (int b = 0; b < B; ++b) {
+      const int* stg = c->stage_host + (size_t)b * c->stage_stride;
+      n_emit_host[b] = stg[0];
+      for (int t = 0; t <= d; ++t) emitted_host[(size_t)b * (d + 1) + t] = t < stg[0] ? stg[3 + t] : -1;
+    }
+    px->rolled_k = px->rolled_d = px->verified_k = px->verified_d = 0;
+    return CDSL_OK;
+  });
+}
+
+int cdsl_prefix_lengths(cdsl_ctx* c, const cdsl_prefix* px, int32_t* lengths_host) {
+  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  if (!px || !lengths_host) return fail(c, CDSL_EINVAL, "null argument");
+  for (int b = 0; b < px->B; ++b) lengths_host[b] = px->len[b];
+  return CDSL_OK;
+}
+
+int cdsl_profile_enable(cdsl_ctx* c, int32_t enable) {
+  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  return guarded(c, [&]() {
+    CK(hipStreamSynchronize(c->st));
+    harvest(c);
+    c->acc = cdsl_kernel_stats{};
+    c->prof = enable != 0;
+    return CDSL_OK;
+  });
+}
+
+int cdsl_profile_read(cdsl_ctx* c, cdsl_kernel_stats* out) {
+  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  if (!out) return fail(c, CDSL_EINVAL, "null argument");
+  return guarded(c, [&]() {
+    CK(hipStreamSynchronize(c->st));
+    harvest(c);
+    *out = c->acc;
+    return CDSL_OK;
+  });
+}
+
+int cdsl_free_prefix(cdsl_ctx* c, cdsl_prefix* px) {
+  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  if (!px) return CDSL_OK;
+  return guarded(c, [&]() {
+    CK(hipStreamSynchronize(c->st));
+    for (int blk : px->owned) c->free_blocks.push_back(blk);
+    for (void* p : {(void*)px->Lp, (void*)px->table_dev, (void*)px->gen, (void*)px->gen_len}) {
+      auto it = std::find(c->allocs.begin(), c->allocs.end(), p);
+      if (it != c->allocs.end()) {
+        (void)hipFree(p);
+        c->allocs.erase(it);
+      }
+    }
+    delete px;
+    c->live_prefixes--;
+    return CDSL_OK;
+  });
+}
+
+// ---------------------------------------------------------------------------
+// kernel-level entry points (include/cdsl_ops.h)
+// ---------------------------------------------------------------------------
+size_t cdsl_op_gemm_workspace(int32_t M, int32_t N, int32_t K, int32_t dtype) {
+  if (M <= 0 || N <= 0 || K <= 0) return 0;
+  return gemm_workspace_bytes(M, N, K, dtype);
+}
+
+int cdsl_op_gemm(const void* A, const void* B, float* C, int32_t M, int32_t N, int32_t K, int32_t dtype,
+                 int32_t epilogue, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!A || !B || !C) return fail(nullptr, CDSL_EINVAL, "null argument");
+  if (dtype != CDSL_F32 && dtype != CDSL_BF16) return fail(nullptr, CDSL_EINVAL, "bad dtype");
+  if (epilogue != CDSL_EPI_STORE && epilogue != CDSL_EPI_RESIDUAL) return fail(nullptr, CDSL_EINVAL, "bad epilogue");
+  if (gemm_check(M, N, K, dtype) != 0) return fail(nullptr, CDSL_EINVAL, "unsupported shape");
+  if (gemm_workspace_bytes(M, N, K, dtype) > workspace_bytes)
+    return fail(nullptr, CDSL_EINVAL, "workspace too small");
+  hipError_t e = gemm_launch(A, B, C, M, N, K, N, dtype, epilogue, workspace, workspace_bytes, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(nullptr, CDSL_EDEVICE, hipGetErrorString(e));
+  return CDSL_OK;
+}
+
+int cdsl_op_logit_rows(const float* logits, int32_t M, int32_t V, const int32_t* gather, int32_t kk, float* lp,
+                       int32_t* amax, int32_t* topk_ids, float* topk_lp, void* stream) {
+  if (!logits || M < 0 || V <= 0 || kk < 0 || kk > 16 || kk > V) return fail(nullptr, CDSL_EINVAL, "bad argument");
+  if ((gather && !lp) || (kk > 0 && (!topk_ids || !topk_lp))) return fail(nullptr, CDSL_EINVAL, "missing output");
+  LogitArgs la{};
+  la.logits = logits;
+  la.V = V;
+  la.want_lse = (gather || kk > 0) ? 1 : 0;
+  la.kk = kk;
+  la.amax = amax;
+  la.lp = gather ? lp : nullptr;
+  la.gather_tok = gather;
+  la.topk_ids = topk_ids;
+  la.topk_lp = topk_lp;
+  hipError_t e = logit_rows_launch(la, M, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(nullptr, CDSL_EDEVICE, hipGetErrorString(e));
+  return CDSL_OK;
+}
+
+}  // extern "C"

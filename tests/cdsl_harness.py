@@ -1,0 +1,177 @@
+"""Test harness: the same seeded workload on the GPU library and on the CPU
+oracle, and the step-by-step comparison rules.
+
+Comparison rules (for the GPU against the float64 oracle):
+* token ids (beam heads, draft argmax, target argmax) and the selected beam
+  are bit-exact wherever the oracle's deciding margin exceeds TOK_MARGIN;
+  below it either choice is correct, and since every later quantity then
+  depends on that choice, the trajectory comparison stops there (counted);
+* log-probs within LP_TOL (1e-4 fp32, 2e-2 bf16), beam scores within
+  (d + 1) * LP_TOL.
+No GPU value is ever fed into the oracle.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+from typing import List, Optional
+
+import numpy as np
+
+import cdsl_inputs as ci
+import oracle
+
+TOK_MARGIN = 1e-2
+
+
+def lp_tol(dtype):
+    return 1e-4 if dtype == "f32" else 2e-2
+
+
+@dataclass
+class Setup:
+    wl: object
+    draft_np: dict
+    target_np: dict
+    odraft: object
+    otarget: object
+    engine: object = None
+    kws: Optional[np.ndarray] = None
+    rw: Optional[np.ndarray] = None
+
+    def prompts(self, B, first=0):
+        return ci.prompts(self.wl.seed, B, self.wl.prompt_len, self.wl.target.vocab, first=first)
+
+
+def make_setup(name, draft_is_target=False, B=None, max_steps=8, k=None, d=None, **wl_over):
+    wl = ci.workload(name)
+    if wl_over:
+        wl = wl.with_(**wl_over)
+    if draft_is_target:
+        wl = wl.with_(draft=wl.target)
+    tw = ci.model_weights(wl.target, wl.seed, 1, wl.dtype)
+    dw = tw if draft_is_target else ci.model_weights(wl.draft, wl.seed, 0, wl.dtype)
+    s = Setup(wl, dw, tw, oracle.Decoder(wl.draft, dw), oracle.Decoder(wl.target, tw))
+    B = max(B or wl.batch, 64)
+    if wl.reward.startswith("keyword"):
+        s.kws = ci.keywords(wl.seed, B, wl.n_keywords, wl.target.vocab)
+    else:
+        s.rw = ci.reward_head(wl.seed, wl.target.d_model)
+    return s
+
+
+def make_engine(s: Setup, B, max_steps=8, k=None, d=None):
+    import torch
+    from paper_2412_10418_amd.engine import Engine
+    dwd, twd = Engine.upload(s.wl, s.draft_np, s.target_np)
+    s.engine = Engine(s.wl, dwd, twd, max_steps=max_steps, max_batch=B, k=k, d=d)
+    return s.engine
+
+
+@dataclass
+class Report:
+    steps_compared: int = 0
+    stopped: str = ""
+    max_lp_err: float = 0.0
+    max_score_err: float = 0.0
+    checks: int = 0
+
+
+def _first_diff(a, b):
+    for u, (x, y) in enumerate(zip(a, b)):
+        if int(x) != int(y):
+            return u
+    return -1
+
+
+def compare_step(rep: Report, wl, k, d, o_step, g_heads, g_head_lp, g_look, g_ver, g_reward, g_beam, g_emit,
+                 tol) -> bool:
+    """Compare one prompt's step; returns False when a legal near-tie
+    divergence ends the trajectory comparison (raises on a real mismatch)."""
+    # a1 beam heads: ordered top-k of s_t
+    oh = o_step.heads
+    u = _first_diff(g_heads, oh)
+    if u >= 0:
+        assert o_step.head_margins[u] <= TOK_MARGIN, (u, list(g_heads), list(oh), o_step.head_margins)
+        rep.stopped = f"beam-head near tie (margin {o_step.head_margins[u]:.2e})"
+        return False
+    assert np.max(np.abs(g_head_lp - o_step.head_lp)) <= tol
+    # a2 rollout
+    ox = o_step.roll.x
+    assert np.array_equal(g_look[:, 0], oh)
+    for i in range(k):
+        u = _first_diff(g_look[i, 1:], ox[i])
+        if u >= 0:
+            assert o_step.roll.margin[i, u] <= TOK_MARGIN, (i, u, g_look[i], ox[i], o_step.roll.margin[i])
+            rep.stopped = f"draft near tie (beam {i}, j {u}, margin {o_step.roll.margin[i, u]:.2e})"
+            return False
+    # a3-a5 verification of identical inputs
+    ve = o_step.ver
+    lp_err = np.max(np.abs(g_ver["logprobs"] - ve.logprobs))
+    assert lp_err <= tol, lp_err
+    rep.max_lp_err = max(rep.max_lp_err, lp_err)
+    ok = ve.margin > TOK_MARGIN
+    assert np.array_equal(g_ver["target_argmax"][ok], ve.y[ok])
+    if np.all(ok) or np.array_equal(g_ver["target_argmax"], ve.y):
+        assert np.array_equal(g_ver["n_accept"], ve.n)
+    elif not np.array_equal(g_ver["n_accept"], ve.n):
+        rep.stopped = "target argmax near tie"
+        return False
+    sc_err = np.max(np.abs(g_ver["scores"] - ve.scores))
+    assert sc_err <= tol * (d + 1), sc_err
+    rep.max_score_err = max(rep.max_score_err, sc_err)
+    # a6 reward
+    if wl.reward.startswith("keyword"):
+        assert np.array_equal(g_reward, o_step.reward)
+    else:
+        assert np.max(np.abs(g_reward - o_step.reward)) <= 10 * tol
+    # a7 select
+    comb = np.sort(o_step.combined)[::-1]
+    gap = comb[0] - comb[1] if len(comb) > 1 else math.inf
+    if int(g_beam) != o_step.beam:
+        assert gap <= TOK_MARGIN * (d + 2), (g_beam, o_step.beam, o_step.combined)
+        rep.stopped = f"selection near tie (gap {gap:.2e})"
+        return False
+    # a8 commit
+    assert list(g_emit) == list(o_step.emitted)
+    rep.checks += 1
+    return True
+
+
+def run_and_compare(s: Setup, B: int, steps: int, check_prompts, k=None, d=None, alpha=None):
+    """Run ``steps`` GPU steps on a batch of B prompts and compare the listed
+    prompts step by step with independent oracle runs."""
+    import torch
+    wl = s.wl
+    k = k or wl.k
+    d = d or wl.d
+    alpha = wl.alpha if alpha is None else alpha
+    eng = s.engine
+    prompts = s.prompts(B)
+    st = eng.start(torch.from_numpy(prompts).cuda(), k=k)
+    kw_t = torch.from_numpy(s.kws[:B]).cuda() if s.kws is not None else None
+    rw_t = torch.from_numpy(s.rw).cuda() if s.rw is not None else None
+    ost = {b: oracle.prefill(s.odraft, s.otarget, prompts[b]) for b in check_prompts}
+    reps = {b: Report() for b in check_prompts}
+    live = set(check_prompts)
+    tol = lp_tol(wl.dtype)
+    for t in range(steps):
+        heads = st.beams.cpu().numpy().copy()
+        head_lp = st.head_lp.cpu().numpy().copy()
+        bf = eng.step(st, keywords=kw_t, reward_w=rw_t, alpha=alpha, k=k, d=d)
+        look = bf.lookaheads.cpu().numpy()
+        ver = {kk: (v.cpu().numpy() if v is not None else None) for kk, v in bf.verify.items()}
+        rew = bf.reward.cpu().numpy()
+        beam = bf.beam.cpu().numpy()
+        for b in list(live):
+            o = oracle.step(s.odraft, s.otarget, ost[b], k, d, alpha, wl.reward,
+                            kws=s.kws[b] if s.kws is not None else None, w=s.rw)
+            gv = {kk: (v[b] if v is not None else None) for kk, v in ver.items()}
+            cont = compare_step(reps[b], wl, k, d, o, heads[b], head_lp[b], look[b], gv, rew[b], beam[b],
+                                eng._last_emitted[b], tol)
+            if cont:
+                reps[b].steps_compared += 1
+                ost[b] = o.state
+            else:
+                live.discard(b)
+    return st, reps
