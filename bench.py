@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--d", type=int, default=None)
     ap.add_argument("--profile-steps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain 256 MiB device copy (reference for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -187,6 +189,14 @@ def main():
     log(f"instrumented: kernel time {kern_ms / args.profile_steps:.2f} ms/step of "
         f"{prof_wall / args.profile_steps:.2f} ms/step wall")
     emitted = sum(len(e) for e in st.emitted)
+    if args.calibrate_copy:
+        src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("calibration: 3 copies of 256 MiB (reads 262144 KiB, writes 262144 KiB per copy)")
+        del src, dst
     st.prefix.free()
     eng.close()
     del eng

@@ -6,8 +6,10 @@ namespace cdsl {
 
 struct AttnArgs {
   PassDesc p;
-  const void* Q;          // [M][H][hd] (model dtype), rotary already applied
-  void* O;                // [M][H][hd] (model dtype)
+  const float* Q;         // [M][H][hd] fp32, rotary already applied
+  float* O;               // [M][H][hd] fp32 output (fp32 models)
+  bf16* Ohi;              // [M][H][hd] hi / lo planes (bf16-weight models)
+  bf16* Olo;
   KVPool pool;
   int layer;
   int H, Hkv, G;

@@ -136,7 +136,7 @@ __global__ __launch_bounds__(256) void attn_mfma(AttnArgs a) {
   // Q^T fragments (B operand): row lr, dims 32s + 8lg .. +8, as hi/lo
   bf16x8 qh[KS], ql[KS];
   {
-    const float* qrow = (const float*)a.Q + ((long long)ri.m * a.H + ri.h) * HD + lg * 8;
+    const float* qrow = a.Q + ((long long)ri.m * a.H + ri.h) * HD + lg * 8;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
@@ -239,10 +239,19 @@ __global__ __launch_bounds__(256) void attn_mfma(AttnArgs a) {
   const long long rowid = (long long)ri.m * a.H + ri.h;
   if (a.nsplit == 1) {
     const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-    float* o = (float*)a.O + rowid * HD + lg * 4;
+    const long long o = rowid * HD + lg * 4;
 #pragma unroll
     for (int t = 0; t < DT; ++t) {
-      *(float4*)(o + t * 16) = make_float4(acc[t][0] * inv, acc[t][1] * inv, acc[t][2] * inv, acc[t][3] * inv);
+      bf16x4 hv, lv;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        bf16 h, l;
+        split_bf16(acc[t][e] * inv, h, l);
+        hv[e] = h;
+        lv[e] = l;
+      }
+      *(bf16x4*)(a.Ohi + o + t * 16) = hv;
+      *(bf16x4*)(a.Olo + o + t * 16) = lv;
     }
   } else {
     const long long prow = (long long)split * a.rows_total + rowid;
@@ -257,7 +266,7 @@ __global__ __launch_bounds__(256) void attn_mfma(AttnArgs a) {
 }
 
 // Merge the split partials of every (row, head): one wave per row.
-template <typename T, int HD>
+template <int HD>
 __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
   const long long row = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -282,7 +291,12 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
 #pragma unroll
   for (int u = 0; u < PER; ++u) {
     int d = lane + 64 * u;
-    if (d < HD) ((T*)a.O)[row * HD + d] = from_f32<T>(o[u] * inv);
+    if (d < HD) {
+      bf16 h, lo;
+      split_bf16(o[u] * inv, h, lo);
+      a.Ohi[row * HD + d] = h;
+      a.Olo[row * HD + d] = lo;
+    }
   }
 }
 
@@ -310,7 +324,7 @@ __global__ __launch_bounds__(64) void attn_f32(AttnArgs a) {
   const int nS = p.mode == kSuffix ? (p.j0 + p.R + kBlock - 1) / kBlock : 0;
   const int nP = p.mode == kSuffix ? (Lp + kBlock - 1) / kBlock : (Lp + p.R + kBlock - 1) / kBlock;
   const int nkeys = (nP + p.kp * nS) * kBlock;
-  const float* q = (const float*)a.Q + ((long long)m * a.H + h) * HD;
+  const float* q = a.Q + ((long long)m * a.H + h) * HD;
   const float* kbase = (const float*)a.pool.k + (long long)a.layer * a.pool.layer_elems;
   const float* vbase = (const float*)a.pool.v + (long long)a.layer * a.pool.layer_elems;
   constexpr int PER = (HD + 63) / 64;
@@ -359,7 +373,7 @@ __global__ __launch_bounds__(64) void attn_f32(AttnArgs a) {
 #pragma unroll
   for (int u = 0; u < PER; ++u) {
     int d = lane + 64 * u;
-    if (d < HD) ((float*)a.O)[rowid * HD + d] = acc[u] * inv;
+    if (d < HD) a.O[rowid * HD + d] = acc[u] * inv;
   }
 }
 
@@ -429,9 +443,9 @@ hipError_t attn_combine_launch(const AttnArgs& args, const AttnPlan& pl, int hd,
   a.blocks_per_split = pl.blocks_per_split;
   dim3 cg((unsigned)((a.rows_total + 3) / 4));
   switch (hd) {
-    case 32: attn_combine<float, 32><<<cg, 256, 0, st>>>(a); break;
-    case 64: attn_combine<float, 64><<<cg, 256, 0, st>>>(a); break;
-    case 128: attn_combine<float, 128><<<cg, 256, 0, st>>>(a); break;
+    case 32: attn_combine<32><<<cg, 256, 0, st>>>(a); break;
+    case 64: attn_combine<64><<<cg, 256, 0, st>>>(a); break;
+    case 128: attn_combine<128><<<cg, 256, 0, st>>>(a); break;
   }
   return hipGetLastError();
 }

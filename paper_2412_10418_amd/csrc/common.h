@@ -10,6 +10,9 @@ typedef __bf16 bf16;
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+// native 16-byte vector for raw copies (HIP's uint4 wraps a union, which
+// keeps the optimizer from holding it in registers)
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBlock = 16;        // tokens per KV block (= one MFMA key tile)
 constexpr int kMaxK = 16;         // beams
@@ -85,6 +88,14 @@ __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
+}
+
+// An fp32 activation as the bf16 pair (hi, lo) with x ~= hi + lo to about
+// 2^-17 relative.  Weights are exactly bf16, so a projection over split
+// activations (hi * W + lo * W, two MFMA products) keeps fp32-level accuracy.
+__device__ __forceinline__ void split_bf16(float x, bf16& hi, bf16& lo) {
+  hi = (bf16)x;
+  lo = (bf16)(x - (float)hi);
 }
 
 // (value, id) ordering used by every argmax / top-k: larger value first,

@@ -3,24 +3,44 @@
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 
+#include "common.h"
+
 namespace cdsl {
 
 enum GemmEpilogue { kEpiStore = 0, kEpiResidual = 1, kEpiSwiGLU = 2 };
 
-// C = A[M,K] * B[N,K]^T with A fp32 (activations).  dtype 1: B bf16
-// (weights; A is split into bf16 hi + lo so the product keeps fp32-level
-// accuracy); dtype 0: B fp32.
-//   kEpiStore:    C fp32 [M, ldc]  = product
-//   kEpiResidual: C fp32 [M, ldc] += product
-//   kEpiSwiGLU:   (bf16 only) B packs, per group of 32 rows, 16 gate rows
-//                 then the 16 matching up rows; C fp32 [M, ldc = N/2]
-//                 receives silu(gate) * up.
+// The activation operand: bf16 hi / lo planes [M, K] (bf16-weight models) or
+// one fp32 matrix [M, K] (fp32-weight models).
+struct GemmOperand {
+  const bf16* hi;
+  const bf16* lo;
+  const float* f32;
+};
+
+// Where the product goes: fp32 [M, ldc] for kEpiStore / kEpiResidual, the
+// bf16 hi / lo planes [M, ldc] of silu(gate) * up for kEpiSwiGLU.
+struct GemmOut {
+  float* f32;
+  bf16* hi;
+  bf16* lo;
+  int ldc;
+};
+
+// C = A[M,K] * W[N,K]^T, fp32 accumulate.  dtype 1: W bf16 (A as hi / lo
+// planes, two MFMA products per step); dtype 0: W fp32 (A fp32).
+//   kEpiStore:    C  = product
+//   kEpiResidual: C += product
+//   kEpiSwiGLU:   (bf16 only) W packs, per group of 32 rows, 16 gate rows
+//                 then the 16 matching up rows; the output (ldc = N/2)
+//                 receives silu(gate) * up as hi / lo planes.
 size_t gemm_workspace_bytes(int M, int N, int K, int dtype);
 int gemm_check(int M, int N, int K, int dtype);
 // 0: dense bf16 kernel, 1: skinny bf16 kernel, 2: fp32 kernel
 int gemm_kind(int M, int N, int K, int dtype);
-hipError_t gemm_launch(const void* A, const void* B, void* C, int M, int N, int K, int ldc, int dtype, int epi,
-                       void* ws, size_t ws_bytes, hipStream_t st);
+// prefill selects a separately named instantiation of the dense kernel
+hipError_t gemm_launch(const GemmOperand& A, const void* B, const GemmOut& out, int M, int N, int K, int dtype,
+                       int epi, void* ws, size_t ws_bytes, hipStream_t st, bool prefill = false);
 hipError_t swiglu_f32_launch(const float* gu, float* act, int M, int F, hipStream_t st);
+hipError_t split_planes_launch(const float* x, bf16* hi, bf16* lo, long long n, hipStream_t st);
 
 }  // namespace cdsl

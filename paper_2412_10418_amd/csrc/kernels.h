@@ -38,8 +38,8 @@ __host__ __device__ inline long long rowmap_index(const RowMap& r, int m) {
 }
 
 hipError_t embed_launch(const PassDesc& p, const void* emb, float* h, int D, int V, int dtype, hipStream_t st);
-hipError_t rmsnorm_launch(const float* x, const float* g, void* out, int rows, int D, float eps, int last_only, int R,
-                          float* hid, int dtype, hipStream_t st);
+hipError_t rmsnorm_launch(const float* x, const float* g, float* out32, bf16* ohi, bf16* olo, int rows, int D,
+                          float eps, int last_only, int R, float* hid, hipStream_t st);
 hipError_t rope_kv_launch(const PassDesc& p, const float* qkv, void* qout, const KVPool& pool, int layer,
                           const float* cos_t, const float* sin_t, int H, int Hkv, int hd, int dtype, hipStream_t st);
 hipError_t logit_rows_launch(const LogitArgs& a, int M, hipStream_t st);

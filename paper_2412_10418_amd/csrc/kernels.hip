@@ -49,11 +49,13 @@ __global__ __launch_bounds__(256) void embed_rows(PassDesc p, const T* __restric
 
 // out[r] = x[src(r)] / sqrt(mean(x^2) + eps) * g.  src(r) = r, or the last
 // row of beam r when last_only (prompt prefill: only the last position needs
-// logits).  hid (fp32) additionally receives the normed row of every beam's
-// last row (the reward reads it).
-template <typename T>
+// logits).  The result goes to out32 (fp32) or, for bf16-weight models, to
+// the hi / lo planes that the next projection consumes.  hid (fp32)
+// additionally receives the normed row of every beam's last row (the reward
+// reads it).
 __global__ __launch_bounds__(256) void rmsnorm_rows(const float* __restrict__ x, const float* __restrict__ g,
-                                                    T* __restrict__ out, int D, float eps, int last_only, int R,
+                                                    float* __restrict__ out32, bf16* __restrict__ ohi,
+                                                    bf16* __restrict__ olo, int D, float eps, int last_only, int R,
                                                     float* __restrict__ hid) {
   __shared__ float sh[4];
   const int r = blockIdx.x;
@@ -63,12 +65,19 @@ __global__ __launch_bounds__(256) void rmsnorm_rows(const float* __restrict__ x,
   for (int c = threadIdx.x; c < D; c += 256) ss = fmaf(xr[c], xr[c], ss);
   ss = block_sum<4>(ss, sh);
   const float inv = rsqrtf(ss / (float)D + eps);
-  T* o = out + (long long)r * D;
+  const long long o = (long long)r * D;
   const bool want_hid = hid && (last_only || (r % R) == R - 1);
   float* hr = want_hid ? hid + (long long)(last_only ? r : r / R) * D : nullptr;
   for (int c = threadIdx.x; c < D; c += 256) {
-    float v = xr[c] * inv * g[c];
-    o[c] = from_f32<T>(v);
+    const float v = xr[c] * inv * g[c];
+    if (out32) {
+      out32[o + c] = v;
+    } else {
+      bf16 h, l;
+      split_bf16(v, h, l);
+      ohi[o + c] = h;
+      olo[o + c] = l;
+    }
     if (hr) hr[c] = v;
   }
 }
@@ -480,11 +489,10 @@ hipError_t embed_launch(const PassDesc& p, const void* emb, float* h, int D, int
   return hipGetLastError();
 }
 
-hipError_t rmsnorm_launch(const float* x, const float* g, void* out, int rows, int D, float eps, int last_only, int R,
-                          float* hid, int dtype, hipStream_t st) {
+hipError_t rmsnorm_launch(const float* x, const float* g, float* out32, bf16* ohi, bf16* olo, int rows, int D,
+                          float eps, int last_only, int R, float* hid, hipStream_t st) {
   if (rows == 0) return hipSuccess;
-  (void)dtype;   // activations are fp32 for every weight dtype
-  rmsnorm_rows<float><<<rows, 256, 0, st>>>(x, g, (float*)out, D, eps, last_only, R, hid);
+  rmsnorm_rows<<<rows, 256, 0, st>>>(x, g, out32, ohi, olo, D, eps, last_only, R, hid);
   return hipGetLastError();
 }
 

@@ -43,12 +43,12 @@ struct Model {
 
 struct Workspace {
   int Mmax = 0, Mlog = 0;
-  float* h = nullptr;
-  void* u = nullptr;
-  float* qkv = nullptr;
-  void* q = nullptr;
-  void* o = nullptr;
-  void* act = nullptr;
+  float* h = nullptr;        // residual stream [M, D]
+  float* qkv = nullptr;      // [M, (H + 2 Hkv) hd]
+  float* q = nullptr;        // [M, H, hd] after rotary
+  // projection inputs: hi / lo bf16 planes (bf16 weights) or fp32
+  bf16 *uh = nullptr, *ul = nullptr, *oh = nullptr, *ol = nullptr, *ah = nullptr, *al = nullptr;
+  float *u32 = nullptr, *o32 = nullptr, *act32 = nullptr;
   float* gu32 = nullptr;
   float* logits = nullptr;
   float* part_o = nullptr;
@@ -340,15 +340,23 @@ void alloc_workspace(cdsl_ctx* c) {
     Hm = std::max<size_t>(Hm, md.c.n_heads);
     HDm = std::max<size_t>(HDm, md.hd);
   }
-  const size_t es = 4;   // activations are fp32 for every weight dtype
   const size_t M = w.Mmax;
   w.h = dev_alloc<float>(c, M * Dm);
-  w.u = dev_alloc_bytes(c, M * Dm * es);
   w.qkv = dev_alloc<float>(c, M * QKVm);
-  w.q = dev_alloc_bytes(c, M * HQm * es);
-  w.o = dev_alloc_bytes(c, M * HQm * es);
-  w.act = dev_alloc_bytes(c, M * Fm * es);
-  if (c->dtype == CDSL_F32) w.gu32 = dev_alloc<float>(c, M * 2 * Fm);
+  w.q = dev_alloc<float>(c, M * HQm);
+  if (c->dtype == CDSL_BF16) {
+    w.uh = dev_alloc<bf16>(c, M * Dm);
+    w.ul = dev_alloc<bf16>(c, M * Dm);
+    w.oh = dev_alloc<bf16>(c, M * HQm);
+    w.ol = dev_alloc<bf16>(c, M * HQm);
+    w.ah = dev_alloc<bf16>(c, M * Fm);
+    w.al = dev_alloc<bf16>(c, M * Fm);
+  } else {
+    w.u32 = dev_alloc<float>(c, M * Dm);
+    w.o32 = dev_alloc<float>(c, M * HQm);
+    w.act32 = dev_alloc<float>(c, M * Fm);
+    w.gu32 = dev_alloc<float>(c, M * 2 * Fm);
+  }
   w.logits = dev_alloc<float>(c, (size_t)w.Mlog * Vm);
   // attention split partials sized for the verification / rollout passes
   w.part_rows = (size_t)std::max(verify_rows, roll_rows) * Hm;
@@ -374,14 +382,15 @@ void alloc_workspace(cdsl_ctx* c) {
 // ---------------------------------------------------------------------------
 // model runner
 // ---------------------------------------------------------------------------
-void gemm(cdsl_ctx* c, const void* A, const void* B, void* C, int M, int N, int K, int ldc, int epi) {
+void gemm(cdsl_ctx* c, const GemmOperand& A, const void* W, const GemmOut& out, int M, int N, int K, int epi,
+          bool prefill) {
   const double wes = c->dtype == CDSL_BF16 ? 2.0 : 4.0;   // weight element size
-  double out = epi == kEpiSwiGLU ? (double)M * (N / 2) * 4.0
-                                 : (double)M * N * 4.0 * (epi == kEpiResidual ? 2.0 : 1.0);
+  const double outb = epi == kEpiSwiGLU ? (double)M * (N / 2) * 4.0
+                                        : (double)M * N * 4.0 * (epi == kEpiResidual ? 2.0 : 1.0);
   const int kind = gemm_kind(M, N, K, c->dtype);
   const int cls = kind == 0 ? CDSL_K_GEMM_DENSE : kind == 1 ? CDSL_K_GEMM_SKINNY : CDSL_K_GEMM_F32;
-  Span sp(c, cls, 2.0 * M * N * (double)K, (double)M * K * 4.0 + (double)N * K * wes + out);
-  CK(gemm_launch(A, B, C, M, N, K, ldc, c->dtype, epi, c->ws.gemm_ws, c->ws.gemm_ws_bytes, c->st));
+  Span sp(c, cls, 2.0 * M * N * (double)K, (double)M * K * 4.0 + (double)N * K * wes + outb);
+  CK(gemm_launch(A, W, out, M, N, K, c->dtype, epi, c->ws.gemm_ws, c->ws.gemm_ws_bytes, c->st, prefill));
 }
 
 // Forward pass of one model over the rows of p.  With want_logits, the
@@ -389,7 +398,7 @@ void gemm(cdsl_ctx* c, const void* A, const void* B, void* C, int M, int N, int 
 // through the LM head into ws.logits; hid receives fp32 final-normed rows of
 // every beam's last row when non-null.
 void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, long long sum_prefix_len,
-              bool want_logits, bool last_only, float* hid) {
+              bool want_logits, bool last_only, float* hid, bool prefill = false) {
   Workspace& w = c->ws;
   const auto& k = md.c;
   const int M = p.M();
@@ -422,7 +431,9 @@ void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, lon
   AttnArgs aa{};
   aa.p = p;
   aa.Q = w.q;
-  aa.O = w.o;
+  aa.O = w.o32;
+  aa.Ohi = w.oh;
+  aa.Olo = w.ol;
   aa.pool = md.pool;
   aa.H = H;
   aa.Hkv = Hkv;
@@ -434,12 +445,16 @@ void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, lon
   const double norm_bytes = (double)M * D * (4.0 + es);
   const double rope_bytes = (double)M * md.qkv_n * (4.0 + es);
   const double comb_bytes = (double)pl.nsplit * M * H * (hd + 2) * 4.0 + (double)M * H * hd * es;
+  const bool bf = dt == CDSL_BF16;
+  const GemmOperand Au{w.uh, w.ul, w.u32}, Ao{w.oh, w.ol, w.o32}, Aact{w.ah, w.al, w.act32};
+  const GemmOut to_qkv{w.qkv, nullptr, nullptr, md.qkv_n}, to_h{w.h, nullptr, nullptr, D};
+  const GemmOut to_act{nullptr, w.ah, w.al, F}, to_gu{w.gu32, nullptr, nullptr, 2 * F};
   for (int l = 0; l < k.n_layers; ++l) {
     {
       Span sp(c, CDSL_K_ROWWISE, 0.0, norm_bytes);
-      CK(rmsnorm_launch(w.h, md.g1[l], w.u, M, D, k.rms_eps, 0, 1, nullptr, dt, c->st));
+      CK(rmsnorm_launch(w.h, md.g1[l], w.u32, w.uh, w.ul, M, D, k.rms_eps, 0, 1, nullptr, c->st));
     }
-    gemm(c, w.u, md.wqkv[l], w.qkv, M, md.qkv_n, D, md.qkv_n, kEpiStore);
+    gemm(c, Au, md.wqkv[l], to_qkv, M, md.qkv_n, D, kEpiStore, prefill);
     {
       Span sp(c, CDSL_K_ROWWISE, 0.0, rope_bytes);
       CK(rope_kv_launch(p, w.qkv, w.q, md.pool, l, md.cos_t, md.sin_t, H, Hkv, hd, dt, c->st));
@@ -453,27 +468,27 @@ void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, lon
       Span sp(c, CDSL_K_ATTN_COMBINE, 0.0, comb_bytes);
       CK(attn_combine_launch(aa, pl, hd, c->st));
     }
-    gemm(c, w.o, md.wo[l], w.h, M, D, H * hd, D, kEpiResidual);
+    gemm(c, Ao, md.wo[l], to_h, M, D, H * hd, kEpiResidual, prefill);
     {
       Span sp(c, CDSL_K_ROWWISE, 0.0, norm_bytes);
-      CK(rmsnorm_launch(w.h, md.g2[l], w.u, M, D, k.rms_eps, 0, 1, nullptr, dt, c->st));
+      CK(rmsnorm_launch(w.h, md.g2[l], w.u32, w.uh, w.ul, M, D, k.rms_eps, 0, 1, nullptr, c->st));
     }
-    if (dt == CDSL_BF16) {
-      gemm(c, w.u, md.wgu[l], w.act, M, 2 * F, D, F, kEpiSwiGLU);
+    if (bf) {
+      gemm(c, Au, md.wgu[l], to_act, M, 2 * F, D, kEpiSwiGLU, prefill);
     } else {
-      gemm(c, w.u, md.wgu[l], w.gu32, M, 2 * F, D, 2 * F, kEpiStore);
+      gemm(c, Au, md.wgu[l], to_gu, M, 2 * F, D, kEpiStore, prefill);
       Span sp(c, CDSL_K_ROWWISE, 0.0, (double)M * F * 12.0);
-      CK(swiglu_f32_launch(w.gu32, (float*)w.act, M, F, c->st));
+      CK(swiglu_f32_launch(w.gu32, w.act32, M, F, c->st));
     }
-    gemm(c, w.act, md.wd[l], w.h, M, D, F, D, kEpiResidual);
+    gemm(c, Aact, md.wd[l], to_h, M, D, F, kEpiResidual, prefill);
   }
   if (!want_logits) return;
   const int rows = last_only ? p.nb * p.kp : M;
   {
     Span sp(c, CDSL_K_ROWWISE, 0.0, (double)rows * D * (4.0 + es));
-    CK(rmsnorm_launch(w.h, md.gf, w.u, rows, D, k.rms_eps, last_only ? 1 : 0, p.R, hid, dt, c->st));
+    CK(rmsnorm_launch(w.h, md.gf, w.u32, w.uh, w.ul, rows, D, k.rms_eps, last_only ? 1 : 0, p.R, hid, c->st));
   }
-  gemm(c, w.u, md.lm, w.logits, rows, k.vocab, D, k.vocab, kEpiStore);
+  gemm(c, Au, md.lm, GemmOut{w.logits, nullptr, nullptr, k.vocab}, rows, k.vocab, D, kEpiStore, prefill);
 }
 
 void logit_rows(cdsl_ctx* c, const LogitArgs& la, int M) {
@@ -672,8 +687,8 @@ int cdsl_prefill(cdsl_ctx* c, const int32_t* tokens, int32_t B, int32_t L, int32
       p.tok = tokens;
       p.tok_stride = L;
       p.tok_off = 0;
-      run_pass(c, c->m[0], p, 0, 0, false, false, nullptr);
-      run_pass(c, c->m[1], p, 0, 0, true, true, nullptr);
+      run_pass(c, c->m[0], p, 0, 0, false, false, nullptr, true);
+      run_pass(c, c->m[1], p, 0, 0, true, true, nullptr, true);
       LogitArgs la{};
       la.logits = c->ws.logits;
       la.V = c->m[1].c.vocab;
@@ -961,9 +976,15 @@ int cdsl_free_prefix(cdsl_ctx* c, cdsl_prefix* px) {
 // ---------------------------------------------------------------------------
 // kernel-level entry points (include/cdsl_ops.h)
 // ---------------------------------------------------------------------------
+// bf16 weights: the fp32 activation operand is split into its hi / lo planes
+// at the start of the workspace, followed by the split-K planes
+static size_t op_planes_bytes(int M, int K, int dtype) {
+  return dtype == CDSL_BF16 ? ((size_t)2 * M * K * sizeof(bf16) + 255) & ~(size_t)255 : 0;
+}
+
 size_t cdsl_op_gemm_workspace(int32_t M, int32_t N, int32_t K, int32_t dtype) {
   if (M <= 0 || N <= 0 || K <= 0) return 0;
-  return gemm_workspace_bytes(M, N, K, dtype);
+  return op_planes_bytes(M, K, dtype) + gemm_workspace_bytes(M, N, K, dtype);
 }
 
 int cdsl_op_gemm(const void* A, const void* B, float* C, int32_t M, int32_t N, int32_t K, int32_t dtype,
@@ -972,9 +993,21 @@ int cdsl_op_gemm(const void* A, const void* B, float* C, int32_t M, int32_t N, i
   if (dtype != CDSL_F32 && dtype != CDSL_BF16) return fail(nullptr, CDSL_EINVAL, "bad dtype");
   if (epilogue != CDSL_EPI_STORE && epilogue != CDSL_EPI_RESIDUAL) return fail(nullptr, CDSL_EINVAL, "bad epilogue");
   if (gemm_check(M, N, K, dtype) != 0) return fail(nullptr, CDSL_EINVAL, "unsupported shape");
-  if (gemm_workspace_bytes(M, N, K, dtype) > workspace_bytes)
+  if (cdsl_op_gemm_workspace(M, N, K, dtype) > workspace_bytes)
     return fail(nullptr, CDSL_EINVAL, "workspace too small");
-  hipError_t e = gemm_launch(A, B, C, M, N, K, N, dtype, epilogue, workspace, workspace_bytes, (hipStream_t)stream);
+  if (M == 0) return CDSL_OK;
+  hipStream_t st = (hipStream_t)stream;
+  GemmOperand op{nullptr, nullptr, (const float*)A};
+  const size_t pb = op_planes_bytes(M, K, dtype);
+  if (dtype == CDSL_BF16) {
+    bf16* hi = (bf16*)workspace;
+    bf16* lo = hi + (size_t)M * K;
+    hipError_t e = split_planes_launch((const float*)A, hi, lo, (long long)M * K, st);
+    if (e != hipSuccess) return fail(nullptr, CDSL_EDEVICE, hipGetErrorString(e));
+    op = GemmOperand{hi, lo, nullptr};
+  }
+  hipError_t e = gemm_launch(op, B, GemmOut{C, nullptr, nullptr, N}, M, N, K, dtype, epilogue,
+                             (char*)workspace + pb, workspace_bytes - pb, st);
   if (e != hipSuccess) return fail(nullptr, CDSL_EDEVICE, hipGetErrorString(e));
   return CDSL_OK;
 }
