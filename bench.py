@@ -42,25 +42,159 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--summarize-profile", nargs=4, metavar=("BENCH_JSON", "TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
+                    help="write a markdown summary of rocprofv3 runs of this script (kernel trace, FETCH_SIZE and "
+                         "WRITE_SIZE passes with --calibrate-copy) and exit; no GPU needed")
+    ap.add_argument("--summary-out", default=None)
+    ap.add_argument("--commands", default=None, help="text file with the exact profiling commands (for the summary)")
     return ap.parse_args()
 
 
-def roofline(stats):
+# Kernel (rocprofv3 name pattern) and source files behind each timed class.
+CLASS_KERNEL = {
+    "gemm_dense": (r"gemm_bf16_dense<[^>]*, 0>\(", ["gemm.hip", "gemm.h", "common.h"]),
+    "gemm_skinny": (r"gemm_bf16_skinny<", ["gemm.hip", "gemm.h", "common.h"]),
+    "attention": (r"attn_mfma<", ["attention.hip", "attention.h", "common.h"]),
+    "splitk_reduce": (r"splitk_reduce_kernel", ["gemm.hip", "gemm.h", "common.h"]),
+}
+TRAFFIC_TAG = "<!-- traffic "
+
+
+def source_digest(files):
+    import hashlib
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2412_10418_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(cls, workload):
+    """HBM bytes per launch of the class's kernel from a committed rocprofv3
+    counter summary, or None when there is none for this workload or the
+    kernel's sources changed since the counters were taken."""
+    if cls not in CLASS_KERNEL:
+        return None
+    d = os.path.join(ROOT, "profiles")
+    if not os.path.isdir(d):
+        return None
+    digest = source_digest(CLASS_KERNEL[cls][1])
+    for fn in sorted(os.listdir(d)):
+        if not fn.endswith(".md"):
+            continue
+        with open(os.path.join(d, fn)) as fh:
+            for line in fh:
+                if line.startswith(TRAFFIC_TAG):
+                    rec = json.loads(line[len(TRAFFIC_TAG):].rstrip().rstrip("->").strip())
+                    if rec.get("class") == cls and rec.get("workload") == workload and rec.get("source") == digest:
+                        return rec
+    return None
+
+
+def roofline(stats, workload):
     """Dominant kernel class of the instrumented steps and its roofline."""
     best = max(stats, key=lambda nm: stats[nm]["ms"])
     st = stats[best]
     sec = st["ms"] / 1e3
-    per_launch_ms = st["ms"] / max(1, st["launches"])
+    n = max(1, st["launches"])
+    per_launch_ms = st["ms"] / n
+    tr = stored_traffic(best, workload)
+    extra = {"kernel": best, "avg_launch_us": round(per_launch_ms * 1e3, 2), "launches": st["launches"],
+             "alg_bytes_per_launch": round(st["bytes"] / n), "traffic_unit": "HBM bytes per launch",
+             "traffic_source": tr["file"] if tr else None}
+    traffic = tr["bytes_per_launch"] if tr else None
     if best in ("gemm_dense",):
         ach = st["flops"] / sec / 1e12
         return best, {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_MFMA_BF16_TFS, "unit": "TFLOP/s",
-                      "frac": round(ach / PEAK_MFMA_BF16_TFS, 4), "traffic": None,
-                      "kernel": best, "avg_launch_us": round(per_launch_ms * 1e3, 2),
-                      "launches": st["launches"]}
+                      "frac": round(ach / PEAK_MFMA_BF16_TFS, 4), "traffic": traffic,
+                      "alg_flops_per_launch": round(st["flops"] / n), **extra}
     ach = st["bytes"] / sec / 1e9
     return best, {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                  "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None, "kernel": best,
-                  "avg_launch_us": round(per_launch_ms * 1e3, 2), "launches": st["launches"]}
+                  "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": traffic, **extra}
+
+
+def summarize_profile(args):
+    """Markdown summary of the three rocprofv3 runs of this script."""
+    import csv
+    import re
+    bench_json, trace_dir, fetch_dir, write_dir = args.summarize_profile
+    with open(bench_json) as fh:
+        line = [ln for ln in fh.read().splitlines() if ln.startswith("{")][-1]
+    b = json.loads(line)
+    wl = b["config"]["workload"]
+    stats = list(csv.DictReader(open(os.path.join(trace_dir, "bench_kernel_stats.csv"))))
+    total = sum(float(r["TotalDurationNs"]) for r in stats)
+
+    def counters(dn):
+        rows = list(csv.DictReader(open(os.path.join(dn, "bench_counter_collection.csv"))))
+        return rows
+
+    fetch, write = counters(fetch_dir), counters(write_dir)
+    copy_bytes_kib = 262144.0
+
+    def copy_scale(rows):
+        # the last three dispatches are the 256 MiB calibration copies
+        cal = [float(r["Counter_Value"]) for r in rows[-3:] if "copyBuffer" in r["Kernel_Name"]]
+        if len(cal) != 3:
+            raise SystemExit("calibration copies not found at the end of the counter run")
+        return copy_bytes_kib / (sum(cal) / 3), sum(cal) / 3
+
+    fs, fcal = copy_scale(fetch)
+    ws, wcal = copy_scale(write)
+    out = [f"# rocprofv3 summary: CDSL step, workload {wl}", ""]
+    if args.commands:
+        out += ["Commands (run from the repository root on one MI355X):", "", "```"]
+        out += [ln.rstrip() for ln in open(args.commands) if ln.strip()]
+        out += ["```", ""]
+    out += [f"Bench line of the traced run: {b['ms_per_step']} ms/step, {b['value']} {b['unit']} "
+            f"(B={b['config']['batch']}, k={b['config']['k']}, d={b['config']['d']}).", "",
+            "## Kernel trace (--kernel-trace --stats), top kernels by total time", "",
+            "| kernel | calls | total ms | avg us | share |", "|---|---:|---:|---:|---:|"]
+    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"]))[:16]:
+        nm = r["Name"]
+        nm = nm.replace("cdsl::(anonymous namespace)::", "").replace("cdsl::", "")
+        nm = nm.split("(")[0] if not nm.startswith("_Z") else nm
+        out.append(f"| `{nm[:80]}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.2f} | "
+                   f"{float(r['AverageNs']) / 1e3:.2f} | {100 * float(r['TotalDurationNs']) / total:.1f}% |")
+    out += ["", "Calls include the prompt prefill (separately named `gemm_bf16_dense<..., 1>`) and the warmup, "
+            "timed and instrumented steps.", "",
+            "## HBM traffic (FETCH_SIZE and WRITE_SIZE passes)", "",
+            f"Calibration: a plain 256 MiB device copy (262144 KiB read, 262144 KiB written) reads "
+            f"FETCH_SIZE = {fcal:.1f} KiB and WRITE_SIZE = {wcal:.1f} KiB per dispatch, so the counters are "
+            f"scaled by {fs:.4f} (fetch) and {ws:.4f} (write).", "",
+            "| class | kernel | dispatches | FETCH KiB | WRITE KiB | HBM MB per launch (scaled) | "
+            "bench alg. MB per launch | rocprof avg us | bench avg us |",
+            "|---|---|---:|---:|---:|---:|---:|---:|---:|"]
+    recs = []
+    for cls, (pat, files) in CLASS_KERNEL.items():
+        rx = re.compile(pat)
+        fv = [float(r["Counter_Value"]) for r in fetch if rx.search(r["Kernel_Name"])]
+        wv = [float(r["Counter_Value"]) for r in write if rx.search(r["Kernel_Name"])]
+        tv = [r for r in stats if rx.search(r["Name"])]
+        if not fv or not wv or not tv:
+            continue
+        calls = sum(int(r["Calls"]) for r in tv)
+        avg_us = sum(float(r["TotalDurationNs"]) for r in tv) / calls / 1e3
+        f_kib, w_kib = sum(fv) / len(fv), sum(wv) / len(wv)
+        bpl = (f_kib * fs + w_kib * ws) * 1024.0
+        kb = b.get("kernels", {}).get(cls, {})
+        alg = b["roofline"].get("alg_bytes_per_launch") if b["roofline"].get("kernel") == cls else None
+        out.append(f"| {cls} | `{pat}` | {len(fv)} | {f_kib:.0f} | {w_kib:.0f} | {bpl / 1e6:.1f} | "
+                   f"{alg / 1e6 if alg else float('nan'):.1f} | {avg_us:.2f} | {kb.get('avg_launch_us', float('nan'))} |")
+        recs.append({"class": cls, "workload": wl, "source": source_digest(files),
+                     "file": os.path.basename(args.summary_out or "summary.md"),
+                     "fetch_kib_per_dispatch": round(f_kib, 1), "write_kib_per_dispatch": round(w_kib, 1),
+                     "fetch_scale": round(fs, 4), "write_scale": round(ws, 4),
+                     "bytes_per_launch": round(bpl), "rocprof_avg_us": round(avg_us, 2)})
+    out += ["", "The bench times each class with HIP events around its launches on the library stream; "
+            "its average per launch is expected to agree with the rocprofv3 average of the same kernel.", ""]
+    out += [TRAFFIC_TAG + json.dumps(r) + " -->" for r in recs]
+    text = "\n".join(out) + "\n"
+    if args.summary_out:
+        with open(args.summary_out, "w") as fh:
+            fh.write(text)
+    else:
+        sys.stdout.write(text)
 
 
 def class_table(stats, step_ms_total):
@@ -82,12 +216,11 @@ def class_table(stats, step_ms_total):
     return out
 
 
-def cpu_baseline(wl, dw, tw, prompt, kws, rw, k, d):
-    """The float64 oracle on one prompt: prefill (untimed), then the timed
-    sample = the full verification of the k*d block + the greedy rollout of
-    ONE beam (d draft forwards), scaled to a whole step as
-    t_verify + k * t_one_beam + t_reward_select_commit."""
-    import numpy as np
+def cpu_baseline(wl, dw, tw, prompt, kws, rw, k, d, min_s=10.0, max_steps=8):
+    """The float64 oracle on one prompt of the workload: prefill (untimed),
+    then whole CDSL steps (beam heads, rollout of all k beams, tree
+    verification, reward, selection, commit) until at least ``min_s`` seconds
+    of timed work; rate = k * d * steps / time."""
     import oracle
     threads = os.environ.get("OMP_NUM_THREADS") or str(os.cpu_count())
     od, ot = oracle.Decoder(wl.draft, dw), oracle.Decoder(wl.target, tw)
@@ -95,33 +228,26 @@ def cpu_baseline(wl, dw, tw, prompt, kws, rw, k, d):
     st = oracle.prefill(od, ot, prompt)
     t_prefill = time.perf_counter() - t0
     log(f"cpu baseline: oracle prefill {t_prefill:.1f}s")
-    heads, hlp, _ = oracle.beam_heads(st, k)
-    t0 = time.perf_counter()
-    ro = oracle.rollout(od, st, heads[:1], d)
-    t_beam = time.perf_counter() - t0
-    log(f"cpu baseline: one-beam rollout {t_beam:.1f}s")
-    x = np.concatenate([ro.x, np.tile(ro.x[:1], (k - 1, 1))]) if k > 1 else ro.x
-    t0 = time.perf_counter()
-    ve = oracle.verify(ot, st, heads, hlp, x)
-    t_ver = time.perf_counter() - t0
-    log(f"cpu baseline: verification {t_ver:.1f}s")
-    t0 = time.perf_counter()
-    r = oracle.reward_for(wl.reward, st.generated, heads, x, ve.hidden, kws, rw)
-    b = oracle.select_beam(ve.scores, r, wl.alpha)
-    emitted = [int(heads[b])] + [int(t) for t in x[b, :int(ve.n[b])]]
-    oracle.commit(od, ot, st, emitted)
-    t_tail = time.perf_counter() - t0
-    t_step = t_ver + k * t_beam + t_tail
-    return {"value": round(k * d / t_step, 4), "unit": "lookahead tokens verified/s", "cores": int(threads),
+    n, t_steps = 0, 0.0
+    while n < max_steps and t_steps < min_s:
+        t0 = time.perf_counter()
+        res = oracle.step(od, ot, st, k, d, wl.alpha, wl.reward, kws, rw)
+        t_steps += time.perf_counter() - t0
+        st = res.state
+        n += 1
+        log(f"cpu baseline: step {n} {t_steps:.1f}s")
+    return {"value": round(k * d * n / t_steps, 4), "unit": "lookahead tokens verified/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": (f"1 prompt x 1 step of workload '{wl.name}' in float64: verification of the "
-                       f"{k}x{d} block {t_ver:.1f}s + rollout of 1 beam {t_beam:.1f}s (x{k} beams) + "
-                       f"reward/select/commit {t_tail:.1f}s; prompt prefill {t_prefill:.1f}s untimed"),
-            "s_per_prompt_step": round(t_step, 3)}
+            "sample": (f"1 prompt of workload '{wl.name}' (prompt {len(prompt)} tokens, k={k}, d={d}) in float64: "
+                       f"{n} whole CDSL steps in {t_steps:.1f}s; prompt prefill {t_prefill:.1f}s untimed"),
+            "s_per_prompt_step": round(t_steps / n, 3)}
 
 
 def main():
     args = parse()
+    if args.summarize_profile:
+        summarize_profile(args)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path shards by prompt "
               "across GPUs with no exchange, but only the one-GPU step is built and timed)", file=sys.stderr)
@@ -182,7 +308,7 @@ def main():
     stats = eng.ctx.profile_read()
     prof_wall = (time.perf_counter() - t0) * 1e3
     eng.ctx.profile_enable(False)
-    dom, roof = roofline(stats)
+    dom, roof = roofline(stats, wl.name)
     kern_ms = sum(v["ms"] for v in stats.values())
     table = class_table(stats, kern_ms)
     log(json.dumps(table, indent=1))

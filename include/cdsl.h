@@ -204,7 +204,8 @@ enum {
   CDSL_K_ROWWISE = 5,      /* embedding, RMSNorm, rotary + KV write      */
   CDSL_K_STEP = 6,         /* scores, rewards, select, commit, promote   */
   CDSL_K_GEMM_F32 = 7,     /* fp32 projection                            */
-  CDSL_K_CLASSES = 8
+  CDSL_K_SPLITK_REDUCE = 8,/* sum of split-K partials + epilogue         */
+  CDSL_K_CLASSES = 9
 };
 typedef struct cdsl_kernel_stats {
   int64_t launches[CDSL_K_CLASSES];

@@ -45,12 +45,12 @@ class Model(C.Structure):
 
 
 KERNEL_CLASSES = ["gemm_dense", "gemm_skinny", "attention", "attn_combine", "logit_rows", "rowwise", "step",
-                  "gemm_f32"]
+                  "gemm_f32", "splitk_reduce"]
 
 
 class KernelStats(C.Structure):
-    _fields_ = [("launches", C.c_int64 * 8), ("ms", C.c_double * 8), ("flops", C.c_double * 8),
-                ("bytes", C.c_double * 8)]
+    _fields_ = [("launches", C.c_int64 * len(KERNEL_CLASSES)), ("ms", C.c_double * len(KERNEL_CLASSES)),
+                ("flops", C.c_double * len(KERNEL_CLASSES)), ("bytes", C.c_double * len(KERNEL_CLASSES))]
 
 
 class Limits(C.Structure):

@@ -37,9 +37,15 @@ size_t gemm_workspace_bytes(int M, int N, int K, int dtype);
 int gemm_check(int M, int N, int K, int dtype);
 // 0: dense bf16 kernel, 1: skinny bf16 kernel, 2: fp32 kernel
 int gemm_kind(int M, int N, int K, int dtype);
+// Called between the main kernel and the split-K reduce, when there is one
+// (lets the caller time the two kernels separately).
+struct GemmHook {
+  virtual void before_reduce(int ksplit) = 0;
+};
 // prefill selects a separately named instantiation of the dense kernel
 hipError_t gemm_launch(const GemmOperand& A, const void* B, const GemmOut& out, int M, int N, int K, int dtype,
-                       int epi, void* ws, size_t ws_bytes, hipStream_t st, bool prefill = false);
+                       int epi, void* ws, size_t ws_bytes, hipStream_t st, bool prefill = false,
+                       GemmHook* hook = nullptr);
 hipError_t swiglu_f32_launch(const float* gu, float* act, int M, int F, hipStream_t st);
 hipError_t split_planes_launch(const float* x, bf16* hi, bf16* lo, long long n, hipStream_t st);
 

@@ -599,7 +599,7 @@ int gemm_check(int M, int N, int K, int dtype) {
 }
 
 hipError_t gemm_launch(const GemmOperand& A, const void* B, const GemmOut& out, int M, int N, int K, int dtype,
-                       int epi, void* ws, size_t ws_bytes, hipStream_t st, bool prefill) {
+                       int epi, void* ws, size_t ws_bytes, hipStream_t st, bool prefill, GemmHook* hook) {
   if (M == 0) return hipSuccess;
   Plan p = make_plan(M, N, K, dtype);
   if (p.kind == 2) {
@@ -658,6 +658,7 @@ hipError_t gemm_launch(const GemmOperand& A, const void* B, const GemmOut& out, 
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.ksplit == 1) return e;
   const long long outs = epi == kEpiSwiGLU ? (long long)M * (N / 2) : (long long)M * N;
+  if (hook) hook->before_reduce(p.ksplit);
   splitk_reduce_kernel<<<(unsigned)((outs + 255) / 256), 256, 0, st>>>(a);
   return hipGetLastError();
 }

@@ -183,7 +183,8 @@ struct Span {
     c->acc.flops[cls] += flops;
     c->acc.bytes[cls] += bytes;
   }
-  ~Span() {
+  // records the end event now (idempotent)
+  void close() {
     if (!a) return;
     hipEvent_t b = nullptr;
     if (!c->ev_free.empty()) {
@@ -191,11 +192,14 @@ struct Span {
       c->ev_free.pop_back();
     } else if (hipEventCreate(&b) != hipSuccess) {
       c->ev_free.push_back(a);
+      a = nullptr;
       return;
     }
     (void)hipEventRecord(b, c->st);
     c->pend.push_back({a, b, cls});
+    a = nullptr;
   }
+  ~Span() { close(); }
 };
 
 bool cfg_ok(const cdsl_model_config& c, std::string& why) {
@@ -385,12 +389,36 @@ void alloc_workspace(cdsl_ctx* c) {
 void gemm(cdsl_ctx* c, const GemmOperand& A, const void* W, const GemmOut& out, int M, int N, int K, int epi,
           bool prefill) {
   const double wes = c->dtype == CDSL_BF16 ? 2.0 : 4.0;   // weight element size
+  // output bytes: fp32 store, fp32 read-modify-write, or the two bf16 planes
+  // of the half-width SwiGLU output
   const double outb = epi == kEpiSwiGLU ? (double)M * (N / 2) * 4.0
                                         : (double)M * N * 4.0 * (epi == kEpiResidual ? 2.0 : 1.0);
   const int kind = gemm_kind(M, N, K, c->dtype);
   const int cls = kind == 0 ? CDSL_K_GEMM_DENSE : kind == 1 ? CDSL_K_GEMM_SKINNY : CDSL_K_GEMM_F32;
+  // with split-K, the main kernel writes fp32 partial planes and the reduce
+  // kernel (timed as its own class) reads them and applies the epilogue
+  struct Hook : GemmHook {
+    cdsl_ctx* c = nullptr;
+    Span* main = nullptr;
+    double outb = 0.0, plane = 0.0;
+    Span* red = nullptr;
+    alignas(Span) unsigned char buf[sizeof(Span)];
+    void before_reduce(int ksplit) override {
+      main->close();
+      red = new (buf) Span(c, CDSL_K_SPLITK_REDUCE, 0.0, ksplit * plane + outb);
+    }
+    ~Hook() {
+      if (red) red->~Span();
+    }
+  };
   Span sp(c, cls, 2.0 * M * N * (double)K, (double)M * K * 4.0 + (double)N * K * wes + outb);
-  CK(gemm_launch(A, W, out, M, N, K, c->dtype, epi, c->ws.gemm_ws, c->ws.gemm_ws_bytes, c->st, prefill));
+  Hook hk;
+  hk.c = c;
+  hk.main = &sp;
+  hk.outb = outb;
+  hk.plane = (double)M * N * 4.0;
+  CK(gemm_launch(A, W, out, M, N, K, c->dtype, epi, c->ws.gemm_ws, c->ws.gemm_ws_bytes, c->st, prefill,
+                 c->prof ? &hk : nullptr));
 }
 
 // Forward pass of one model over the rows of p.  With want_logits, the
