@@ -59,7 +59,7 @@ enum { CDSL_F32 = 0, CDSL_BF16 = 1 };
 /* Shape of one Llama-style decoder: pre-norm RMSNorm, rotary embedding
  * (rotate-half pairing, 0-based positions), grouped-query attention,
  * SwiGLU MLP, no biases, untied LM head.  head_dim = d_model / n_heads and
- * must be 32, 64 or 128. */
+ * must be 32, 64 or 128 (64 or 128 for CDSL_BF16). */
 typedef struct cdsl_model_config {
   int32_t n_layers;
   int32_t d_model;
@@ -69,7 +69,9 @@ typedef struct cdsl_model_config {
   int32_t vocab;
   float rope_theta;
   float rms_eps;
-  int32_t dtype;      /* CDSL_F32 or CDSL_BF16: weights, activations, KV */
+  int32_t dtype;      /* CDSL_F32 or CDSL_BF16: the weight type.  Activations
+                         and KV values are fp32 either way (CDSL_BF16 keeps
+                         them as bf16 hi + lo pairs where MFMAs read them). */
 } cdsl_model_config;
 
 /* Weights of one decoder, device pointers in the dtype of cfg (norm gains

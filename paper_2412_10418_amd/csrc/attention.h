@@ -10,7 +10,7 @@ struct AttnArgs {
   float* O;               // [M][H][hd] fp32 output (fp32 models)
   bf16* Ohi;              // [M][H][hd] hi / lo planes (bf16-weight models)
   bf16* Olo;
-  KVPool pool;
+  KVPool pool;            // fp32 format (fp32 models) or split bf16 planes
   int layer;
   int H, Hkv, G;
   long long rows_total;   // M * H
@@ -19,6 +19,11 @@ struct AttnArgs {
   float* part_ml;         // [nsplit][M*H][2]  (running max in log2 units, sum)
   int nsplit, blocks_per_split;
 };
+
+// key blocks one workgroup (one key split) handles at most
+constexpr int kAttnMaxList = 256;
+// key splits of one pass at most
+constexpr int kAttnMaxSplits = 16;
 
 struct AttnPlan {
   int row_tiles, row_groups, threads;

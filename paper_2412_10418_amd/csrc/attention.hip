@@ -1,6 +1,6 @@
 // Attention of one decoder layer over the paged KV cache.
 //
-// Workgroup = (key split, prompt x KV head, group of 4 row tiles).  The
+// Workgroup = (key split, prompt x KV head, group of 32-row tiles).  The
 // query rows of one prompt and one KV head are ALL beams x all rows of the
 // beam x the G query heads sharing that KV head, so every shared-prefix KV
 // block is read once for all k beams (speculative lookaheads of every beam
@@ -9,19 +9,23 @@
 // slots 0..j0+j of beam i: the tree mask of the verification pass, and the
 // causal mask of one rollout step.
 //
-// Per wave: 16 query rows.  Scores are computed transposed,
-//   S^T[16 keys, 16 rows] = K[16, hd] . Q^T[hd, 16]      (MFMA 16x16x32)
-// so that lane (row r, group g) ends up holding P[r][keys 4g..4g+3] of two
-// consecutive blocks -- exactly the B fragment of
-//   O^T[hd, 16 rows] += V^T[hd, 32 keys] . P^T[32 keys, 16 rows]
-// with V stored transposed per block ([hd][16 tokens]): no shuffles or LDS
-// round trip between the two products.  Q, K, V and P are fp32, each MFMA
-// operand is split into bf16 hi + lo and a product takes three MFMAs
-// (hi*hi + hi*lo + lo*hi), keeping fp32-level accuracy.  Online softmax in
-// the log2 domain;
-// the row max / sum are reduced across the 4 lanes of a row with xor
-// shuffles.  Key splits write (m, l, unnormalised O) partials that a
-// combine kernel merges in split order (deterministic).
+// bf16-weight models (attn_split): the KV pool holds fp32 values as bf16
+// (hi, lo) planes.  The workgroup first lists the key blocks its rows can
+// see, then streams them in pairs (32 keys) through double-buffered LDS,
+// the next pair's global loads in flight while the current pair is
+// computed.  Per wave: 32 query rows.  Scores are computed transposed,
+//   S^T[32 keys, 32 rows] = K[32, hd] . Q^T[hd, 32]      (MFMA 32x32x16)
+// so that lane (row c, half g) holds P[c][keys 8q + 4g + e] -- exactly the
+// B fragment of
+//   O^T[hd, 32 rows] += V^T[hd, 32 keys] . P^T[32 keys, 32 rows]
+// once V's slots within a block are stored in that key order: no shuffles
+// or LDS round trip between the two products.  Every product takes three
+// MFMAs (hi*hi + hi*lo + lo*hi), keeping fp32-level accuracy.  Online
+// softmax in the log2 domain; the row max / sum combine the two lanes of a
+// row with one xor shuffle.  Key splits write (m, l, unnormalised O)
+// partials that a combine kernel merges in split order (deterministic).
+#include <algorithm>
+
 #include "attention.h"
 #include "common.h"
 
@@ -89,157 +93,281 @@ __device__ __forceinline__ f32x4 mfma3(const bf16x8& ah, const bf16x8& al, const
   return c;
 }
 
+// The beams, prefix-key limit and suffix-slot limit that rows [ra, rb] of a
+// (prompt, KV head) can see.  Rows of one beam have increasing j, so the
+// largest j of the range is that of rb unless the range crosses a beam.
+struct Window {
+  int i_lo, i_hi, key_lim, slot_lim;
+};
+
+__device__ __forceinline__ Window row_window(const PassDesc& p, int ra, int rb, int G, int Lp) {
+  const int t_lo = ra / G, t_hi = rb / G;
+  const int jmax = (t_lo / p.R == t_hi / p.R) ? t_hi % p.R : p.R - 1;
+  Window w;
+  w.i_lo = t_lo / p.R;
+  w.i_hi = t_hi / p.R;
+  w.key_lim = p.mode == kSuffix ? Lp : Lp + jmax + 1;
+  w.slot_lim = p.j0 + jmax;
+  return w;
+}
+
+__device__ __forceinline__ bool window_sees(const Window& w, int owner, int base) {
+  if (owner < 0) return base < w.key_lim;
+  return owner >= w.i_lo && owner <= w.i_hi && base <= w.slot_lim;
+}
+
 template <int HD>
-__global__ __launch_bounds__(256) void attn_mfma(AttnArgs a) {
-  constexpr int KS = HD / 32;   // k-steps of the score product
-  constexpr int DT = HD / 16;   // output tiles of 16 dims
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_split(AttnArgs a) {
+  constexpr int NT = 256;                      // 4 waves x 16 rows
+  constexpr int KCH = HD / 8;                  // 16-byte chunks per K row
+  constexpr int KPL = 2 * kBlock * HD;         // LDS K plane: 2 blocks x 16 keys x HD
+  constexpr int VPL = 2 * HD * kBlock;         // LDS V plane: HD x (4 groups x (4 keys of A, 4 of B))
+  constexpr int BUF = 2 * KPL + 2 * VPL;       // K hi, K lo, V hi, V lo
+  constexpr int UNIT = 2 * kBlock * HD;        // pool unit (both planes), bf16
+  constexpr int UCH = UNIT / 8;                // 16-byte chunks per unit
+  constexpr int PER = 4 * UCH / NT;            // chunks per thread per pair
+  constexpr int KS = HD / 32;                  // k-steps of the score product
+  constexpr int DT = HD / 16;                  // 16-dim output tiles
+  static_assert(UCH % NT == 0, "static chunk regions");
+  __shared__ __attribute__((aligned(16))) bf16 lds[2][BUF];
+  __shared__ int lblk[kAttnMaxList];
+  __shared__ int lmeta[kAttnMaxList];   // base * 32 + owner + 1
+  __shared__ int lcount;
+
   const PassDesc& p = a.p;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int split = blockIdx.x;
   const int bi = blockIdx.y / a.Hkv, kvh = blockIdx.y % a.Hkv;
   const int b = pass_batch(p, bi);
   const int G = a.G;
   const int nrows = p.kp * p.R * G;
-  const int r0 = (blockIdx.z * 4 + wave) * 16;
-  if (r0 >= nrows) return;
+  const int wg_r0 = blockIdx.z * 64;
+  if (wg_r0 >= nrows) return;   // uniform over the workgroup
   const int Lp = p.Lp[b];
 
-  const RowInfo ri = decode_row(p, r0 + lr, nrows, bi, kvh, G, Lp);
-
-  // key blocks of this prompt and this split
   const int nS = p.mode == kSuffix ? (p.j0 + p.R + kBlock - 1) / kBlock : 0;
   const int nP = p.mode == kSuffix ? (Lp + kBlock - 1) / kBlock : (Lp + p.R + kBlock - 1) / kBlock;
   const int nK = nP + p.kp * nS;
   const int qbeg = split * a.blocks_per_split;
-  const int qend = min(nK, qbeg + a.blocks_per_split);
+  // the host keeps blocks_per_split <= kAttnMaxList; the clamp only guards LDS
+  const int qend = min(min(nK, qbeg + a.blocks_per_split), qbeg + kAttnMaxList);
 
-  // wave-uniform relevance: beams and positions covered by this wave's rows
-  const int rlast = min(r0 + 15, nrows - 1);
-  const int t_lo = r0 / G, t_hi = rlast / G;
-  const int i_lo = t_lo / p.R, i_hi = t_hi / p.R;
-  int jmax = 0;
-  for (int t = t_lo; t <= t_hi; ++t) jmax = max(jmax, t % p.R);
-  const int key_lim = p.mode == kSuffix ? Lp : Lp + jmax + 1;       // prefix keys < key_lim
-  const int slot_lim = p.j0 + jmax;                                 // suffix slots <= slot_lim
-  auto relevant = [&](int q) -> bool {
-    if (q < nP) return q * kBlock < key_lim;
-    int qq = q - nP;
-    int owner = qq / nS, sub = qq % nS;
-    return owner >= i_lo && owner <= i_hi && sub * kBlock <= slot_lim;
-  };
-  auto next_rel = [&](int q) -> int {
-    while (q < qend && !relevant(q)) ++q;
-    return q;
-  };
+  // this wave's rows (a wave past the last row still stages key blocks)
+  const int rw0 = wg_r0 + wave * 16;
+  const bool wave_has_rows = rw0 < nrows;
+  const RowInfo ri = decode_row(p, rw0 + lr, nrows, bi, kvh, G, Lp);
+  const Window wwin = row_window(p, min(rw0, nrows - 1), min(rw0 + 15, nrows - 1), G, Lp);
 
-  // Q^T fragments (B operand): row lr, dims 32s + 8lg .. +8, as hi/lo
-  bf16x8 qh[KS], ql[KS];
-  {
-    const float* qrow = a.Q + ((long long)ri.m * a.H + ri.h) * HD + lg * 8;
+  // Q^T fragments (B operand): row lr, dims 32s + 8lg .. +8, as hi / lo;
+  // issued before the key-block list so the two latencies overlap
+  float4 qx[KS][2];
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
-      if (ri.valid) {
-        x0 = *(const float4*)(qrow + s * 32);
-        x1 = *(const float4*)(qrow + s * 32 + 4);
-      }
-      split8(x0, x1, qh[s], ql[s]);
+  for (int s = 0; s < KS; ++s) {
+    qx[s][0] = qx[s][1] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (ri.valid) {
+      const float* qrow = a.Q + ((long long)ri.m * a.H + ri.h) * HD + s * 32 + lg * 8;
+      qx[s][0] = *(const float4*)qrow;
+      qx[s][1] = *(const float4*)(qrow + 4);
     }
   }
 
-  const float* kbase = (const float*)a.pool.k + (long long)a.layer * a.pool.layer_elems;
-  const float* vbase = (const float*)a.pool.v + (long long)a.layer * a.pool.layer_elems;
+  // list of the key blocks that some row of the workgroup can see
+  if (wave == 0) {
+    const Window ww = row_window(p, wg_r0, min(wg_r0 + 64, nrows) - 1, G, Lp);
+    int n = 0;
+    for (int c0 = qbeg; c0 < qend; c0 += 64) {
+      const int q = c0 + lane;
+      int owner = -1, base = 0, blk = 0;
+      bool rel = false;
+      if (q < qend) {
+        blk = key_block(p, b, q, nP, nS, owner, base);
+        rel = window_sees(ww, owner, base);
+      }
+      const unsigned long long m = __ballot(rel);
+      const int pos = n + __popcll(m & ((1ull << lane) - 1ull));
+      if (rel) {
+        lblk[pos] = blk;
+        lmeta[pos] = base * 32 + owner + 1;
+      }
+      n += __popcll(m);
+    }
+    if (lane == 0) lcount = n;
+  }
+  __syncthreads();
+  const int n = lcount;
+  const int npairs = (n + 1) / 2;
+
+  bf16x8 qh[KS], ql[KS];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) split8(qx[s][0], qx[s][1], qh[s], ql[s]);
+
+  // staging: chunk q = tid + NT * u of a pair is region q / UCH (K of block
+  // A, K of block B, V of A, V of B) at 16-byte offset q % UCH of the unit.
+  // K rows are XOR-swizzled by 16-byte chunk (c ^ (row & 7)).  A V row of
+  // the pair (one dim, 64 bytes) holds, for key group g = 0..3, keys
+  // 4g..4g+3 of block A then of block B: the V^T fragment of one lane.
+  const bf16* kpool = (const bf16*)a.pool.k + (long long)a.layer * 2 * a.pool.layer_elems;
+  const bf16* vpool = (const bf16*)a.pool.v + (long long)a.layer * 2 * a.pool.layer_elems;
+  auto dst_of = [&](int u) __attribute__((always_inline)) {
+    const int region = (NT * u) / UCH, w = (tid + NT * u) % UCH;
+    const int plane = w / (UCH / 2), wp = w % (UCH / 2);
+    if (region < 2) {
+      const int row = region * kBlock + wp / KCH, c = wp % KCH;
+      return plane * KPL + row * HD + ((c ^ (row & 7)) << 3);
+    }
+    // 16-byte chunk wp = (dim, half h) holds keys 8h..8h+7 of one block
+    const int dim = wp >> 1, h = wp & 1;
+    return 2 * KPL + plane * VPL + dim * 32 + h * 16 + (region - 2) * 4;
+  };
+  // staging registers: pair pi + 1 is in flight while pair pi is computed
+  u32x4 stg[PER];
+  auto gload = [&](u32x4* r, int pi) __attribute__((always_inline)) {
+    const int eA = min(2 * pi, n - 1);
+    const int eB = min(2 * pi + 1, n - 1);
+    const long long ua = ((long long)lblk[eA] * a.Hkv + kvh) * UNIT;
+    const long long ub = ((long long)lblk[eB] * a.Hkv + kvh) * UNIT;
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int region = (NT * u) / UCH;   // exact: tid < NT <= UCH
+      const bf16* base = (region < 2 ? kpool : vpool) + ((region & 1) ? ub : ua);
+      r[u] = *(const u32x4*)(base + ((tid + NT * u) % UCH) * 8);
+    }
+  };
+  auto sstore = [&](const u32x4* r, int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int region = (NT * u) / UCH;
+      bf16* d = &lds[buf][dst_of(u)];
+      if (region < 2) {
+        *(u32x4*)d = r[u];
+      } else {
+        // keys 8h..8h+3 -> group 2h, keys 8h+4..8h+7 -> group 2h + 1
+        *(uint2*)d = make_uint2(r[u].x, r[u].y);
+        *(uint2*)(d + 8) = make_uint2(r[u].z, r[u].w);
+      }
+    }
+  };
 
   f32x4 acc[DT];
 #pragma unroll
   for (int t = 0; t < DT; ++t) acc[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+  // Running max m_run (log2 units) and sum l_run of this lane's row.  The
+  // exponentials use a possibly stale max: it is only raised (and O, l
+  // rescaled) once the true max exceeds it by more than kLazy, so
+  // probabilities stay below 2^kLazy and the rescale is rare.  O / l does
+  // not depend on which max was used.
+  constexpr float kLazy = 8.f;
   float m_run = -INFINITY, l_run = 0.f;
+  // Visibility of a key at absolute slot x of a block of owner o to this
+  // lane's row: x <= lim_pre for prefix blocks (o < 0), x <= lim_own for
+  // the suffix blocks of the row's own beam, never for other beams.
+  const int lim_pre = !ri.valid ? -1 : (p.mode == kSuffix ? Lp - 1 : ri.pos);
+  const int lim_own = ri.valid ? p.j0 + ri.j : -1;
+  auto limit = [&](int owner, int base) __attribute__((always_inline)) {
+    return (owner < 0 ? lim_pre : (owner == ri.i ? lim_own : -1)) - base;
+  };
 
-  int q = next_rel(qbeg);
-  while (q < qend) {
-    const int qa = q;
-    const int qb = next_rel(qa + 1);
-    q = qb < qend ? next_rel(qb + 1) : qend;
-    const bool hasB = qb < qend;
-
-    int ownA, baseA, ownB = -2, baseB = 0;
-    const int blkA = key_block(p, b, qa, nP, nS, ownA, baseA);
-    const int blkB = hasB ? key_block(p, b, qb, nP, nS, ownB, baseB) : 0;
-
-    // scores of the two blocks
-    f32x4 sA = {0.f, 0.f, 0.f, 0.f}, sB = {0.f, 0.f, 0.f, 0.f};
-    {
-      const float* kA = kbase + ((long long)blkA * a.Hkv + kvh) * (kBlock * HD) + lr * HD + lg * 8;
+  // One pair of key blocks (A, B) from LDS buffer buf.  Scores transposed:
+  // S^T[16 keys, 16 rows] = K . Q^T per block, so lane (row lr, group lg)
+  // holds keys 4lg..4lg+3 of A and of B -- which, in that order, is the
+  // lane's B fragment of O^T[16 dims, 16 rows] += V^T[16 dims, 32 keys] .
+  // P^T[32 keys, 16 rows] when the V^T fragment takes the same keys.
+  auto compute = [&](int buf, int pi) __attribute__((always_inline)) {
+    const int eA = 2 * pi, eB = 2 * pi + 1;
+    const bool hasB = eB < n;
+    const int mA = lmeta[eA], mB = hasB ? lmeta[eB] : 0;
+    const int ownA = (mA & 31) - 1, baseA = mA >> 5;
+    const int ownB = (mB & 31) - 1, baseB = mB >> 5;
+    const bool relA = window_sees(wwin, ownA, baseA);
+    const bool relB = hasB && window_sees(wwin, ownB, baseB);
+    if (!wave_has_rows || (!relA && !relB)) return;
+    const bf16* L = lds[buf];
+    f32x4 sA = {0.f, 0.f, 0.f, 0.f}, sB = sA;
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        bf16x8 kh, kl;
-        split8(*(const float4*)(kA + s * 32), *(const float4*)(kA + s * 32 + 4), kh, kl);
-        sA = mfma3(kh, kl, qh[s], ql[s], sA);
-      }
-      if (hasB) {
-        const float* kB = kbase + ((long long)blkB * a.Hkv + kvh) * (kBlock * HD) + lr * HD + lg * 8;
-#pragma unroll
-        for (int s = 0; s < KS; ++s) {
-          bf16x8 kh, kl;
-          split8(*(const float4*)(kB + s * 32), *(const float4*)(kB + s * 32 + 4), kh, kl);
-          sB = mfma3(kh, kl, qh[s], ql[s], sB);
-        }
-      }
+    for (int s = 0; s < KS; ++s) {
+      const int rowA = lr, rowB = kBlock + lr;
+      const int offA = rowA * HD + (((4 * s + lg) ^ (rowA & 7)) << 3);
+      const int offB = rowB * HD + (((4 * s + lg) ^ (rowB & 7)) << 3);
+      const bf16x8 kah = *(const bf16x8*)(L + offA), kal = *(const bf16x8*)(L + KPL + offA);
+      const bf16x8 kbh = *(const bf16x8*)(L + offB), kbl = *(const bf16x8*)(L + KPL + offB);
+      sA = mfma3(kah, kal, qh[s], ql[s], sA);
+      sB = mfma3(kbh, kbl, qh[s], ql[s], sB);
     }
+    const int tA = limit(ownA, baseA) - 4 * lg;
+    const int tB = (hasB ? limit(ownB, baseB) : -1) - 4 * lg;
     float sv[8];
     float mt = -INFINITY;
+    if (__all(tA >= 3 && tB >= 3)) {   // every key of both blocks visible
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int t = lg * 4 + e;
-      sv[e] = key_valid(p, ownA, baseA + t, ri, Lp) ? sA[e] * a.scale_log2 : -INFINITY;
-      sv[4 + e] = (hasB && key_valid(p, ownB, baseB + t, ri, Lp)) ? sB[e] * a.scale_log2 : -INFINITY;
+      for (int e = 0; e < 4; ++e) {
+        sv[e] = sA[e] * a.scale_log2;
+        sv[4 + e] = sB[e] * a.scale_log2;
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        sv[e] = e <= tA ? sA[e] * a.scale_log2 : -INFINITY;
+        sv[4 + e] = e <= tB ? sB[e] * a.scale_log2 : -INFINITY;
+      }
     }
 #pragma unroll
     for (int e = 0; e < 8; ++e) mt = fmaxf(mt, sv[e]);
     mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float m_new = fmaxf(m_run, mt);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float corr = exp2f(m_run - m_use);
+    const bool raise = mt > m_run + kLazy;   // true for the first visible key
+    if (__ballot(raise)) {
+      const float m_to = raise ? mt : m_run;
+      const float corr = m_to == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_to);
+      l_run *= corr;
+#pragma unroll
+      for (int t = 0; t < DT; ++t) acc[t] *= corr;
+      m_run = m_to;
+    }
+    const float m_use = m_run == -INFINITY ? 0.f : m_run;
     float psum = 0.f;
-    float pv[8];
+    bf16x8 ph, pl;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      pv[e] = exp2f(sv[e] - m_use);
-      psum += pv[e];
+      const float pv = __builtin_amdgcn_exp2f(sv[e] - m_use);
+      psum += pv;
+      const bf16 h = (bf16)pv;
+      ph[e] = h;
+      pl[e] = (bf16)(pv - (float)h);
     }
-    bf16x8 ph, pl;
-    split8(make_float4(pv[0], pv[1], pv[2], pv[3]), make_float4(pv[4], pv[5], pv[6], pv[7]), ph, pl);
-    l_run = l_run * corr + psum;
-    m_run = m_new;
+    l_run += psum;
+    // V^T fragment: dim 16t + lr, keys 4lg..4lg+3 of A then of B
 #pragma unroll
     for (int t = 0; t < DT; ++t) {
-      acc[t][0] *= corr;
-      acc[t][1] *= corr;
-      acc[t][2] *= corr;
-      acc[t][3] *= corr;
-    }
-    // O^T += V^T . P^T
-    const float* vA = vbase + ((long long)blkA * a.Hkv + kvh) * (HD * kBlock) + lr * kBlock + lg * 4;
-    const float* vB = vbase + ((long long)blkB * a.Hkv + kvh) * (HD * kBlock) + lr * kBlock + lg * 4;
-#pragma unroll
-    for (int t = 0; t < DT; ++t) {
-      const float4 va = *(const float4*)(vA + t * 16 * kBlock);
-      const float4 vb = hasB ? *(const float4*)(vB + t * 16 * kBlock) : make_float4(0.f, 0.f, 0.f, 0.f);
-      bf16x8 vh, vl;
-      split8(va, vb, vh, vl);
+      const int voff = 2 * KPL + (t * 16 + lr) * 32 + lg * 8;
+      const bf16x8 vh = *(const bf16x8*)(L + voff), vl = *(const bf16x8*)(L + VPL + voff);
       acc[t] = mfma3(vh, vl, ph, pl, acc[t]);
     }
+  };
+
+  // pair pi sits in LDS buffer pi & 1
+  if (npairs > 0) {
+    gload(stg, 0);
+    sstore(stg, 0);
+    __syncthreads();
+  }
+  for (int pi = 0; pi < npairs; ++pi) {
+    const bool more = pi + 1 < npairs;
+    if (more) gload(stg, pi + 1);
+    compute(pi & 1, pi);
+    if (more) sstore(stg, (pi + 1) & 1);
+    __syncthreads();
   }
 
+  if (!wave_has_rows) return;
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
   if (!ri.valid) return;
   const long long rowid = (long long)ri.m * a.H + ri.h;
+  // lane (row lr, lg) holds dims 16t + 4lg .. +3
   if (a.nsplit == 1) {
     const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-    const long long o = rowid * HD + lg * 4;
 #pragma unroll
     for (int t = 0; t < DT; ++t) {
       bf16x4 hv, lv;
@@ -250,8 +378,9 @@ __global__ __launch_bounds__(256) void attn_mfma(AttnArgs a) {
         hv[e] = h;
         lv[e] = l;
       }
-      *(bf16x4*)(a.Ohi + o + t * 16) = hv;
-      *(bf16x4*)(a.Olo + o + t * 16) = lv;
+      const long long o = rowid * HD + t * 16 + lg * 4;
+      *(bf16x4*)(a.Ohi + o) = hv;
+      *(bf16x4*)(a.Olo + o) = lv;
     }
   } else {
     const long long prow = (long long)split * a.rows_total + rowid;
@@ -265,35 +394,48 @@ __global__ __launch_bounds__(256) void attn_mfma(AttnArgs a) {
   }
 }
 
-// Merge the split partials of every (row, head): one wave per row.
+// Merge the split partials of every (row, head): one wave per row.  Lane s
+// reads split s's (m, l); every partial O load is issued before the weights
+// exp2(m_s - max) are formed, so a row costs two memory round trips.
 template <int HD>
 __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
   const long long row = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= a.rows_total) return;
-  float mx = -INFINITY;
-  for (int s = 0; s < a.nsplit; ++s) mx = fmaxf(mx, a.part_ml[((long long)s * a.rows_total + row) * 2]);
-  const float mu = mx == -INFINITY ? 0.f : mx;
   constexpr int PER = (HD + 63) / 64;
-  float o[PER] = {};
-  float l = 0.f;
-  for (int s = 0; s < a.nsplit; ++s) {
-    const long long pr = (long long)s * a.rows_total + row;
-    const float w = exp2f(a.part_ml[pr * 2] - mu);
-    l += w * a.part_ml[pr * 2 + 1];
+  const int ns = a.nsplit;   // <= kAttnMaxSplits (the plan guarantees it)
+  float ms = -INFINITY, ls = 0.f;
+  if (lane < ns) {
+    const long long pr = (long long)lane * a.rows_total + row;
+    ms = a.part_ml[pr * 2];
+    ls = a.part_ml[pr * 2 + 1];
+  }
+  float o[kAttnMaxSplits][PER];
+#pragma unroll
+  for (int s = 0; s < kAttnMaxSplits; ++s)
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
-      int d = lane + 64 * u;
-      if (d < HD) o[u] += w * a.part_o[pr * HD + d];
+      const int d = lane + 64 * u;
+      o[s][u] = (s < ns && d < HD) ? a.part_o[((long long)s * a.rows_total + row) * HD + d] : 0.f;
     }
+  const float mx = wave_max(ms);
+  const float mu = mx == -INFINITY ? 0.f : mx;
+  const float ws = lane < ns ? exp2f(ms - mu) : 0.f;
+  const float l = wave_sum(ws * ls);
+  float acc[PER] = {};
+#pragma unroll
+  for (int s = 0; s < kAttnMaxSplits; ++s) {
+    const float w = __shfl(ws, s, 64);
+#pragma unroll
+    for (int u = 0; u < PER; ++u) acc[u] = fmaf(w, o[s][u], acc[u]);
   }
   const float inv = l > 0.f ? 1.f / l : 0.f;
 #pragma unroll
   for (int u = 0; u < PER; ++u) {
-    int d = lane + 64 * u;
+    const int d = lane + 64 * u;
     if (d < HD) {
       bf16 h, lo;
-      split_bf16(o[u] * inv, h, lo);
+      split_bf16(acc[u] * inv, h, lo);
       a.Ohi[row * HD + d] = h;
       a.Olo[row * HD + d] = lo;
     }
@@ -383,9 +525,6 @@ AttnPlan attn_plan(const PassDesc& p, int H, int Hkv, int hd, int dtype, int max
   AttnPlan pl{};
   const int G = H / Hkv;
   const int nrows = p.kp * p.R * G;
-  pl.row_tiles = (nrows + 15) / 16;
-  pl.row_groups = (pl.row_tiles + 3) / 4;
-  pl.threads = 64 * (pl.row_tiles < 4 ? pl.row_tiles : 4);
   const int nS = p.mode == kSuffix ? (p.j0 + p.R + kBlock - 1) / kBlock : 0;
   const int nP = p.mode == kSuffix ? (max_prefix_len + kBlock - 1) / kBlock
                                    : (max_prefix_len + p.R + kBlock - 1) / kBlock;
@@ -395,17 +534,22 @@ AttnPlan attn_plan(const PassDesc& p, int H, int Hkv, int hd, int dtype, int max
     pl.blocks_per_split = nK;
     return pl;
   }
-  // enough workgroups to cover the CUs several times, >= 2 blocks per split
+  // 16-row tiles, 4 waves per workgroup (a wave without rows still stages
+  // its share of the key blocks)
+  pl.row_tiles = (nrows + 15) / 16;
+  pl.threads = 256;
+  pl.row_groups = (pl.row_tiles + 3) / 4;
+  // enough workgroups for two per CU, >= 1 key-block pair per split, and at
+  // most kAttnMaxList key blocks per split; no split (and no combine) when
+  // the grid already holds two workgroups per CU
   const int base = p.nb * Hkv * pl.row_groups;
-  int want = (1024 + base - 1) / base;
-  int maxs = (nK + 1) / 2;
-  int s = want < maxs ? want : maxs;
-  if (s > max_splits) s = max_splits;
-  if (s < 1) s = 1;
+  int s = base >= 512 ? 1 : (1024 + base - 1) / base;
+  s = std::min(s, (nK + 1) / 2);
+  s = std::max(s, (nK + kAttnMaxList - 1) / kAttnMaxList);
+  s = std::max(1, std::min(s, std::min(max_splits, kAttnMaxSplits)));
   int bps = (nK + s - 1) / s;
   bps += bps & 1;
-  s = (nK + bps - 1) / bps;
-  if (s < 1) s = 1;
+  s = std::max(1, (nK + bps - 1) / bps);
   pl.nsplit = s;
   pl.blocks_per_split = bps;
   return pl;
@@ -426,11 +570,11 @@ hipError_t attn_launch(const AttnArgs& args, const AttnPlan& pl, int hd, int dty
     }
     return hipGetLastError();
   }
+  if (pl.blocks_per_split > kAttnMaxList) return hipErrorInvalidValue;
   dim3 grid(pl.nsplit, a.p.nb * a.Hkv, pl.row_groups);
   switch (hd) {
-    case 32: attn_mfma<32><<<grid, pl.threads, 0, st>>>(a); break;
-    case 64: attn_mfma<64><<<grid, pl.threads, 0, st>>>(a); break;
-    case 128: attn_mfma<128><<<grid, pl.threads, 0, st>>>(a); break;
+    case 64: attn_split<64><<<grid, 256, 0, st>>>(a); break;
+    case 128: attn_split<128><<<grid, 256, 0, st>>>(a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

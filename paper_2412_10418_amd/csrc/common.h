@@ -65,6 +65,13 @@ struct KVPool {
   int Hkv, hd;
 };
 
+// KV pool format of bf16-weight models.  A unit (layer, block, KV head) has
+// the byte size of the fp32 unit (16 * hd * 4 bytes) and holds each fp32
+// value as a bf16 (hi, lo) pair, plane by plane:
+//   K unit: [hi | lo][16 tokens][hd]
+//   V unit: [hi | lo][hd][16 tokens]
+__host__ __device__ inline long long split_unit_elems(int hd) { return 2LL * kBlock * hd; }
+
 template <typename T>
 __device__ __forceinline__ float to_f32(T x);
 template <>

@@ -136,6 +136,69 @@ __global__ __launch_bounds__(256) void rope_kv_write(PassDesc p, const float* __
   }
 }
 
+// Same for bf16-weight models, whose KV pool holds each fp32 value as a
+// bf16 (hi, lo) pair in the split unit format (K [plane][16][hd], V
+// [plane][hd][16]).  q stays fp32.
+__global__ __launch_bounds__(256) void rope_kv_write_split(PassDesc p, const float* __restrict__ qkv,
+                                                           float* __restrict__ qout, KVPool pool, int layer,
+                                                           const float* __restrict__ cos_t,
+                                                           const float* __restrict__ sin_t, int H, int Hkv, int hd) {
+  const int m = blockIdx.x;
+  int bi, b, i, j;
+  row_decode(p, m, bi, b, i, j);
+  const int Lp = p.Lp[b];
+  int pos, blk, slot;
+  if (p.mode == kSuffix) {
+    const int s = p.j0 + j;
+    pos = Lp + s;
+    blk = p.stable[(long long)b * p.s_stride_b + i * p.s_stride_i + s / kBlock];
+    slot = s % kBlock;
+  } else {
+    pos = Lp + j;
+    blk = p.ptable[(long long)b * p.ptable_stride + pos / kBlock];
+    slot = pos % kBlock;
+  }
+  const int half = hd / 2;
+  const long long unit = split_unit_elems(hd);
+  const long long plane = (long long)kBlock * hd;
+  const float* row = qkv + (long long)m * (H + 2 * Hkv) * hd;
+  const float* ct = cos_t + (long long)pos * half;
+  const float* stt = sin_t + (long long)pos * half;
+  bf16* kb = (bf16*)pool.k + (long long)layer * 2 * pool.layer_elems + (long long)blk * Hkv * unit;
+  bf16* vb = (bf16*)pool.v + (long long)layer * 2 * pool.layer_elems + (long long)blk * Hkv * unit;
+  const int npairs = (H + Hkv) * half;
+  for (int u = threadIdx.x; u < npairs; u += 256) {
+    const int hh = u / half, d = u % half;
+    const float x1 = row[hh * hd + d], x2 = row[hh * hd + d + half];
+    const float c = ct[d], s = stt[d];
+    const float y1 = x1 * c - x2 * s, y2 = x2 * c + x1 * s;
+    if (hh < H) {
+      float* q = qout + ((long long)m * H + hh) * hd;
+      q[d] = y1;
+      q[d + half] = y2;
+    } else {
+      bf16* kr = kb + (long long)(hh - H) * unit + (long long)slot * hd;
+      bf16 h, l;
+      split_bf16(y1, h, l);
+      kr[d] = h;
+      kr[plane + d] = l;
+      split_bf16(y2, h, l);
+      kr[d + half] = h;
+      kr[plane + d + half] = l;
+    }
+  }
+  const float* vrow = row + (long long)(H + Hkv) * hd;
+  const int vs = slot;
+  for (int u = threadIdx.x; u < Hkv * hd; u += 256) {
+    const int hh = u / hd, d = u % hd;
+    bf16* vr = vb + (long long)hh * unit + (long long)d * kBlock + vs;
+    bf16 h, l;
+    split_bf16(vrow[u], h, l);
+    vr[0] = h;
+    vr[plane] = l;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Logits row statistics, one workgroup per row, one read of the row:
 // online logsumexp, argmax, thread-local top-KK lists merged by KK rounds of
@@ -455,6 +518,45 @@ __global__ __launch_bounds__(256) void promote_kernel(int k, KVPool pool, int n_
   }
 }
 
+// promote_kernel for the split bf16 pool format
+__global__ __launch_bounds__(256) void promote_split_kernel(int k, KVPool pool, int n_layers,
+                                                            const int* __restrict__ stage, int stage_stride, int dlim,
+                                                            const int* __restrict__ Lp, const int* __restrict__ ptable,
+                                                            int ptable_stride, const int* __restrict__ stable,
+                                                            int s_stride_b, int s_stride_i) {
+  const int b = blockIdx.x;
+  const int layer = blockIdx.y;
+  const int* st = stage + (long long)b * stage_stride;
+  const int ne = st[0];
+  if (ne <= 0) return;
+  const int cnt = min(ne, dlim);
+  const int i = st[2];
+  const int L0 = Lp[b];
+  const int hd = pool.hd, Hkv = pool.Hkv;
+  const long long unit = split_unit_elems(hd);
+  const long long plane = (long long)kBlock * hd;
+  bf16* kl = (bf16*)pool.k + (long long)layer * 2 * pool.layer_elems;
+  bf16* vl = (bf16*)pool.v + (long long)layer * 2 * pool.layer_elems;
+  const int per_tok = Hkv * hd;
+  for (int u = threadIdx.x; u < cnt * per_tok; u += 256) {
+    const int t = u / per_tok, rem = u % per_tok;
+    const int hh = rem / hd, dd = rem % hd;
+    const int sblk = stable[(long long)b * s_stride_b + i * s_stride_i + t / kBlock];
+    const int sslot = t % kBlock;
+    const int pos = L0 + t;
+    const int pblk = ptable[(long long)b * ptable_stride + pos / kBlock];
+    const int pslot = pos % kBlock;
+    const bf16* ks = kl + ((long long)sblk * Hkv + hh) * unit + (long long)sslot * hd + dd;
+    bf16* kd = kl + ((long long)pblk * Hkv + hh) * unit + (long long)pslot * hd + dd;
+    kd[0] = ks[0];
+    kd[plane] = ks[plane];
+    const bf16* vs = vl + ((long long)sblk * Hkv + hh) * unit + (long long)dd * kBlock + sslot;
+    bf16* vd = vl + ((long long)pblk * Hkv + hh) * unit + (long long)dd * kBlock + pslot;
+    vd[0] = vs[0];
+    vd[plane] = vs[plane];
+  }
+}
+
 __global__ void advance_kernel(int B, const int* __restrict__ stage, int stage_stride, int dlim,
                                int* __restrict__ Lp) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
@@ -500,8 +602,11 @@ hipError_t rope_kv_launch(const PassDesc& p, const float* qkv, void* qout, const
                           const float* cos_t, const float* sin_t, int H, int Hkv, int hd, int dtype, hipStream_t st) {
   const int M = p.M();
   if (M == 0) return hipSuccess;
-  (void)dtype;   // q and the KV cache are fp32 for every weight dtype
-  rope_kv_write<float><<<M, 256, 0, st>>>(p, qkv, (float*)qout, pool, layer, cos_t, sin_t, H, Hkv, hd);
+  // q is fp32 for every weight dtype; the KV pool is fp32 or split bf16
+  if (dtype == 1)
+    rope_kv_write_split<<<M, 256, 0, st>>>(p, qkv, (float*)qout, pool, layer, cos_t, sin_t, H, Hkv, hd);
+  else
+    rope_kv_write<float><<<M, 256, 0, st>>>(p, qkv, (float*)qout, pool, layer, cos_t, sin_t, H, Hkv, hd);
   return hipGetLastError();
 }
 
@@ -555,9 +660,12 @@ hipError_t promote_launch(int B, int k, const KVPool& pool, int n_layers, const 
                           const int* Lp, const int* ptable, int ptable_stride, const int* stable, int s_stride_b,
                           int s_stride_i, int dtype, hipStream_t st) {
   dim3 grid(B, n_layers);
-  (void)dtype;
-  promote_kernel<float><<<grid, 256, 0, st>>>(k, pool, n_layers, stage, stage_stride, dlim, Lp, ptable,
-                                              ptable_stride, stable, s_stride_b, s_stride_i);
+  if (dtype == 1)
+    promote_split_kernel<<<grid, 256, 0, st>>>(k, pool, n_layers, stage, stage_stride, dlim, Lp, ptable,
+                                                ptable_stride, stable, s_stride_b, s_stride_i);
+  else
+    promote_kernel<float><<<grid, 256, 0, st>>>(k, pool, n_layers, stage, stage_stride, dlim, Lp, ptable,
+                                                ptable_stride, stable, s_stride_b, s_stride_i);
   return hipGetLastError();
 }
 

@@ -21,7 +21,7 @@ using namespace cdsl;
 
 namespace {
 
-constexpr int kMaxSplits = 16;
+constexpr int kMaxSplits = kAttnMaxSplits;
 
 struct Fail {
   int code;
@@ -214,6 +214,10 @@ bool cfg_ok(const cdsl_model_config& c, std::string& why) {
   int hd = c.d_model / c.n_heads;
   if (hd != 32 && hd != 64 && hd != 128) {
     why = "head_dim must be 32, 64 or 128";
+    return false;
+  }
+  if (c.dtype == CDSL_BF16 && hd == 32) {
+    why = "bf16 models need head_dim 64 or 128";
     return false;
   }
   if (c.dtype != CDSL_F32 && c.dtype != CDSL_BF16) {
