@@ -42,10 +42,15 @@ int gemm_kind(int M, int N, int K, int dtype);
 struct GemmHook {
   virtual void before_reduce(int ksplit) = 0;
 };
-// prefill selects a separately named instantiation of the dense kernel
+// prefill selects a separately named instantiation of the dense kernel.
+// With deferred != null, a K split is left unreduced: the ksplit fp32
+// planes [ksplit][M][N] stay at the start of ws for the caller to consume
+// (before the next projection), the epilogue is not applied, and *deferred
+// receives ksplit (1: no split, the epilogue was applied as usual).
+// kEpiSwiGLU is never deferred.
 hipError_t gemm_launch(const GemmOperand& A, const void* B, const GemmOut& out, int M, int N, int K, int dtype,
                        int epi, void* ws, size_t ws_bytes, hipStream_t st, bool prefill = false,
-                       GemmHook* hook = nullptr);
+                       GemmHook* hook = nullptr, int* deferred = nullptr);
 hipError_t swiglu_f32_launch(const float* gu, float* act, int M, int F, hipStream_t st);
 hipError_t split_planes_launch(const float* x, bf16* hi, bf16* lo, long long n, hipStream_t st);
 

@@ -26,6 +26,7 @@
 #include <stdlib.h>
 
 #include <type_traits>
+#include <utility>
 
 #include "common.h"
 #include "gemm.h"
@@ -304,141 +305,194 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dense(GemmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// skinny kernel: MT x 16 rows, 64 columns per workgroup (16 per wave)
+// skinny kernel: MT x 16 rows, CT x 16 columns per wave, 4 waves
+//
+// Weight streaming.  Each wave keeps RING K stages of its weight fragments in
+// flight in registers, straight from HBM (one 16-byte load per column tile
+// and k-step).  The activation stage (hi and lo planes, MT x 16 rows x 64 K)
+// goes through double-buffered LDS, XOR-swizzled like the dense kernel, and
+// each activation fragment feeds CT MFMA column tiles.  The main loop is
+// free of branches around memory operations: prefetches past the last stage
+// re-read it (L2 hits), so the compiler's in-order vmcnt accounting stays
+// exact and the ring is never drained early.
 // ---------------------------------------------------------------------------
 constexpr int SKC = 64;            // K per stage (2 MFMA k-steps)
-constexpr int SRING = 4;           // weight stages in flight per wave
-constexpr int SLD = SKC + kPad;
 
-template <int MT>
+template <int MT, int CT, int RING>
 __global__ __launch_bounds__(256) void gemm_bf16_skinny(GemmArgs a) {
   constexpr int BM = MT * 16;
-  constexpr int ACH = BM * (SKC / 8);            // 16-B chunks per plane per stage
+  constexpr int BN = 4 * CT * 16;                 // columns per workgroup
+  constexpr int ACH = BM * (SKC / 8);             // 16-B chunks per plane per stage
   constexpr int APT = 2 * ACH / 256;              // per thread (hi + lo) = MT
   static_assert(2 * ACH % 256 == 0, "whole chunks per thread");
-  __shared__ __attribute__((aligned(16))) bf16 Ah[2][BM][SLD];
-  __shared__ __attribute__((aligned(16))) bf16 Al[2][BM][SLD];
+  __shared__ __attribute__((aligned(16))) bf16 As[2][2][BM * SKC];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
-  const int tile = blockIdx.x;
-  const int n0 = tile * 64 + wave * 16;
+  const int n0 = blockIdx.x * BN + wave * CT * 16;
   const int kbeg = blockIdx.z * a.kchunk;
   const int kend = min(a.K, kbeg + a.kchunk);
   const int nst = (kend - kbeg) / SKC;
 
-  const bf16* bptr = a.B + (long long)min(n0 + lr, a.N - 1) * a.K + kbeg + lg * 8;
+  const bf16* bptr[CT];
+#pragma unroll
+  for (int j = 0; j < CT; ++j) bptr[j] = a.B + (long long)min(n0 + j * 16 + lr, a.N - 1) * a.K + kbeg + lg * 8;
 
-  bf16x8 ring[SRING][2];
-  u32x4 ar[APT];
+  bf16x8 ring[RING][CT][2];
   auto bload = [&](int c, auto slot_c) __attribute__((always_inline)) {
     constexpr int sl = decltype(slot_c)::value;
-    ring[sl][0] = *(const bf16x8*)(bptr + c * SKC);
-    ring[sl][1] = *(const bf16x8*)(bptr + c * SKC + 32);
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int j = 0; j < CT; ++j) ring[sl][j][s] = *(const bf16x8*)(bptr[j] + c * SKC + s * 32);
   };
-  // activation rows past M are clamped to the last row (their outputs are
-  // discarded)
-  auto aload = [&](int c) __attribute__((always_inline)) {
+  // activation chunk q of a stage: plane q / ACH, row (q % ACH) / 8, 16-byte
+  // column q % 8; rows past M are clamped to the last row (their outputs are
+  // discarded).  NA register sets: A(c + NA) is fetched at stage c and
+  // written to LDS at stage c + NA - 1, so each activation load has NA - 1
+  // stages to arrive.
+  constexpr int NA = 4;
+  static_assert(RING % NA == 0, "register sets rotate with the ring");
+  u32x4 ar[NA][APT];
+  auto aload = [&](int c, auto set_c) __attribute__((always_inline)) {
+    constexpr int st = decltype(set_c)::value;
     const int k0 = kbeg + c * SKC;
 #pragma unroll
     for (int u = 0; u < APT; ++u) {
-      const int ci = tid + 256 * u;
-      const int pl = ci >= ACH;
-      const int cc = ci - pl * ACH;
-      const int row = min(cc / (SKC / 8), a.M - 1), col = (cc % (SKC / 8)) * 8;
-      const bf16* src = pl ? a.Alo : a.Ahi;
-      ar[u] = *(const u32x4*)(src + (long long)row * a.K + k0 + col);
+      const int q = tid + 256 * u;
+      const int pl = q / ACH, cc = q % ACH;
+      const int row = min(cc / 8, a.M - 1), col = (cc % 8) * 8;
+      ar[st][u] = *(const u32x4*)((pl ? a.Alo : a.Ahi) + (long long)row * a.K + k0 + col);
     }
   };
-  auto astore = [&](auto buf_c) __attribute__((always_inline)) {
-    constexpr int bb = decltype(buf_c)::value;
+  auto astore = [&](int buf, auto set_c) __attribute__((always_inline)) {
+    constexpr int st = decltype(set_c)::value;
 #pragma unroll
     for (int u = 0; u < APT; ++u) {
-      const int ci = tid + 256 * u;
-      const int pl = ci >= ACH;
-      const int cc = ci - pl * ACH;
-      const int row = cc / (SKC / 8), col = (cc % (SKC / 8)) * 8;
-      if (pl) *(u32x4*)&Al[bb][row][col] = ar[u];
-      else *(u32x4*)&Ah[bb][row][col] = ar[u];
+      const int q = tid + 256 * u;
+      const int pl = q / ACH, cc = q % ACH;
+      const int row = cc / 8, c = cc % 8;
+      *(u32x4*)&As[buf][pl][row * SKC + ((c ^ (row & 7)) << 3)] = ar[st][u];
     }
   };
 
-  f32x4 acc[MT];
+  f32x4 acc[MT][CT];
 #pragma unroll
-  for (int i = 0; i < MT; ++i) acc[i] = (f32x4){0.f, 0.f, 0.f, 0.f};
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < CT; ++j) acc[i][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
 
-  // prologue: A(0) -> LDS, weights of stages 0..SRING-1, A(1) in registers
-  if (nst > 0) {
-    aload(0);
-    astore(ic<0>{});
-    bload(0, ic<0>{});
-    if (1 < nst) bload(1, ic<1>{});
-    if (2 < nst) bload(2, ic<2>{});
-    if (3 < nst) bload(3, ic<3>{});
-    if (1 < nst) aload(1);
-    __syncthreads();
-  }
-  // stage c: MFMAs on LDS buffer c & 1 and ring slot c % SRING; then refill
-  // that slot with stage c + SRING, move A(c + 1) to LDS and fetch A(c + 2)
-  auto stage = [&](int c, auto slot_c) __attribute__((always_inline)) {
+  auto mma = [&](int cur, auto slot_c) __attribute__((always_inline)) {
     constexpr int sl = decltype(slot_c)::value;
-    constexpr int cur = sl & 1;
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
+    for (int s = 0; s < 2; ++s)
 #pragma unroll
       for (int i = 0; i < MT; ++i) {
-        const bf16x8 ah = *(const bf16x8*)&Ah[cur][i * 16 + lr][s * 32 + lg * 8];
-        const bf16x8 al = *(const bf16x8*)&Al[cur][i * 16 + lr][s * 32 + lg * 8];
-        acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, ring[sl][s], acc[i], 0, 0, 0);
-        acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, ring[sl][s], acc[i], 0, 0, 0);
+        const int row = i * 16 + lr;
+        const int off = row * SKC + (((s * 4 + lg) ^ (row & 7)) << 3);
+        const bf16x8 ah = *(const bf16x8*)&As[cur][0][off];
+        const bf16x8 al = *(const bf16x8*)&As[cur][1][off];
+#pragma unroll
+        for (int j = 0; j < CT; ++j) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, ring[sl][j][s], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, ring[sl][j][s], acc[i][j], 0, 0, 0);
+        }
       }
-    }
-    if (c + SRING < nst) bload(c + SRING, slot_c);
-    if (c + 1 < nst) astore(ic<cur ^ 1>{});
-    if (c + 2 < nst) aload(c + 2);
+  };
+
+  // stage c (ring slot c % RING, register set c % NA): MFMAs on LDS buffer
+  // c & 1; refill the ring slot with stage c + RING; write A(c + 1) (set
+  // (c + 1) % NA) to the other buffer; fetch A(c + NA) into the set freed by
+  // A(c)
+  auto stage = [&](int c, auto slot_c) __attribute__((always_inline)) {
+    constexpr int sl = decltype(slot_c)::value;
+    mma(c & 1, slot_c);
+    bload(min(c + RING, nst - 1), slot_c);
+    astore((c + 1) & 1, ic<(sl + 1) % NA>{});
+    aload(min(c + NA, nst - 1), ic<sl % NA>{});
     __syncthreads();
   };
-  for (int c = 0; c < nst; c += SRING) {
-    stage(c, ic<0>{});
-    if (c + 1 < nst) stage(c + 1, ic<1>{});
-    if (c + 2 < nst) stage(c + 2, ic<2>{});
-    if (c + 3 < nst) stage(c + 3, ic<3>{});
+  auto stage_tail = [&](int c, auto slot_c) __attribute__((always_inline)) {
+    constexpr int sl = decltype(slot_c)::value;
+    if (c < nst) {
+      mma(c & 1, slot_c);
+      if (c + 1 < nst) astore((c + 1) & 1, ic<(sl + 1) % NA>{});
+      if (c + NA < nst) aload(c + NA, ic<sl % NA>{});
+      __syncthreads();
+    }
+  };
+
+  if (nst > 0) {
+    [&]<int... U>(std::integer_sequence<int, U...>) {
+      (aload(min(U, nst - 1), ic<U>{}), ...);
+    }(std::make_integer_sequence<int, NA>{});
+    [&]<int... U>(std::integer_sequence<int, U...>) {
+      (bload(min(U, nst - 1), ic<U>{}), ...);
+    }(std::make_integer_sequence<int, RING>{});
+    astore(0, ic<0>{});
+    __syncthreads();
   }
+  int c = 0;
+  for (; c + RING <= nst; c += RING) {
+    [&]<int... U>(std::integer_sequence<int, U...>) {
+      (stage(c + U, ic<U>{}), ...);
+    }(std::make_integer_sequence<int, RING>{});
+  }
+  // tail stages (fewer than RING left)
+  [&]<int... U>(std::integer_sequence<int, U...>) {
+    (stage_tail(c + U, ic<U>{}), ...);
+  }(std::make_integer_sequence<int, RING>{});
 
   if (a.ksplit > 1) {
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) part_store(a, i * 16 + lg * 4 + e, n0 + lr, acc[i][e]);
+      for (int j = 0; j < CT; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) part_store(a, i * 16 + lg * 4 + e, n0 + j * 16 + lr, acc[i][j][e]);
     return;
   }
   if (a.epi == kEpiSwiGLU) {
-    // gate = wave tile with (wave & 1) == 0, up = the next wave's tile: swap
-    // through LDS (the activation buffers are free by now) so the gate wave
-    // owns both.
-    static_assert(sizeof(float) * 2 * MT * 4 * 64 <= sizeof(Ah), "exchange fits");
-    float (*xch)[MT * 4][64] = reinterpret_cast<float (*)[MT * 4][64]>(&Ah[0][0][0]);
-    if (wave & 1) {
+    if constexpr (CT % 2 == 0) {
+      // column tiles 2t (gate) and 2t + 1 (up) of the packed weight are in
+      // this wave
 #pragma unroll
       for (int i = 0; i < MT; ++i)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) xch[wave >> 1][i * 4 + e][lane] = acc[i][e];
-    }
-    __syncthreads();
-    if ((wave & 1) == 0) {
+        for (int j = 0; j < CT; j += 2)
 #pragma unroll
-      for (int i = 0; i < MT; ++i)
+          for (int e = 0; e < 4; ++e)
+            epi_swiglu(a, i * 16 + lg * 4 + e, n0 + j * 16 + lr, acc[i][j][e], acc[i][j + 1][e]);
+    } else {
+      // gate = wave tile with (wave & 1) == 0, up = the next wave's tile:
+      // swap through LDS (the activation buffers are free by now) so the
+      // gate wave owns both
+      static_assert(sizeof(float) * 2 * MT * 4 * 64 <= sizeof(As), "exchange fits");
+      float (*xch)[MT * 4][64] = reinterpret_cast<float (*)[MT * 4][64]>(&As[0][0][0]);
+      if (wave & 1) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          epi_swiglu(a, i * 16 + lg * 4 + e, n0 + lr, acc[i][e], xch[wave >> 1][i * 4 + e][lane]);
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) xch[wave >> 1][i * 4 + e][lane] = acc[i][0][e];
+      }
+      __syncthreads();
+      if ((wave & 1) == 0) {
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            epi_swiglu(a, i * 16 + lg * 4 + e, n0 + lr, acc[i][0][e], xch[wave >> 1][i * 4 + e][lane]);
+      }
     }
     return;
   }
 #pragma unroll
   for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) epi_store(a, i * 16 + lg * 4 + e, n0 + lr, acc[i][e]);
+    for (int j = 0; j < CT; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) epi_store(a, i * 16 + lg * 4 + e, n0 + j * 16 + lr, acc[i][j][e]);
 }
 
 // ---------------------------------------------------------------------------
@@ -535,11 +589,13 @@ int dense_cfg() {
 struct Plan {
   int kind;          // 0 dense, 1 skinny, 2 f32
   int cfg;           // dense tile configuration
-  int mt;            // skinny row tiles
+  int mt, ct;        // skinny row tiles, 16-column tiles per wave
   int tiles_m, tiles_n;
   int ksplit, kchunk;
   size_t ws_bytes;
 };
+
+constexpr int skinny_ring(int ct) { return ct == 1 ? 8 : 4; }
 
 Plan make_plan(int M, int N, int K, int dtype) {
   Plan p{};
@@ -550,13 +606,20 @@ Plan make_plan(int M, int N, int K, int dtype) {
   if (M <= 128 && K % SKC == 0) {
     p.kind = 1;
     p.mt = (M + 15) / 16;
-    p.tiles_m = 1;
-    p.tiles_n = (N + 63) / 64;
-    // ~2 workgroups per CU, each streaming >= 2 * SRING stages
+    // Wide projections (>= 200 tiles of 64 columns: gate/up, LM head) run
+    // 16 columns per wave with no K split, so no partial planes are written.
+    // Narrow ones run 32 columns per wave (each activation fragment feeds
+    // two MFMA tiles) with K split to about 256 workgroups, each streaming
+    // whole rings of K stages.
     const int nst = K / SKC;
-    int s = (512 + p.tiles_n - 1) / p.tiles_n;
-    s = max(1, min(s, nst / (2 * SRING)));
-    const int per = (nst + s - 1) / s;
+    p.ct = (N + 63) / 64 >= 200 ? 1 : 2;
+    const int ring = skinny_ring(p.ct);
+    p.tiles_m = 1;
+    p.tiles_n = (N + 64 * p.ct - 1) / (64 * p.ct);
+    int s = p.ct == 1 ? 1 : (256 + p.tiles_n - 1) / p.tiles_n;
+    s = max(1, min(s, nst / ring));
+    int per = (nst + s - 1) / s;
+    if (nst >= ring) per = (per + ring - 1) / ring * ring;
     s = (nst + per - 1) / per;
     p.ksplit = s;
     p.kchunk = per * SKC;
@@ -599,7 +662,9 @@ int gemm_check(int M, int N, int K, int dtype) {
 }
 
 hipError_t gemm_launch(const GemmOperand& A, const void* B, const GemmOut& out, int M, int N, int K, int dtype,
-                       int epi, void* ws, size_t ws_bytes, hipStream_t st, bool prefill, GemmHook* hook) {
+                       int epi, void* ws, size_t ws_bytes, hipStream_t st, bool prefill, GemmHook* hook,
+                       int* deferred) {
+  if (deferred) *deferred = 1;
   if (M == 0) return hipSuccess;
   Plan p = make_plan(M, N, K, dtype);
   if (p.kind == 2) {
@@ -644,19 +709,29 @@ hipError_t gemm_launch(const GemmOperand& A, const void* B, const GemmOut& out, 
 #undef CDSL_DENSE
   } else {
     dim3 grid(p.tiles_n, 1, p.ksplit);
+#define CDSL_SKINNY(MT)                                                                     \
+  case MT:                                                                                  \
+    if (p.ct == 2) gemm_bf16_skinny<MT, 2, skinny_ring(2)><<<grid, 256, 0, st>>>(a);        \
+    else gemm_bf16_skinny<MT, 1, skinny_ring(1)><<<grid, 256, 0, st>>>(a);                  \
+    break;
     switch (p.mt) {
-      case 1: gemm_bf16_skinny<1><<<grid, 256, 0, st>>>(a); break;
-      case 2: gemm_bf16_skinny<2><<<grid, 256, 0, st>>>(a); break;
-      case 3: gemm_bf16_skinny<3><<<grid, 256, 0, st>>>(a); break;
-      case 4: gemm_bf16_skinny<4><<<grid, 256, 0, st>>>(a); break;
-      case 5: gemm_bf16_skinny<5><<<grid, 256, 0, st>>>(a); break;
-      case 6: gemm_bf16_skinny<6><<<grid, 256, 0, st>>>(a); break;
-      case 7: gemm_bf16_skinny<7><<<grid, 256, 0, st>>>(a); break;
-      default: gemm_bf16_skinny<8><<<grid, 256, 0, st>>>(a); break;
+      CDSL_SKINNY(1)
+      CDSL_SKINNY(2)
+      CDSL_SKINNY(3)
+      CDSL_SKINNY(4)
+      CDSL_SKINNY(5)
+      CDSL_SKINNY(6)
+      CDSL_SKINNY(7)
+      default: CDSL_SKINNY(8)
     }
+#undef CDSL_SKINNY
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.ksplit == 1) return e;
+  if (deferred && epi != kEpiSwiGLU) {
+    *deferred = p.ksplit;
+    return hipSuccess;
+  }
   const long long outs = epi == kEpiSwiGLU ? (long long)M * (N / 2) : (long long)M * N;
   if (hook) hook->before_reduce(p.ksplit);
   splitk_reduce_kernel<<<(unsigned)((outs + 255) / 256), 256, 0, st>>>(a);

@@ -38,10 +38,15 @@ __host__ __device__ inline long long rowmap_index(const RowMap& r, int m) {
 }
 
 hipError_t embed_launch(const PassDesc& p, const void* emb, float* h, int D, int V, int dtype, hipStream_t st);
-hipError_t rmsnorm_launch(const float* x, const float* g, float* out32, bf16* ohi, bf16* olo, int rows, int D,
-                          float eps, int last_only, int R, float* hid, hipStream_t st);
+// S > 0: fold S split planes part[S][rows][D] into x first (written back);
+// g == null then only folds.
+hipError_t rmsnorm_launch(float* x, const float* g, float* out32, bf16* ohi, bf16* olo, int rows, int D,
+                          float eps, int last_only, int R, float* hid, hipStream_t st, const float* part = nullptr,
+                          int S = 0);
+// S > 1: qkv holds S split planes of the projection (bf16-weight models)
 hipError_t rope_kv_launch(const PassDesc& p, const float* qkv, void* qout, const KVPool& pool, int layer,
-                          const float* cos_t, const float* sin_t, int H, int Hkv, int hd, int dtype, hipStream_t st);
+                          const float* cos_t, const float* sin_t, int H, int Hkv, int hd, int dtype, hipStream_t st,
+                          int S = 0);
 hipError_t logit_rows_launch(const LogitArgs& a, int M, hipStream_t st);
 hipError_t beam_scores_launch(int BK, int d, const int* look, const int* y, const float* lp, const float* head_lp,
                               int* n_accept, float* scores, hipStream_t st);

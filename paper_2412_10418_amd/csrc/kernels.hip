@@ -53,16 +53,57 @@ __global__ __launch_bounds__(256) void embed_rows(PassDesc p, const T* __restric
 // the hi / lo planes that the next projection consumes.  hid (fp32)
 // additionally receives the normed row of every beam's last row (the reward
 // reads it).
-__global__ __launch_bounds__(256) void rmsnorm_rows(const float* __restrict__ x, const float* __restrict__ g,
+//
+// With S > 0 split planes part[S][rows][D] of a residual projection, the
+// row is first completed: x[r] += sum of the planes in split order (the
+// same arithmetic as the split-K reduce), written back to x.  g == null
+// then only folds.
+__global__ __launch_bounds__(256) void rmsnorm_rows(float* __restrict__ x, const float* __restrict__ g,
                                                     float* __restrict__ out32, bf16* __restrict__ ohi,
                                                     bf16* __restrict__ olo, int D, float eps, int last_only, int R,
-                                                    float* __restrict__ hid) {
+                                                    float* __restrict__ hid, const float* __restrict__ part, int S,
+                                                    int rows) {
   __shared__ float sh[4];
   const int r = blockIdx.x;
   const int src = last_only ? r * R + (R - 1) : r;
-  const float* xr = x + (long long)src * D;
+  float* xr = x + (long long)src * D;
   float ss = 0.f;
-  for (int c = threadIdx.x; c < D; c += 256) ss = fmaf(xr[c], xr[c], ss);
+  if (S > 0) {
+    // float4 columns; the planes are loaded eight at a time (independent
+    // loads in flight) and added in split order
+    const long long plane = (long long)rows * D;
+    const float* pr = part + (long long)src * D;
+    for (int c = threadIdx.x * 4; c < D; c += 1024) {
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int z0 = 0; z0 < S; z0 += 8) {
+        float4 t[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          t[u] = z0 + u < S ? *(const float4*)(pr + (z0 + u) * plane + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (z0 + u < S) {
+            v.x += t[u].x;
+            v.y += t[u].y;
+            v.z += t[u].z;
+            v.w += t[u].w;
+          }
+      }
+      const float4 h = *(const float4*)(xr + c);
+      v.x += h.x;
+      v.y += h.y;
+      v.z += h.z;
+      v.w += h.w;
+      *(float4*)(xr + c) = v;
+      ss = fmaf(v.x, v.x, ss);
+      ss = fmaf(v.y, v.y, ss);
+      ss = fmaf(v.z, v.z, ss);
+      ss = fmaf(v.w, v.w, ss);
+    }
+  } else {
+    for (int c = threadIdx.x; c < D; c += 256) ss = fmaf(xr[c], xr[c], ss);
+  }
+  if (!g) return;
   ss = block_sum<4>(ss, sh);
   const float inv = rsqrtf(ss / (float)D + eps);
   const long long o = (long long)r * D;
@@ -139,10 +180,13 @@ __global__ __launch_bounds__(256) void rope_kv_write(PassDesc p, const float* __
 // Same for bf16-weight models, whose KV pool holds each fp32 value as a
 // bf16 (hi, lo) pair in the split unit format (K [plane][16][hd], V
 // [plane][hd][16]).  q stays fp32.
+// With S > 0, qkv holds S split planes [S][M][(H + 2 Hkv) hd] of the
+// projection, summed here in split order.
 __global__ __launch_bounds__(256) void rope_kv_write_split(PassDesc p, const float* __restrict__ qkv,
                                                            float* __restrict__ qout, KVPool pool, int layer,
                                                            const float* __restrict__ cos_t,
-                                                           const float* __restrict__ sin_t, int H, int Hkv, int hd) {
+                                                           const float* __restrict__ sin_t, int H, int Hkv, int hd,
+                                                           int S) {
   const int m = blockIdx.x;
   int bi, b, i, j;
   row_decode(p, m, bi, b, i, j);
@@ -161,41 +205,82 @@ __global__ __launch_bounds__(256) void rope_kv_write_split(PassDesc p, const flo
   const int half = hd / 2;
   const long long unit = split_unit_elems(hd);
   const long long plane = (long long)kBlock * hd;
-  const float* row = qkv + (long long)m * (H + 2 * Hkv) * hd;
+  const int W = (H + 2 * Hkv) * hd;
+  const float* row = qkv + (long long)m * W;
+  const long long split_plane = (long long)p.nb * p.kp * p.R * W;
+  // four consecutive values of the row (summed over the split planes in
+  // split order, eight planes' loads in flight at a time)
+  auto val4 = [&](int idx) {
+    if (S <= 0) return *(const float4*)(row + idx);
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int z0 = 0; z0 < S; z0 += 8) {
+      float4 t[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        t[u] = z0 + u < S ? *(const float4*)(row + (z0 + u) * split_plane + idx) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (z0 + u < S) {
+          v.x += t[u].x;
+          v.y += t[u].y;
+          v.z += t[u].z;
+          v.w += t[u].w;
+        }
+    }
+    return v;
+  };
   const float* ct = cos_t + (long long)pos * half;
   const float* stt = sin_t + (long long)pos * half;
   bf16* kb = (bf16*)pool.k + (long long)layer * 2 * pool.layer_elems + (long long)blk * Hkv * unit;
   bf16* vb = (bf16*)pool.v + (long long)layer * 2 * pool.layer_elems + (long long)blk * Hkv * unit;
-  const int npairs = (H + Hkv) * half;
-  for (int u = threadIdx.x; u < npairs; u += 256) {
-    const int hh = u / half, d = u % half;
-    const float x1 = row[hh * hd + d], x2 = row[hh * hd + d + half];
-    const float c = ct[d], s = stt[d];
-    const float y1 = x1 * c - x2 * s, y2 = x2 * c + x1 * s;
+  // q and k heads: rotate-half pairs (d, d + hd/2), four d at a time
+  const int q4 = half / 4;
+  for (int u = threadIdx.x; u < (H + Hkv) * q4; u += 256) {
+    const int hh = u / q4, d = (u % q4) * 4;
+    const float4 x1 = val4(hh * hd + d), x2 = val4(hh * hd + d + half);
+    const float4 c = *(const float4*)(ct + d), sn = *(const float4*)(stt + d);
+    const float y1[4] = {x1.x * c.x - x2.x * sn.x, x1.y * c.y - x2.y * sn.y, x1.z * c.z - x2.z * sn.z,
+                         x1.w * c.w - x2.w * sn.w};
+    const float y2[4] = {x2.x * c.x + x1.x * sn.x, x2.y * c.y + x1.y * sn.y, x2.z * c.z + x1.z * sn.z,
+                         x2.w * c.w + x1.w * sn.w};
     if (hh < H) {
-      float* q = qout + ((long long)m * H + hh) * hd;
-      q[d] = y1;
-      q[d + half] = y2;
+      float* q = qout + ((long long)m * H + hh) * hd + d;
+      *(float4*)q = make_float4(y1[0], y1[1], y1[2], y1[3]);
+      *(float4*)(q + half) = make_float4(y2[0], y2[1], y2[2], y2[3]);
     } else {
-      bf16* kr = kb + (long long)(hh - H) * unit + (long long)slot * hd;
-      bf16 h, l;
-      split_bf16(y1, h, l);
-      kr[d] = h;
-      kr[plane + d] = l;
-      split_bf16(y2, h, l);
-      kr[d + half] = h;
-      kr[plane + d + half] = l;
+      bf16* kr = kb + (long long)(hh - H) * unit + (long long)slot * hd + d;
+      bf16x4 h1, l1, h2, l2;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        bf16 h, l;
+        split_bf16(y1[e], h, l);
+        h1[e] = h;
+        l1[e] = l;
+        split_bf16(y2[e], h, l);
+        h2[e] = h;
+        l2[e] = l;
+      }
+      *(bf16x4*)kr = h1;
+      *(bf16x4*)(kr + plane) = l1;
+      *(bf16x4*)(kr + half) = h2;
+      *(bf16x4*)(kr + plane + half) = l2;
     }
   }
-  const float* vrow = row + (long long)(H + Hkv) * hd;
-  const int vs = slot;
-  for (int u = threadIdx.x; u < Hkv * hd; u += 256) {
-    const int hh = u / hd, d = u % hd;
-    bf16* vr = vb + (long long)hh * unit + (long long)d * kBlock + vs;
-    bf16 h, l;
-    split_bf16(vrow[u], h, l);
-    vr[0] = h;
-    vr[plane] = l;
+  // v: [hd][16] per block and head
+  const int voff = (H + Hkv) * hd;
+  for (int u = threadIdx.x; u < Hkv * hd / 4; u += 256) {
+    const int e0 = u * 4;
+    const int hh = e0 / hd, d = e0 % hd;
+    const float4 v = val4(voff + e0);
+    const float vv[4] = {v.x, v.y, v.z, v.w};
+    bf16* vr = vb + (long long)hh * unit + (long long)d * kBlock + slot;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      bf16 h, l;
+      split_bf16(vv[e], h, l);
+      vr[e * kBlock] = h;
+      vr[e * kBlock + plane] = l;
+    }
   }
 }
 
@@ -591,20 +676,24 @@ hipError_t embed_launch(const PassDesc& p, const void* emb, float* h, int D, int
   return hipGetLastError();
 }
 
-hipError_t rmsnorm_launch(const float* x, const float* g, float* out32, bf16* ohi, bf16* olo, int rows, int D,
-                          float eps, int last_only, int R, float* hid, hipStream_t st) {
+hipError_t rmsnorm_launch(float* x, const float* g, float* out32, bf16* ohi, bf16* olo, int rows, int D,
+                          float eps, int last_only, int R, float* hid, hipStream_t st, const float* part, int S) {
   if (rows == 0) return hipSuccess;
-  rmsnorm_rows<<<rows, 256, 0, st>>>(x, g, out32, ohi, olo, D, eps, last_only, R, hid);
+  if (S > 0 && last_only) return hipErrorInvalidValue;
+  rmsnorm_rows<<<rows, 256, 0, st>>>(x, g, out32, ohi, olo, D, eps, last_only, R, hid, part, S, rows);
   return hipGetLastError();
 }
 
 hipError_t rope_kv_launch(const PassDesc& p, const float* qkv, void* qout, const KVPool& pool, int layer,
-                          const float* cos_t, const float* sin_t, int H, int Hkv, int hd, int dtype, hipStream_t st) {
+                          const float* cos_t, const float* sin_t, int H, int Hkv, int hd, int dtype, hipStream_t st,
+                          int S) {
   const int M = p.M();
   if (M == 0) return hipSuccess;
   // q is fp32 for every weight dtype; the KV pool is fp32 or split bf16
   if (dtype == 1)
-    rope_kv_write_split<<<M, 256, 0, st>>>(p, qkv, (float*)qout, pool, layer, cos_t, sin_t, H, Hkv, hd);
+    rope_kv_write_split<<<M, 256, 0, st>>>(p, qkv, (float*)qout, pool, layer, cos_t, sin_t, H, Hkv, hd, S);
+  else if (S > 1)
+    return hipErrorInvalidValue;
   else
     rope_kv_write<float><<<M, 256, 0, st>>>(p, qkv, (float*)qout, pool, layer, cos_t, sin_t, H, Hkv, hd);
   return hipGetLastError();

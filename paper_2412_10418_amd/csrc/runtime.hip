@@ -390,8 +390,10 @@ void alloc_workspace(cdsl_ctx* c) {
 // ---------------------------------------------------------------------------
 // model runner
 // ---------------------------------------------------------------------------
-void gemm(cdsl_ctx* c, const GemmOperand& A, const void* W, const GemmOut& out, int M, int N, int K, int epi,
-          bool prefill) {
+// Returns the number of split planes left in the GEMM workspace for the
+// caller to fold (1: none) when defer is set.
+int gemm(cdsl_ctx* c, const GemmOperand& A, const void* W, const GemmOut& out, int M, int N, int K, int epi,
+         bool prefill, bool defer = false) {
   const double wes = c->dtype == CDSL_BF16 ? 2.0 : 4.0;   // weight element size
   // output bytes: fp32 store, fp32 read-modify-write, or the two bf16 planes
   // of the half-width SwiGLU output
@@ -421,8 +423,10 @@ void gemm(cdsl_ctx* c, const GemmOperand& A, const void* W, const GemmOut& out, 
   hk.main = &sp;
   hk.outb = outb;
   hk.plane = (double)M * N * 4.0;
+  int planes = 1;
   CK(gemm_launch(A, W, out, M, N, K, c->dtype, epi, c->ws.gemm_ws, c->ws.gemm_ws_bytes, c->st, prefill,
-                 c->prof ? &hk : nullptr));
+                 c->prof ? &hk : nullptr, defer ? &planes : nullptr));
+  return planes;
 }
 
 // Forward pass of one model over the rows of p.  With want_logits, the
@@ -481,15 +485,21 @@ void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, lon
   const GemmOperand Au{w.uh, w.ul, w.u32}, Ao{w.oh, w.ol, w.o32}, Aact{w.ah, w.al, w.act32};
   const GemmOut to_qkv{w.qkv, nullptr, nullptr, md.qkv_n}, to_h{w.h, nullptr, nullptr, D};
   const GemmOut to_act{nullptr, w.ah, w.al, F}, to_gu{w.gu32, nullptr, nullptr, 2 * F};
+  // Residual projections (W_o, W_down) and the q/k/v projection may leave
+  // their K split unreduced: the planes are folded by the kernel that
+  // consumes the result (RMSNorm of the residual stream, rotary + KV
+  // write), which saves a reduce launch per projection.
+  const float* planes_ws = (const float*)w.gemm_ws;
+  {
+    Span sp(c, CDSL_K_ROWWISE, 0.0, norm_bytes);
+    CK(rmsnorm_launch(w.h, md.g1[0], w.u32, w.uh, w.ul, M, D, k.rms_eps, 0, 1, nullptr, c->st));
+  }
   for (int l = 0; l < k.n_layers; ++l) {
+    const int sq = gemm(c, Au, md.wqkv[l], to_qkv, M, md.qkv_n, D, kEpiStore, prefill, bf);
     {
-      Span sp(c, CDSL_K_ROWWISE, 0.0, norm_bytes);
-      CK(rmsnorm_launch(w.h, md.g1[l], w.u32, w.uh, w.ul, M, D, k.rms_eps, 0, 1, nullptr, c->st));
-    }
-    gemm(c, Au, md.wqkv[l], to_qkv, M, md.qkv_n, D, kEpiStore, prefill);
-    {
-      Span sp(c, CDSL_K_ROWWISE, 0.0, rope_bytes);
-      CK(rope_kv_launch(p, w.qkv, w.q, md.pool, l, md.cos_t, md.sin_t, H, Hkv, hd, dt, c->st));
+      Span sp(c, CDSL_K_ROWWISE, 0.0, rope_bytes + (sq > 1 ? (double)sq * M * md.qkv_n * 4.0 : 0.0));
+      CK(rope_kv_launch(p, sq > 1 ? planes_ws : w.qkv, w.q, md.pool, l, md.cos_t, md.sin_t, H, Hkv, hd, dt, c->st,
+                        sq > 1 ? sq : 0));
     }
     aa.layer = l;
     {
@@ -500,10 +510,11 @@ void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, lon
       Span sp(c, CDSL_K_ATTN_COMBINE, 0.0, comb_bytes);
       CK(attn_combine_launch(aa, pl, hd, c->st));
     }
-    gemm(c, Ao, md.wo[l], to_h, M, D, H * hd, kEpiResidual, prefill);
+    const int so = gemm(c, Ao, md.wo[l], to_h, M, D, H * hd, kEpiResidual, prefill, bf);
     {
-      Span sp(c, CDSL_K_ROWWISE, 0.0, norm_bytes);
-      CK(rmsnorm_launch(w.h, md.g2[l], w.u32, w.uh, w.ul, M, D, k.rms_eps, 0, 1, nullptr, c->st));
+      Span sp(c, CDSL_K_ROWWISE, 0.0, norm_bytes + (so > 1 ? (double)(so + 1) * M * D * 4.0 : 0.0));
+      CK(rmsnorm_launch(w.h, md.g2[l], w.u32, w.uh, w.ul, M, D, k.rms_eps, 0, 1, nullptr, c->st,
+                        so > 1 ? planes_ws : nullptr, so > 1 ? so : 0));
     }
     if (bf) {
       gemm(c, Au, md.wgu[l], to_act, M, 2 * F, D, kEpiSwiGLU, prefill);
@@ -512,7 +523,15 @@ void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, lon
       Span sp(c, CDSL_K_ROWWISE, 0.0, (double)M * F * 12.0);
       CK(swiglu_f32_launch(w.gu32, w.act32, M, F, c->st));
     }
-    gemm(c, Aact, md.wd[l], to_h, M, D, F, kEpiResidual, prefill);
+    const int sd = gemm(c, Aact, md.wd[l], to_h, M, D, F, kEpiResidual, prefill, bf);
+    const bool last = l + 1 == k.n_layers;
+    if (!last || sd > 1) {
+      // next layer's attention norm (or, after the last layer, only the
+      // fold: the final norm below may take just the last rows)
+      Span sp(c, CDSL_K_ROWWISE, 0.0, (last ? 0.0 : norm_bytes) + (sd > 1 ? (double)(sd + 1) * M * D * 4.0 : 0.0));
+      CK(rmsnorm_launch(w.h, last ? nullptr : md.g1[l + 1], w.u32, w.uh, w.ul, M, D, k.rms_eps, 0, 1, nullptr, c->st,
+                        sd > 1 ? planes_ws : nullptr, sd > 1 ? sd : 0));
+    }
   }
   if (!want_logits) return;
   const int rows = last_only ? p.nb * p.kp : M;
