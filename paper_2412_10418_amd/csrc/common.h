@@ -9,6 +9,7 @@ namespace cdsl {
 typedef __bf16 bf16;
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2v;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 // native 16-byte vector for raw copies (HIP's uint4 wraps a union, which
 // keeps the optimizer from holding it in registers)

@@ -179,38 +179,22 @@ __global__ __launch_bounds__(256) void rope_kv_write(PassDesc p, const float* __
 
 // Same for bf16-weight models, whose KV pool holds each fp32 value as a
 // bf16 (hi, lo) pair in the split unit format (K [plane][16][hd], V
-// [plane][hd][16]).  q stays fp32.
-// With S > 0, qkv holds S split planes [S][M][(H + 2 Hkv) hd] of the
-// projection, summed here in split order.
-__global__ __launch_bounds__(256) void rope_kv_write_split(PassDesc p, const float* __restrict__ qkv,
-                                                           float* __restrict__ qout, KVPool pool, int layer,
-                                                           const float* __restrict__ cos_t,
-                                                           const float* __restrict__ sin_t, int H, int Hkv, int hd,
-                                                           int S) {
-  const int m = blockIdx.x;
-  int bi, b, i, j;
-  row_decode(p, m, bi, b, i, j);
-  const int Lp = p.Lp[b];
-  int pos, blk, slot;
-  if (p.mode == kSuffix) {
-    const int s = p.j0 + j;
-    pos = Lp + s;
-    blk = p.stable[(long long)b * p.s_stride_b + i * p.s_stride_i + s / kBlock];
-    slot = s % kBlock;
-  } else {
-    pos = Lp + j;
-    blk = p.ptable[(long long)b * p.ptable_stride + pos / kBlock];
-    slot = pos % kBlock;
-  }
-  const int half = hd / 2;
-  const long long unit = split_unit_elems(hd);
-  const long long plane = (long long)kBlock * hd;
-  const int W = (H + 2 * Hkv) * hd;
-  const float* row = qkv + (long long)m * W;
-  const long long split_plane = (long long)p.nb * p.kp * p.R * W;
-  // four consecutive values of the row (summed over the split planes in
-  // split order, eight planes' loads in flight at a time)
-  auto val4 = [&](int idx) {
+// [plane][hd][16]).  q stays fp32.  With S > 0, qkv holds S split planes
+// [S][M][(H + 2 Hkv) hd] of the projection, summed here in split order.
+//
+// Workgroups 0..M-1 take one row each (rotary q and k, the K write).
+// Workgroups M.. take one (beam, KV head) each, one thread per head dim,
+// and write V: the rows of a beam sit in consecutive slots, so each thread
+// writes a run of slots of its dim row with wide stores instead of one
+// 2-byte store per row into a different 32-byte row.
+struct QkvRow {
+  const float* qkv;
+  long long split_plane;
+  int S;
+  // four consecutive values of row m at column idx (summed over the split
+  // planes in split order, eight planes' loads in flight at a time)
+  __device__ __forceinline__ float4 val4(long long m, int W, int idx) const {
+    const float* row = qkv + m * W;
     if (S <= 0) return *(const float4*)(row + idx);
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int z0 = 0; z0 < S; z0 += 8) {
@@ -228,59 +212,148 @@ __global__ __launch_bounds__(256) void rope_kv_write_split(PassDesc p, const flo
         }
     }
     return v;
-  };
-  const float* ct = cos_t + (long long)pos * half;
-  const float* stt = sin_t + (long long)pos * half;
-  bf16* kb = (bf16*)pool.k + (long long)layer * 2 * pool.layer_elems + (long long)blk * Hkv * unit;
-  bf16* vb = (bf16*)pool.v + (long long)layer * 2 * pool.layer_elems + (long long)blk * Hkv * unit;
-  // q and k heads: rotate-half pairs (d, d + hd/2), four d at a time
-  const int q4 = half / 4;
-  for (int u = threadIdx.x; u < (H + Hkv) * q4; u += 256) {
-    const int hh = u / q4, d = (u % q4) * 4;
-    const float4 x1 = val4(hh * hd + d), x2 = val4(hh * hd + d + half);
-    const float4 c = *(const float4*)(ct + d), sn = *(const float4*)(stt + d);
-    const float y1[4] = {x1.x * c.x - x2.x * sn.x, x1.y * c.y - x2.y * sn.y, x1.z * c.z - x2.z * sn.z,
-                         x1.w * c.w - x2.w * sn.w};
-    const float y2[4] = {x2.x * c.x + x1.x * sn.x, x2.y * c.y + x1.y * sn.y, x2.z * c.z + x1.z * sn.z,
-                         x2.w * c.w + x1.w * sn.w};
-    if (hh < H) {
-      float* q = qout + ((long long)m * H + hh) * hd + d;
-      *(float4*)q = make_float4(y1[0], y1[1], y1[2], y1[3]);
-      *(float4*)(q + half) = make_float4(y2[0], y2[1], y2[2], y2[3]);
-    } else {
-      bf16* kr = kb + (long long)(hh - H) * unit + (long long)slot * hd + d;
-      bf16x4 h1, l1, h2, l2;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        bf16 h, l;
-        split_bf16(y1[e], h, l);
-        h1[e] = h;
-        l1[e] = l;
-        split_bf16(y2[e], h, l);
-        h2[e] = h;
-        l2[e] = l;
-      }
-      *(bf16x4*)kr = h1;
-      *(bf16x4*)(kr + plane) = l1;
-      *(bf16x4*)(kr + half) = h2;
-      *(bf16x4*)(kr + plane + half) = l2;
-    }
   }
-  // v: [hd][16] per block and head
-  const int voff = (H + Hkv) * hd;
-  for (int u = threadIdx.x; u < Hkv * hd / 4; u += 256) {
-    const int e0 = u * 4;
-    const int hh = e0 / hd, d = e0 % hd;
-    const float4 v = val4(voff + e0);
-    const float vv[4] = {v.x, v.y, v.z, v.w};
-    bf16* vr = vb + (long long)hh * unit + (long long)d * kBlock + slot;
+  __device__ __forceinline__ float val(long long m, int W, int idx) const {
+    const float* row = qkv + m * W;
+    if (S <= 0) return row[idx];
+    float v = 0.f;
+    for (int z = 0; z < S; ++z) v += row[z * split_plane + idx];
+    return v;
+  }
+};
+
+__device__ __forceinline__ void kv_slot(const PassDesc& p, int b, int i, int j, int Lp, int& blk, int& slot,
+                                        int& pos) {
+  if (p.mode == kSuffix) {
+    const int s = p.j0 + j;
+    pos = Lp + s;
+    blk = p.stable[(long long)b * p.s_stride_b + i * p.s_stride_i + s / kBlock];
+    slot = s % kBlock;
+  } else {
+    pos = Lp + j;
+    blk = p.ptable[(long long)b * p.ptable_stride + pos / kBlock];
+    slot = pos % kBlock;
+  }
+}
+
+__global__ __launch_bounds__(256) void rope_kv_write_split(PassDesc p, const float* __restrict__ qkv,
+                                                           float* __restrict__ qout, KVPool pool, int layer,
+                                                           const float* __restrict__ cos_t,
+                                                           const float* __restrict__ sin_t, int H, int Hkv, int hd,
+                                                           int S) {
+  const int M = p.nb * p.kp * p.R;
+  const int W = (H + 2 * Hkv) * hd;
+  const QkvRow src{qkv, (long long)M * W, S};
+  const int half = hd / 2;
+  const long long unit = split_unit_elems(hd);
+  const long long plane = (long long)kBlock * hd;
+  bf16* kl = (bf16*)pool.k + (long long)layer * 2 * pool.layer_elems;
+  bf16* vl = (bf16*)pool.v + (long long)layer * 2 * pool.layer_elems;
+  if ((int)blockIdx.x < M) {
+    const int m = blockIdx.x;
+    int bi, b, i, j;
+    row_decode(p, m, bi, b, i, j);
+    int blk, slot, pos;
+    kv_slot(p, b, i, j, p.Lp[b], blk, slot, pos);
+    const float* ct = cos_t + (long long)pos * half;
+    const float* stt = sin_t + (long long)pos * half;
+    bf16* kb = kl + (long long)blk * Hkv * unit;
+    // q and k heads: rotate-half pairs (d, d + hd/2), four d at a time
+    const int q4 = half / 4;
+    for (int u = threadIdx.x; u < (H + Hkv) * q4; u += 256) {
+      const int hh = u / q4, d = (u % q4) * 4;
+      const float4 x1 = src.val4(m, W, hh * hd + d), x2 = src.val4(m, W, hh * hd + d + half);
+      const float4 c = *(const float4*)(ct + d), sn = *(const float4*)(stt + d);
+      const float y1[4] = {x1.x * c.x - x2.x * sn.x, x1.y * c.y - x2.y * sn.y, x1.z * c.z - x2.z * sn.z,
+                           x1.w * c.w - x2.w * sn.w};
+      const float y2[4] = {x2.x * c.x + x1.x * sn.x, x2.y * c.y + x1.y * sn.y, x2.z * c.z + x1.z * sn.z,
+                           x2.w * c.w + x1.w * sn.w};
+      if (hh < H) {
+        float* q = qout + ((long long)m * H + hh) * hd + d;
+        *(float4*)q = make_float4(y1[0], y1[1], y1[2], y1[3]);
+        *(float4*)(q + half) = make_float4(y2[0], y2[1], y2[2], y2[3]);
+      } else {
+        bf16* kr = kb + (long long)(hh - H) * unit + (long long)slot * hd + d;
+        bf16x4 h1, l1, h2, l2;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      bf16 h, l;
-      split_bf16(vv[e], h, l);
-      vr[e * kBlock] = h;
-      vr[e * kBlock + plane] = l;
+        for (int e = 0; e < 4; ++e) {
+          bf16 h, l;
+          split_bf16(y1[e], h, l);
+          h1[e] = h;
+          l1[e] = l;
+          split_bf16(y2[e], h, l);
+          h2[e] = h;
+          l2[e] = l;
+        }
+        *(bf16x4*)kr = h1;
+        *(bf16x4*)(kr + plane) = l1;
+        *(bf16x4*)(kr + half) = h2;
+        *(bf16x4*)(kr + plane + half) = l2;
+      }
     }
+    return;
+  }
+  // V of one (beam group, KV head): thread d < hd owns dim row d
+  const int task = blockIdx.x - M;
+  const int g = task / Hkv, hh = task % Hkv;
+  const int d = threadIdx.x;
+  if (d >= hd) return;
+  const int bi = g / p.kp, i = g % p.kp;
+  const int b = pass_batch(p, bi);
+  const int Lp = p.Lp[b];
+  const int voff = (H + Hkv) * hd + hh * hd + d;
+  const long long m0 = (long long)g * p.R;
+  int j = 0;
+  while (j < p.R) {
+    int blk, slot, pos;
+    kv_slot(p, b, i, j, Lp, blk, slot, pos);
+    const int n = min(p.R - j, kBlock - slot);   // rows of this block: slots [slot, slot + n)
+    bf16 vh[kBlock], vlo[kBlock];
+#pragma unroll
+    for (int t = 0; t < kBlock; ++t) {
+      vh[t] = (bf16)0.f;
+      vlo[t] = (bf16)0.f;
+      if (t >= slot && t < slot + n) {
+        bf16 h, l;
+        split_bf16(src.val(m0 + j + (t - slot), W, voff), h, l);
+        vh[t] = h;
+        vlo[t] = l;
+      }
+    }
+    bf16* row = vl + ((long long)blk * Hkv + hh) * unit + (long long)d * kBlock;
+    // widest stores inside [slot, slot + n): whole 8-slot halves as 16 bytes,
+    // else slot pairs as 4 bytes, else single slots
+#pragma unroll
+    for (int h8 = 0; h8 < 2; ++h8) {
+      const int t0 = h8 * 8;
+      if (t0 >= slot && t0 + 8 <= slot + n) {
+        bf16x8 a, c;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          a[e] = vh[t0 + e];
+          c[e] = vlo[t0 + e];
+        }
+        *(bf16x8*)(row + t0) = a;
+        *(bf16x8*)(row + plane + t0) = c;
+      } else {
+#pragma unroll
+        for (int t = t0; t < t0 + 8; t += 2) {
+          const bool in0 = t >= slot && t < slot + n, in1 = t + 1 >= slot && t + 1 < slot + n;
+          if (in0 && in1) {
+            bf16x2v a = {vh[t], vh[t + 1]}, c = {vlo[t], vlo[t + 1]};
+            *(bf16x2v*)(row + t) = a;
+            *(bf16x2v*)(row + plane + t) = c;
+          } else if (in0) {
+            row[t] = vh[t];
+            row[plane + t] = vlo[t];
+          } else if (in1) {
+            row[t + 1] = vh[t + 1];
+            row[plane + t + 1] = vlo[t + 1];
+          }
+        }
+      }
+    }
+    j += n;
   }
 }
 
@@ -690,8 +763,11 @@ hipError_t rope_kv_launch(const PassDesc& p, const float* qkv, void* qout, const
   const int M = p.M();
   if (M == 0) return hipSuccess;
   // q is fp32 for every weight dtype; the KV pool is fp32 or split bf16
-  if (dtype == 1)
-    rope_kv_write_split<<<M, 256, 0, st>>>(p, qkv, (float*)qout, pool, layer, cos_t, sin_t, H, Hkv, hd, S);
+  if (dtype == 1) {
+    if (hd > 256) return hipErrorInvalidValue;
+    const int tasks = p.nb * p.kp * Hkv;   // V: one workgroup per (beam group, KV head)
+    rope_kv_write_split<<<M + tasks, 256, 0, st>>>(p, qkv, (float*)qout, pool, layer, cos_t, sin_t, H, Hkv, hd, S);
+  }
   else if (S > 1)
     return hipErrorInvalidValue;
   else
