@@ -39,6 +39,7 @@ def parse():
     ap.add_argument("--k", type=int, default=None)
     ap.add_argument("--d", type=int, default=None)
     ap.add_argument("--profile-steps", type=int, default=3)
+    ap.add_argument("--phase-steps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (reference for HBM byte counters)")
@@ -197,6 +198,27 @@ def summarize_profile(args):
         sys.stdout.write(text)
 
 
+def phase_rooflines(wl, B, k, d, ms, sum_prefix):
+    """Algorithmic rates of the rollout (HBM-bound: every draft forward
+    streams the draft weights and the prefix KV of every prompt once) and of
+    the verification (MFMA-bound: 2 M flops per weight, M = B k d rows)."""
+    dr, tg = wl.draft, wl.target
+    kv_tok = lambda m: m.n_layers * 2 * m.n_kv_heads * m.head_dim * 4.0   # fp32-equivalent K + V
+    ro_bytes = d * (dr.n_params(with_embeddings=False) * 2.0 + sum_prefix * kv_tok(dr))
+    ve_flops = 2.0 * B * k * d * tg.n_params(with_embeddings=False)
+    out = {"rollout_ms": round(ms["rollout"], 3), "verify_ms": round(ms["verify"], 3),
+           "tail_ms": round(ms["tail"], 3)}
+    if ms["rollout"] > 0:
+        gbs = ro_bytes / (ms["rollout"] * 1e-3) / 1e9
+        out.update({"rollout_GB_per_s": round(gbs, 1), "rollout_hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
+                    "rollout_bytes": round(ro_bytes)})
+    if ms["verify"] > 0:
+        tfs = ve_flops / (ms["verify"] * 1e-3) / 1e12
+        out.update({"verify_TFLOP_per_s": round(tfs, 1), "verify_mfma_frac": round(tfs / PEAK_MFMA_BF16_TFS, 4),
+                    "verify_gemm_flops": round(ve_flops)})
+    return out
+
+
 def class_table(stats, step_ms_total):
     out = {}
     for nm, st in stats.items():
@@ -270,7 +292,7 @@ def main():
     log(f"weights generated in {time.perf_counter() - t0:.1f}s")
     t0 = time.perf_counter()
     dwd, twd = Engine.upload(wl, dw, tw)
-    total_steps = args.warmup + args.steps + args.profile_steps
+    total_steps = args.warmup + args.steps + args.profile_steps + args.phase_steps
     eng = Engine(wl, dwd, twd, max_steps=total_steps + 2, max_batch=B, k=k, d=d)
     del dwd, twd
     torch.cuda.empty_cache()
@@ -299,6 +321,21 @@ def main():
     ms_step = elapsed * 1e3 / args.steps
     tok_s = B * k * d * args.steps / elapsed
     log(f"timed {args.steps} steps: {ms_step:.2f} ms/step, {tok_s:.0f} lookahead tokens verified/s")
+
+    # phase timing (rollout | verify | reward + select + commit), median over steps
+    phase = {"rollout": [], "verify": [], "tail": []}
+    lens = []
+    for _ in range(args.phase_steps):
+        lens.append(float(np.sum(st.prefix.lengths())))
+        marks = []
+        eng.step(st, keywords=kw_t, reward_w=rw_t, k=k, d=d, marks=marks)
+        torch.cuda.synchronize()
+        phase["rollout"].append(marks[0].elapsed_time(marks[1]))
+        phase["verify"].append(marks[1].elapsed_time(marks[2]))
+        phase["tail"].append(marks[2].elapsed_time(marks[3]))
+    phases = phase_rooflines(wl, B, k, d, {nm: float(np.median(v)) for nm, v in phase.items()},
+                             float(np.mean(lens)) if lens else float(B * L))
+    log(json.dumps(phases))
 
     # instrumented steps: per-kernel-class HIP event timing
     eng.ctx.profile_enable(True)
@@ -358,6 +395,7 @@ def main():
                    "reward": wl.reward, "prefill_ms": round(prefill_s * 1e3, 1),
                    "tokens_emitted": emitted},
         "roofline": roof,
+        "phases": phases,
         "kernels": table,
         "cpu_baseline": cpu,
     }

@@ -77,17 +77,28 @@ class Engine:
 
     def step(self, st: DecodeState, keywords: Optional[torch.Tensor] = None,
              reward_w: Optional[torch.Tensor] = None, alpha: Optional[float] = None,
-             k: Optional[int] = None, d: Optional[int] = None) -> StepBuffers:
+             k: Optional[int] = None, d: Optional[int] = None, marks: Optional[list] = None) -> StepBuffers:
         """One lookahead step.  Updates ``st`` in place; returns the step's
-        buffers (valid until the next step with the same shape)."""
+        buffers (valid until the next step with the same shape).  With a list
+        ``marks``, timing events are appended before the rollout, after it,
+        after the verification and after the commit."""
+        def mark():
+            if marks is not None:
+                e = torch.cuda.Event(enable_timing=True)
+                e.record()
+                marks.append(e)
+
         k = k or self.k
         d = d or self.d
         alpha = self.wl.alpha if alpha is None else alpha
         B = st.prefix.B
         bf = self.buffers(B, k, d)
         c = self.ctx
+        mark()
         c.cdsl_rollout(st.prefix, st.beams, k, d, bf.lookaheads)
+        mark()
         c.cdsl_verify(st.prefix, bf.lookaheads, k, d, st.head_lp, out=bf.verify)
+        mark()
         kind = self.wl.reward
         if kind == "linear":
             c.cdsl_reward_linear(bf.verify["hidden"], reward_w, bf.reward)
@@ -99,6 +110,7 @@ class Engine:
         em, nb, nlp = c.cdsl_commit(st.prefix, bf.lookaheads, bf.beam, bf.verify["n_accept"],
                                     bf.verify["row_topk_ids"], bf.verify["row_topk_lp"], k, d,
                                     bf.next_beams, bf.next_head_lp)
+        mark()
         for b in range(B):
             st.emitted[b].extend(em[b])
         st.beams, bf.next_beams = bf.next_beams, st.beams
