@@ -55,7 +55,8 @@ def parse():
 CLASS_KERNEL = {
     "gemm_dense": (r"gemm_bf16_dense<[^>]*, 0>\(", ["gemm.hip", "gemm.h", "common.h"]),
     "gemm_skinny": (r"gemm_bf16_skinny<", ["gemm.hip", "gemm.h", "common.h"]),
-    "attention": (r"attn_mfma<", ["attention.hip", "attention.h", "common.h"]),
+    "attention": (r"attn_split<", ["attention.hip", "attention.h", "common.h"]),
+    "attn_combine": (r"attn_combine<", ["attention.hip", "attention.h", "common.h"]),
     "splitk_reduce": (r"splitk_reduce_kernel", ["gemm.hip", "gemm.h", "common.h"]),
 }
 TRAFFIC_TAG = "<!-- traffic "
