@@ -318,13 +318,14 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dense(GemmArgs a) {
 // ---------------------------------------------------------------------------
 constexpr int SKC = 64;            // K per stage (2 MFMA k-steps)
 
-template <int MT, int CT, int RING>
-__global__ __launch_bounds__(256) void gemm_bf16_skinny(GemmArgs a) {
+template <int MT, int CT, int RING, int NWV>
+__global__ __launch_bounds__(64 * NWV) void gemm_bf16_skinny(GemmArgs a) {
+  constexpr int NT = 64 * NWV;
   constexpr int BM = MT * 16;
-  constexpr int BN = 4 * CT * 16;                 // columns per workgroup
+  constexpr int BN = NWV * CT * 16;               // columns per workgroup
   constexpr int ACH = BM * (SKC / 8);             // 16-B chunks per plane per stage
-  constexpr int APT = 2 * ACH / 256;              // per thread (hi + lo) = MT
-  static_assert(2 * ACH % 256 == 0, "whole chunks per thread");
+  constexpr int APT = 2 * ACH / NT;               // per thread (hi + lo)
+  static_assert(2 * ACH % NT == 0, "whole chunks per thread");
   __shared__ __attribute__((aligned(16))) bf16 As[2][2][BM * SKC];
 
   const int tid = threadIdx.x;
@@ -352,7 +353,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_skinny(GemmArgs a) {
   // discarded).  NA register sets: A(c + NA) is fetched at stage c and
   // written to LDS at stage c + NA - 1, so each activation load has NA - 1
   // stages to arrive.
-  constexpr int NA = 4;
+  constexpr int NA = NWV == 4 ? 4 : 2;
   static_assert(RING % NA == 0, "register sets rotate with the ring");
   u32x4 ar[NA][APT];
   auto aload = [&](int c, auto set_c) __attribute__((always_inline)) {
@@ -360,7 +361,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_skinny(GemmArgs a) {
     const int k0 = kbeg + c * SKC;
 #pragma unroll
     for (int u = 0; u < APT; ++u) {
-      const int q = tid + 256 * u;
+      const int q = tid + NT * u;
       const int pl = q / ACH, cc = q % ACH;
       const int row = min(cc / 8, a.M - 1), col = (cc % 8) * 8;
       ar[st][u] = *(const u32x4*)((pl ? a.Alo : a.Ahi) + (long long)row * a.K + k0 + col);
@@ -370,7 +371,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_skinny(GemmArgs a) {
     constexpr int st = decltype(set_c)::value;
 #pragma unroll
     for (int u = 0; u < APT; ++u) {
-      const int q = tid + 256 * u;
+      const int q = tid + NT * u;
       const int pl = q / ACH, cc = q % ACH;
       const int row = cc / 8, c = cc % 8;
       *(u32x4*)&As[buf][pl][row * SKC + ((c ^ (row & 7)) << 3)] = ar[st][u];
@@ -589,7 +590,7 @@ int dense_cfg() {
 struct Plan {
   int kind;          // 0 dense, 1 skinny, 2 f32
   int cfg;           // dense tile configuration
-  int mt, ct;        // skinny row tiles, 16-column tiles per wave
+  int mt, ct, nwv;   // skinny row tiles, 16-column tiles per wave, waves
   int tiles_m, tiles_n;
   int ksplit, kchunk;
   size_t ws_bytes;
@@ -607,16 +608,19 @@ Plan make_plan(int M, int N, int K, int dtype) {
     p.kind = 1;
     p.mt = (M + 15) / 16;
     // Wide projections (>= 200 tiles of 64 columns: gate/up, LM head) run
-    // 16 columns per wave with no K split, so no partial planes are written.
-    // Narrow ones run 32 columns per wave (each activation fragment feeds
-    // two MFMA tiles) with K split to about 256 workgroups, each streaming
-    // whole rings of K stages.
+    // with no K split, so no partial planes are written: 32 columns per
+    // wave (each activation fragment feeds two MFMA tiles) when that still
+    // gives >= 200 workgroups, else 16.  Narrow ones run 32 columns per wave
+    // with K split to about 256 workgroups, each streaming whole rings of K
+    // stages.
     const int nst = K / SKC;
-    p.ct = (N + 63) / 64 >= 200 ? 1 : 2;
+    const bool wide = (N + 63) / 64 >= 200;
+    p.ct = (!wide || (N + 127) / 128 >= 200) ? 2 : 1;
+    p.nwv = 4;
     const int ring = skinny_ring(p.ct);
     p.tiles_m = 1;
-    p.tiles_n = (N + 64 * p.ct - 1) / (64 * p.ct);
-    int s = p.ct == 1 ? 1 : (256 + p.tiles_n - 1) / p.tiles_n;
+    p.tiles_n = (N + p.nwv * p.ct * 16 - 1) / (p.nwv * p.ct * 16);
+    int s = wide ? 1 : (256 + p.tiles_n - 1) / p.tiles_n;
     s = max(1, min(s, nst / ring));
     int per = (nst + s - 1) / s;
     if (nst >= ring) per = (per + ring - 1) / ring * ring;
@@ -727,8 +731,8 @@ hipError_t gemm_launch(const GemmOperand& A, const void* B, const GemmOut& out, 
     dim3 grid(p.tiles_n, 1, p.ksplit);
 #define CDSL_SKINNY(MT)                                                                     \
   case MT:                                                                                  \
-    if (p.ct == 2) gemm_bf16_skinny<MT, 2, skinny_ring(2)><<<grid, 256, 0, st>>>(a);        \
-    else gemm_bf16_skinny<MT, 1, skinny_ring(1)><<<grid, 256, 0, st>>>(a);                  \
+    if (p.ct == 2) gemm_bf16_skinny<MT, 2, skinny_ring(2), 4><<<grid, 256, 0, st>>>(a);       \
+    else gemm_bf16_skinny<MT, 1, skinny_ring(1), 4><<<grid, 256, 0, st>>>(a);                  \
     break;
     switch (p.mt) {
       CDSL_SKINNY(1)

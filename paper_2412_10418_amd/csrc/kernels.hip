@@ -58,12 +58,13 @@ __global__ __launch_bounds__(256) void embed_rows(PassDesc p, const T* __restric
 // row is first completed: x[r] += sum of the planes in split order (the
 // same arithmetic as the split-K reduce), written back to x.  g == null
 // then only folds.
-__global__ __launch_bounds__(256) void rmsnorm_rows(float* __restrict__ x, const float* __restrict__ g,
+template <int NT>
+__global__ __launch_bounds__(NT) void rmsnorm_rows(float* __restrict__ x, const float* __restrict__ g,
                                                     float* __restrict__ out32, bf16* __restrict__ ohi,
                                                     bf16* __restrict__ olo, int D, float eps, int last_only, int R,
                                                     float* __restrict__ hid, const float* __restrict__ part, int S,
                                                     int rows) {
-  __shared__ float sh[4];
+  __shared__ float sh[NT / 64];
   const int r = blockIdx.x;
   const int src = last_only ? r * R + (R - 1) : r;
   float* xr = x + (long long)src * D;
@@ -73,7 +74,7 @@ __global__ __launch_bounds__(256) void rmsnorm_rows(float* __restrict__ x, const
     // loads in flight) and added in split order
     const long long plane = (long long)rows * D;
     const float* pr = part + (long long)src * D;
-    for (int c = threadIdx.x * 4; c < D; c += 1024) {
+    for (int c = threadIdx.x * 4; c < D; c += 4 * NT) {
       float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
       for (int z0 = 0; z0 < S; z0 += 8) {
         float4 t[8];
@@ -101,15 +102,15 @@ __global__ __launch_bounds__(256) void rmsnorm_rows(float* __restrict__ x, const
       ss = fmaf(v.w, v.w, ss);
     }
   } else {
-    for (int c = threadIdx.x; c < D; c += 256) ss = fmaf(xr[c], xr[c], ss);
+    for (int c = threadIdx.x; c < D; c += NT) ss = fmaf(xr[c], xr[c], ss);
   }
   if (!g) return;
-  ss = block_sum<4>(ss, sh);
+  ss = block_sum<NT / 64>(ss, sh);
   const float inv = rsqrtf(ss / (float)D + eps);
   const long long o = (long long)r * D;
   const bool want_hid = hid && (last_only || (r % R) == R - 1);
   float* hr = want_hid ? hid + (long long)(last_only ? r : r / R) * D : nullptr;
-  for (int c = threadIdx.x; c < D; c += 256) {
+  for (int c = threadIdx.x; c < D; c += NT) {
     const float v = xr[c] * inv * g[c];
     if (out32) {
       out32[o + c] = v;
@@ -236,7 +237,8 @@ __device__ __forceinline__ void kv_slot(const PassDesc& p, int b, int i, int j, 
   }
 }
 
-__global__ __launch_bounds__(256) void rope_kv_write_split(PassDesc p, const float* __restrict__ qkv,
+template <int NT>
+__global__ __launch_bounds__(NT) void rope_kv_write_split(PassDesc p, const float* __restrict__ qkv,
                                                            float* __restrict__ qout, KVPool pool, int layer,
                                                            const float* __restrict__ cos_t,
                                                            const float* __restrict__ sin_t, int H, int Hkv, int hd,
@@ -260,7 +262,7 @@ __global__ __launch_bounds__(256) void rope_kv_write_split(PassDesc p, const flo
     bf16* kb = kl + (long long)blk * Hkv * unit;
     // q and k heads: rotate-half pairs (d, d + hd/2), four d at a time
     const int q4 = half / 4;
-    for (int u = threadIdx.x; u < (H + Hkv) * q4; u += 256) {
+    for (int u = threadIdx.x; u < (H + Hkv) * q4; u += NT) {
       const int hh = u / q4, d = (u % q4) * 4;
       const float4 x1 = src.val4(m, W, hh * hd + d), x2 = src.val4(m, W, hh * hd + d + half);
       const float4 c = *(const float4*)(ct + d), sn = *(const float4*)(stt + d);
@@ -753,7 +755,12 @@ hipError_t rmsnorm_launch(float* x, const float* g, float* out32, bf16* ohi, bf1
                           float eps, int last_only, int R, float* hid, hipStream_t st, const float* part, int S) {
   if (rows == 0) return hipSuccess;
   if (S > 0 && last_only) return hipErrorInvalidValue;
-  rmsnorm_rows<<<rows, 256, 0, st>>>(x, g, out32, ohi, olo, D, eps, last_only, R, hid, part, S, rows);
+  // few rows (the rollout): more threads per row keep more split planes'
+  // loads in flight
+  if (rows < 256)
+    rmsnorm_rows<1024><<<rows, 1024, 0, st>>>(x, g, out32, ohi, olo, D, eps, last_only, R, hid, part, S, rows);
+  else
+    rmsnorm_rows<256><<<rows, 256, 0, st>>>(x, g, out32, ohi, olo, D, eps, last_only, R, hid, part, S, rows);
   return hipGetLastError();
 }
 
@@ -766,7 +773,12 @@ hipError_t rope_kv_launch(const PassDesc& p, const float* qkv, void* qout, const
   if (dtype == 1) {
     if (hd > 256) return hipErrorInvalidValue;
     const int tasks = p.nb * p.kp * Hkv;   // V: one workgroup per (beam group, KV head)
-    rope_kv_write_split<<<M + tasks, 256, 0, st>>>(p, qkv, (float*)qout, pool, layer, cos_t, sin_t, H, Hkv, hd, S);
+    // few rows (the rollout): wider row tasks keep more split planes' loads
+    // in flight
+    if (M < 256)
+      rope_kv_write_split<512><<<M + tasks, 512, 0, st>>>(p, qkv, (float*)qout, pool, layer, cos_t, sin_t, H, Hkv, hd, S);
+    else
+      rope_kv_write_split<256><<<M + tasks, 256, 0, st>>>(p, qkv, (float*)qout, pool, layer, cos_t, sin_t, H, Hkv, hd, S);
   }
   else if (S > 1)
     return hipErrorInvalidValue;
