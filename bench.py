@@ -334,9 +334,11 @@ def main():
         phase["rollout"].append(marks[0].elapsed_time(marks[1]))
         phase["verify"].append(marks[1].elapsed_time(marks[2]))
         phase["tail"].append(marks[2].elapsed_time(marks[3]))
-    phases = phase_rooflines(wl, B, k, d, {nm: float(np.median(v)) for nm, v in phase.items()},
-                             float(np.mean(lens)) if lens else float(B * L))
-    log(json.dumps(phases))
+    phases = None
+    if args.phase_steps > 0:
+        phases = phase_rooflines(wl, B, k, d, {nm: float(np.median(v)) for nm, v in phase.items()},
+                                 float(np.mean(lens)))
+        log(json.dumps(phases))
 
     # instrumented steps: per-kernel-class HIP event timing
     eng.ctx.profile_enable(True)
@@ -346,12 +348,15 @@ def main():
     stats = eng.ctx.profile_read()
     prof_wall = (time.perf_counter() - t0) * 1e3
     eng.ctx.profile_enable(False)
-    dom, roof = roofline(stats, wl.name)
     kern_ms = sum(v["ms"] for v in stats.values())
-    table = class_table(stats, kern_ms)
-    log(json.dumps(table, indent=1))
-    log(f"instrumented: kernel time {kern_ms / args.profile_steps:.2f} ms/step of "
-        f"{prof_wall / args.profile_steps:.2f} ms/step wall")
+    if args.profile_steps > 0 and kern_ms > 0:
+        dom, roof = roofline(stats, wl.name)
+        table = class_table(stats, kern_ms)
+        log(json.dumps(table, indent=1))
+        log(f"instrumented: kernel time {kern_ms / args.profile_steps:.2f} ms/step of "
+            f"{prof_wall / args.profile_steps:.2f} ms/step wall")
+    else:   # no instrumented steps: no roofline object
+        dom, roof, table = None, None, {}
     emitted = sum(len(e) for e in st.emitted)
     if args.calibrate_copy:
         src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")

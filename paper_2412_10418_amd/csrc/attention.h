@@ -27,6 +27,7 @@ constexpr int kAttnMaxSplits = 16;
 
 struct AttnPlan {
   int row_tiles, row_groups, threads;
+  int kw;                 // key groups per row tile (1, 2 or 4)
   int nsplit, blocks_per_split;
 };
 

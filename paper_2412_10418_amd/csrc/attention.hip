@@ -116,9 +116,18 @@ __device__ __forceinline__ bool window_sees(const Window& w, int owner, int base
   return owner >= w.i_lo && owner <= w.i_hi && base <= w.slot_lim;
 }
 
-template <int HD>
+// KW = key groups: the 4 waves are (4 / KW) row tiles x KW key groups,
+// and one iteration stages KW pairs of key blocks: wave (rt, kw) computes
+// pair kw of it for row tile rt, and the key groups of a row tile merge
+// their (m, l, O) states at the end.  KW > 1 keeps every wave busy, and
+// the grid full, when a (prompt, KV head) has few row tiles (the rollout:
+// k beams x G heads); the chain of dependent memory round trips (block
+// table, then one per iteration) is then short.
+template <int HD, int KW>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_split(AttnArgs a) {
-  constexpr int NT = 256;                      // 4 waves x 16 rows
+  constexpr int NT = 256;                      // 4 waves
+  constexpr int RTW = 4 / KW;                  // row tiles per workgroup
+  constexpr int NPI = KW;                      // pairs per iteration
   constexpr int KCH = HD / 8;                  // 16-byte chunks per K row
   constexpr int KPL = 2 * kBlock * HD;         // LDS K plane: 2 blocks x 16 keys x HD
   constexpr int VPL = 2 * HD * kBlock;         // LDS V plane: HD x (4 groups x (4 keys of A, 4 of B))
@@ -129,7 +138,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   constexpr int KS = HD / 32;                  // k-steps of the score product
   constexpr int DT = HD / 16;                  // 16-dim output tiles
   static_assert(UCH % NT == 0, "static chunk regions");
-  __shared__ __attribute__((aligned(16))) bf16 lds[2][BUF];
+  __shared__ __attribute__((aligned(16))) bf16 lds[2][NPI][BUF];
   __shared__ int lblk[kAttnMaxList];
   __shared__ int lmeta[kAttnMaxList];   // base * 32 + owner + 1
   __shared__ int lcount;
@@ -143,7 +152,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   const int b = pass_batch(p, bi);
   const int G = a.G;
   const int nrows = p.kp * p.R * G;
-  const int wg_r0 = blockIdx.z * 64;
+  const int wg_r0 = blockIdx.z * 16 * RTW;
   if (wg_r0 >= nrows) return;   // uniform over the workgroup
   const int Lp = p.Lp[b];
 
@@ -155,7 +164,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   const int qend = min(min(nK, qbeg + a.blocks_per_split), qbeg + kAttnMaxList);
 
   // this wave's rows (a wave past the last row still stages key blocks)
-  const int rw0 = wg_r0 + wave * 16;
+  const int rt = wave / KW, kw = wave % KW;
+  const int rw0 = wg_r0 + rt * 16;
   const bool wave_has_rows = rw0 < nrows;
   const RowInfo ri = decode_row(p, rw0 + lr, nrows, bi, kvh, G, Lp);
   const Window wwin = row_window(p, min(rw0, nrows - 1), min(rw0 + 15, nrows - 1), G, Lp);
@@ -175,7 +185,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
 
   // list of the key blocks that some row of the workgroup can see
   if (wave == 0) {
-    const Window ww = row_window(p, wg_r0, min(wg_r0 + 64, nrows) - 1, G, Lp);
+    const Window ww = row_window(p, wg_r0, min(wg_r0 + 16 * RTW, nrows) - 1, G, Lp);
     int n = 0;
     for (int c0 = qbeg; c0 < qend; c0 += 64) {
       const int q = c0 + lane;
@@ -198,6 +208,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   __syncthreads();
   const int n = lcount;
   const int npairs = (n + 1) / 2;
+  const int niters = (npairs + NPI - 1) / NPI;
 
   bf16x8 qh[KS], ql[KS];
 #pragma unroll
@@ -221,33 +232,41 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     const int dim = wp >> 1, h = wp & 1;
     return 2 * KPL + plane * VPL + dim * 32 + h * 16 + (region - 2) * 4;
   };
-  // staging registers: pair pi + 1 is in flight while pair pi is computed
-  u32x4 stg[PER];
-  auto gload = [&](u32x4* r, int pi) __attribute__((always_inline)) {
-    const int eA = min(2 * pi, n - 1);
-    const int eB = min(2 * pi + 1, n - 1);
-    const long long ua = ((long long)lblk[eA] * a.Hkv + kvh) * UNIT;
-    const long long ub = ((long long)lblk[eB] * a.Hkv + kvh) * UNIT;
+  // staging registers: the pairs of iteration it + 1 are in flight while
+  // those of iteration it are computed (pairs past the last one re-read
+  // the last block and are not computed)
+  u32x4 stg[NPI][PER];
+  auto gload = [&](int it) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < PER; ++u) {
-      const int region = (NT * u) / UCH;   // exact: tid < NT <= UCH
-      const bf16* base = (region < 2 ? kpool : vpool) + ((region & 1) ? ub : ua);
-      r[u] = *(const u32x4*)(base + ((tid + NT * u) % UCH) * 8);
-    }
-  };
-  auto sstore = [&](const u32x4* r, int buf) __attribute__((always_inline)) {
+    for (int q = 0; q < NPI; ++q) {
+      const int pi = it * NPI + q;
+      const int eA = min(2 * pi, n - 1);
+      const int eB = min(2 * pi + 1, n - 1);
+      const long long ua = ((long long)lblk[eA] * a.Hkv + kvh) * UNIT;
+      const long long ub = ((long long)lblk[eB] * a.Hkv + kvh) * UNIT;
 #pragma unroll
-    for (int u = 0; u < PER; ++u) {
-      const int region = (NT * u) / UCH;
-      bf16* d = &lds[buf][dst_of(u)];
-      if (region < 2) {
-        *(u32x4*)d = r[u];
-      } else {
-        // keys 8h..8h+3 -> group 2h, keys 8h+4..8h+7 -> group 2h + 1
-        *(uint2*)d = make_uint2(r[u].x, r[u].y);
-        *(uint2*)(d + 8) = make_uint2(r[u].z, r[u].w);
+      for (int u = 0; u < PER; ++u) {
+        const int region = (NT * u) / UCH;   // exact: tid < NT <= UCH
+        const bf16* base = (region < 2 ? kpool : vpool) + ((region & 1) ? ub : ua);
+        stg[q][u] = *(const u32x4*)(base + ((tid + NT * u) % UCH) * 8);
       }
     }
+  };
+  auto sstore = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < NPI; ++q)
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int region = (NT * u) / UCH;
+        bf16* d = &lds[buf][q][dst_of(u)];
+        if (region < 2) {
+          *(u32x4*)d = stg[q][u];
+        } else {
+          // keys 8h..8h+3 -> group 2h, keys 8h+4..8h+7 -> group 2h + 1
+          *(uint2*)d = make_uint2(stg[q][u].x, stg[q][u].y);
+          *(uint2*)(d + 8) = make_uint2(stg[q][u].z, stg[q][u].w);
+        }
+      }
   };
 
   f32x4 acc[DT];
@@ -274,8 +293,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   // holds keys 4lg..4lg+3 of A and of B -- which, in that order, is the
   // lane's B fragment of O^T[16 dims, 16 rows] += V^T[16 dims, 32 keys] .
   // P^T[32 keys, 16 rows] when the V^T fragment takes the same keys.
-  auto compute = [&](int buf, int pi) __attribute__((always_inline)) {
+  auto compute = [&](int buf, int slot, int pi) __attribute__((always_inline)) {
     const int eA = 2 * pi, eB = 2 * pi + 1;
+    if (eA >= n) return;   // past the last pair (uniform over the wave)
     const bool hasB = eB < n;
     const int mA = lmeta[eA], mB = hasB ? lmeta[eB] : 0;
     const int ownA = (mA & 31) - 1, baseA = mA >> 5;
@@ -283,7 +303,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     const bool relA = window_sees(wwin, ownA, baseA);
     const bool relB = hasB && window_sees(wwin, ownB, baseB);
     if (!wave_has_rows || (!relA && !relB)) return;
-    const bf16* L = lds[buf];
+    const bf16* L = lds[buf][slot];
     f32x4 sA = {0.f, 0.f, 0.f, 0.f}, sB = sA;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
@@ -346,24 +366,55 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     }
   };
 
-  // pair pi sits in LDS buffer pi & 1
-  if (npairs > 0) {
-    gload(stg, 0);
-    sstore(stg, 0);
+  // iteration it (pairs it * NPI .. + NPI - 1) sits in LDS buffer it & 1
+  if (niters > 0) {
+    gload(0);
+    sstore(0);
     __syncthreads();
   }
-  for (int pi = 0; pi < npairs; ++pi) {
-    const bool more = pi + 1 < npairs;
-    if (more) gload(stg, pi + 1);
-    compute(pi & 1, pi);
-    if (more) sstore(stg, (pi + 1) & 1);
+  for (int it = 0; it < niters; ++it) {
+    const bool more = it + 1 < niters;
+    if (more) gload(it + 1);
+    compute(it & 1, kw, it * NPI + kw);
+    if (more) sstore((it + 1) & 1);
     __syncthreads();
   }
 
-  if (!wave_has_rows) return;
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
-  if (!ri.valid) return;
+  if constexpr (KW > 1) {
+    // key groups 1.. hand (m, l, O) to group 0 of their row tile through
+    // LDS (free after the loop's last barrier); group 0 merges them in
+    // group order
+    constexpr int SLOT = (2 + 4 * DT) * 64;   // floats per wave
+    float* X = (float*)&lds[0][0][0];
+    if (wave_has_rows && kw > 0) {
+      float* x = X + (rt * (KW - 1) + kw - 1) * SLOT;
+      x[lane] = m_run;
+      x[64 + lane] = l_run;
+#pragma unroll
+      for (int t = 0; t < DT; ++t)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[(2 + 4 * t + e) * 64 + lane] = acc[t][e];
+    }
+    __syncthreads();
+    if (kw > 0 || !wave_has_rows) return;
+#pragma unroll
+    for (int q = 1; q < KW; ++q) {
+      const float* x = X + (rt * (KW - 1) + q - 1) * SLOT;
+      const float mq = x[lane], lq = x[64 + lane];
+      const float mn = fmaxf(m_run, mq);
+      const float s0 = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - mn);
+      const float s1 = mq == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mq - mn);
+      l_run = l_run * s0 + lq * s1;
+#pragma unroll
+      for (int t = 0; t < DT; ++t)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[t][e] = acc[t][e] * s0 + x[(2 + 4 * t + e) * 64 + lane] * s1;
+      m_run = mn;
+    }
+  }
+  if (!wave_has_rows || !ri.valid) return;
   const long long rowid = (long long)ri.m * a.H + ri.h;
   // lane (row lr, lg) holds dims 16t + 4lg .. +3
   if (a.nsplit == 1) {
@@ -535,15 +586,22 @@ AttnPlan attn_plan(const PassDesc& p, int H, int Hkv, int hd, int dtype, int max
     return pl;
   }
   // 16-row tiles, 4 waves per workgroup (a wave without rows still stages
-  // its share of the key blocks)
+  // its share of the key blocks).  At most 2 row tiles: the waves become
+  // key groups instead -- 4 of them and one row tile per workgroup at
+  // hd = 64; 2, with both row tiles in one workgroup, at hd = 128 (LDS:
+  // 2 x 32 KB per key group).
   pl.row_tiles = (nrows + 15) / 16;
   pl.threads = 256;
-  pl.row_groups = (pl.row_tiles + 3) / 4;
+  pl.kw = pl.row_tiles <= 2 ? (hd == 64 ? 4 : 2) : 1;
+  const int rtw = 4 / pl.kw;
+  pl.row_groups = (pl.row_tiles + rtw - 1) / rtw;
   // enough workgroups for two per CU, >= 1 key-block pair per split, and at
-  // most kAttnMaxList key blocks per split; no split (and no combine) when
-  // the grid already holds two workgroups per CU
+  // most kAttnMaxList key blocks per split; no split (and no combine
+  // launch) when the grid already holds two workgroups per CU or when a
+  // workgroup's chain of pair iterations is short
   const int base = p.nb * Hkv * pl.row_groups;
-  int s = base >= 512 ? 1 : (1024 + base - 1) / base;
+  const int iters1 = ((nK + 1) / 2 + pl.kw - 1) / pl.kw;
+  int s = (base >= 512 || iters1 <= 8) ? 1 : (1024 + base - 1) / base;
   s = std::min(s, (nK + 1) / 2);
   s = std::max(s, (nK + kAttnMaxList - 1) / kAttnMaxList);
   s = std::max(1, std::min(s, std::min(max_splits, kAttnMaxSplits)));
@@ -572,10 +630,15 @@ hipError_t attn_launch(const AttnArgs& args, const AttnPlan& pl, int hd, int dty
   }
   if (pl.blocks_per_split > kAttnMaxList) return hipErrorInvalidValue;
   dim3 grid(pl.nsplit, a.p.nb * a.Hkv, pl.row_groups);
-  switch (hd) {
-    case 64: attn_split<64><<<grid, 256, 0, st>>>(a); break;
-    case 128: attn_split<128><<<grid, 256, 0, st>>>(a); break;
-    default: return hipErrorInvalidValue;
+  // LDS: 2 buffers x KW pairs of 16 KB (hd 64) or 32 KB (hd 128)
+  if (hd == 64) {
+    if (pl.kw == 4) attn_split<64, 4><<<grid, 256, 0, st>>>(a);
+    else attn_split<64, 1><<<grid, 256, 0, st>>>(a);
+  } else if (hd == 128) {
+    if (pl.kw == 2) attn_split<128, 2><<<grid, 256, 0, st>>>(a);
+    else attn_split<128, 1><<<grid, 256, 0, st>>>(a);
+  } else {
+    return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }

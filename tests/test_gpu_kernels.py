@@ -26,6 +26,8 @@ def _bf16_mat(rng, shape, scale=1.0):
     (129, 384, 256),       # first dense shape, ragged
     (800, 4096, 4096),     # target o-projection of the verification block (split K)
     (800, 1300, 1024),     # dense, ragged columns of the last tile
+    (333, 700, 576),       # dense, ragged rows and columns, odd number of K stages
+    (160, 256, 64),        # dense, exactly one block and one K stage
     (50, 200, 512),        # skinny, ragged columns
 ])
 def test_gemm_bf16_matches_float64(M, N, K):
