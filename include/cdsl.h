@@ -19,6 +19,10 @@
  *   cdsl_commit    emits the selected beam's head plus its accepted tokens
  *                  (S1 action of Sec. 3.2.3, no bonus token), makes them part
  *                  of the shared prefix and produces the next beam heads
+ *   cdsl_rollout_with, cdsl_reward_keywords_upto, cdsl_commit_heads
+ *                  the pieces of the paper's full controller (Alg. 1 states
+ *                  S1..S4) and of its baselines CDLH (target-rolled
+ *                  lookaheads) and CDLH-appx. (draft-rolled, unverified)
  *
  * Conventions
  *   - Every call returns CDSL_OK (0) or a negative CDSL_E* code; the message
@@ -29,8 +33,9 @@
  *     They are owned by the caller and only read/written during the call
  *     (device work is ordered on the context's stream).
  *   - Calls are asynchronous on the stream given to cdsl_init, except
- *     cdsl_commit, which synchronises that stream once (it must learn how
- *     many tokens each prompt emitted to manage the KV blocks).
+ *     cdsl_commit and cdsl_commit_heads, which synchronise that stream once
+ *     (they must learn how many tokens each prompt emitted to manage the KV
+ *     blocks).
  *   - Shapes are row-major, innermost last.  Token ids are int32 in [0, V).
  *   - Nothing is allocated after cdsl_init except by cdsl_prefill (the
  *     prefix handle's bookkeeping; KV blocks come from the pool sized at
@@ -130,6 +135,15 @@ int cdsl_prefill(cdsl_ctx* ctx, const int32_t* tokens, int32_t B, int32_t L,
 int cdsl_rollout(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* beams,
                  int32_t k, int32_t d, int32_t* lookaheads);
 
+/* cdsl_rollout with a choice of roller: 0 = the draft model (as
+ * cdsl_rollout), 1 = the target model.  The target rolls the lookaheads of
+ * the lookahead-heuristic baseline (CDLH: Sec. 2.1 and the appendix
+ * algorithm, lookaheads generated by M_p); the draft rolls those of its
+ * approximate variant (CDLH-appx., Sec. 3.1).  Same layout, ordering and
+ * errors as cdsl_rollout, plus EINVAL for another roller. */
+int cdsl_rollout_with(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* beams,
+                      int32_t k, int32_t d, int32_t roller, int32_t* lookaheads);
+
 /* Target verification of lookaheads[B, k, d+1] (any values, not only those
  * of the last rollout: the call depends on its arguments and the prefix
  * only).  Feeds rows (i, j) = lookaheads[b, i, j], j = 0..d-1, at positions
@@ -149,6 +163,17 @@ int cdsl_verify(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookaheads,
                 int32_t* target_argmax, int32_t* n_accept, float* scores,
                 int32_t* row_topk_ids, float* row_topk_lp, float* hidden);
 
+/* cdsl_verify with a top-k width kk (1..max_k) that differs from the beam
+ * count: row_topk_ids / row_topk_lp are [B, k, d, kk].  The paper's Alg. 1
+ * drafts one sequence (k = 1) but its Step-2 needs the k best target tokens
+ * after the accepted ones (Sec. 3.2.3).  cdsl_verify is kk = k.  Errors as
+ * cdsl_verify, plus ERANGE for kk. */
+int cdsl_verify_kk(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookaheads,
+                   int32_t k, int32_t d, int32_t kk, const float* head_lp,
+                   float* logprobs, int32_t* target_argmax, int32_t* n_accept,
+                   float* scores, int32_t* row_topk_ids, float* row_topk_lp,
+                   float* hidden);
+
 /* Keyword reward: for every beam, the number of distinct keywords of
  * keywords[b, 0..n_kw) that occur in generated-so-far + lookaheads[b, i,
  * 0..d] (the prompt is not searched).  With normalize != 0 the count is
@@ -158,6 +183,17 @@ int cdsl_reward_keywords(cdsl_ctx* ctx, cdsl_prefix* prefix,
                          const int32_t* lookaheads, int32_t k, int32_t d,
                          const int32_t* keywords, int32_t n_kw, int32_t normalize,
                          float* reward);
+
+/* cdsl_reward_keywords over a shorter window: generated-so-far + the head
+ * of beam i + its first upto[b, i] lookahead tokens (clamped to 0..d);
+ * upto [B, k] int32 on the device, or NULL for all d.  With upto = the
+ * verify's n_accept this is the reward of the accepted tokens, R(x_1..x_n)
+ * in the rejection step of the paper's Alg. 1 (Sec. 3.2.2-3.2.3).  Errors
+ * as cdsl_reward_keywords. */
+int cdsl_reward_keywords_upto(cdsl_ctx* ctx, cdsl_prefix* prefix,
+                              const int32_t* lookaheads, int32_t k, int32_t d,
+                              const int32_t* upto, const int32_t* keywords,
+                              int32_t n_kw, int32_t normalize, float* reward);
 
 /* Linear reward head: reward[b, i] = dot(w, hidden[b, i, :]), hidden as
  * written by cdsl_verify, w [D] fp32.  Errors: EINVAL. */
@@ -184,6 +220,33 @@ int cdsl_commit(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookaheads,
                 const int32_t* row_topk_ids, const float* row_topk_lp,
                 int32_t k, int32_t d, int32_t* emitted_host,
                 int32_t* n_emit_host, int32_t* next_beams, float* next_head_lp);
+
+/* cdsl_commit after cdsl_verify_kk: row_topk_* are [B, k, d, kk] and
+ * next_beams / next_head_lp [B, kk].  cdsl_commit is kk = k.  Errors as
+ * cdsl_commit; ESTATE also when the last verify used another kk. */
+int cdsl_commit_kk(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookaheads,
+                   const int32_t* beam, const int32_t* n_accept,
+                   const int32_t* row_topk_ids, const float* row_topk_lp,
+                   int32_t k, int32_t d, int32_t kk, int32_t* emitted_host,
+                   int32_t* n_emit_host, int32_t* next_beams, float* next_head_lp);
+
+/* Head-only commit: after a rollout (no verification needed), prompt b with
+ * mask_host[b] != 0 (mask_host NULL: every prompt) emits the head of beam
+ * beam[b], c = lookaheads[b, beam[b], 0], and nothing else: one token
+ * generated by lookahead-heuristic decoding (CDLH / CDLH-appx., Sec. 2.1,
+ * 3.1 and the appendix algorithm; also the single token of the S2/S3/S4
+ * branches of Sec. 3.2.3).  The token is fed through both models at the end
+ * of the prefix; the rolled suffixes are dropped.  emitted_host[b] is the
+ * token or -1 (host, [B]); next_beams / next_head_lp [B, kk] of emitting
+ * prompts receive the top-kk of the target after it, the other prompts'
+ * rows are left as they are.  Synchronises the context stream once.
+ * Errors: EINVAL (beam -1 or out of range for an emitting prompt), ERANGE
+ * (max_ctx, kk), ENOMEM, ESTATE (no rollout with this k and d since the
+ * last commit). */
+int cdsl_commit_heads(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookaheads,
+                      const int32_t* beam, int32_t k, int32_t d, int32_t kk,
+                      const int32_t* mask_host, int32_t* emitted_host,
+                      int32_t* next_beams, float* next_head_lp);
 
 /* Current length (prompt + emitted) of every prompt: lengths_host[B]. */
 int cdsl_prefix_lengths(cdsl_ctx* ctx, const cdsl_prefix* prefix,

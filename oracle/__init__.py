@@ -10,7 +10,9 @@ implementation of the same architecture; incremental = full recompute =
 tree-parallel verification; greedy rollout = argmax of a full forward; k = 1
 reduces to plain greedy decoding of the target; draft = target accepts every
 lookahead token; beam selection against brute-force enumeration on a tiny
-vocabulary; the paper's worked reward value (2 of 5 concepts -> 0.4).
+vocabulary; the paper's worked reward value (2 of 5 concepts -> 0.4); the
+lookahead-heuristic baselines and the Alg. 1 controller against greedy
+decoding of the target and against full recomputation.
 """
 from .decoder import Decoder, KVCache, ForwardOut, rms_norm, rope  # noqa: F401
 from .cdsl import (  # noqa: F401
@@ -18,4 +20,5 @@ from .cdsl import (  # noqa: F401
     log_softmax, argmax_lowest, topk_ids, top2_margin, leading_matches,
     keyword_hits, keyword_coverage, select_beam, reward_for,
     verify_rows_tree, verify_rows_per_beam,
+    keyword_reward, argmax_first, lookahead_heads, cdlh_step, controller_step, HeadStep, ControllerStep,
 )

@@ -279,3 +279,138 @@ def step(draft: Decoder, target: Decoder, st: PromptState, k: int, d: int, alpha
     emitted = [int(heads[b])] + [int(t) for t in ro.x[b, :n]]
     nst = commit(draft, target, st, emitted)
     return StepResult(heads, head_lp, hm, ro, ve, r, comb, b, emitted, nst)
+
+
+# ----------------------------------------------------------------------------
+# the baselines (CDLH, CDLH-appx.) and the full controller (Alg. 1 states)
+# ----------------------------------------------------------------------------
+def keyword_reward(kind: str, window: Sequence[int], kws: Sequence[int]) -> float:
+    """The lexical reward R of Sec. 4.1 on one token window: the number of
+    distinct concepts present, or that number over the number of concepts."""
+    if kind == "keyword_count":
+        return float(keyword_hits(window, kws))
+    if kind == "keyword_coverage":
+        return keyword_coverage(window, kws)
+    raise ValueError(f"the controller and the baselines take a lexical reward, not {kind!r}")
+
+
+def argmax_first(values: Sequence[float]) -> int:
+    """Index of the largest value, the first one on ties (the strict '>'
+    update of the appendix algorithm)."""
+    best = 0
+    for i in range(1, len(values)):
+        if values[i] > values[best]:
+            best = i
+    return best
+
+
+@dataclass
+class HeadStep:
+    heads: np.ndarray          # [k] top-k of M_p at the prefix end
+    x: np.ndarray              # [k, d] greedy lookahead of every head (by the roller)
+    margin: np.ndarray         # [k, d] top-2 margin of the roller at each draw
+    reward: np.ndarray         # [k]
+    pick: int
+    token: int                 # the one emitted token
+    state: PromptState         # after it
+    head_margin: float         # smallest gap among the target's top-(k+1) logits
+
+
+def lookahead_heads(roller: Decoder, roller_cache: KVCache, st: PromptState, k: int, d: int):
+    """The k candidate tokens of the appendix algorithm -- the top-k of M_p
+    at the prefix end, value descending, lowest id first on ties -- each
+    followed by d greedy tokens of the roller on its own copy of the cache."""
+    heads = topk_ids(st.s_logits, k)
+    x = np.zeros((k, d), np.int64)
+    mg = np.zeros((k, d))
+    for i, c in enumerate(heads):
+        cache = roller_cache
+        fed = int(c)
+        for j in range(d):
+            out, cache = roller.extend(cache, [fed])
+            z = out.logits[0]
+            x[i, j] = argmax_lowest(z)
+            mg[i, j] = top2_margin(z)
+            fed = int(x[i, j])
+    return heads, x, mg
+
+
+def cdlh_step(roller_is_target: bool, draft: Decoder, target: Decoder, st: PromptState, k: int, d: int,
+              reward_kind: str, kws: Sequence[int], prefer_first_at: Optional[float] = None) -> HeadStep:
+    """One token of lookahead-heuristic decoding (Sec. 2.1 and the appendix
+    algorithm): every top-k candidate of M_p is extended by d greedy tokens,
+    by M_p itself (CDLH) or by the draft M_q (CDLH-appx., Sec. 3.1); R scores
+    generated-so-far + candidate + lookahead (the prompt is left out, as in
+    the step), and the best candidate is the one token emitted.
+
+    prefer_first_at = r_t gives Step-1 of Alg. 1 with b = 1: the first
+    candidate -- M_p's own greedy token -- is taken when its lookahead
+    reaches the reward threshold, else Step-2 picks the best."""
+    roller = target if roller_is_target else draft
+    cache = st.target_cache if roller_is_target else st.draft_cache
+    heads, x, mg = lookahead_heads(roller, cache, st, k, d)
+    r = np.array([keyword_reward(reward_kind, list(st.generated) + [int(heads[i])] + [int(t) for t in x[i]], kws)
+                  for i in range(k)])
+    if prefer_first_at is not None and r[0] >= prefer_first_at:
+        pick = 0
+    else:
+        pick = argmax_first(r)
+    tok = int(heads[pick])
+    top = np.sort(st.s_logits)[::-1][:k + 1]
+    hm = float(np.min(-np.diff(top))) if len(top) > 1 else math.inf
+    return HeadStep(heads, x, mg, r, pick, tok, commit(draft, target, st, [tok]), hm)
+
+
+@dataclass
+class ControllerStep:
+    head: int                  # c: M_p's greedy token at the prefix end
+    head_lp: float
+    head_margin: float         # gap between the target's top two logits
+    x: np.ndarray              # [d] draft lookahead after c
+    draft_margin: np.ndarray   # [d] top-2 margins of the draft draws
+    ver: Verify                # k = 1 verification of [c, x_1..x_{d-1}]
+    n: int
+    a: float                   # n / d
+    r: float                   # R(generated + c + x_1..x_n)
+    state: str                 # "S1", "S2/S3" or "S4"
+    extra: Optional[HeadStep]  # the one-token action of S2/S3 and S4
+    emitted: List[int]
+    after: PromptState
+
+
+def controller_step(draft: Decoder, target: Decoder, st: PromptState, k: int, d: int, a_t: float, r_t: float,
+                    b: int, reward_kind: str, kws: Sequence[int]) -> ControllerStep:
+    """One iteration of Alg. 1 (Sec. 3.2.1-3.2.3) with hard rejection.
+
+    Readings: the draft starts after M_p's greedy token c (the head of the
+    k = 1 step) instead of straight from pfx; that token is emitted in every
+    state, like the accepted lookahead tokens.  The acceptance is a = n / d
+    and the reward r = R(generated + c + x_1..x_n), the accepted window.
+      S1 (a >= a_t and r >= r_t): O = [c, x_1..x_n].
+      S2/S3 (a < a_t): O = [c, x_1..x_n] + one token.  Step-1 with b = 1
+          takes M_p's greedy token X_1 after that if its draft lookahead
+          scores R >= r_t; otherwise (and with b = 0) Step-2, i.e. the
+          CDLH-appx. token with k candidates.
+      S4 (a >= a_t, r < r_t): O = [c, x_1..x_n] + the CDLH-appx. token.
+    b > 1 is not taken: it would need M_p tokens appended tentatively and
+    dropped again when the reward stays low (the selected configurations of
+    the paper use b <= 1)."""
+    if b not in (0, 1):
+        raise ValueError("b must be 0 or 1")
+    heads, head_lp, hm = beam_heads(st, 1)
+    c = int(heads[0])
+    ro = rollout(draft, st, [c], d)
+    ve = verify(target, st, [c], head_lp, ro.x)
+    n = int(ve.n[0])
+    a = n / d
+    acc = [c] + [int(t) for t in ro.x[0, :n]]
+    r = keyword_reward(reward_kind, list(st.generated) + acc, kws)
+    st1 = commit(draft, target, st, acc)
+    if a >= a_t and r >= r_t:
+        return ControllerStep(c, float(head_lp[0]), float(hm[0]), ro.x[0], ro.margin[0], ve, n, a, r, "S1", None,
+                              acc, st1)
+    state = "S2/S3" if a < a_t else "S4"
+    pref = r_t if (state == "S2/S3" and b == 1) else None
+    hs = cdlh_step(False, draft, target, st1, k, d, reward_kind, kws, prefer_first_at=pref)
+    return ControllerStep(c, float(head_lp[0]), float(hm[0]), ro.x[0], ro.margin[0], ve, n, a, r, state, hs,
+                          acc + [hs.token], hs.state)

@@ -20,8 +20,11 @@ CDSL_EPI_STORE, CDSL_EPI_RESIDUAL = 0, 1
 ERR_NAMES = {0: "OK", -1: "EINVAL", -2: "ERANGE", -3: "ENOMEM", -4: "EDEVICE", -5: "ESTATE"}
 
 EXPORTS = [
-    "cdsl_init", "cdsl_prefill", "cdsl_rollout", "cdsl_verify", "cdsl_reward_keywords",
-    "cdsl_reward_linear", "cdsl_select", "cdsl_commit", "cdsl_prefix_lengths",
+    "cdsl_init", "cdsl_prefill", "cdsl_rollout", "cdsl_rollout_with", "cdsl_verify", "cdsl_verify_kk",
+    "cdsl_reward_keywords",
+    "cdsl_reward_keywords_upto", "cdsl_reward_linear", "cdsl_select", "cdsl_commit", "cdsl_commit_kk",
+    "cdsl_commit_heads",
+    "cdsl_prefix_lengths",
     "cdsl_free_prefix", "cdsl_destroy", "cdsl_last_error", "cdsl_profile_enable", "cdsl_profile_read",
     "cdsl_op_gemm_workspace", "cdsl_op_gemm", "cdsl_op_logit_rows",
 ]
@@ -75,6 +78,11 @@ def lib():
         "cdsl_init": ([C.POINTER(Model), C.POINTER(Model), C.POINTER(Limits), vp, C.POINTER(vp)], i32),
         "cdsl_prefill": ([vp, vp, i32, i32, i32, C.POINTER(vp), vp, vp], i32),
         "cdsl_rollout": ([vp, vp, vp, i32, i32, vp], i32),
+        "cdsl_rollout_with": ([vp, vp, vp, i32, i32, i32, vp], i32),
+        "cdsl_reward_keywords_upto": ([vp, vp, vp, i32, i32, vp, vp, i32, i32, vp], i32),
+        "cdsl_commit_heads": ([vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp], i32),
+        "cdsl_verify_kk": ([vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp], i32),
+        "cdsl_commit_kk": ([vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp], i32),
         "cdsl_verify": ([vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp], i32),
         "cdsl_reward_keywords": ([vp, vp, vp, i32, i32, vp, i32, i32, vp], i32),
         "cdsl_reward_linear": ([vp, vp, vp, i32, i32, i32, vp], i32),
@@ -252,21 +260,41 @@ class Context:
         _check(rc, self.handle)
         return lookaheads
 
+    def cdsl_rollout_with(self, prefix: Prefix, beams: torch.Tensor, k: int, d: int, roller: int,
+                          lookaheads: Optional[torch.Tensor] = None) -> torch.Tensor:
+        if lookaheads is None:
+            lookaheads = torch.empty((prefix.B, k, d + 1), dtype=torch.int32, device=beams.device)
+        rc = lib().cdsl_rollout_with(self.handle, prefix.handle, _ptr(beams, torch.int32, "beams"), k, d,
+                                     int(roller), _ptr(lookaheads, torch.int32, "lookaheads"))
+        _check(rc, self.handle)
+        return lookaheads
+
     def cdsl_verify(self, prefix: Prefix, lookaheads: torch.Tensor, k: int, d: int, head_lp: torch.Tensor,
-                    want_hidden: bool = False, out: Optional[dict] = None) -> dict:
+                    want_hidden: bool = False, out: Optional[dict] = None, kk: Optional[int] = None) -> dict:
+        """kk: top-k width of row_topk (default k; another value uses cdsl_verify_kk)."""
         B = prefix.B
         dev = lookaheads.device
+        kk = k if kk is None else kk
         if out is None:
             out = {
                 "logprobs": torch.empty((B, k, d), dtype=torch.float32, device=dev),
                 "target_argmax": torch.empty((B, k, d), dtype=torch.int32, device=dev),
                 "n_accept": torch.empty((B, k), dtype=torch.int32, device=dev),
                 "scores": torch.empty((B, k), dtype=torch.float32, device=dev),
-                "row_topk_ids": torch.empty((B, k, d, k), dtype=torch.int32, device=dev),
-                "row_topk_lp": torch.empty((B, k, d, k), dtype=torch.float32, device=dev),
+                "row_topk_ids": torch.empty((B, k, d, kk), dtype=torch.int32, device=dev),
+                "row_topk_lp": torch.empty((B, k, d, kk), dtype=torch.float32, device=dev),
                 "hidden": (torch.empty((B, k, self.target_shape.d_model), dtype=torch.float32, device=dev)
                            if want_hidden else None),
             }
+        if kk != k:
+            rc = lib().cdsl_verify_kk(self.handle, prefix.handle, _ptr(lookaheads, torch.int32, "lookaheads"), k,
+                                      d, kk, _ptr(head_lp, torch.float32, "head_lp"), out["logprobs"].data_ptr(),
+                                      out["target_argmax"].data_ptr(), out["n_accept"].data_ptr(),
+                                      out["scores"].data_ptr(), out["row_topk_ids"].data_ptr(),
+                                      out["row_topk_lp"].data_ptr(),
+                                      out["hidden"].data_ptr() if out.get("hidden") is not None else None)
+            _check(rc, self.handle)
+            return out
         rc = lib().cdsl_verify(self.handle, prefix.handle, _ptr(lookaheads, torch.int32, "lookaheads"), k, d,
                                _ptr(head_lp, torch.float32, "head_lp"), out["logprobs"].data_ptr(),
                                out["target_argmax"].data_ptr(), out["n_accept"].data_ptr(),
@@ -283,6 +311,18 @@ class Context:
         rc = lib().cdsl_reward_keywords(self.handle, prefix.handle, _ptr(lookaheads, torch.int32, "lookaheads"),
                                         k, d, _ptr(keywords, torch.int32, "keywords"), keywords.shape[1],
                                         1 if normalize else 0, reward.data_ptr())
+        _check(rc, self.handle)
+        return reward
+
+    def cdsl_reward_keywords_upto(self, prefix: Prefix, lookaheads, k, d, upto: Optional[torch.Tensor], keywords,
+                                  normalize: bool, reward: Optional[torch.Tensor] = None):
+        if reward is None:
+            reward = torch.empty((prefix.B, k), dtype=torch.float32, device=lookaheads.device)
+        rc = lib().cdsl_reward_keywords_upto(self.handle, prefix.handle,
+                                             _ptr(lookaheads, torch.int32, "lookaheads"), k, d,
+                                             _ptr(upto, torch.int32, "upto") if upto is not None else None,
+                                             _ptr(keywords, torch.int32, "keywords"), keywords.shape[1],
+                                             1 if normalize else 0, reward.data_ptr())
         _check(rc, self.handle)
         return reward
 
@@ -306,23 +346,49 @@ class Context:
         return beam
 
     def cdsl_commit(self, prefix: Prefix, lookaheads, beam, n_accept, row_topk_ids, row_topk_lp, k, d,
-                    next_beams: Optional[torch.Tensor] = None, next_head_lp: Optional[torch.Tensor] = None):
+                    next_beams: Optional[torch.Tensor] = None, next_head_lp: Optional[torch.Tensor] = None,
+                    kk: Optional[int] = None):
+        """kk: top-k width of row_topk and of the next heads (default k; another
+        value uses cdsl_commit_kk)."""
         B = prefix.B
         dev = lookaheads.device
+        kk = k if kk is None else kk
         if next_beams is None:
-            next_beams = torch.empty((B, k), dtype=torch.int32, device=dev)
+            next_beams = torch.empty((B, kk), dtype=torch.int32, device=dev)
         if next_head_lp is None:
-            next_head_lp = torch.empty((B, k), dtype=torch.float32, device=dev)
+            next_head_lp = torch.empty((B, kk), dtype=torch.float32, device=dev)
         emitted = (C.c_int32 * (B * (d + 1)))()
         n_emit = (C.c_int32 * B)()
-        rc = lib().cdsl_commit(self.handle, prefix.handle, _ptr(lookaheads, torch.int32, "lookaheads"),
-                               _ptr(beam, torch.int32, "beam"), _ptr(n_accept, torch.int32, "n_accept"),
-                               _ptr(row_topk_ids, torch.int32, "row_topk_ids"),
-                               _ptr(row_topk_lp, torch.float32, "row_topk_lp"), k, d, emitted, n_emit,
-                               next_beams.data_ptr(), next_head_lp.data_ptr())
+        args = (_ptr(lookaheads, torch.int32, "lookaheads"), _ptr(beam, torch.int32, "beam"),
+                _ptr(n_accept, torch.int32, "n_accept"), _ptr(row_topk_ids, torch.int32, "row_topk_ids"),
+                _ptr(row_topk_lp, torch.float32, "row_topk_lp"))
+        if kk != k:
+            rc = lib().cdsl_commit_kk(self.handle, prefix.handle, *args, k, d, kk, emitted, n_emit,
+                                      next_beams.data_ptr(), next_head_lp.data_ptr())
+        else:
+            rc = lib().cdsl_commit(self.handle, prefix.handle, *args, k, d, emitted, n_emit,
+                                   next_beams.data_ptr(), next_head_lp.data_ptr())
         _check(rc, self.handle)
         em = [[emitted[b * (d + 1) + t] for t in range(n_emit[b])] for b in range(B)]
         return em, next_beams, next_head_lp
+
+    def cdsl_commit_heads(self, prefix: Prefix, lookaheads, beam, k, d, mask: Optional[List[int]],
+                          next_beams: torch.Tensor, next_head_lp: torch.Tensor) -> List[int]:
+        """Head-only commit; returns the emitted token per prompt (-1: none).
+        next_beams / next_head_lp [B, kk] are updated in place for emitting
+        prompts."""
+        B = prefix.B
+        kk = next_beams.shape[1]
+        m = None
+        if mask is not None:
+            m = (C.c_int32 * B)(*[1 if v else 0 for v in mask])
+        emitted = (C.c_int32 * B)()
+        rc = lib().cdsl_commit_heads(self.handle, prefix.handle, _ptr(lookaheads, torch.int32, "lookaheads"),
+                                     _ptr(beam, torch.int32, "beam"), k, d, kk, m, emitted,
+                                     _ptr(next_beams, torch.int32, "next_beams"),
+                                     _ptr(next_head_lp, torch.float32, "next_head_lp"))
+        _check(rc, self.handle)
+        return [emitted[b] for b in range(B)]
 
 
 # ---------------------------------------------------------------------------

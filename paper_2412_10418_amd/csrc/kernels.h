@@ -53,10 +53,14 @@ hipError_t beam_scores_launch(int BK, int d, const int* look, const int* y, cons
 hipError_t select_launch(int B, int k, const float* scores, const float* reward, float alpha, int reward_only,
                          int* beam, hipStream_t st);
 hipError_t reward_keywords_launch(int B, int k, int d, const int* gen, int gen_stride, const int* gen_len,
-                                  const int* look, const int* kws, int n_kw, int normalize, float* reward,
-                                  hipStream_t st);
+                                  const int* look, const int* upto, const int* kws, int n_kw, int normalize,
+                                  float* reward, hipStream_t st);
 hipError_t reward_linear_launch(int BK, const float* hidden, const float* w, int D, float* reward, hipStream_t st);
-hipError_t commit_launch(int B, int k, int d, const int* look, const int* beam, const int* n_accept,
+// head-only commit (mask[b] != 0: emit the head of beam[b]); see kernels.hip
+hipError_t commit_heads_launch(int B, int k, int d, const int* look, const int* beam, const int* mask, int* stage,
+                               int stage_stride, int* gen, int gen_stride, int* gen_len, int* catch_tok,
+                               hipStream_t st);
+hipError_t commit_launch(int B, int k, int d, int kk, const int* look, const int* beam, const int* n_accept,
                          const int* rtk_ids, const float* rtk_lp, int* next_beams, float* next_head_lp, int* stage,
                          int stage_stride, int* gen, int gen_stride, int* gen_len, int* catch_tok, hipStream_t st);
 hipError_t promote_launch(int B, int k, const KVPool& pool, int n_layers, const int* stage, int stage_stride, int dlim,

@@ -559,10 +559,12 @@ __global__ void select_kernel(int B, int k, const float* __restrict__ scores, co
 }
 
 // Keyword reward, one workgroup per (b, i): distinct keywords present in
-// generated-so-far + lookahead row.
+// generated-so-far + the row's head + its first upto[b, i] lookahead tokens
+// (all d when upto is null).
 __global__ __launch_bounds__(256) void reward_keywords_kernel(int k, int d, const int* __restrict__ gen,
                                                               int gen_stride, const int* __restrict__ gen_len,
                                                               const int* __restrict__ look,
+                                                              const int* __restrict__ upto,
                                                               const int* __restrict__ kws, int n_kw, int normalize,
                                                               float* __restrict__ reward) {
   __shared__ int hit[64];
@@ -573,7 +575,8 @@ __global__ __launch_bounds__(256) void reward_keywords_kernel(int k, int d, cons
   __syncthreads();
   const int* kw = kws + (long long)b * n_kw;
   const int gl = gen_len[b];
-  const int total = gl + d + 1;
+  const int nx = upto ? min(max(upto[bk], 0), d) : d;
+  const int total = gl + nx + 1;
   for (int t = threadIdx.x; t < total; t += 256) {
     const int tok = t < gl ? gen[(long long)b * gen_stride + t] : look[(long long)bk * (d + 1) + (t - gl)];
     for (int u = 0; u < n_kw; ++u)
@@ -606,7 +609,7 @@ __global__ __launch_bounds__(256) void reward_linear_kernel(const float* __restr
 }
 
 // Commit, one thread per prompt.  stage[b] = {n_emit, catch_up, tokens...}.
-__global__ void commit_kernel(int B, int k, int d, const int* __restrict__ look, const int* __restrict__ beam,
+__global__ void commit_kernel(int B, int k, int d, int kk, const int* __restrict__ look, const int* __restrict__ beam,
                               const int* __restrict__ n_accept, const int* __restrict__ rtk_ids,
                               const float* __restrict__ rtk_lp, int* __restrict__ next_beams,
                               float* __restrict__ next_head_lp, int* __restrict__ stage, int stage_stride,
@@ -633,14 +636,45 @@ __global__ void commit_kernel(int B, int k, int d, const int* __restrict__ look,
   }
   gen_len[b] = gl + n + 1;
   if (n < d) {
-    const long long r = ((long long)bk * d + n) * k;
-    for (int u = 0; u < k; ++u) {
-      next_beams[b * k + u] = rtk_ids[r + u];
-      next_head_lp[b * k + u] = rtk_lp[r + u];
+    const long long r = ((long long)bk * d + n) * kk;
+    for (int u = 0; u < kk; ++u) {
+      next_beams[b * kk + u] = rtk_ids[r + u];
+      next_head_lp[b * kk + u] = rtk_lp[r + u];
     }
   } else {
     catch_tok[b] = row[d];
   }
+}
+
+// Head-only commit, one thread per prompt: prompts with mask[b] != 0 emit
+// the head of their selected beam (stage = {1, 0, i, token}, appended to
+// the generated tokens and queued in catch_tok for the one-token pass that
+// puts it into both caches); the others emit nothing (stage[0] = 0).
+__global__ void commit_heads_kernel(int B, int k, int d, const int* __restrict__ look, const int* __restrict__ beam,
+                                    const int* __restrict__ mask, int* __restrict__ stage, int stage_stride,
+                                    int* __restrict__ gen, int gen_stride, int* __restrict__ gen_len,
+                                    int* __restrict__ catch_tok) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  int* st = stage + (long long)b * stage_stride;
+  if (!mask[b]) {
+    st[0] = 0;
+    return;
+  }
+  const int i = beam[b];
+  if (i < 0 || i >= k) {
+    st[0] = -1;
+    return;
+  }
+  const int tok = look[(long long)(b * k + i) * (d + 1)];
+  st[0] = 1;
+  st[1] = 0;
+  st[2] = i;
+  st[3] = tok;
+  const int gl = gen_len[b];
+  gen[(long long)b * gen_stride + gl] = tok;
+  gen_len[b] = gl + 1;
+  catch_tok[b] = tok;
 }
 
 // Copy the selected beam's first cnt suffix slots into the prefix at
@@ -812,10 +846,11 @@ hipError_t select_launch(int B, int k, const float* scores, const float* reward,
 }
 
 hipError_t reward_keywords_launch(int B, int k, int d, const int* gen, int gen_stride, const int* gen_len,
-                                  const int* look, const int* kws, int n_kw, int normalize, float* reward,
-                                  hipStream_t st) {
+                                  const int* look, const int* upto, const int* kws, int n_kw, int normalize,
+                                  float* reward, hipStream_t st) {
   if (B * k == 0) return hipSuccess;
-  reward_keywords_kernel<<<B * k, 256, 0, st>>>(k, d, gen, gen_stride, gen_len, look, kws, n_kw, normalize, reward);
+  reward_keywords_kernel<<<B * k, 256, 0, st>>>(k, d, gen, gen_stride, gen_len, look, upto, kws, n_kw, normalize,
+                                                reward);
   return hipGetLastError();
 }
 
@@ -825,10 +860,18 @@ hipError_t reward_linear_launch(int BK, const float* hidden, const float* w, int
   return hipGetLastError();
 }
 
-hipError_t commit_launch(int B, int k, int d, const int* look, const int* beam, const int* n_accept,
+hipError_t commit_heads_launch(int B, int k, int d, const int* look, const int* beam, const int* mask, int* stage,
+                               int stage_stride, int* gen, int gen_stride, int* gen_len, int* catch_tok,
+                               hipStream_t st) {
+  commit_heads_kernel<<<(B + 63) / 64, 64, 0, st>>>(B, k, d, look, beam, mask, stage, stage_stride, gen, gen_stride,
+                                                    gen_len, catch_tok);
+  return hipGetLastError();
+}
+
+hipError_t commit_launch(int B, int k, int d, int kk, const int* look, const int* beam, const int* n_accept,
                          const int* rtk_ids, const float* rtk_lp, int* next_beams, float* next_head_lp, int* stage,
                          int stage_stride, int* gen, int gen_stride, int* gen_len, int* catch_tok, hipStream_t st) {
-  commit_kernel<<<(B + 63) / 64, 64, 0, st>>>(B, k, d, look, beam, n_accept, rtk_ids, rtk_lp, next_beams,
+  commit_kernel<<<(B + 63) / 64, 64, 0, st>>>(B, k, d, kk, look, beam, n_accept, rtk_ids, rtk_lp, next_beams,
                                               next_head_lp, stage, stage_stride, gen, gen_stride, gen_len, catch_tok);
   return hipGetLastError();
 }

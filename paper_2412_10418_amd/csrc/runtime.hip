@@ -70,7 +70,7 @@ struct cdsl_prefix {
   int* gen = nullptr;          // device [B][gen_stride] emitted tokens
   int* gen_len = nullptr;      // device [B]
   int rolled_k = 0, rolled_d = 0;
-  int verified_k = 0, verified_d = 0;
+  int verified_k = 0, verified_d = 0, verified_kk = 0;
 };
 
 struct cdsl_ctx {
@@ -92,6 +92,7 @@ struct cdsl_ctx {
   int* ids_host = nullptr;     // pinned [max_B]
   int* ids_dev = nullptr;      // device [max_B]
   int* catch_tok = nullptr;    // device [max_B]
+  int* mask_dev = nullptr;     // device [max_B] (head-only commit mask)
   int live_prefixes = 0;
   std::vector<void*> allocs;
   std::string err;
@@ -662,6 +663,7 @@ int cdsl_init(const cdsl_model* draft, const cdsl_model* target, const cdsl_limi
     c->stage = dev_alloc<int>(c, (size_t)l.max_batch * c->stage_stride);
     c->ids_dev = dev_alloc<int>(c, l.max_batch);
     c->catch_tok = dev_alloc<int>(c, l.max_batch);
+    c->mask_dev = dev_alloc<int>(c, l.max_batch);
     CK(hipHostMalloc((void**)&c->stage_host, (size_t)l.max_batch * c->stage_stride * sizeof(int), 0));
     CK(hipHostMalloc((void**)&c->table_host, (size_t)l.max_batch * c->pstride * sizeof(int), 0));
     CK(hipHostMalloc((void**)&c->ids_host, (size_t)l.max_batch * sizeof(int), 0));
@@ -766,7 +768,13 @@ int cdsl_prefill(cdsl_ctx* c, const int32_t* tokens, int32_t B, int32_t L, int32
 }
 
 int cdsl_rollout(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, int32_t d, int32_t* lookaheads) {
+  return cdsl_rollout_with(c, px, beams, k, d, 0, lookaheads);
+}
+
+int cdsl_rollout_with(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, int32_t d, int32_t roller,
+                      int32_t* lookaheads) {
   if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  if (roller != 0 && roller != 1) return fail(c, CDSL_EINVAL, "roller must be 0 (draft) or 1 (target)");
   if (!px || !beams || !lookaheads) return fail(c, CDSL_EINVAL, "null argument");
   if (k <= 0 || d <= 0) return fail(c, CDSL_EINVAL, "k and d must be positive");
   if (k > c->lim.max_k || d > c->lim.max_d) return fail(c, CDSL_ERANGE, "k or d beyond the limits");
@@ -785,10 +793,10 @@ int cdsl_rollout(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, 
       p.tok = lookaheads;
       p.tok_stride = d + 1;
       p.tok_off = j0;
-      run_pass(c, c->m[0], p, Lmax, sum_len(px), true, false, nullptr);
+      run_pass(c, c->m[roller], p, Lmax, sum_len(px), true, false, nullptr);
       LogitArgs la{};
       la.logits = c->ws.logits;
-      la.V = c->m[0].c.vocab;
+      la.V = c->m[roller].c.vocab;
       la.want_lse = 0;
       la.kk = 0;
       la.amax = lookaheads;
@@ -808,7 +816,15 @@ int cdsl_rollout(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, 
 int cdsl_verify(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d, const float* head_lp,
                 float* logprobs, int32_t* target_argmax, int32_t* n_accept, float* scores, int32_t* row_topk_ids,
                 float* row_topk_lp, float* hidden) {
+  return cdsl_verify_kk(c, px, look, k, d, k, head_lp, logprobs, target_argmax, n_accept, scores, row_topk_ids,
+                        row_topk_lp, hidden);
+}
+
+int cdsl_verify_kk(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d, int32_t kk,
+                   const float* head_lp, float* logprobs, int32_t* target_argmax, int32_t* n_accept, float* scores,
+                   int32_t* row_topk_ids, float* row_topk_lp, float* hidden) {
   if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  if (kk <= 0 || kk > c->lim.max_k) return fail(c, CDSL_ERANGE, "top-k width beyond the limits");
   if (!px || !look || !head_lp || !logprobs || !target_argmax || !n_accept || !scores || !row_topk_ids ||
       !row_topk_lp)
     return fail(c, CDSL_EINVAL, "null argument");
@@ -831,7 +847,7 @@ int cdsl_verify(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, in
     la.logits = c->ws.logits;
     la.V = c->m[1].c.vocab;
     la.want_lse = 1;
-    la.kk = k;
+    la.kk = kk;
     la.amax = target_argmax;
     la.lp = logprobs;
     la.gather_tok = look;
@@ -848,18 +864,25 @@ int cdsl_verify(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, in
     }
     px->verified_k = k;
     px->verified_d = d;
+    px->verified_kk = kk;
     return CDSL_OK;
   });
 }
 
 int cdsl_reward_keywords(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d,
                          const int32_t* keywords, int32_t n_kw, int32_t normalize, float* reward) {
+  return cdsl_reward_keywords_upto(c, px, look, k, d, nullptr, keywords, n_kw, normalize, reward);
+}
+
+int cdsl_reward_keywords_upto(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d,
+                              const int32_t* upto, const int32_t* keywords, int32_t n_kw, int32_t normalize,
+                              float* reward) {
   if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
   if (!px || !look || !keywords || !reward) return fail(c, CDSL_EINVAL, "null argument");
   if (k <= 0 || d <= 0 || n_kw <= 0 || n_kw > 64) return fail(c, CDSL_EINVAL, "bad k, d or n_kw (1..64)");
   return guarded(c, [&]() {
     Span sp(c, CDSL_K_STEP, 0.0, (double)px->B * k * (d + 1) * 4.0);
-    CK(reward_keywords_launch(px->B, k, d, px->gen, c->lim.max_ctx, px->gen_len, look, keywords, n_kw, normalize,
+    CK(reward_keywords_launch(px->B, k, d, px->gen, c->lim.max_ctx, px->gen_len, look, upto, keywords, n_kw, normalize,
                               reward, c->st));
     return CDSL_OK;
   });
@@ -892,17 +915,25 @@ int cdsl_select(cdsl_ctx* c, const float* scores, const float* reward, float alp
 int cdsl_commit(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, const int32_t* n_accept,
                 const int32_t* rtk_ids, const float* rtk_lp, int32_t k, int32_t d, int32_t* emitted_host,
                 int32_t* n_emit_host, int32_t* next_beams, float* next_head_lp) {
+  return cdsl_commit_kk(c, px, look, beam, n_accept, rtk_ids, rtk_lp, k, d, k, emitted_host, n_emit_host,
+                        next_beams, next_head_lp);
+}
+
+int cdsl_commit_kk(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, const int32_t* n_accept,
+                   const int32_t* rtk_ids, const float* rtk_lp, int32_t k, int32_t d, int32_t kk,
+                   int32_t* emitted_host, int32_t* n_emit_host, int32_t* next_beams, float* next_head_lp) {
   if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
   if (!px || !look || !beam || !n_accept || !rtk_ids || !rtk_lp || !emitted_host || !n_emit_host || !next_beams ||
       !next_head_lp)
     return fail(c, CDSL_EINVAL, "null argument");
   if (px->rolled_k != k || px->rolled_d != d || px->verified_k != k || px->verified_d != d)
     return fail(c, CDSL_ESTATE, "commit needs a rollout and a verify with the same k and d");
+  if (px->verified_kk != kk) return fail(c, CDSL_ESTATE, "commit needs a verify with the same top-k width");
   return guarded(c, [&]() {
     const int B = px->B;
     {
       Span sp(c, CDSL_K_STEP, 0.0, (double)B * (d + 1 + 2 * k) * 4.0);
-      CK(commit_launch(B, k, d, look, beam, n_accept, rtk_ids, rtk_lp, next_beams, next_head_lp, c->stage,
+      CK(commit_launch(B, k, d, kk, look, beam, n_accept, rtk_ids, rtk_lp, next_beams, next_head_lp, c->stage,
                        c->stage_stride, px->gen, c->lim.max_ctx, px->gen_len, c->catch_tok, c->st));
     }
     CK(hipMemcpyAsync(c->stage_host, c->stage, (size_t)B * c->stage_stride * sizeof(int), hipMemcpyDeviceToHost,
@@ -958,7 +989,7 @@ int cdsl_commit(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t
       la.logits = c->ws.logits;
       la.V = c->m[1].c.vocab;
       la.want_lse = 1;
-      la.kk = k;
+      la.kk = kk;
       la.topk_ids = next_beams;
       la.topk_lp = next_head_lp;
       la.topk_rows = c->ids_dev;
@@ -970,6 +1001,85 @@ int cdsl_commit(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t
       const int* stg = c->stage_host + (size_t)b * c->stage_stride;
       n_emit_host[b] = stg[0];
       for (int t = 0; t <= d; ++t) emitted_host[(size_t)b * (d + 1) + t] = t < stg[0] ? stg[3 + t] : -1;
+    }
+    px->rolled_k = px->rolled_d = px->verified_k = px->verified_d = 0;
+    return CDSL_OK;
+  });
+}
+
+int cdsl_commit_heads(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, int32_t k, int32_t d,
+                      int32_t kk, const int32_t* mask_host, int32_t* emitted_host, int32_t* next_beams,
+                      float* next_head_lp) {
+  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  if (kk <= 0 || kk > c->lim.max_k) return fail(c, CDSL_ERANGE, "top-k width beyond the limits");
+  if (!px || !look || !beam || !emitted_host || !next_beams || !next_head_lp)
+    return fail(c, CDSL_EINVAL, "null argument");
+  if (px->rolled_k != k || px->rolled_d != d)
+    return fail(c, CDSL_ESTATE, "commit_heads needs a rollout with the same k and d");
+  return guarded(c, [&]() {
+    const int B = px->B;
+    for (int b = 0; b < B; ++b) c->ids_host[b] = mask_host ? (mask_host[b] != 0) : 1;
+    CK(hipMemcpyAsync(c->mask_dev, c->ids_host, (size_t)B * sizeof(int), hipMemcpyHostToDevice, c->st));
+    {
+      Span sp(c, CDSL_K_STEP, 0.0, (double)B * 16.0);
+      CK(commit_heads_launch(B, k, d, look, beam, c->mask_dev, c->stage, c->stage_stride, px->gen, c->lim.max_ctx,
+                             px->gen_len, c->catch_tok, c->st));
+    }
+    CK(hipMemcpyAsync(c->stage_host, c->stage, (size_t)B * c->stage_stride * sizeof(int), hipMemcpyDeviceToHost,
+                      c->st));
+    CK(hipStreamSynchronize(c->st));
+    if (c->prof) harvest(c);
+    int n = 0;
+    for (int b = 0; b < B; ++b) {
+      const int* stg = c->stage_host + (size_t)b * c->stage_stride;
+      if (stg[0] < 0) {
+        g_err = "invalid beam index (NaN reward?) for prompt " + std::to_string(b);
+        throw Fail{CDSL_EINVAL};
+      }
+      if (stg[0] == 0) continue;
+      if (px->len[b] + 1 > c->lim.max_ctx) {
+        g_err = "prompt " + std::to_string(b) + " exceeds max_ctx";
+        throw Fail{CDSL_ERANGE};
+      }
+      ensure_blocks(c, px, b, px->len[b] + 1);
+      c->ids_host[n++] = b;
+    }
+    if (n > 0) {
+      // the chosen heads go through both models as one appended row each
+      // (the rolled suffixes are dropped), and the target row gives the
+      // next heads
+      upload_table(c, px);
+      CK(hipMemcpyAsync(c->ids_dev, c->ids_host, n * sizeof(int), hipMemcpyHostToDevice, c->st));
+      PassDesc p = base_pass(c, px);
+      p.mode = kAppend;
+      p.nb = n;
+      p.kp = 1;
+      p.R = 1;
+      p.j0 = 0;
+      p.prompt_ids = c->ids_dev;
+      p.tok = c->catch_tok;
+      p.tok_stride = 1;
+      p.tok_off = 0;
+      const int Lmax = max_len(px);
+      long long sl = 0;
+      for (int u = 0; u < n; ++u) sl += px->len[c->ids_host[u]];
+      run_pass(c, c->m[0], p, Lmax, sl, false, false, nullptr);
+      run_pass(c, c->m[1], p, Lmax, sl, true, false, nullptr);
+      LogitArgs la{};
+      la.logits = c->ws.logits;
+      la.V = c->m[1].c.vocab;
+      la.want_lse = 1;
+      la.kk = kk;
+      la.topk_ids = next_beams;
+      la.topk_lp = next_head_lp;
+      la.topk_rows = c->ids_dev;
+      logit_rows(c, la, n);
+      CK(add_launch(n, c->ids_dev, px->Lp, 1, c->st));
+      for (int u = 0; u < n; ++u) px->len[c->ids_host[u]] += 1;
+    }
+    for (int b = 0; b < B; ++b) {
+      const int* stg = c->stage_host + (size_t)b * c->stage_stride;
+      emitted_host[b] = stg[0] > 0 ? stg[3] : -1;
     }
     px->rolled_k = px->rolled_d = px->verified_k = px->verified_d = 0;
     return CDSL_OK;

@@ -3,6 +3,12 @@
 A step is rollout -> verify -> reward -> select -> commit on the context
 stream, with the step's device buffers allocated once per (B, k, d) so the
 steady-state loop allocates nothing.
+
+Also the paper's baselines and its full controller on the same calls:
+``head_step`` emits one token of lookahead-heuristic decoding (CDLH with the
+target as the roller, CDLH-appx. with the draft; Sec. 2.1, 3.1 and the
+appendix algorithm), and ``controller_step`` runs one iteration of Alg. 1
+(states S1 .. S4 of Sec. 3.2.3 with thresholds a_t, r_t and b <= 1).
 """
 from __future__ import annotations
 
@@ -117,6 +123,113 @@ class Engine:
         st.head_lp, bf.next_head_lp = bf.next_head_lp, st.head_lp
         self._last_emitted = em
         return bf
+
+    # -- the baselines and the full controller ---------------------------------
+    def _heads_buffers(self, B: int, k: int, d: int):
+        key = ("heads", B, k, d)
+        if key not in self._bufs:
+            dev = self.device
+            self._bufs[key] = {"look": torch.zeros(B, k, d + 1, dtype=torch.int32, device=dev),
+                               "reward": torch.zeros(B, k, device=dev),
+                               "beam": torch.zeros(B, dtype=torch.int32, device=dev)}
+        return self._bufs[key]
+
+    def _controller_buffers(self, B: int, k: int, d: int):
+        key = ("ctrl", B, k, d)
+        if key not in self._bufs:
+            dev = self.device
+            z = lambda *s, dt=torch.float32: torch.zeros(s, dtype=dt, device=dev)
+            i32 = torch.int32
+            self._bufs[key] = {
+                "look": z(B, 1, d + 1, dt=i32), "heads": z(B, 1, dt=i32), "head_lp": z(B, 1),
+                "verify": {"logprobs": z(B, 1, d), "target_argmax": z(B, 1, d, dt=i32),
+                           "n_accept": z(B, 1, dt=i32), "scores": z(B, 1),
+                           "row_topk_ids": z(B, 1, d, k, dt=i32), "row_topk_lp": z(B, 1, d, k), "hidden": None},
+                "reward": z(B, 1), "beam": z(B, dt=i32), "next_beams": z(B, k, dt=i32), "next_head_lp": z(B, k)}
+        return self._bufs[key]
+
+    def head_step(self, st: DecodeState, keywords: torch.Tensor, roller: int, k: Optional[int] = None,
+                  d: Optional[int] = None, mask: Optional[List[bool]] = None,
+                  prefer_first_at: Optional[List[Optional[float]]] = None) -> dict:
+        """One token of lookahead-heuristic decoding for every prompt (or the
+        prompts with mask[b]): the k heads of ``st`` (top-k of the target) are
+        rolled d tokens by the roller (1 = target: CDLH, 0 = draft:
+        CDLH-appx.), scored by the lexical reward, and the best head is
+        emitted.  prefer_first_at[b] = r_t makes prompt b take head 0 when its
+        reward reaches r_t (Step-1 of Alg. 1 with b = 1)."""
+        k = k or self.k
+        d = d or self.d
+        B = st.prefix.B
+        hb = self._heads_buffers(B, k, d)
+        c = self.ctx
+        normalize = self.wl.reward == "keyword_coverage"
+        c.cdsl_rollout_with(st.prefix, st.beams, k, d, roller, hb["look"])
+        c.cdsl_reward_keywords(st.prefix, hb["look"], k, d, keywords, normalize=normalize, reward=hb["reward"])
+        if prefer_first_at is None:
+            c.cdsl_select(hb["reward"], hb["reward"], math.inf, hb["beam"])
+            r = None
+        else:
+            r = hb["reward"].cpu().tolist()
+            picks = []
+            for b in range(B):
+                rb = r[b]
+                t = prefer_first_at[b]
+                if t is not None and rb[0] >= t:
+                    picks.append(0)
+                else:
+                    best = 0
+                    for i in range(1, k):
+                        if rb[i] > rb[best]:
+                            best = i
+                    picks.append(best)
+            hb["beam"].copy_(torch.tensor(picks, dtype=torch.int32))
+        toks = c.cdsl_commit_heads(st.prefix, hb["look"], hb["beam"], k, d, mask, st.beams, st.head_lp)
+        for b in range(B):
+            if toks[b] >= 0:
+                st.emitted[b].append(toks[b])
+        return {"tokens": toks, "lookaheads": hb["look"], "reward": hb["reward"], "beam": hb["beam"]}
+
+    def controller_step(self, st: DecodeState, keywords: torch.Tensor, a_t: float, r_t: float, b: int,
+                        k: Optional[int] = None, d: Optional[int] = None) -> dict:
+        """One iteration of Alg. 1 for every prompt, with the readings of the
+        oracle's ``controller_step``: draft d tokens after the target's greedy
+        head c (k = 1 rollout), verify them (top-k width k for the next
+        heads), a = n / d, r = R(generated + c + x_1..x_n); emit [c, x_1..x_n]
+        everywhere, then one more token (CDLH-appx., with Step-1 first for
+        b = 1) for the prompts not in S1."""
+        if b not in (0, 1):
+            raise ValueError("b must be 0 or 1")
+        k = k or self.k
+        d = d or self.d
+        B = st.prefix.B
+        cb = self._controller_buffers(B, k, d)
+        c = self.ctx
+        normalize = self.wl.reward == "keyword_coverage"
+        cb["heads"].copy_(st.beams[:, :1])
+        cb["head_lp"].copy_(st.head_lp[:, :1])
+        c.cdsl_rollout(st.prefix, cb["heads"], 1, d, cb["look"])
+        c.cdsl_verify(st.prefix, cb["look"], 1, d, cb["head_lp"], out=cb["verify"], kk=k)
+        c.cdsl_reward_keywords_upto(st.prefix, cb["look"], 1, d, cb["verify"]["n_accept"], keywords,
+                                    normalize=normalize, reward=cb["reward"])
+        n = cb["verify"]["n_accept"][:, 0].cpu().tolist()
+        r = cb["reward"][:, 0].cpu().tolist()
+        states = []
+        for i in range(B):
+            a = n[i] / d
+            states.append("S1" if (a >= a_t and r[i] >= r_t) else ("S2/S3" if a < a_t else "S4"))
+        em, _, _ = c.cdsl_commit(st.prefix, cb["look"], cb["beam"], cb["verify"]["n_accept"],
+                                 cb["verify"]["row_topk_ids"], cb["verify"]["row_topk_lp"], 1, d,
+                                 cb["next_beams"], cb["next_head_lp"], kk=k)
+        for i in range(B):
+            st.emitted[i].extend(em[i])
+        st.beams.copy_(cb["next_beams"])
+        st.head_lp.copy_(cb["next_head_lp"])
+        extra = None
+        need = [s_ != "S1" for s_ in states]
+        if any(need):
+            pref = [r_t if (states[i] == "S2/S3" and b == 1) else None for i in range(B)]
+            extra = self.head_step(st, keywords, 0, k=k, d=d, mask=need, prefer_first_at=pref)
+        return {"states": states, "n": n, "r": r, "emitted": em, "extra": extra}
 
     def close(self):
         self.ctx.close()

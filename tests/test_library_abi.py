@@ -61,6 +61,13 @@ def test_error_paths_without_device(lib):
     assert b"null" in L.cdsl_last_error(None)
     assert L.cdsl_destroy(None) == binding.CDSL_OK
     assert L.cdsl_rollout(None, None, None, 1, 1, None) == binding.CDSL_EINVAL
+    assert L.cdsl_rollout_with(None, None, None, 1, 1, 0, None) == binding.CDSL_EINVAL
+    assert L.cdsl_verify_kk(None, None, None, 1, 1, 1, None, None, None, None, None, None, None,
+                            None) == binding.CDSL_EINVAL
+    assert L.cdsl_commit_kk(None, None, None, None, None, None, None, 1, 1, 1, None, None, None,
+                            None) == binding.CDSL_EINVAL
+    assert L.cdsl_commit_heads(None, None, None, None, 1, 1, 1, None, None, None, None) == binding.CDSL_EINVAL
+    assert L.cdsl_reward_keywords_upto(None, None, None, 1, 1, None, None, 1, 0, None) == binding.CDSL_EINVAL
     assert L.cdsl_op_logit_rows(None, 1, 1, None, 0, None, None, None, None, None) == binding.CDSL_EINVAL
     assert L.cdsl_op_gemm_workspace(80, 3072, 2048, binding.CDSL_BF16) > 0
     assert L.cdsl_op_gemm_workspace(0, 3072, 2048, binding.CDSL_BF16) == 0

@@ -290,3 +290,150 @@ def test_inputs_do_not_depend_on_batch_size():
     ka = ci.keywords(0, 4, 3, 1000)
     assert all(len(set(r)) == 3 for r in ka)
     assert np.array_equal(ka[2:], ci.keywords(0, 2, 3, 1000, first=2))
+
+
+# ---------------------------------------------------------------------------
+# the baselines (CDLH, CDLH-appx.) and the Alg. 1 controller
+# ---------------------------------------------------------------------------
+def _hf_greedy_tail(hf, seq, d):
+    """d greedy tokens after seq by full recomputation (independent path)."""
+    return [int(t) for t in _hf_greedy(hf, seq, d)]
+
+
+def _hf_greedy(hf, seq, n):
+    from hf_ref import hf_greedy
+    return hf_greedy(hf, seq, n)
+
+
+def _brute_cdlh(hf_roller, hf_target, tokens, n_prompt, k, d, kws, kind):
+    """The appendix algorithm written out with full forwards: candidates =
+    top-k of the target (value desc, id asc), each extended by d greedy
+    tokens of the roller, scored by the concept count over generated +
+    candidate + lookahead; first best wins."""
+    from hf_ref import hf_logits
+    z = hf_logits(hf_target, tokens)[-1]
+    order = sorted(range(len(z)), key=lambda v: (-z[v], v))[:k]
+    scores = []
+    for c in order:
+        look = _hf_greedy_tail(hf_roller, list(tokens) + [c], d)
+        window = list(tokens[n_prompt:]) + [c] + look
+        hits = len(set(window) & set(kws))
+        scores.append(hits / len(set(kws)) if kind == "keyword_coverage" else float(hits))
+    best = max(range(k), key=lambda i: (scores[i], -i))
+    return order, scores, best
+
+
+@pytest.mark.parametrize("roller_is_target", [False, True])
+def test_lookahead_heuristic_k1_is_greedy_decoding(models, roller_is_target):
+    """One candidate: CDLH and CDLH-appx. emit the target's greedy tokens."""
+    draft, target, st0 = _state(models, n=6)
+    hf_t = models["mha"][3]
+    st, out = st0, []
+    for _ in range(4):
+        hs = oracle.cdlh_step(roller_is_target, draft, target, st, 1, 3, "keyword_count", [1, 2, 3])
+        out.append(hs.token)
+        st = hs.state
+    assert out == _hf_greedy(hf_t, st0.tokens, 4)
+
+
+@pytest.mark.parametrize("roller_is_target", [False, True])
+def test_lookahead_heuristic_choice_matches_full_recompute(models, roller_is_target):
+    draft, target, st = _state(models, n=8)
+    hf_d, hf_t = models["gqa"][3], models["mha"][3]
+    k, d = 4, 3
+    # concepts taken from the third candidate's own lookahead, so that the
+    # rewards differ and the choice is not the first candidate by default
+    from hf_ref import hf_logits
+    z = hf_logits(hf_t, st.tokens)[-1]
+    c3 = sorted(range(len(z)), key=lambda v: (-z[v], v))[2]
+    roller = hf_t if roller_is_target else hf_d
+    kws = _hf_greedy_tail(roller, list(st.tokens) + [c3], d)[:2] + [63]
+    for kind in ("keyword_count", "keyword_coverage"):
+        hs = oracle.cdlh_step(roller_is_target, draft, target, st, k, d, kind, kws)
+        order, scores, best = _brute_cdlh(roller, hf_t, st.tokens, st.n_prompt, k, d, kws, kind)
+        assert list(hs.heads) == order
+        assert np.allclose(hs.reward, scores)
+        assert hs.pick == best and hs.token == order[best]
+        # the emitted token extends the prefix and the next distribution is
+        # the target's after it
+        full = target.full(hs.state.tokens).logits[-1]
+        assert hs.state.tokens == list(st.tokens) + [order[best]]
+        assert np.max(np.abs(hs.state.s - oracle.log_softmax(full))) < 1e-10
+
+
+def test_controller_always_s1_is_greedy_decoding(models):
+    """a_t = 0, r_t = -inf: every iteration is S1 (emit the head and the
+    accepted tokens), which is lossless greedy decoding of the target."""
+    draft, target, st0 = _state(models, n=7)
+    st, out = st0, []
+    for _ in range(4):
+        cs = oracle.controller_step(draft, target, st, 3, 3, 0.0, -math.inf, 0, "keyword_count", [4, 5])
+        assert cs.state == "S1" and cs.extra is None
+        out += cs.emitted
+        st = cs.after
+    assert out == _hf_greedy(models["mha"][3], st0.tokens, len(out))
+
+
+def test_controller_step1_with_low_threshold_takes_target_greedy(models):
+    """a_t above 1 forces S2/S3; with b = 1 and r_t = -inf Step-1 always
+    succeeds on M_p's greedy token, so the output is still greedy decoding
+    of the target."""
+    draft, target, st0 = _state(models, n=7)
+    st, out = st0, []
+    for _ in range(3):
+        cs = oracle.controller_step(draft, target, st, 3, 3, 2.0, -math.inf, 1, "keyword_count", [4, 5])
+        assert cs.state == "S2/S3" and cs.extra.pick == 0
+        out += cs.emitted
+        st = cs.after
+    assert out == _hf_greedy(models["mha"][3], st0.tokens, len(out))
+
+
+@pytest.mark.parametrize("a_t,r_t,b,state", [(2.0, -math.inf, 0, "S2/S3"), (0.0, math.inf, 1, "S4"),
+                                             (2.0, math.inf, 1, "S2/S3")])
+def test_controller_step2_is_the_cdlh_appx_token(models, a_t, r_t, b, state):
+    """Step-2 (and S4): the token after the accepted ones is CDLH-appx.'s
+    choice, computed here by full recomputation; a and r are checked against
+    their definitions."""
+    from hf_ref import hf_logits
+    draft, target, st = _state(models, n=9)
+    hf_d, hf_t = models["gqa"][3], models["mha"][3]
+    k, d, kws = 3, 4, [7, 11, 13, 40]
+    cs = oracle.controller_step(draft, target, st, k, d, a_t, r_t, b, "keyword_count", kws)
+    assert cs.state == state
+    # head, draft lookahead and acceptance by full recomputation
+    c = int(np.argmax(hf_logits(hf_t, st.tokens)[-1]))
+    x = _hf_greedy_tail(hf_d, list(st.tokens) + [c], d)
+    seq = list(st.tokens) + [c]
+    n = 0
+    for j in range(d):
+        if int(np.argmax(hf_logits(hf_t, seq)[-1])) != x[j]:
+            break
+        seq.append(x[j])
+        n += 1
+    assert cs.head == c and list(cs.x) == x and cs.n == n and cs.a == n / d
+    acc = [c] + x[:n]
+    assert cs.r == float(len(set(acc) & set(kws)))
+    order, scores, best = _brute_cdlh(hf_d, hf_t, list(st.tokens) + acc, st.n_prompt, k, d, kws, "keyword_count")
+    assert cs.emitted == acc + [order[best]]
+
+
+def test_controller_visits_every_state_on_the_tiny_workload():
+    """On the seeded `tiny` workload the controller settings of the GPU
+    parity tests reach S1, S2/S3 and S4 (S1 and S4 with the target as its
+    own draft, where every lookahead is accepted), so every branch is
+    compared."""
+    wl = ci.workload("tiny")
+    tw = ci.model_weights(wl.target, wl.seed, 1, wl.dtype)
+    dw = ci.model_weights(wl.draft, wl.seed, 0, wl.dtype)
+    od, ot = oracle.Decoder(wl.draft, dw), oracle.Decoder(wl.target, tw)
+    kws = ci.keywords(wl.seed, 64, wl.n_keywords, wl.target.vocab)
+    prompts = ci.prompts(wl.seed, 3, wl.prompt_len, wl.target.vocab)
+    seen = {}
+    for dm, a_t, r_t, bb in [(od, 0.5, 1.0, 1), (od, 0.5, 1.0, 0), (ot, 0.5, 0.0, 0), (ot, 0.5, 1.0, 1)]:
+        for b in range(3):
+            st = oracle.prefill(dm, ot, prompts[b])
+            for _ in range(3):
+                cs = oracle.controller_step(dm, ot, st, wl.k, wl.d, a_t, r_t, bb, wl.reward, kws[b])
+                seen[cs.state] = seen.get(cs.state, 0) + 1
+                st = cs.after
+    assert set(seen) == {"S1", "S2/S3", "S4"}, seen
