@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--d", type=int, default=None)
     ap.add_argument("--profile-steps", type=int, default=3)
     ap.add_argument("--phase-steps", type=int, default=3)
+    ap.add_argument("--methods-steps", type=int, default=3,
+                    help="iterations timed per decoding method in the 'methods' comparison (0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (reference for HBM byte counters)")
@@ -266,6 +268,57 @@ def cpu_baseline(wl, dw, tw, prompt, kws, rw, k, d, min_s=10.0, max_steps=8):
             "s_per_prompt_step": round(t_steps / n, 3)}
 
 
+# the controller's thresholds in the methods comparison: the paper's
+# CommonGen setting for most (draft, target) pairs (d = 3 there; here the
+# workload's d), with the concept-coverage reward
+METHOD_A_T, METHOD_R_T, METHOD_B = 0.3, 0.3, 1
+
+
+def measure_methods(eng, wl, prompts, k, d, steps):
+    """Wall-clock of the paper's decoding methods on the same models and
+    prompts, with the concept-coverage reward (4 seeded concepts per prompt):
+    the CDSL step (the timed path above, here with that reward), one
+    iteration of the full controller (Alg. 1), and one token of CDLH-appx.
+    (draft lookaheads) and of CDLH (target lookaheads).  Each method starts
+    from a fresh prefill, runs one untimed iteration, then `steps` timed
+    ones.  Tokens per iteration depend on how often the target accepts the
+    draft's tokens, which for independent random models is rarely."""
+    import numpy as np
+    import torch
+    import cdsl_inputs as ci
+    B = prompts.shape[0]
+    kws = torch.from_numpy(ci.keywords(wl.seed, B, 4, wl.target.vocab)).cuda()
+    p = torch.from_numpy(prompts).cuda()
+    runs = {
+        "cdsl_step": lambda st: eng.step(st, keywords=kws, k=k, d=d, alpha=math.inf, reward="keyword_coverage"),
+        "alg1": lambda st: eng.controller_step(st, kws, METHOD_A_T, METHOD_R_T, METHOD_B, k=k, d=d, normalize=True),
+        "cdlh_appx": lambda st: eng.head_step(st, kws, 0, k=k, d=d, normalize=True),
+        "cdlh": lambda st: eng.head_step(st, kws, 1, k=k, d=d, normalize=True),
+    }
+    out = {}
+    for name, fn in runs.items():
+        st = eng.start(p, k=k)
+        fn(st)
+        torch.cuda.synchronize()
+        before = sum(len(e) for e in st.emitted)
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            fn(st)
+        torch.cuda.synchronize()
+        sec = time.perf_counter() - t0
+        toks = sum(len(e) for e in st.emitted) - before
+        out[name] = {"ms_per_iteration": round(sec * 1e3 / steps, 2),
+                     "tokens_per_iteration_per_prompt": round(toks / (steps * B), 3),
+                     "tokens_per_s": round(toks / sec, 1)}
+        st.prefix.free()
+    base = out["cdlh"]["tokens_per_s"]
+    for name in out:
+        out[name]["speedup_vs_cdlh"] = round(out[name]["tokens_per_s"] / base, 2) if base > 0 else None
+    out["settings"] = {"reward": "keyword_coverage, 4 concepts per prompt", "k": k, "d": d,
+                       "a_t": METHOD_A_T, "r_t": METHOD_R_T, "b": METHOD_B, "timed_iterations": steps}
+    return out
+
+
 def main():
     args = parse()
     if args.summarize_profile:
@@ -294,6 +347,9 @@ def main():
     t0 = time.perf_counter()
     dwd, twd = Engine.upload(wl, dw, tw)
     total_steps = args.warmup + args.steps + args.profile_steps + args.phase_steps
+    # the methods comparison restarts from the prompt; its controller
+    # iterations emit at most d + 2 tokens each
+    total_steps = max(total_steps, 2 * (args.methods_steps + 1) + 1)
     eng = Engine(wl, dwd, twd, max_steps=total_steps + 2, max_batch=B, k=k, d=d)
     del dwd, twd
     torch.cuda.empty_cache()
@@ -358,6 +414,10 @@ def main():
     else:   # no instrumented steps: no roofline object
         dom, roof, table = None, None, {}
     emitted = sum(len(e) for e in st.emitted)
+    st.prefix.free()
+    methods = measure_methods(eng, wl, prompts, k, d, args.methods_steps) if args.methods_steps > 0 else None
+    if methods:
+        log(json.dumps(methods))
     if args.calibrate_copy:
         src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
@@ -366,7 +426,6 @@ def main():
         torch.cuda.synchronize()
         log("calibration: 3 copies of 256 MiB (reads 262144 KiB, writes 262144 KiB per copy)")
         del src, dst
-    st.prefix.free()
     eng.close()
     del eng
     torch.cuda.empty_cache()
@@ -402,6 +461,7 @@ def main():
                    "tokens_emitted": emitted},
         "roofline": roof,
         "phases": phases,
+        "methods": methods,
         "kernels": table,
         "cpu_baseline": cpu,
     }

@@ -19,7 +19,8 @@
  *   cdsl_commit    emits the selected beam's head plus its accepted tokens
  *                  (S1 action of Sec. 3.2.3, no bonus token), makes them part
  *                  of the shared prefix and produces the next beam heads
- *   cdsl_rollout_with, cdsl_reward_keywords_upto, cdsl_commit_heads
+ *   cdsl_rollout_with, cdsl_reward_keywords_upto, cdsl_controller_states,
+ *   cdsl_select_first, cdsl_commit_heads
  *                  the pieces of the paper's full controller (Alg. 1 states
  *                  S1..S4) and of its baselines CDLH (target-rolled
  *                  lookaheads) and CDLH-appx. (draft-rolled, unverified)
@@ -205,6 +206,29 @@ int cdsl_reward_linear(cdsl_ctx* ctx, const float* hidden, const float* w,
  * reward makes beam[b] = -1, which cdsl_commit reports as EINVAL. */
 int cdsl_select(cdsl_ctx* ctx, const float* scores, const float* reward,
                 float alpha, int32_t B, int32_t k, int32_t* beam);
+
+/* Reward-only selection with Step-1 of the controller (Sec. 3.2.3, S2/S3
+ * with b = 1): beam[b] = 0 when reward[b, 0] >= first_at[b] (head 0 is the
+ * target's greedy token), otherwise argmax_i reward[b, i] with the lowest i
+ * on ties.  first_at[b] = NaN disables the rule for prompt b (plain Alg. 2
+ * argmax, as CDLH-appx. in Step-2).  reward is [B, k], first_at [B], beam
+ * [B], all device.  A NaN reward makes beam[b] = -1 (reported by the next
+ * commit as EINVAL).  Errors: EINVAL for null pointers or B, k <= 0. */
+int cdsl_select_first(cdsl_ctx* ctx, const float* reward, const float* first_at,
+                      int32_t B, int32_t k, int32_t* beam);
+
+/* The controller's state per prompt after a k = 1 lookahead (Sec. 3.2.3,
+ * Alg. 1 decision between S1..S4): a = n_accept[b] / d compared in float64
+ * with a_t, r = reward[b] (the accepted window's reward, float32 widened to
+ * float64) with r_t.  state[b] = 1 (S1: a >= a_t and r >= r_t), 2 (S2/S3:
+ * a < a_t) or 4 (S4: a >= a_t, r < r_t).  first_at[b] = r_t for state 2
+ * when b = 1 (the input cdsl_select_first takes for Step-1), NaN otherwise.
+ * n_accept and reward are [B] (the k = 1 outputs of cdsl_verify and
+ * cdsl_reward_keywords_upto), state and first_at [B]; all device.  Errors:
+ * EINVAL for null pointers, B or d <= 0, b not in {0, 1}, NaN thresholds. */
+int cdsl_controller_states(cdsl_ctx* ctx, const int32_t* n_accept, const float* reward,
+                           int32_t B, int32_t d, double a_t, double r_t, int32_t b,
+                           int32_t* state, float* first_at);
 
 /* Commit the selected beams.  Emits, per prompt, O = [c_i*, x_i*,1..n]
  * with n = n_accept[b, i*]: emitted_host[b, 0..n] and n_emit_host[b] = n+1

@@ -22,7 +22,8 @@ ERR_NAMES = {0: "OK", -1: "EINVAL", -2: "ERANGE", -3: "ENOMEM", -4: "EDEVICE", -
 EXPORTS = [
     "cdsl_init", "cdsl_prefill", "cdsl_rollout", "cdsl_rollout_with", "cdsl_verify", "cdsl_verify_kk",
     "cdsl_reward_keywords",
-    "cdsl_reward_keywords_upto", "cdsl_reward_linear", "cdsl_select", "cdsl_commit", "cdsl_commit_kk",
+    "cdsl_reward_keywords_upto", "cdsl_reward_linear", "cdsl_select", "cdsl_select_first", "cdsl_controller_states",
+    "cdsl_commit", "cdsl_commit_kk",
     "cdsl_commit_heads",
     "cdsl_prefix_lengths",
     "cdsl_free_prefix", "cdsl_destroy", "cdsl_last_error", "cdsl_profile_enable", "cdsl_profile_read",
@@ -87,6 +88,8 @@ def lib():
         "cdsl_reward_keywords": ([vp, vp, vp, i32, i32, vp, i32, i32, vp], i32),
         "cdsl_reward_linear": ([vp, vp, vp, i32, i32, i32, vp], i32),
         "cdsl_select": ([vp, vp, vp, f32, i32, i32, vp], i32),
+        "cdsl_select_first": ([vp, vp, vp, i32, i32, vp], i32),
+        "cdsl_controller_states": ([vp, vp, vp, i32, i32, C.c_double, C.c_double, i32, vp, vp], i32),
         "cdsl_commit": ([vp, vp, vp, vp, vp, vp, vp, i32, i32, vp, vp, vp, vp], i32),
         "cdsl_prefix_lengths": ([vp, vp, vp], i32),
         "cdsl_free_prefix": ([vp, vp], i32),
@@ -344,6 +347,35 @@ class Context:
                                _ptr(reward, torch.float32, "reward"), float(alpha), B, k, beam.data_ptr())
         _check(rc, self.handle)
         return beam
+
+    def cdsl_select_first(self, reward: torch.Tensor, first_at: torch.Tensor,
+                          beam: Optional[torch.Tensor] = None) -> torch.Tensor:
+        B, k = reward.shape
+        if first_at.shape != (B,):
+            raise ValueError("first_at must be [B]")
+        if beam is None:
+            beam = torch.empty(B, dtype=torch.int32, device=reward.device)
+        rc = lib().cdsl_select_first(self.handle, _ptr(reward, torch.float32, "reward"),
+                                     _ptr(first_at, torch.float32, "first_at"), B, k, beam.data_ptr())
+        _check(rc, self.handle)
+        return beam
+
+    def cdsl_controller_states(self, n_accept: torch.Tensor, reward: torch.Tensor, d: int, a_t: float,
+                               r_t: float, b: int, state: Optional[torch.Tensor] = None,
+                               first_at: Optional[torch.Tensor] = None):
+        """n_accept / reward: [B] (or [B, 1]) k = 1 outputs; returns (state, first_at)."""
+        B = n_accept.numel()
+        if reward.numel() != B:
+            raise ValueError("n_accept and reward must have B elements")
+        if state is None:
+            state = torch.empty(B, dtype=torch.int32, device=n_accept.device)
+        if first_at is None:
+            first_at = torch.empty(B, dtype=torch.float32, device=n_accept.device)
+        rc = lib().cdsl_controller_states(self.handle, _ptr(n_accept, torch.int32, "n_accept"),
+                                          _ptr(reward, torch.float32, "reward"), B, d, float(a_t), float(r_t),
+                                          int(b), state.data_ptr(), first_at.data_ptr())
+        _check(rc, self.handle)
+        return state, first_at
 
     def cdsl_commit(self, prefix: Prefix, lookaheads, beam, n_accept, row_topk_ids, row_topk_lp, k, d,
                     next_beams: Optional[torch.Tensor] = None, next_head_lp: Optional[torch.Tensor] = None,

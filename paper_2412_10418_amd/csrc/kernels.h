@@ -51,7 +51,9 @@ hipError_t logit_rows_launch(const LogitArgs& a, int M, hipStream_t st);
 hipError_t beam_scores_launch(int BK, int d, const int* look, const int* y, const float* lp, const float* head_lp,
                               int* n_accept, float* scores, hipStream_t st);
 hipError_t select_launch(int B, int k, const float* scores, const float* reward, float alpha, int reward_only,
-                         int* beam, hipStream_t st);
+                         const float* first_at, int* beam, hipStream_t st);
+hipError_t controller_states_launch(int B, int d, const int* n_accept, const float* reward, double a_t, double r_t,
+                                    int b1, int* state, float* first_at, hipStream_t st);
 hipError_t reward_keywords_launch(int B, int k, int d, const int* gen, int gen_stride, const int* gen_len,
                                   const int* look, const int* upto, const int* kws, int n_kw, int normalize,
                                   float* reward, hipStream_t st);

@@ -539,10 +539,24 @@ __global__ void beam_scores_kernel(int BK, int d, const int* __restrict__ look, 
   scores[bk] = s;
 }
 
+// first_at (optional, [B]): Step-1 of the controller with b = 1 keeps the
+// greedy head (beam 0) when its reward reaches first_at[b]; NaN = no such rule.
 __global__ void select_kernel(int B, int k, const float* __restrict__ scores, const float* __restrict__ reward,
-                              float alpha, int reward_only, int* __restrict__ beam) {
+                              float alpha, int reward_only, const float* __restrict__ first_at,
+                              int* __restrict__ beam) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= B) return;
+  if (first_at) {
+    const float t = first_at[b], r0 = reward[b * k];
+    if (isnan(r0)) {
+      beam[b] = -1;
+      return;
+    }
+    if (!isnan(t) && r0 >= t) {
+      beam[b] = 0;
+      return;
+    }
+  }
   int best = -1;
   float bv = -INFINITY;
   bool bad = false;
@@ -556,6 +570,22 @@ __global__ void select_kernel(int B, int k, const float* __restrict__ scores, co
     }
   }
   beam[b] = bad ? -1 : best;
+}
+
+// Alg. 1 state of each prompt after a k = 1 lookahead: a = n / d (float64,
+// as the thresholds are given), r = the accepted window's reward.
+// state: 1 = S1 (a >= a_t and r >= r_t), 2 = S2/S3 (a < a_t), 4 = S4.
+// first_at[b] = r_t where Step-1 with b = 1 applies (state 2, b1 set), else NaN.
+__global__ void controller_states_kernel(int B, int d, const int* __restrict__ n_accept,
+                                         const float* __restrict__ reward, double a_t, double r_t, int b1,
+                                         int* __restrict__ state, float* __restrict__ first_at) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const double a = (double)n_accept[b] / (double)d;
+  const double r = (double)reward[b];
+  const int s = a < a_t ? 2 : (r >= r_t ? 1 : 4);
+  state[b] = s;
+  first_at[b] = (s == 2 && b1) ? (float)r_t : __int_as_float(0x7fc00000);
 }
 
 // Keyword reward, one workgroup per (b, i): distinct keywords present in
@@ -839,9 +869,16 @@ hipError_t beam_scores_launch(int BK, int d, const int* look, const int* y, cons
 }
 
 hipError_t select_launch(int B, int k, const float* scores, const float* reward, float alpha, int reward_only,
-                         int* beam, hipStream_t st) {
+                         const float* first_at, int* beam, hipStream_t st) {
   if (B == 0) return hipSuccess;
-  select_kernel<<<(B + 127) / 128, 128, 0, st>>>(B, k, scores, reward, alpha, reward_only, beam);
+  select_kernel<<<(B + 127) / 128, 128, 0, st>>>(B, k, scores, reward, alpha, reward_only, first_at, beam);
+  return hipGetLastError();
+}
+
+hipError_t controller_states_launch(int B, int d, const int* n_accept, const float* reward, double a_t, double r_t,
+                                    int b1, int* state, float* first_at, hipStream_t st) {
+  if (B == 0) return hipSuccess;
+  controller_states_kernel<<<(B + 127) / 128, 128, 0, st>>>(B, d, n_accept, reward, a_t, r_t, b1, state, first_at);
   return hipGetLastError();
 }
 

@@ -907,7 +907,31 @@ int cdsl_select(cdsl_ctx* c, const float* scores, const float* reward, float alp
   return guarded(c, [&]() {
     const int reward_only = isinf(alpha) ? 1 : 0;
     Span sp(c, CDSL_K_STEP, 0.0, (double)B * k * 8.0);
-    CK(select_launch(B, k, scores, reward, reward_only ? 0.f : alpha, reward_only, beam, c->st));
+    CK(select_launch(B, k, scores, reward, reward_only ? 0.f : alpha, reward_only, nullptr, beam, c->st));
+    return CDSL_OK;
+  });
+}
+
+int cdsl_select_first(cdsl_ctx* c, const float* reward, const float* first_at, int32_t B, int32_t k,
+                      int32_t* beam) {
+  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  if (!reward || !first_at || !beam || B <= 0 || k <= 0) return fail(c, CDSL_EINVAL, "bad argument");
+  return guarded(c, [&]() {
+    Span sp(c, CDSL_K_STEP, 0.0, (double)B * (k * 4.0 + 8.0));
+    CK(select_launch(B, k, reward, reward, 0.f, 1, first_at, beam, c->st));
+    return CDSL_OK;
+  });
+}
+
+int cdsl_controller_states(cdsl_ctx* c, const int32_t* n_accept, const float* reward, int32_t B, int32_t d,
+                           double a_t, double r_t, int32_t b, int32_t* state, float* first_at) {
+  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  if (!n_accept || !reward || !state || !first_at || B <= 0 || d <= 0) return fail(c, CDSL_EINVAL, "bad argument");
+  if (b != 0 && b != 1) return fail(c, CDSL_EINVAL, "b must be 0 or 1");
+  if (isnan(a_t) || isnan(r_t)) return fail(c, CDSL_EINVAL, "thresholds must not be NaN");
+  return guarded(c, [&]() {
+    Span sp(c, CDSL_K_STEP, 0.0, (double)B * 16.0);
+    CK(controller_states_launch(B, d, n_accept, reward, a_t, r_t, b, state, first_at, c->st));
     return CDSL_OK;
   });
 }

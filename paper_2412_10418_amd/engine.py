@@ -20,6 +20,9 @@ import torch
 
 from .binding import Context, Prefix, upload_weights
 
+# state codes of cdsl_controller_states
+STATE_NAMES = {1: "S1", 2: "S2/S3", 4: "S4"}
+
 
 @dataclass
 class StepBuffers:
@@ -83,11 +86,13 @@ class Engine:
 
     def step(self, st: DecodeState, keywords: Optional[torch.Tensor] = None,
              reward_w: Optional[torch.Tensor] = None, alpha: Optional[float] = None,
-             k: Optional[int] = None, d: Optional[int] = None, marks: Optional[list] = None) -> StepBuffers:
+             k: Optional[int] = None, d: Optional[int] = None, marks: Optional[list] = None,
+             reward: Optional[str] = None) -> StepBuffers:
         """One lookahead step.  Updates ``st`` in place; returns the step's
         buffers (valid until the next step with the same shape).  With a list
         ``marks``, timing events are appended before the rollout, after it,
-        after the verification and after the commit."""
+        after the verification and after the commit.  ``reward`` overrides the
+        workload's reward kind."""
         def mark():
             if marks is not None:
                 e = torch.cuda.Event(enable_timing=True)
@@ -105,7 +110,7 @@ class Engine:
         mark()
         c.cdsl_verify(st.prefix, bf.lookaheads, k, d, st.head_lp, out=bf.verify)
         mark()
-        kind = self.wl.reward
+        kind = reward or self.wl.reward
         if kind == "linear":
             c.cdsl_reward_linear(bf.verify["hidden"], reward_w, bf.reward)
         else:
@@ -145,44 +150,33 @@ class Engine:
                 "verify": {"logprobs": z(B, 1, d), "target_argmax": z(B, 1, d, dt=i32),
                            "n_accept": z(B, 1, dt=i32), "scores": z(B, 1),
                            "row_topk_ids": z(B, 1, d, k, dt=i32), "row_topk_lp": z(B, 1, d, k), "hidden": None},
-                "reward": z(B, 1), "beam": z(B, dt=i32), "next_beams": z(B, k, dt=i32), "next_head_lp": z(B, k)}
+                "reward": z(B, 1), "beam": z(B, dt=i32), "next_beams": z(B, k, dt=i32), "next_head_lp": z(B, k),
+                "state": z(B, dt=i32), "first_at": z(B)}
         return self._bufs[key]
 
     def head_step(self, st: DecodeState, keywords: torch.Tensor, roller: int, k: Optional[int] = None,
                   d: Optional[int] = None, mask: Optional[List[bool]] = None,
-                  prefer_first_at: Optional[List[Optional[float]]] = None) -> dict:
+                  first_at: Optional[torch.Tensor] = None,
+                  normalize: Optional[bool] = None) -> dict:
         """One token of lookahead-heuristic decoding for every prompt (or the
         prompts with mask[b]): the k heads of ``st`` (top-k of the target) are
         rolled d tokens by the roller (1 = target: CDLH, 0 = draft:
         CDLH-appx.), scored by the lexical reward, and the best head is
-        emitted.  prefer_first_at[b] = r_t makes prompt b take head 0 when its
-        reward reaches r_t (Step-1 of Alg. 1 with b = 1)."""
+        emitted.  first_at (device [B], NaN = off) makes prompt b take head 0
+        when its reward reaches first_at[b] (Step-1 of Alg. 1 with b = 1)."""
         k = k or self.k
         d = d or self.d
         B = st.prefix.B
         hb = self._heads_buffers(B, k, d)
         c = self.ctx
-        normalize = self.wl.reward == "keyword_coverage"
+        if normalize is None:
+            normalize = self.wl.reward == "keyword_coverage"
         c.cdsl_rollout_with(st.prefix, st.beams, k, d, roller, hb["look"])
         c.cdsl_reward_keywords(st.prefix, hb["look"], k, d, keywords, normalize=normalize, reward=hb["reward"])
-        if prefer_first_at is None:
+        if first_at is None:
             c.cdsl_select(hb["reward"], hb["reward"], math.inf, hb["beam"])
-            r = None
         else:
-            r = hb["reward"].cpu().tolist()
-            picks = []
-            for b in range(B):
-                rb = r[b]
-                t = prefer_first_at[b]
-                if t is not None and rb[0] >= t:
-                    picks.append(0)
-                else:
-                    best = 0
-                    for i in range(1, k):
-                        if rb[i] > rb[best]:
-                            best = i
-                    picks.append(best)
-            hb["beam"].copy_(torch.tensor(picks, dtype=torch.int32))
+            c.cdsl_select_first(hb["reward"], first_at, hb["beam"])
         toks = c.cdsl_commit_heads(st.prefix, hb["look"], hb["beam"], k, d, mask, st.beams, st.head_lp)
         for b in range(B):
             if toks[b] >= 0:
@@ -190,7 +184,8 @@ class Engine:
         return {"tokens": toks, "lookaheads": hb["look"], "reward": hb["reward"], "beam": hb["beam"]}
 
     def controller_step(self, st: DecodeState, keywords: torch.Tensor, a_t: float, r_t: float, b: int,
-                        k: Optional[int] = None, d: Optional[int] = None) -> dict:
+                        k: Optional[int] = None, d: Optional[int] = None,
+                        normalize: Optional[bool] = None) -> dict:
         """One iteration of Alg. 1 for every prompt, with the readings of the
         oracle's ``controller_step``: draft d tokens after the target's greedy
         head c (k = 1 rollout), verify them (top-k width k for the next
@@ -204,31 +199,32 @@ class Engine:
         B = st.prefix.B
         cb = self._controller_buffers(B, k, d)
         c = self.ctx
-        normalize = self.wl.reward == "keyword_coverage"
+        if normalize is None:
+            normalize = self.wl.reward == "keyword_coverage"
         cb["heads"].copy_(st.beams[:, :1])
         cb["head_lp"].copy_(st.head_lp[:, :1])
         c.cdsl_rollout(st.prefix, cb["heads"], 1, d, cb["look"])
         c.cdsl_verify(st.prefix, cb["look"], 1, d, cb["head_lp"], out=cb["verify"], kk=k)
         c.cdsl_reward_keywords_upto(st.prefix, cb["look"], 1, d, cb["verify"]["n_accept"], keywords,
                                     normalize=normalize, reward=cb["reward"])
-        n = cb["verify"]["n_accept"][:, 0].cpu().tolist()
-        r = cb["reward"][:, 0].cpu().tolist()
-        states = []
-        for i in range(B):
-            a = n[i] / d
-            states.append("S1" if (a >= a_t and r[i] >= r_t) else ("S2/S3" if a < a_t else "S4"))
+        c.cdsl_controller_states(cb["verify"]["n_accept"], cb["reward"], d, a_t, r_t, b, cb["state"], cb["first_at"])
         em, _, _ = c.cdsl_commit(st.prefix, cb["look"], cb["beam"], cb["verify"]["n_accept"],
                                  cb["verify"]["row_topk_ids"], cb["verify"]["row_topk_lp"], 1, d,
                                  cb["next_beams"], cb["next_head_lp"], kk=k)
+        # commit has synchronised the stream: these reads only copy
+        codes = cb["state"].cpu().tolist()
+        n = cb["verify"]["n_accept"][:, 0].cpu().tolist()
+        r = cb["reward"][:, 0].cpu().tolist()
+        states = [STATE_NAMES[x] for x in codes]
         for i in range(B):
             st.emitted[i].extend(em[i])
         st.beams.copy_(cb["next_beams"])
         st.head_lp.copy_(cb["next_head_lp"])
         extra = None
-        need = [s_ != "S1" for s_ in states]
+        need = [x != 1 for x in codes]
         if any(need):
-            pref = [r_t if (states[i] == "S2/S3" and b == 1) else None for i in range(B)]
-            extra = self.head_step(st, keywords, 0, k=k, d=d, mask=need, prefer_first_at=pref)
+            extra = self.head_step(st, keywords, 0, k=k, d=d, mask=need, first_at=cb["first_at"],
+                                   normalize=normalize)
         return {"states": states, "n": n, "r": r, "emitted": em, "extra": extra}
 
     def close(self):

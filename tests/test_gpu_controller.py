@@ -1,12 +1,12 @@
 """The paper's baselines (CDLH, CDLH-appx.) and its full controller (Alg. 1
 states S1..S4) on the GPU, through the C ABI, against the float64 oracle.
 
-Token choices are compared while every deciding margin of the oracle (top-k
-boundaries, greedy draws, acceptance tests) exceeds the margin of the
-workload's precision (1e-3 for fp32, whose logits match the oracle to ~1e-6;
-TOK_MARGIN for bf16); a prompt's comparison stops at its first closer call
-(either choice is correct there).  Rewards are concept counts, exact on both
-sides."""
+Every token choice is compared.  Where the GPU and the oracle choose
+differently, the oracle's deciding margin there (top-k boundary, greedy draw,
+acceptance test) must be within the margin of the workload's precision (1e-3
+for fp32, whose logits match the oracle to ~1e-6; TOK_MARGIN for bf16):
+either choice is then correct, and that prompt's comparison ends.  Rewards
+are concept counts, exact on both sides."""
 import math
 
 import numpy as np
@@ -42,21 +42,81 @@ def _margin(s):
 
 
 def _oracle_states(s, B):
-    return [oracle.prefill(s.odraft, s.otarget, p) for p in s.prompts(B)]
+    """Prefilled oracle states of the first B prompts, kept on the setup (the
+    oracle's states are immutable values)."""
+    cache = s.__dict__.setdefault("_ost", {})
+    if B not in cache:
+        cache[B] = [oracle.prefill(s.odraft, s.otarget, p) for p in s.prompts(B)]
+    return list(cache[B])
 
 
-@pytest.mark.parametrize("roller", [0, 1])
-def test_head_steps_match_oracle(tiny, roller):
-    """CDLH (roller 1, the target) and CDLH-appx. (roller 0, the draft):
-    8 one-token steps for 6 prompts."""
-    s, eng = tiny, tiny.engine
-    B, k, d = 6, s.wl.k, s.wl.d
+def _first_diff(a, b):
+    for u, (x, y) in enumerate(zip(a, b)):
+        if int(x) != int(y):
+            return u
+    return -1
+
+
+def _cmp_head_step(M, look, rew, tok, hs):
+    """One prompt's one-token lookahead step (GPU lookaheads [k, d+1],
+    rewards [k], token) against the oracle's HeadStep.  Returns "" when
+    everything matched, else the near tie that ended the comparison."""
+    u = _first_diff(look[:, 0], hs.heads)
+    if u >= 0:
+        assert hs.head_margin <= M, (list(look[:, 0]), list(hs.heads), hs.head_margin)
+        return f"head near tie ({hs.head_margin:.1e})"
+    for i in range(len(hs.heads)):
+        u = _first_diff(look[i, 1:], hs.x[i])
+        if u >= 0:
+            assert hs.margin[i, u] <= M, (i, u, list(look[i]), list(hs.x[i]), hs.margin[i])
+            return f"rollout near tie ({hs.margin[i, u]:.1e})"
+    assert np.allclose(rew, hs.reward, rtol=0, atol=1e-6), (rew, hs.reward)
+    assert tok == hs.token
+    return ""
+
+
+def _cmp_controller(M, look, y, out, b, cs):
+    """One prompt's Alg. 1 iteration: GPU lookahead [d+1], target argmax of
+    the verified rows [d], the engine's outputs, against ControllerStep."""
+    got = list(out["emitted"][b])
+    if got[0] != cs.head:
+        assert cs.head_margin <= M, (got[0], cs.head, cs.head_margin)
+        return f"head near tie ({cs.head_margin:.1e})"
+    u = _first_diff(look[1:], cs.x)
+    if u >= 0:
+        assert cs.draft_margin[u] <= M, (u, list(look), list(cs.x), cs.draft_margin)
+        return f"draft near tie ({cs.draft_margin[u]:.1e})"
+    u = _first_diff(y, cs.ver.y[0])
+    if u >= 0:
+        assert cs.ver.margin[0, u] <= M, (u, list(y), list(cs.ver.y[0]), cs.ver.margin[0])
+        if out["n"][b] != cs.n:
+            return f"acceptance near tie ({cs.ver.margin[0, u]:.1e})"
+    assert out["n"][b] == cs.n
+    assert out["r"][b] == pytest.approx(cs.r, abs=1e-6)
+    assert out["states"][b] == cs.state
+    ex = out["extra"]
+    if cs.extra is not None:
+        assert ex is not None and ex["tokens"][b] >= 0
+        why = _cmp_head_step(M, ex["lookaheads"][b].cpu().numpy(), ex["reward"][b].cpu().numpy(),
+                             ex["tokens"][b], cs.extra)
+        if why:
+            return why
+        got.append(ex["tokens"][b])
+    else:
+        assert ex is None or ex["tokens"][b] < 0
+    assert got == cs.emitted
+    return ""
+
+
+def _run_head_steps(s, B, steps, roller):
+    eng = s.engine
+    k, d = s.wl.k, s.wl.d
     st = eng.start(torch.from_numpy(s.prompts(B)).cuda())
     kw = torch.from_numpy(s.kws[:B]).cuda()
     ost = _oracle_states(s, B)
     alive = [True] * B
     compared = 0
-    for _ in range(8):
+    for _ in range(steps):
         out = eng.head_step(st, kw, roller)
         look = out["lookaheads"].cpu().numpy()
         rew = out["reward"].cpu().numpy()
@@ -64,70 +124,73 @@ def test_head_steps_match_oracle(tiny, roller):
             if not alive[b]:
                 continue
             hs = oracle.cdlh_step(roller == 1, s.odraft, s.otarget, ost[b], k, d, s.wl.reward, s.kws[b])
-            if hs.head_margin <= _margin(s) or float(hs.margin.min()) <= _margin(s):
+            why = _cmp_head_step(_margin(s), look[b], rew[b], out["tokens"][b], hs)
+            if why:
+                print(f"prompt {b}: stopped after {compared} compared steps: {why}")
                 alive[b] = False
                 continue
-            assert list(look[b, :, 0]) == list(hs.heads)
-            assert (look[b, :, 1:] == hs.x).all()
-            assert np.array_equal(rew[b], hs.reward.astype(np.float32))
-            assert out["tokens"][b] == hs.token
             ost[b] = hs.state
             compared += 1
-    assert compared >= 10   # the oracle's margins allow 14 (roller 0) and 11 (roller 1)
     for b in range(B):
         if alive[b]:
             assert st.emitted[b] == ost[b].generated
     assert st.prefix.lengths() == [s.wl.prompt_len + len(e) for e in st.emitted]
     st.prefix.free()
+    print("compared", compared)
+    return compared
 
 
-@pytest.mark.parametrize("which,a_t,r_t,bb,state", [
-    ("tiny", 0.5, 1.0, 1, "S2/S3"), ("tiny", 0.5, 1.0, 0, "S2/S3"),
-    ("tiny_same", 0.5, 0.0, 0, "S1"), ("tiny_same", 0.5, 1.0, 1, "S4")])
-def test_controller_steps_match_oracle(request, which, a_t, r_t, bb, state):
-    """Alg. 1 with hard rejection, 5 iterations for 3 prompts: the state of
-    every prompt, n, r and the emitted tokens."""
-    s = request.getfixturevalue(which)
+def _run_controller(s, B, steps, a_t, r_t, bb):
     eng = s.engine
-    B, k, d = 3, s.wl.k, s.wl.d
+    k, d = s.wl.k, s.wl.d
     st = eng.start(torch.from_numpy(s.prompts(B)).cuda())
     kw = torch.from_numpy(s.kws[:B]).cuda()
     ost = _oracle_states(s, B)
     alive = [True] * B
     seen = set()
     compared = 0
-    for _ in range(5):
+    cb = eng._controller_buffers(B, k, d)
+    for _ in range(steps):
         out = eng.controller_step(st, kw, a_t, r_t, bb)
+        look = cb["look"][:, 0].cpu().numpy()
+        y = cb["verify"]["target_argmax"][:, 0].cpu().numpy()
         for b in range(B):
             if not alive[b]:
                 continue
             cs = oracle.controller_step(s.odraft, s.otarget, ost[b], k, d, a_t, r_t, bb, s.wl.reward, s.kws[b])
-            # deciding margins: the head, the draft draws, the acceptance
-            # tests, and for the extra token its candidates and their draws
-            m = min(cs.head_margin, float(cs.draft_margin.min()), float(cs.ver.margin[0].min()))
-            if cs.extra is not None:
-                m = min(m, cs.extra.head_margin, float(cs.extra.margin.min()))
-            if m <= _margin(s):
+            why = _cmp_controller(_margin(s), look[b], y[b], out, b, cs)
+            if why:
+                print(f"prompt {b}: stopped after {compared} compared steps: {why}")
                 alive[b] = False
                 continue
-            assert out["n"][b] == cs.n
-            assert out["r"][b] == pytest.approx(cs.r)
-            assert out["states"][b] == cs.state
-            got = list(out["emitted"][b])
-            if out["extra"] is not None and out["extra"]["tokens"][b] >= 0:
-                got.append(out["extra"]["tokens"][b])
-            assert got == cs.emitted
             seen.add(cs.state)
             ost[b] = cs.after
             compared += 1
-    assert compared >= 5    # the oracle's margins allow 6 to 10 per setting
-    print("states seen:", sorted(seen))
-    assert state in seen
     for b in range(B):
         if alive[b]:
             assert st.emitted[b] == ost[b].generated
     assert st.prefix.lengths() == [s.wl.prompt_len + len(e) for e in st.emitted]
     st.prefix.free()
+    print("compared", compared, "states seen:", sorted(seen))
+    return compared, seen
+
+
+@pytest.mark.parametrize("roller", [0, 1])
+def test_head_steps_match_oracle(tiny, roller):
+    """CDLH (roller 1, the target) and CDLH-appx. (roller 0, the draft):
+    8 one-token steps for 6 prompts."""
+    assert _run_head_steps(tiny, 6, 8, roller) >= 10
+
+
+@pytest.mark.parametrize("which,a_t,r_t,bb,state", [
+    ("tiny", 0.5, 1.0, 1, "S2/S3"), ("tiny", 0.5, 1.0, 0, "S2/S3"),
+    ("tiny_same", 0.5, 0.0, 0, "S1"), ("tiny_same", 0.5, 1.0, 1, "S4")])
+def test_controller_steps_match_oracle(request, which, a_t, r_t, bb, state):
+    """Alg. 1 with hard rejection, 5 iterations for 3 prompts: the head, the
+    draft, the acceptance, n, r, the state and the emitted tokens."""
+    compared, seen = _run_controller(request.getfixturevalue(which), 3, 5, a_t, r_t, bb)
+    assert compared >= 5
+    assert state in seen
 
 
 def test_controller_error_paths(tiny):
@@ -143,3 +206,27 @@ def test_controller_error_paths(tiny):
                                   torch.zeros(1, dtype=torch.int32, device="cuda"), s.wl.k, s.wl.d, None,
                                   st.beams, st.head_lp)
     st.prefix.free()
+
+
+@pytest.fixture(scope="module")
+def small():
+    s = make_setup("small")
+    make_engine(s, B=2, max_steps=12)
+    yield s
+    s.engine.close()
+
+
+# the float64 oracle of the 24-layer target takes ~15 s per step on the host
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("roller", [0, 1])
+def test_small_bf16_head_steps_match_oracle(small, roller):
+    """bf16 weights: CDLH rolls with the hd = 128 target (4 key groups do
+    not fit, so 2 key groups and both row tiles per workgroup), CDLH-appx.
+    with the hd = 64 draft; 2 one-token steps for 2 prompts."""
+    assert _run_head_steps(small, 2, 2, roller) >= 1
+
+
+@pytest.mark.timeout(900)
+def test_small_bf16_controller_matches_oracle(small):
+    compared, _ = _run_controller(small, 2, 2, 0.4, 0.3, 1)
+    assert compared >= 1
