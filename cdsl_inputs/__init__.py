@@ -241,3 +241,15 @@ def keywords(seed: int, batch: int, n_kw: int, vocab: int, first: int = 0) -> np
 def reward_head(seed: int, d_model: int) -> np.ndarray:
     g = np.random.default_rng([seed, 3])
     return g.standard_normal(d_model, dtype=np.float32) * np.float32(0.02)
+
+
+def uniforms(seed: int, which: int, step: int, batch: int, k: int, d: int, first: int = 0) -> np.ndarray:
+    """float32 [batch, k, d] draws from U[0, 1) for speculative sampling:
+    which = 0 for the acceptance tests, 1 for the residual draws; row i
+    belongs to prompt ``first + i`` at decoding step ``step``.  Both sides
+    read these float32 values, so the oracle's draws equal the kernels'."""
+    out = np.empty((batch, k, d), dtype=np.float32)
+    for i in range(batch):
+        g = np.random.default_rng([seed, 4 + which, step, first + i])
+        out[i] = g.random((k, d), dtype=np.float32)
+    return out

@@ -12,7 +12,9 @@ reduces to plain greedy decoding of the target; draft = target accepts every
 lookahead token; beam selection against brute-force enumeration on a tiny
 vocabulary; the paper's worked reward value (2 of 5 concepts -> 0.4); the
 lookahead-heuristic baselines and the Alg. 1 controller against greedy
-decoding of the target and against full recomputation.
+decoding of the target and against full recomputation; speculative
+sampling's acceptance rate and residual draw against their closed forms, and
+the pair against the theorem that it reproduces the target distribution.
 """
 from .decoder import Decoder, KVCache, ForwardOut, rms_norm, rope  # noqa: F401
 from .cdsl import (  # noqa: F401
@@ -21,4 +23,5 @@ from .cdsl import (  # noqa: F401
     keyword_hits, keyword_coverage, select_beam, reward_for,
     verify_rows_tree, verify_rows_per_beam,
     keyword_reward, argmax_first, lookahead_heads, cdlh_step, controller_step, HeadStep, ControllerStep,
+    soft_accept_count, soft_accept_margins, residual_sample, SoftResult,
 )

@@ -15,12 +15,18 @@ a3  verification: p_j = M_p(pfx + c_i + x_{i,<j}), j = 1..d, all k*d rows
 a4  l_{i,j} = log p_j(x_{i,j}); y_{i,j} = argmax p_j.
 a5  hard rejection: n_i = number of leading j with y_{i,j} = x_{i,j}
     (Alg. 1, rejection loop); a_i = n_i / d; score_i = head_lp_i + sum_j l_{i,j}.
+    Soft rejection (speculative sampling, Sec. 3.2.2): x_{i,j} is rejected
+    when u_{i,j} > min(1, p_j(x_{i,j}) / q_j(x_{i,j})) with u ~ U[0, 1); n_i
+    counts the positions before the first rejection.
 a6  reward r_i over generated-so-far + c_i + x_{i,1..d} (Sec. 3.2.2,
     validation by R; lexical rewards of Sec. 4.1).
 a7  select i* = argmax_i (score_i + alpha * r_i); alpha = inf means the
     reward alone, ties to the lowest index (Alg. 2's strict ">" update).
 a8  commit: emit O = [c_i*, x_i*,1..n_i*] (S1 action, no bonus token from
     M_p; Sec. 3.2.3), pfx <- pfx + O, and s_{t+1} = log_softmax(M_p(pfx)).
+    With soft rejection and n_i* < d, the token drawn at the rejected
+    position from the adjusted distribution (normalised max(0, p - q),
+    Sec. 3.2.2) leads the next beam heads, in place of M_p's greedy token.
 
 Readings where the paper is silent or garbled are listed in the design doc and
 restated next to the code that takes them.
@@ -110,6 +116,7 @@ class PromptState:
     target_cache: KVCache
     s: np.ndarray              # log_softmax of M_p at the end of the prefix
     s_logits: np.ndarray       # the raw target logits of that row
+    lead: Optional[int] = None  # soft rejection's resampled token: the first next head
 
     @property
     def generated(self) -> List[int]:
@@ -132,6 +139,8 @@ def prefill(draft: Decoder, target: Decoder, prompt: Sequence[int]) -> PromptSta
 class Rollout:
     x: np.ndarray              # [k, d] lookahead tokens
     margin: np.ndarray         # [k, d] top-2 margin of the draft logits at each draw
+    lq: Optional[np.ndarray] = None      # [k, d] log q_j(x_{i,j}), the draft's own log-prob
+    logits: Optional[np.ndarray] = None  # [k, d, V] the draft logits of every draw
 
 
 def rollout(draft: Decoder, st: PromptState, heads: Sequence[int], d: int) -> Rollout:
@@ -140,6 +149,8 @@ def rollout(draft: Decoder, st: PromptState, heads: Sequence[int], d: int) -> Ro
     k = len(heads)
     x = np.zeros((k, d), np.int64)
     mg = np.zeros((k, d))
+    lq = np.zeros((k, d))
+    zs = np.zeros((k, d, draft.shape.vocab))
     for i, c in enumerate(heads):
         cache = st.draft_cache
         fed = int(c)
@@ -148,8 +159,10 @@ def rollout(draft: Decoder, st: PromptState, heads: Sequence[int], d: int) -> Ro
             z = out.logits[0]
             x[i, j] = argmax_lowest(z)
             mg[i, j] = top2_margin(z)
+            lq[i, j] = log_softmax(z)[x[i, j]]
+            zs[i, j] = z
             fed = int(x[i, j])
-    return Rollout(x, mg)
+    return Rollout(x, mg, lq, zs)
 
 
 @dataclass
@@ -236,14 +249,84 @@ def reward_for(kind: str, generated: Sequence[int], heads, x, hidden, kws=None, 
     return r
 
 
-def commit(draft: Decoder, target: Decoder, st: PromptState, emitted: Sequence[int]) -> PromptState:
+def commit(draft: Decoder, target: Decoder, st: PromptState, emitted: Sequence[int],
+           lead: Optional[int] = None) -> PromptState:
     """a8: pfx <- pfx + O; both caches are extended by feeding O, and the
-    next head distribution is read at the last emitted token."""
+    next head distribution is read at the last emitted token.  ``lead`` (soft
+    rejection) is the token that heads the next beams."""
     emitted = [int(t) for t in emitted]
     _, dc = draft.extend(st.draft_cache, emitted)
     out, tc = target.extend(st.target_cache, emitted)
     z = out.logits[-1]
-    return PromptState(st.tokens + emitted, st.n_prompt, dc, tc, log_softmax(z), z)
+    return PromptState(st.tokens + emitted, st.n_prompt, dc, tc, log_softmax(z), z,
+                       None if lead is None else int(lead))
+
+
+# ----------------------------------------------------------------------------
+# speculative sampling (soft rejection), Sec. 3.2.2
+# ----------------------------------------------------------------------------
+def soft_accept_count(lp_target: Sequence[float], lp_draft: Sequence[float], u: Sequence[float]) -> int:
+    """Speculative sampling's test on one lookahead: x_j is rejected when
+    u_j > min(1, p_j(x_j) / q_j(x_j)), with u_j ~ U[0, 1) given and the
+    ratio formed from the two log-probs; returns the number of positions
+    before the first rejection."""
+    n = 0
+    for lt, ld, uj in zip(lp_target, lp_draft, u):
+        if float(uj) > min(1.0, math.exp(float(lt) - float(ld))):
+            break
+        n += 1
+    return n
+
+
+def soft_accept_margins(lp_target, lp_draft, u) -> np.ndarray:
+    """Distance of every u_j from its acceptance bound min(1, p/q)."""
+    lt = np.asarray(lp_target, np.float64)
+    ld = np.asarray(lp_draft, np.float64)
+    return np.abs(np.asarray(u, np.float64) - np.minimum(1.0, np.exp(lt - ld)))
+
+
+def residual_sample(zp: np.ndarray, zq: np.ndarray, v: float):
+    """The new token at a rejected position: a draw from the adjusted
+    distribution w = max(0, p - q) / Z, Z = sum(w), with p and q the
+    softmaxes of the target and draft logits there.  The draw inverts the
+    cumulative sum over token ids in ascending order at v * Z: the smallest
+    t with w_0 + ... + w_t > v * Z.  When Z = 0 (p <= q everywhere, which
+    after a rejection only rounding can cause) it is argmax p.  Returns
+    (token, log p(token), margin) with margin = the distance of v * Z from
+    the nearest cumulative boundary, over Z."""
+    p = np.exp(log_softmax(zp))
+    q = np.exp(log_softmax(zq))
+    w = np.maximum(0.0, p - q)
+    Z = float(np.sum(w))
+    lp = np.log(p)
+    if Z <= 0.0:
+        t = argmax_lowest(zp)
+        return t, float(lp[t]), 0.0
+    target = float(v) * Z
+    run = 0.0
+    t = -1
+    for tok in range(len(w)):
+        if w[tok] <= 0.0:
+            continue
+        nxt = run + float(w[tok])
+        if nxt > target:
+            t = tok
+            break
+        run = nxt
+    if t < 0:            # v * Z beyond the rounded total: the last token with mass
+        t = int(np.nonzero(w > 0.0)[0][-1])
+        return t, float(lp[t]), 0.0
+    margin = min(target - run, run + float(w[t]) - target) / Z
+    return t, float(lp[t]), margin
+
+
+@dataclass
+class SoftResult:
+    n: np.ndarray              # [k] positions before the first soft rejection
+    accept_margin: np.ndarray  # [k, d] |u - min(1, p/q)|
+    lead: Optional[int]        # residual draw of the selected beam (None when n = d)
+    lead_lp: Optional[float]
+    lead_margin: float
 
 
 @dataclass
@@ -258,27 +341,55 @@ class StepResult:
     beam: int
     emitted: List[int]
     state: PromptState         # state after the commit
+    soft: Optional[SoftResult] = None
 
 
 def beam_heads(st: PromptState, k: int):
-    """a1: top-k of s_t (value descending, id ascending) and their log-probs."""
-    ids = topk_ids(st.s_logits, k)
-    srt = np.sort(st.s_logits)[::-1][:k + 1]
-    return ids, st.s[ids], -np.diff(srt)
+    """a1: top-k of s_t (value descending, id ascending) and their log-probs.
+    After a soft rejection the resampled token ``st.lead`` comes first and
+    the other k - 1 heads are the top of s_t without it.  The margins are
+    the gaps between consecutive values of the ranked part (inf for the
+    lead, which the residual draw decides)."""
+    if st.lead is None:
+        ids = topk_ids(st.s_logits, k)
+        srt = np.sort(st.s_logits)[::-1][:k + 1]
+        return ids, st.s[ids], -np.diff(srt)
+    rest = [int(t) for t in topk_ids(st.s_logits, k) if int(t) != st.lead][:k - 1]
+    ids = np.array([st.lead] + rest, np.int64)
+    others = np.delete(np.asarray(st.s_logits, np.float64), st.lead)
+    srt = np.sort(others)[::-1][:k]
+    return ids, st.s[ids], np.concatenate([[math.inf], -np.diff(srt)])
 
 
 def step(draft: Decoder, target: Decoder, st: PromptState, k: int, d: int, alpha: float,
-         reward_kind: str, kws=None, w=None, tree: bool = True) -> StepResult:
+         reward_kind: str, kws=None, w=None, tree: bool = True, rejection: str = "hard",
+         u: Optional[np.ndarray] = None, v: Optional[np.ndarray] = None) -> StepResult:
+    """One CDSL step.  rejection = "soft" takes speculative sampling's test
+    with the given uniforms u [k, d] and draws the next lead token with
+    v [k, d] (the entry of the selected beam at its rejected position)."""
     heads, head_lp, hm = beam_heads(st, k)
     ro = rollout(draft, st, heads, d)
     ve = verify(target, st, heads, head_lp, ro.x, tree=tree)
     r = reward_for(reward_kind, st.generated, heads, ro.x, ve.hidden, kws, w)
     comb = r if (math.isinf(alpha) and alpha > 0) else ve.scores + alpha * r
     b = select_beam(ve.scores, r, alpha)
-    n = int(ve.n[b])
+    soft = None
+    if rejection == "soft":
+        ns = np.array([soft_accept_count(ve.logprobs[i], ro.lq[i], u[i]) for i in range(k)], np.int64)
+        am = np.stack([soft_accept_margins(ve.logprobs[i], ro.lq[i], u[i]) for i in range(k)])
+        n = int(ns[b])
+        lead, lead_lp, lm = None, None, math.inf
+        if n < d:
+            lead, lead_lp, lm = residual_sample(ve.logits[b, n], ro.logits[b, n], v[b, n])
+        soft = SoftResult(ns, am, lead, lead_lp, lm)
+    elif rejection == "hard":
+        n = int(ve.n[b])
+        lead = None
+    else:
+        raise ValueError(rejection)
     emitted = [int(heads[b])] + [int(t) for t in ro.x[b, :n]]
-    nst = commit(draft, target, st, emitted)
-    return StepResult(heads, head_lp, hm, ro, ve, r, comb, b, emitted, nst)
+    nst = commit(draft, target, st, emitted, lead)
+    return StepResult(heads, head_lp, hm, ro, ve, r, comb, b, emitted, nst, soft)
 
 
 # ----------------------------------------------------------------------------

@@ -437,3 +437,143 @@ def test_controller_visits_every_state_on_the_tiny_workload():
                 seen[cs.state] = seen.get(cs.state, 0) + 1
                 st = cs.after
     assert set(seen) == {"S1", "S2/S3", "S4"}, seen
+
+
+# ---------------------------------------------------------------------------
+# speculative sampling (soft rejection)
+# ---------------------------------------------------------------------------
+def _grid(N):
+    """Stratified points of U[0, 1): every cell of width 1/N once."""
+    return (np.arange(N) + 0.5) / N
+
+
+def _softmax(z):
+    e = np.exp(np.asarray(z, np.float64) - np.max(z))
+    return e / e.sum()
+
+
+def test_soft_acceptance_rate_is_min_one_ratio():
+    """Over a stratified grid of u the accepted fraction equals min(1, p/q)
+    (to the grid's 1/N), and a run ends at its first rejection."""
+    N = 2000
+    rng = np.random.default_rng(5)
+    for _ in range(12):
+        lt, ld = rng.uniform(-6.0, 0.0, 2)
+        acc = sum(oracle.soft_accept_count([lt], [ld], [u]) for u in _grid(N)) / N
+        assert abs(acc - min(1.0, math.exp(lt - ld))) <= 1.0 / N
+    assert oracle.soft_accept_count([0.0, -9.0, 0.0], [0.0, 0.0, 0.0], [0.5, 0.5, 0.0]) == 1
+    assert oracle.soft_accept_count([-1.0, -1.0], [-2.0, -2.0], [0.999, 0.999]) == 2   # p > q: always kept
+    assert oracle.soft_accept_count([-1.0], [-1.0], [0.0]) == 1
+
+
+def test_residual_draw_is_the_inverse_cdf_of_the_positive_part():
+    """Each draw equals a library inverse-CDF lookup on the normalised
+    max(0, p - q); over a stratified grid of v the frequencies match it and
+    tokens with p <= q are never drawn.  Equal logits fall back to argmax p."""
+    rng = np.random.default_rng(6)
+    V = 9
+    zp, zq = rng.normal(0.0, 2.0, V), rng.normal(0.0, 2.0, V)
+    p, q = _softmax(zp), _softmax(zq)
+    w = np.maximum(0.0, p - q)
+    w /= w.sum()
+    cdf = np.cumsum(w)
+    N = 5000
+    counts = np.zeros(V)
+    for v in _grid(N):
+        t, lp, mg = oracle.residual_sample(zp, zq, v)
+        counts[t] += 1
+        assert t == int(np.searchsorted(cdf, v, side="right"))
+        assert abs(lp - math.log(p[t])) < 1e-12
+        assert 0.0 <= mg <= w[t] / 2 + 1e-12
+    assert np.max(np.abs(counts / N - w)) <= 1.0 / N + 1e-12
+    assert np.all(counts[w == 0.0] == 0)
+    t, _, _ = oracle.residual_sample(zp, zp, 0.3)
+    assert t == int(np.argmax(zp))
+
+
+def _output_distribution(zp, zq, residual=None):
+    """Distribution of speculative sampling's output token when the draft
+    token x is drawn from q: accepted with the oracle's test, else replaced
+    by the oracle's residual draw; enumerated over x and stratified u, v."""
+    residual = residual or oracle.residual_sample
+    lp, lq = oracle.log_softmax(zp), oracle.log_softmax(zq)
+    V = len(zp)
+    Nu = Nv = 1000
+    R = np.zeros(V)
+    for v in _grid(Nv):
+        R[residual(zp, zq, v)[0]] += 1.0 / Nv
+    out = np.zeros(V)
+    for x in range(V):
+        acc = sum(oracle.soft_accept_count([lp[x]], [lq[x]], [u]) for u in _grid(Nu)) / Nu
+        out[x] += math.exp(lq[x]) * acc
+        out += math.exp(lq[x]) * (1.0 - acc) * R
+    return out
+
+
+def test_speculative_sampling_reproduces_the_target_distribution():
+    """The theorem speculative sampling rests on (Leviathan et al., 2023):
+    with x ~ q, accept-or-resample outputs tokens distributed exactly as p."""
+    rng = np.random.default_rng(7)
+    for V in (2, 6):
+        zp, zq = rng.normal(0.0, 1.5, V), rng.normal(0.0, 1.5, V)
+        out = _output_distribution(zp, zq)
+        assert np.max(np.abs(out - _softmax(zp))) < 3e-3
+
+
+def test_swapped_residual_fails_the_distribution_pin():
+    """A planted mistake in the oracle (drawing from max(0, q - p)) breaks
+    the theorem check above."""
+    rng = np.random.default_rng(7)
+    zp, zq = rng.normal(0.0, 1.5, 6), rng.normal(0.0, 1.5, 6)
+    swapped = lambda a, b, v: oracle.residual_sample(b, a, v)
+    out = _output_distribution(zp, zq, swapped)
+    assert np.max(np.abs(out - _softmax(zp))) > 3e-2
+
+
+def test_soft_step_with_draft_equal_to_target_accepts_every_token(models):
+    _, _, dt, _ = models["mha"]
+    st = oracle.prefill(dt, dt, _prompt(6, 64, seed=2))
+    k, d = 3, 4
+    u = np.full((k, d), np.nextafter(np.float32(1.0), np.float32(0.0)), np.float32)
+    r = oracle.step(dt, dt, st, k, d, 1.0, "keyword_count", kws=[5, 6, 7], rejection="soft", u=u, v=u)
+    assert list(r.soft.n) == [d] * k
+    assert r.soft.lead is None and r.state.lead is None
+    assert len(r.emitted) == d + 1
+
+
+def test_soft_step_matches_full_recompute(models):
+    """Every beam's soft count from p and q recomputed by the library models
+    on the full sequences; the selected beam's lead token is the residual
+    draw from those logits at its rejected position, and it heads the next
+    beams, followed by the target's top tokens without it."""
+    from hf_ref import hf_logits
+    draft, target, st = _state(models, n=8)
+    hf_d, hf_t = models["gqa"][3], models["mha"][3]
+    k, d = 3, 4
+    rng = np.random.default_rng(12)
+    seen_lead = 0
+    cur = st
+    for it in range(4):
+        u = rng.random((k, d)).astype(np.float32)
+        v = rng.random((k, d)).astype(np.float32)
+        r = oracle.step(draft, target, cur, k, d, 1.0, "keyword_count", kws=[1, 2, 3], rejection="soft", u=u, v=v)
+        for i in range(k):
+            seq = list(cur.tokens) + [int(r.heads[i])] + [int(t) for t in r.roll.x[i]]
+            L = len(cur.tokens)
+            zt = hf_logits(hf_t, seq[:-1])[L:]          # p_j for x_{i,j}, j = 1..d
+            zd = hf_logits(hf_d, seq[:-1])[L:]
+            lt = [oracle.log_softmax(zt[j])[r.roll.x[i, j]] for j in range(d)]
+            ld = [oracle.log_softmax(zd[j])[r.roll.x[i, j]] for j in range(d)]
+            assert oracle.soft_accept_count(lt, ld, u[i]) == r.soft.n[i]
+            if i == r.beam and r.soft.n[i] < d:
+                n = int(r.soft.n[i])
+                t, _, _ = oracle.residual_sample(zt[n], zd[n], v[i, n])
+                assert t == r.soft.lead
+                seen_lead += 1
+        nxt, _, _ = oracle.beam_heads(r.state, k)
+        if r.soft.lead is not None:
+            zn = hf_logits(hf_t, r.state.tokens)[-1]
+            rest = [int(x) for x in sorted(range(len(zn)), key=lambda x: (-zn[x], x)) if x != r.soft.lead][:k - 1]
+            assert list(nxt) == [r.soft.lead] + rest
+        cur = r.state
+    assert seen_lead >= 1
