@@ -19,6 +19,9 @@
  *   cdsl_commit    emits the selected beam's head plus its accepted tokens
  *                  (S1 action of Sec. 3.2.3, no bonus token), makes them part
  *                  of the shared prefix and produces the next beam heads
+ *   cdsl_rollout_keep, cdsl_verify_soft, cdsl_commit_soft
+ *                  the same step with speculative sampling's soft rejection
+ *                  (Sec. 3.2.2) in place of the argmax test
  *   cdsl_rollout_with, cdsl_reward_keywords_upto, cdsl_controller_states,
  *   cdsl_select_first, cdsl_commit_heads
  *                  the pieces of the paper's full controller (Alg. 1 states
@@ -34,9 +37,9 @@
  *     They are owned by the caller and only read/written during the call
  *     (device work is ordered on the context's stream).
  *   - Calls are asynchronous on the stream given to cdsl_init, except
- *     cdsl_commit and cdsl_commit_heads, which synchronise that stream once
- *     (they must learn how many tokens each prompt emitted to manage the KV
- *     blocks).
+ *     cdsl_commit, cdsl_commit_soft and cdsl_commit_heads, which
+ *     synchronise that stream once (they must learn how many tokens each
+ *     prompt emitted to manage the KV blocks).
  *   - Shapes are row-major, innermost last.  Token ids are int32 in [0, V).
  *   - Nothing is allocated after cdsl_init except by cdsl_prefill (the
  *     prefix handle's bookkeeping; KV blocks come from the pool sized at
@@ -206,6 +209,56 @@ int cdsl_reward_linear(cdsl_ctx* ctx, const float* hidden, const float* w,
  * reward makes beam[b] = -1, which cdsl_commit reports as EINVAL. */
 int cdsl_select(cdsl_ctx* ctx, const float* scores, const float* reward,
                 float alpha, int32_t B, int32_t k, int32_t* beam);
+
+/* Speculative sampling (soft rejection, Sec. 3.2.2) replaces the argmax
+ * test of the verification.  The three calls below are used in place of
+ * cdsl_rollout, cdsl_verify and cdsl_commit (reward and selection are
+ * unchanged); the draft and the target must share one vocabulary V. */
+
+/* cdsl_rollout that also keeps the draft's logits of every draft pass:
+ * draft_logits[B, k, d, V] (fp32, device, caller-owned, B*k*d*V*4 bytes;
+ * entry (b, i, j) is q_{j+1} of beam i, the distribution its token
+ * x_{i,j+1} was drawn from).  The buffer must stay untouched until the
+ * matching cdsl_verify_soft.  Errors as cdsl_rollout; ERANGE if d * V
+ * exceeds 2^31 - 1. */
+int cdsl_rollout_keep(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* beams,
+                      int32_t k, int32_t d, int32_t* lookaheads,
+                      float* draft_logits);
+
+/* cdsl_verify with speculative sampling's test: x_{i,j} is kept while
+ * u[b, i, j-1] <= min(1, p_j(x_{i,j}) / q_j(x_{i,j})), and n_accept counts
+ * the kept tokens before the first rejection.  u and v are [B, k, d]
+ * uniforms in [0, 1) supplied by the caller (the method's random numbers
+ * are inputs).  Outputs, beyond those of cdsl_verify (top-k width k):
+ *   draft_lp[B, k, d]  log q_j(x_{i,j})
+ *   res_ids[B, k, d]   for every fed row, the draw at v from the normalised
+ *                      max(0, p_j - q_j) (token ids in ascending order;
+ *                      argmax p_j if p_j <= q_j everywhere)
+ *   res_lp[B, k, d]    log p_j of that draw.
+ * draft_logits must be the buffer of the last cdsl_rollout_keep on this
+ * prefix with the same k and d (ESTATE otherwise).  Errors as cdsl_verify;
+ * EINVAL if the two models' vocabularies differ. */
+int cdsl_verify_soft(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookaheads,
+                     int32_t k, int32_t d, const float* head_lp,
+                     const float* draft_logits, const float* u, const float* v,
+                     float* logprobs, float* draft_lp, int32_t* target_argmax,
+                     int32_t* n_accept, float* scores, int32_t* row_topk_ids,
+                     float* row_topk_lp, int32_t* res_ids, float* res_lp,
+                     float* hidden);
+
+/* cdsl_commit after cdsl_verify_soft.  Emits [c_i*, x_i*,1..n] as
+ * cdsl_commit does (no bonus token).  When n < d, the next heads are the
+ * residual draw res_ids[b, i*, n] (head_lp res_lp) followed by the k - 1
+ * best tokens of that row's top-k without it; when n = d they are the
+ * target's top-k after the catch-up, as in cdsl_commit.  Errors as
+ * cdsl_commit; ESTATE if the last verification was not soft (and
+ * cdsl_commit returns ESTATE after a soft one). */
+int cdsl_commit_soft(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookaheads,
+                     const int32_t* beam, const int32_t* n_accept,
+                     const int32_t* row_topk_ids, const float* row_topk_lp,
+                     const int32_t* res_ids, const float* res_lp, int32_t k,
+                     int32_t d, int32_t* emitted_host, int32_t* n_emit_host,
+                     int32_t* next_beams, float* next_head_lp);
 
 /* Reward-only selection with Step-1 of the controller (Sec. 3.2.3, S2/S3
  * with b = 1): beam[b] = 0 when reward[b, 0] >= first_at[b] (head 0 is the

@@ -53,6 +53,22 @@ int cdsl_op_logit_rows(const float* logits, int32_t M, int32_t V,
                        int32_t* amax, int32_t* topk_ids, float* topk_lp,
                        void* stream);
 
+/* Speculative sampling rows (Sec. 3.2.2) over target_logits[M, V] (p) and
+ * draft_logits[M, V] (q), fp32, rows ordered (row group g, position j) with
+ * M = G * d; the row's draft token is x = lookaheads[g, j + 1] (an int32
+ * [G, d + 1] array, as cdsl_rollout writes it).  For row m = g * d + j:
+ *   draft_lp[m] = log q(x)
+ *   res_ids[m]  = the draw at v[m] in [0, 1) from w = max(0, p - q) / Z:
+ *                 the smallest token t with w_0 + ... + w_t > v[m] * Z
+ *                 (argmax p, lowest id, when Z = 0)
+ *   res_lp[m]   = log p(res_ids[m]).
+ * This is the kernel cdsl_verify_soft runs after the verification pass.
+ * Errors: EINVAL (null pointers, M not a multiple of d). */
+int cdsl_op_soft_rows(const float* target_logits, const float* draft_logits,
+                      int32_t M, int32_t V, int32_t d, const int32_t* lookaheads,
+                      const float* v, float* draft_lp, int32_t* res_ids,
+                      float* res_lp, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

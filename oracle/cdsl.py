@@ -320,6 +320,19 @@ def residual_sample(zp: np.ndarray, zq: np.ndarray, v: float):
     return t, float(lp[t]), margin
 
 
+def residual_interval(zp: np.ndarray, zq: np.ndarray, t: int):
+    """The part of [0, 1) that draws token t in ``residual_sample``: the
+    cumulative sums of w / Z before and after t (equal when w_t = 0), and Z."""
+    p = np.exp(log_softmax(zp))
+    q = np.exp(log_softmax(zq))
+    w = np.maximum(0.0, p - q)
+    Z = float(np.sum(w))
+    if Z <= 0.0:
+        return 0.0, 0.0, 0.0
+    lo = float(np.sum(w[:t])) / Z
+    return lo, lo + float(w[t]) / Z, Z
+
+
 @dataclass
 class SoftResult:
     n: np.ndarray              # [k] positions before the first soft rejection

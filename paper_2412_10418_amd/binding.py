@@ -20,7 +20,8 @@ CDSL_EPI_STORE, CDSL_EPI_RESIDUAL = 0, 1
 ERR_NAMES = {0: "OK", -1: "EINVAL", -2: "ERANGE", -3: "ENOMEM", -4: "EDEVICE", -5: "ESTATE"}
 
 EXPORTS = [
-    "cdsl_init", "cdsl_prefill", "cdsl_rollout", "cdsl_rollout_with", "cdsl_verify", "cdsl_verify_kk",
+    "cdsl_init", "cdsl_prefill", "cdsl_rollout", "cdsl_rollout_with", "cdsl_rollout_keep", "cdsl_verify",
+    "cdsl_verify_kk", "cdsl_verify_soft", "cdsl_commit_soft", "cdsl_op_soft_rows",
     "cdsl_reward_keywords",
     "cdsl_reward_keywords_upto", "cdsl_reward_linear", "cdsl_select", "cdsl_select_first", "cdsl_controller_states",
     "cdsl_commit", "cdsl_commit_kk",
@@ -80,6 +81,10 @@ def lib():
         "cdsl_prefill": ([vp, vp, i32, i32, i32, C.POINTER(vp), vp, vp], i32),
         "cdsl_rollout": ([vp, vp, vp, i32, i32, vp], i32),
         "cdsl_rollout_with": ([vp, vp, vp, i32, i32, i32, vp], i32),
+        "cdsl_rollout_keep": ([vp, vp, vp, i32, i32, vp, vp], i32),
+        "cdsl_verify_soft": ([vp, vp, vp, i32, i32] + [vp] * 14, i32),
+        "cdsl_commit_soft": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, vp, vp, vp, vp], i32),
+        "cdsl_op_soft_rows": ([vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp], i32),
         "cdsl_reward_keywords_upto": ([vp, vp, vp, i32, i32, vp, vp, i32, i32, vp], i32),
         "cdsl_commit_heads": ([vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp], i32),
         "cdsl_verify_kk": ([vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp], i32),
@@ -168,6 +173,24 @@ def cdsl_op_logit_rows(logits: torch.Tensor, gather: Optional[torch.Tensor], kk:
                                   amax.data_ptr(), tk.data_ptr(), tl.data_ptr(), _stream())
     _check(rc)
     return lp, amax, tk[:, :kk], tl[:, :kk]
+
+
+def cdsl_op_soft_rows(target_logits: torch.Tensor, draft_logits: torch.Tensor, d: int, lookaheads: torch.Tensor,
+                      v: torch.Tensor):
+    """Returns (draft_lp, res_ids, res_lp), each [M]."""
+    M, V = target_logits.shape
+    if draft_logits.shape != (M, V) or v.shape != (M,) or lookaheads.shape != (M // d, d + 1) or M % d:
+        raise ValueError("shapes: logits [M, V] twice, lookaheads [M/d, d+1], v [M]")
+    dev = target_logits.device
+    dlp = torch.empty(M, dtype=torch.float32, device=dev)
+    rid = torch.empty(M, dtype=torch.int32, device=dev)
+    rlp = torch.empty(M, dtype=torch.float32, device=dev)
+    rc = lib().cdsl_op_soft_rows(_ptr(target_logits, torch.float32, "target_logits"),
+                                 _ptr(draft_logits, torch.float32, "draft_logits"), M, V, d,
+                                 _ptr(lookaheads, torch.int32, "lookaheads"), _ptr(v, torch.float32, "v"),
+                                 dlp.data_ptr(), rid.data_ptr(), rlp.data_ptr(), _stream())
+    _check(rc)
+    return dlp, rid, rlp
 
 
 # ---------------------------------------------------------------------------
@@ -271,6 +294,52 @@ class Context:
                                      int(roller), _ptr(lookaheads, torch.int32, "lookaheads"))
         _check(rc, self.handle)
         return lookaheads
+
+    def cdsl_rollout_keep(self, prefix: Prefix, beams: torch.Tensor, k: int, d: int, lookaheads: torch.Tensor,
+                          draft_logits: torch.Tensor) -> torch.Tensor:
+        if draft_logits.numel() != prefix.B * k * d * self.draft_shape.vocab:
+            raise ValueError("draft_logits must be [B, k, d, V]")
+        rc = lib().cdsl_rollout_keep(self.handle, prefix.handle, _ptr(beams, torch.int32, "beams"), k, d,
+                                     _ptr(lookaheads, torch.int32, "lookaheads"),
+                                     _ptr(draft_logits, torch.float32, "draft_logits"))
+        _check(rc, self.handle)
+        return lookaheads
+
+    def cdsl_verify_soft(self, prefix: Prefix, lookaheads: torch.Tensor, k: int, d: int, head_lp: torch.Tensor,
+                         draft_logits: torch.Tensor, u: torch.Tensor, v: torch.Tensor, out: dict,
+                         want_hidden: bool = False) -> dict:
+        """out: the buffers of cdsl_verify plus draft_lp, res_ids, res_lp ([B, k, d])."""
+        B = prefix.B
+        for nm, t in (("u", u), ("v", v)):
+            if t.shape != (B, k, d):
+                raise ValueError(f"{nm} must be [B, k, d]")
+        hid = out.get("hidden") if want_hidden else None
+        rc = lib().cdsl_verify_soft(self.handle, prefix.handle, _ptr(lookaheads, torch.int32, "lookaheads"), k, d,
+                                    _ptr(head_lp, torch.float32, "head_lp"),
+                                    _ptr(draft_logits, torch.float32, "draft_logits"), _ptr(u, torch.float32, "u"),
+                                    _ptr(v, torch.float32, "v"), out["logprobs"].data_ptr(),
+                                    out["draft_lp"].data_ptr(), out["target_argmax"].data_ptr(),
+                                    out["n_accept"].data_ptr(), out["scores"].data_ptr(),
+                                    out["row_topk_ids"].data_ptr(), out["row_topk_lp"].data_ptr(),
+                                    out["res_ids"].data_ptr(), out["res_lp"].data_ptr(),
+                                    hid.data_ptr() if hid is not None else None)
+        _check(rc, self.handle)
+        return out
+
+    def cdsl_commit_soft(self, prefix: Prefix, lookaheads, beam, n_accept, row_topk_ids, row_topk_lp, res_ids,
+                         res_lp, k, d, next_beams: torch.Tensor, next_head_lp: torch.Tensor):
+        B = prefix.B
+        emitted = (C.c_int32 * (B * (d + 1)))()
+        n_emit = (C.c_int32 * B)()
+        rc = lib().cdsl_commit_soft(self.handle, prefix.handle, _ptr(lookaheads, torch.int32, "lookaheads"),
+                                    _ptr(beam, torch.int32, "beam"), _ptr(n_accept, torch.int32, "n_accept"),
+                                    _ptr(row_topk_ids, torch.int32, "row_topk_ids"),
+                                    _ptr(row_topk_lp, torch.float32, "row_topk_lp"),
+                                    _ptr(res_ids, torch.int32, "res_ids"), _ptr(res_lp, torch.float32, "res_lp"),
+                                    k, d, emitted, n_emit, _ptr(next_beams, torch.int32, "next_beams"),
+                                    _ptr(next_head_lp, torch.float32, "next_head_lp"))
+        _check(rc, self.handle)
+        return [[emitted[b * (d + 1) + t] for t in range(n_emit[b])] for b in range(B)]
 
     def cdsl_verify(self, prefix: Prefix, lookaheads: torch.Tensor, k: int, d: int, head_lp: torch.Tensor,
                     want_hidden: bool = False, out: Optional[dict] = None, kk: Optional[int] = None) -> dict:

@@ -13,8 +13,9 @@ struct RowMap {
 };
 
 struct LogitArgs {
-  const float* logits;     // [M][V]
+  const float* logits;     // [M][ld] (ld = V when 0)
   int V;
+  long long ld;
   int want_lse;            // 0: argmax only
   int kk;                  // top-k per row (0..16)
   int* amax;               // argmax destination (RowMap or [M])
@@ -48,8 +49,13 @@ hipError_t rope_kv_launch(const PassDesc& p, const float* qkv, void* qout, const
                           const float* cos_t, const float* sin_t, int H, int Hkv, int hd, int dtype, hipStream_t st,
                           int S = 0);
 hipError_t logit_rows_launch(const LogitArgs& a, int M, hipStream_t st);
+// lq, u non-null: soft rejection (speculative sampling) instead of the argmax match
 hipError_t beam_scores_launch(int BK, int d, const int* look, const int* y, const float* lp, const float* head_lp,
-                              int* n_accept, float* scores, hipStream_t st);
+                              const float* lq, const float* u, int* n_accept, float* scores, hipStream_t st);
+// speculative sampling rows: draft log-prob of each row's token and the
+// residual draw; see kernels.hip
+hipError_t soft_rows_launch(const float* zp, const float* zq, int M, int V, int d, const int* look, const float* v,
+                            float* draft_lp, int* res_ids, float* res_lp, hipStream_t st);
 hipError_t select_launch(int B, int k, const float* scores, const float* reward, float alpha, int reward_only,
                          const float* first_at, int* beam, hipStream_t st);
 hipError_t controller_states_launch(int B, int d, const int* n_accept, const float* reward, double a_t, double r_t,
@@ -63,8 +69,9 @@ hipError_t commit_heads_launch(int B, int k, int d, const int* look, const int* 
                                int stage_stride, int* gen, int gen_stride, int* gen_len, int* catch_tok,
                                hipStream_t st);
 hipError_t commit_launch(int B, int k, int d, int kk, const int* look, const int* beam, const int* n_accept,
-                         const int* rtk_ids, const float* rtk_lp, int* next_beams, float* next_head_lp, int* stage,
-                         int stage_stride, int* gen, int gen_stride, int* gen_len, int* catch_tok, hipStream_t st);
+                         const int* rtk_ids, const float* rtk_lp, const int* res_ids, const float* res_lp,
+                         int* next_beams, float* next_head_lp, int* stage, int stage_stride, int* gen, int gen_stride,
+                         int* gen_len, int* catch_tok, hipStream_t st);
 hipError_t promote_launch(int B, int k, const KVPool& pool, int n_layers, const int* stage, int stage_stride, int dlim,
                           const int* Lp, const int* ptable, int ptable_stride, const int* stable, int s_stride_b,
                           int s_stride_i, int dtype, hipStream_t st);

@@ -370,7 +370,7 @@ __global__ __launch_bounds__(256) void logit_rows_kernel(LogitArgs a) {
   __shared__ float shs[4];
   const int m = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const float* z = a.logits + (long long)m * a.V;
+  const float* z = a.logits + (long long)m * (a.ld ? a.ld : (long long)a.V);
 
   float mloc = -INFINITY, sloc = 0.f;
   float bv = -INFINITY;
@@ -521,8 +521,11 @@ __global__ __launch_bounds__(256) void logit_rows_kernel(LogitArgs a) {
 // ---------------------------------------------------------------------------
 // Hard rejection (leading matches of target argmax and lookahead) and beam
 // scores, one thread per (b, i).
+// With lq and u (soft rejection, speculative sampling): x_j is kept while
+// u_j <= min(1, p_j(x_j) / q_j(x_j)), the ratio formed from the two log-probs.
 __global__ void beam_scores_kernel(int BK, int d, const int* __restrict__ look, const int* __restrict__ y,
                                    const float* __restrict__ lp, const float* __restrict__ head_lp,
+                                   const float* __restrict__ lq, const float* __restrict__ u,
                                    int* __restrict__ n_accept, float* __restrict__ scores) {
   const int bk = blockIdx.x * blockDim.x + threadIdx.x;
   if (bk >= BK) return;
@@ -530,10 +533,13 @@ __global__ void beam_scores_kernel(int BK, int d, const int* __restrict__ look, 
   bool run = true;
   float s = head_lp[bk];
   for (int j = 0; j < d; ++j) {
-    const int x = look[(long long)bk * (d + 1) + j + 1];
-    if (run && y[(long long)bk * d + j] == x) ++n;
+    const long long r = (long long)bk * d + j;
+    bool keep;
+    if (lq) keep = u[r] <= fminf(1.f, expf(lp[r] - lq[r]));
+    else keep = y[r] == look[(long long)bk * (d + 1) + j + 1];
+    if (run && keep) ++n;
     else run = false;
-    s += lp[(long long)bk * d + j];
+    s += lp[r];
   }
   n_accept[bk] = n;
   scores[bk] = s;
@@ -570,6 +576,159 @@ __global__ void select_kernel(int B, int k, const float* __restrict__ scores, co
     }
   }
   beam[b] = bad ? -1 : best;
+}
+
+// Speculative sampling rows (Sec. 3.2.2), one workgroup per fed row m of a
+// verification (rows ordered (b, i, j), both logit arrays [M][V]):
+//   draft_lp[m] = log q(x), x the row's lookahead token;
+//   res_ids[m]  = the draw at v[m] from w = max(0, p - q) / Z, inverting the
+//                 cumulative sum over token ids in ascending order (argmax p
+//                 when Z = 0), and res_lp[m] = log p of it.
+// Three passes over the rows: both logsumexps and argmax p; per-wave sums
+// of w over four contiguous id segments; one wave walks the segment that
+// holds v * Z with a 64-lane scan per chunk.
+__global__ __launch_bounds__(256) void soft_rows_kernel(const float* __restrict__ zp_all,
+                                                        const float* __restrict__ zq_all, int V, int d,
+                                                        const int* __restrict__ look, const float* __restrict__ v,
+                                                        float* __restrict__ draft_lp, int* __restrict__ res_ids,
+                                                        float* __restrict__ res_lp) {
+  __shared__ float sh_m[2][4], sh_s[2][4], sh_bv[4], part[4];
+  __shared__ int sh_bi[4];
+  __shared__ int sh_res;
+  const int m = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const float* zp = zp_all + (long long)m * V;
+  const float* zq = zq_all + (long long)m * V;
+
+  float mp = -INFINITY, sp = 0.f, mq = -INFINITY, sq = 0.f, bv = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int t = tid; t < V; t += 256) {
+    const float a = zp[t], b = zq[t];
+    if (a > mp) {
+      sp = sp * __expf(mp - a) + 1.f;
+      mp = a;
+    } else {
+      sp += __expf(a - mp);
+    }
+    if (b > mq) {
+      sq = sq * __expf(mq - b) + 1.f;
+      mq = b;
+    } else {
+      sq += __expf(b - mq);
+    }
+    if (vi_better(a, t, bv, bi)) {
+      bv = a;
+      bi = t;
+    }
+  }
+  {
+    float ov;
+    int oi;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      ov = __shfl_xor(bv, o, 64);
+      oi = __shfl_xor(bi, o, 64);
+      if (vi_better(ov, oi, bv, bi)) {
+        bv = ov;
+        bi = oi;
+      }
+    }
+    const float Mp = wave_max(mp), Mq = wave_max(mq);
+    const float s1 = wave_sum(mp == -INFINITY ? 0.f : sp * __expf(mp - Mp));
+    const float s2 = wave_sum(mq == -INFINITY ? 0.f : sq * __expf(mq - Mq));
+    if (lane == 0) {
+      sh_m[0][wv] = Mp;
+      sh_s[0][wv] = s1;
+      sh_m[1][wv] = Mq;
+      sh_s[1][wv] = s2;
+      sh_bv[wv] = bv;
+      sh_bi[wv] = bi;
+    }
+  }
+  __syncthreads();
+  float lse[2];
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const float M = fmaxf(fmaxf(sh_m[r][0], sh_m[r][1]), fmaxf(sh_m[r][2], sh_m[r][3]));
+    float sum = 0.f;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) sum += sh_m[r][u] == -INFINITY ? 0.f : sh_s[r][u] * __expf(sh_m[r][u] - M);
+    lse[r] = M + __logf(sum);
+  }
+  int amax = sh_bi[0];
+  {
+    float av = sh_bv[0];
+    for (int u = 1; u < 4; ++u)
+      if (vi_better(sh_bv[u], sh_bi[u], av, amax)) {
+        av = sh_bv[u];
+        amax = sh_bi[u];
+      }
+  }
+  // per-wave sums of w over contiguous segments (multiples of 64 ids)
+  const int seg = ((V + 255) / 256) * 64;
+  const int s0 = wv * seg, s1 = min(V, s0 + seg);
+  float acc = 0.f;
+  for (int t = s0 + lane; t < s1; t += 64) acc += fmaxf(0.f, __expf(zp[t] - lse[0]) - __expf(zq[t] - lse[1]));
+  acc = wave_sum(acc);
+  if (lane == 0) part[wv] = acc;
+  if (tid == 0) sh_res = -1;
+  __syncthreads();
+  const float Z = part[0] + part[1] + part[2] + part[3];
+  const float T = v[m] * Z;
+  // segment holding T (the last one with mass when rounding leaves T past the total)
+  int sg = -1;
+  float before = 0.f;
+  {
+    float run = 0.f;
+    for (int u = 0; u < 4; ++u) {
+      if (part[u] > 0.f) {
+        if (run + part[u] > T) {
+          sg = u;
+          before = run;
+          break;
+        }
+        sg = u;
+        before = run;
+      }
+      run += part[u];
+    }
+  }
+  if (Z > 0.f && wv == sg) {
+    const int g0 = sg * seg, g1 = min(V, g0 + seg);
+    const float Tl = T - before;
+    float run = 0.f;
+    int last = -1;
+    int found = -1;
+    for (int c0 = g0; c0 < g1; c0 += 64) {
+      const int t = c0 + lane;
+      const float wt = t < g1 ? fmaxf(0.f, __expf(zp[t] - lse[0]) - __expf(zq[t] - lse[1])) : 0.f;
+      float sc = wt;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const float n = __shfl_up(sc, o, 64);
+        if (lane >= o) sc += n;
+      }
+      const unsigned long long hit = __ballot(wt > 0.f && run + sc > Tl);
+      if (hit) {
+        found = c0 + __builtin_ctzll(hit);
+        break;
+      }
+      const unsigned long long mass = __ballot(wt > 0.f);
+      if (mass) last = c0 + 63 - __builtin_clzll(mass);
+      run += __shfl(sc, 63, 64);
+    }
+    if (lane == 0) sh_res = found >= 0 ? found : last;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int res = (Z > 0.f && sh_res >= 0) ? sh_res : amax;
+    const bool ok = res >= 0 && res < V;   // false only for rows without a finite logit
+    if (!ok) res = 0;
+    const int x = look[(long long)(m / d) * (d + 1) + (m % d) + 1];
+    draft_lp[m] = (x >= 0 && x < V) ? zq[x] - lse[1] : __int_as_float(0x7fc00000);
+    res_ids[m] = res;
+    res_lp[m] = ok ? zp[res] - lse[0] : __int_as_float(0x7fc00000);
+  }
 }
 
 // Alg. 1 state of each prompt after a k = 1 lookahead: a = n / d (float64,
@@ -639,9 +798,13 @@ __global__ __launch_bounds__(256) void reward_linear_kernel(const float* __restr
 }
 
 // Commit, one thread per prompt.  stage[b] = {n_emit, catch_up, tokens...}.
+// res_ids / res_lp (soft rejection, [B, k, d]): when n < d the residual draw
+// at the rejected position leads the next heads, followed by the row's top
+// tokens without it.
 __global__ void commit_kernel(int B, int k, int d, int kk, const int* __restrict__ look, const int* __restrict__ beam,
                               const int* __restrict__ n_accept, const int* __restrict__ rtk_ids,
-                              const float* __restrict__ rtk_lp, int* __restrict__ next_beams,
+                              const float* __restrict__ rtk_lp, const int* __restrict__ res_ids,
+                              const float* __restrict__ res_lp, int* __restrict__ next_beams,
                               float* __restrict__ next_head_lp, int* __restrict__ stage, int stage_stride,
                               int* __restrict__ gen, int gen_stride, int* __restrict__ gen_len,
                               int* __restrict__ catch_tok) {
@@ -665,7 +828,20 @@ __global__ void commit_kernel(int B, int k, int d, int kk, const int* __restrict
     gen[(long long)b * gen_stride + gl + t] = row[t];
   }
   gen_len[b] = gl + n + 1;
-  if (n < d) {
+  if (n < d && res_ids) {
+    const long long q = (long long)bk * d + n;
+    const long long r = q * kk;
+    const int lead = res_ids[q];
+    next_beams[b * kk] = lead;
+    next_head_lp[b * kk] = res_lp[q];
+    int o = 1;
+    for (int u = 0; u < kk && o < kk; ++u) {
+      if (rtk_ids[r + u] == lead) continue;
+      next_beams[b * kk + o] = rtk_ids[r + u];
+      next_head_lp[b * kk + o] = rtk_lp[r + u];
+      ++o;
+    }
+  } else if (n < d) {
     const long long r = ((long long)bk * d + n) * kk;
     for (int u = 0; u < kk; ++u) {
       next_beams[b * kk + u] = rtk_ids[r + u];
@@ -862,9 +1038,9 @@ hipError_t logit_rows_launch(const LogitArgs& a, int M, hipStream_t st) {
 }
 
 hipError_t beam_scores_launch(int BK, int d, const int* look, const int* y, const float* lp, const float* head_lp,
-                              int* n_accept, float* scores, hipStream_t st) {
+                              const float* lq, const float* u, int* n_accept, float* scores, hipStream_t st) {
   if (BK == 0) return hipSuccess;
-  beam_scores_kernel<<<(BK + 127) / 128, 128, 0, st>>>(BK, d, look, y, lp, head_lp, n_accept, scores);
+  beam_scores_kernel<<<(BK + 127) / 128, 128, 0, st>>>(BK, d, look, y, lp, head_lp, lq, u, n_accept, scores);
   return hipGetLastError();
 }
 
@@ -872,6 +1048,13 @@ hipError_t select_launch(int B, int k, const float* scores, const float* reward,
                          const float* first_at, int* beam, hipStream_t st) {
   if (B == 0) return hipSuccess;
   select_kernel<<<(B + 127) / 128, 128, 0, st>>>(B, k, scores, reward, alpha, reward_only, first_at, beam);
+  return hipGetLastError();
+}
+
+hipError_t soft_rows_launch(const float* zp, const float* zq, int M, int V, int d, const int* look, const float* v,
+                            float* draft_lp, int* res_ids, float* res_lp, hipStream_t st) {
+  if (M == 0) return hipSuccess;
+  soft_rows_kernel<<<M, 256, 0, st>>>(zp, zq, V, d, look, v, draft_lp, res_ids, res_lp);
   return hipGetLastError();
 }
 
@@ -906,10 +1089,12 @@ hipError_t commit_heads_launch(int B, int k, int d, const int* look, const int* 
 }
 
 hipError_t commit_launch(int B, int k, int d, int kk, const int* look, const int* beam, const int* n_accept,
-                         const int* rtk_ids, const float* rtk_lp, int* next_beams, float* next_head_lp, int* stage,
-                         int stage_stride, int* gen, int gen_stride, int* gen_len, int* catch_tok, hipStream_t st) {
-  commit_kernel<<<(B + 63) / 64, 64, 0, st>>>(B, k, d, kk, look, beam, n_accept, rtk_ids, rtk_lp, next_beams,
-                                              next_head_lp, stage, stage_stride, gen, gen_stride, gen_len, catch_tok);
+                         const int* rtk_ids, const float* rtk_lp, const int* res_ids, const float* res_lp,
+                         int* next_beams, float* next_head_lp, int* stage, int stage_stride, int* gen, int gen_stride,
+                         int* gen_len, int* catch_tok, hipStream_t st) {
+  commit_kernel<<<(B + 63) / 64, 64, 0, st>>>(B, k, d, kk, look, beam, n_accept, rtk_ids, rtk_lp, res_ids, res_lp,
+                                              next_beams, next_head_lp, stage, stage_stride, gen, gen_stride, gen_len,
+                                              catch_tok);
   return hipGetLastError();
 }
 

@@ -71,6 +71,8 @@ struct cdsl_prefix {
   int* gen_len = nullptr;      // device [B]
   int rolled_k = 0, rolled_d = 0;
   int verified_k = 0, verified_d = 0, verified_kk = 0;
+  const float* kept_logits = nullptr;   // draft logits of the last rollout (cdsl_rollout_keep)
+  int verified_soft = 0;
 };
 
 struct cdsl_ctx {
@@ -435,7 +437,8 @@ int gemm(cdsl_ctx* c, const GemmOperand& A, const void* W, const GemmOut& out, i
 // through the LM head into ws.logits; hid receives fp32 final-normed rows of
 // every beam's last row when non-null.
 void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, long long sum_prefix_len,
-              bool want_logits, bool last_only, float* hid, bool prefill = false) {
+              bool want_logits, bool last_only, float* hid, bool prefill = false, float* logits_out = nullptr,
+              int logits_ld = 0) {
   Workspace& w = c->ws;
   const auto& k = md.c;
   const int M = p.M();
@@ -540,7 +543,8 @@ void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, lon
     Span sp(c, CDSL_K_ROWWISE, 0.0, (double)rows * D * (4.0 + es));
     CK(rmsnorm_launch(w.h, md.gf, w.u32, w.uh, w.ul, rows, D, k.rms_eps, last_only ? 1 : 0, p.R, hid, c->st));
   }
-  gemm(c, Au, md.lm, GemmOut{w.logits, nullptr, nullptr, k.vocab}, rows, k.vocab, D, kEpiStore, prefill);
+  gemm(c, Au, md.lm, GemmOut{logits_out ? logits_out : w.logits, nullptr, nullptr, logits_ld ? logits_ld : k.vocab},
+       rows, k.vocab, D, kEpiStore, prefill);
 }
 
 void logit_rows(cdsl_ctx* c, const LogitArgs& la, int M) {
@@ -771,14 +775,20 @@ int cdsl_rollout(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, 
   return cdsl_rollout_with(c, px, beams, k, d, 0, lookaheads);
 }
 
-int cdsl_rollout_with(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, int32_t d, int32_t roller,
-                      int32_t* lookaheads) {
+namespace {
+
+// d sequential passes of the roller over all B*k beams; with keep, the
+// logits of pass j land in keep[(b*k + i)*d + j][V] instead of the workspace
+int rollout_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, int32_t d, int32_t roller,
+                 int32_t* lookaheads, float* keep) {
   if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
   if (roller != 0 && roller != 1) return fail(c, CDSL_EINVAL, "roller must be 0 (draft) or 1 (target)");
   if (!px || !beams || !lookaheads) return fail(c, CDSL_EINVAL, "null argument");
   if (k <= 0 || d <= 0) return fail(c, CDSL_EINVAL, "k and d must be positive");
   if (k > c->lim.max_k || d > c->lim.max_d) return fail(c, CDSL_ERANGE, "k or d beyond the limits");
   if (max_len(px) + d + 1 > c->lim.max_ctx) return fail(c, CDSL_ERANGE, "context would exceed max_ctx");
+  const int V = c->m[roller].c.vocab;
+  if (keep && (long long)d * V > INT32_MAX) return fail(c, CDSL_ERANGE, "d * vocab too large for the kept logits");
   return guarded(c, [&]() {
     const int B = px->B;
     CK(heads_to_lookaheads_launch(B * k, d, beams, lookaheads, c->st));
@@ -793,10 +803,12 @@ int cdsl_rollout_with(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_
       p.tok = lookaheads;
       p.tok_stride = d + 1;
       p.tok_off = j0;
-      run_pass(c, c->m[roller], p, Lmax, sum_len(px), true, false, nullptr);
+      float* dst = keep ? keep + (long long)j0 * V : nullptr;
+      run_pass(c, c->m[roller], p, Lmax, sum_len(px), true, false, nullptr, false, dst, keep ? d * V : 0);
       LogitArgs la{};
-      la.logits = c->ws.logits;
-      la.V = c->m[roller].c.vocab;
+      la.logits = dst ? dst : c->ws.logits;
+      la.V = V;
+      la.ld = keep ? (long long)d * V : 0;
       la.want_lse = 0;
       la.kk = 0;
       la.amax = lookaheads;
@@ -809,8 +821,22 @@ int cdsl_rollout_with(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_
     px->rolled_k = k;
     px->rolled_d = d;
     px->verified_k = px->verified_d = 0;
+    px->kept_logits = keep;
     return CDSL_OK;
   });
+}
+
+}  // namespace
+
+int cdsl_rollout_with(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, int32_t d, int32_t roller,
+                      int32_t* lookaheads) {
+  return rollout_impl(c, px, beams, k, d, roller, lookaheads, nullptr);
+}
+
+int cdsl_rollout_keep(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, int32_t d, int32_t* lookaheads,
+                      float* draft_logits) {
+  if (c && !draft_logits) return fail(c, CDSL_EINVAL, "null argument");
+  return rollout_impl(c, px, beams, k, d, 0, lookaheads, draft_logits);
 }
 
 int cdsl_verify(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d, const float* head_lp,
@@ -820,9 +846,20 @@ int cdsl_verify(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, in
                         row_topk_lp, hidden);
 }
 
-int cdsl_verify_kk(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d, int32_t kk,
-                   const float* head_lp, float* logprobs, int32_t* target_argmax, int32_t* n_accept, float* scores,
-                   int32_t* row_topk_ids, float* row_topk_lp, float* hidden) {
+namespace {
+
+struct SoftArgs {
+  const float* draft_logits;   // [B, k, d, V] from cdsl_rollout_keep
+  const float* u;              // [B, k, d]
+  const float* v;              // [B, k, d]
+  float* draft_lp;             // [B, k, d]
+  int32_t* res_ids;            // [B, k, d]
+  float* res_lp;               // [B, k, d]
+};
+
+int verify_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d, int32_t kk,
+                const float* head_lp, float* logprobs, int32_t* target_argmax, int32_t* n_accept, float* scores,
+                int32_t* row_topk_ids, float* row_topk_lp, float* hidden, const SoftArgs* soft) {
   if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
   if (kk <= 0 || kk > c->lim.max_k) return fail(c, CDSL_ERANGE, "top-k width beyond the limits");
   if (!px || !look || !head_lp || !logprobs || !target_argmax || !n_accept || !scores || !row_topk_ids ||
@@ -831,6 +868,13 @@ int cdsl_verify_kk(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k,
   if (k <= 0 || d <= 0) return fail(c, CDSL_EINVAL, "k and d must be positive");
   if (k > c->lim.max_k || d > c->lim.max_d) return fail(c, CDSL_ERANGE, "k or d beyond the limits");
   if (max_len(px) + d + 1 > c->lim.max_ctx) return fail(c, CDSL_ERANGE, "context would exceed max_ctx");
+  if (soft) {
+    if (!soft->draft_logits || !soft->u || !soft->v || !soft->draft_lp || !soft->res_ids || !soft->res_lp)
+      return fail(c, CDSL_EINVAL, "null argument");
+    if (c->m[0].c.vocab != c->m[1].c.vocab) return fail(c, CDSL_EINVAL, "soft rejection needs one vocabulary");
+    if (soft->draft_logits != px->kept_logits || px->rolled_k != k || px->rolled_d != d)
+      return fail(c, CDSL_ESTATE, "soft verification needs the logits of a cdsl_rollout_keep with the same k, d");
+  }
   return guarded(c, [&]() {
     const int B = px->B;
     PassDesc p = base_pass(c, px);
@@ -858,15 +902,40 @@ int cdsl_verify_kk(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k,
     la.topk_ids = row_topk_ids;
     la.topk_lp = row_topk_lp;
     logit_rows(c, la, p.M());
+    if (soft) {
+      Span sp(c, CDSL_K_LOGIT_ROWS, 0.0, (double)p.M() * la.V * 4.0 * 2.0);
+      CK(soft_rows_launch(c->ws.logits, soft->draft_logits, p.M(), la.V, d, look, soft->v, soft->draft_lp,
+                          soft->res_ids, soft->res_lp, c->st));
+    }
     {
-      Span sp(c, CDSL_K_STEP, 0.0, (double)B * k * d * 12.0);
-      CK(beam_scores_launch(B * k, d, look, target_argmax, logprobs, head_lp, n_accept, scores, c->st));
+      Span sp(c, CDSL_K_STEP, 0.0, (double)B * k * d * (soft ? 20.0 : 12.0));
+      CK(beam_scores_launch(B * k, d, look, target_argmax, logprobs, head_lp, soft ? soft->draft_lp : nullptr,
+                            soft ? soft->u : nullptr, n_accept, scores, c->st));
     }
     px->verified_k = k;
     px->verified_d = d;
     px->verified_kk = kk;
+    px->verified_soft = soft ? 1 : 0;
     return CDSL_OK;
   });
+}
+
+}  // namespace
+
+int cdsl_verify_kk(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d, int32_t kk,
+                   const float* head_lp, float* logprobs, int32_t* target_argmax, int32_t* n_accept, float* scores,
+                   int32_t* row_topk_ids, float* row_topk_lp, float* hidden) {
+  return verify_impl(c, px, look, k, d, kk, head_lp, logprobs, target_argmax, n_accept, scores, row_topk_ids,
+                     row_topk_lp, hidden, nullptr);
+}
+
+int cdsl_verify_soft(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d, const float* head_lp,
+                     const float* draft_logits, const float* u, const float* v, float* logprobs, float* draft_lp,
+                     int32_t* target_argmax, int32_t* n_accept, float* scores, int32_t* row_topk_ids,
+                     float* row_topk_lp, int32_t* res_ids, float* res_lp, float* hidden) {
+  const SoftArgs sa{draft_logits, u, v, draft_lp, res_ids, res_lp};
+  return verify_impl(c, px, look, k, d, k, head_lp, logprobs, target_argmax, n_accept, scores, row_topk_ids,
+                     row_topk_lp, hidden, &sa);
 }
 
 int cdsl_reward_keywords(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d,
@@ -943,9 +1012,38 @@ int cdsl_commit(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t
                         next_beams, next_head_lp);
 }
 
+namespace {
+int commit_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, const int32_t* n_accept,
+                const int32_t* rtk_ids, const float* rtk_lp, const int32_t* res_ids, const float* res_lp, int32_t k,
+                int32_t d, int32_t kk, int32_t* emitted_host, int32_t* n_emit_host, int32_t* next_beams,
+                float* next_head_lp);
+}  // namespace
+
 int cdsl_commit_kk(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, const int32_t* n_accept,
                    const int32_t* rtk_ids, const float* rtk_lp, int32_t k, int32_t d, int32_t kk,
                    int32_t* emitted_host, int32_t* n_emit_host, int32_t* next_beams, float* next_head_lp) {
+  if (c && px && px->verified_soft)
+    return fail(c, CDSL_ESTATE, "the last verification was soft: commit it with cdsl_commit_soft");
+  return commit_impl(c, px, look, beam, n_accept, rtk_ids, rtk_lp, nullptr, nullptr, k, d, kk, emitted_host,
+                     n_emit_host, next_beams, next_head_lp);
+}
+
+int cdsl_commit_soft(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, const int32_t* n_accept,
+                     const int32_t* rtk_ids, const float* rtk_lp, const int32_t* res_ids, const float* res_lp,
+                     int32_t k, int32_t d, int32_t* emitted_host, int32_t* n_emit_host, int32_t* next_beams,
+                     float* next_head_lp) {
+  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  if (!res_ids || !res_lp) return fail(c, CDSL_EINVAL, "null argument");
+  if (px && !px->verified_soft) return fail(c, CDSL_ESTATE, "cdsl_commit_soft needs a cdsl_verify_soft");
+  return commit_impl(c, px, look, beam, n_accept, rtk_ids, rtk_lp, res_ids, res_lp, k, d, k, emitted_host,
+                     n_emit_host, next_beams, next_head_lp);
+}
+
+namespace {
+int commit_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, const int32_t* n_accept,
+                const int32_t* rtk_ids, const float* rtk_lp, const int32_t* res_ids, const float* res_lp, int32_t k,
+                int32_t d, int32_t kk, int32_t* emitted_host, int32_t* n_emit_host, int32_t* next_beams,
+                float* next_head_lp) {
   if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
   if (!px || !look || !beam || !n_accept || !rtk_ids || !rtk_lp || !emitted_host || !n_emit_host || !next_beams ||
       !next_head_lp)
@@ -957,8 +1055,8 @@ int cdsl_commit_kk(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int3
     const int B = px->B;
     {
       Span sp(c, CDSL_K_STEP, 0.0, (double)B * (d + 1 + 2 * k) * 4.0);
-      CK(commit_launch(B, k, d, kk, look, beam, n_accept, rtk_ids, rtk_lp, next_beams, next_head_lp, c->stage,
-                       c->stage_stride, px->gen, c->lim.max_ctx, px->gen_len, c->catch_tok, c->st));
+      CK(commit_launch(B, k, d, kk, look, beam, n_accept, rtk_ids, rtk_lp, res_ids, res_lp, next_beams, next_head_lp,
+                       c->stage, c->stage_stride, px->gen, c->lim.max_ctx, px->gen_len, c->catch_tok, c->st));
     }
     CK(hipMemcpyAsync(c->stage_host, c->stage, (size_t)B * c->stage_stride * sizeof(int), hipMemcpyDeviceToHost,
                       c->st));
@@ -1027,9 +1125,12 @@ int cdsl_commit_kk(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int3
       for (int t = 0; t <= d; ++t) emitted_host[(size_t)b * (d + 1) + t] = t < stg[0] ? stg[3 + t] : -1;
     }
     px->rolled_k = px->rolled_d = px->verified_k = px->verified_d = 0;
+    px->verified_soft = 0;
+    px->kept_logits = nullptr;
     return CDSL_OK;
   });
 }
+}  // namespace
 
 int cdsl_commit_heads(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, int32_t k, int32_t d,
                       int32_t kk, const int32_t* mask_host, int32_t* emitted_host, int32_t* next_beams,
@@ -1106,6 +1207,8 @@ int cdsl_commit_heads(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const i
       emitted_host[b] = stg[0] > 0 ? stg[3] : -1;
     }
     px->rolled_k = px->rolled_d = px->verified_k = px->verified_d = 0;
+    px->verified_soft = 0;
+    px->kept_logits = nullptr;
     return CDSL_OK;
   });
 }
@@ -1217,3 +1320,15 @@ int cdsl_op_logit_rows(const float* logits, int32_t M, int32_t V, const int32_t*
 }
 
 }  // extern "C"
+
+int cdsl_op_soft_rows(const float* target_logits, const float* draft_logits, int32_t M, int32_t V, int32_t d,
+                      const int32_t* lookaheads, const float* v, float* draft_lp, int32_t* res_ids, float* res_lp,
+                      void* stream) {
+  if (!target_logits || !draft_logits || !lookaheads || !v || !draft_lp || !res_ids || !res_lp || M < 0 || V <= 0 ||
+      d <= 0 || M % d != 0)
+    return fail(nullptr, CDSL_EINVAL, "bad argument");
+  hipError_t e = soft_rows_launch(target_logits, draft_logits, M, V, d, lookaheads, v, draft_lp, res_ids, res_lp,
+                                  (hipStream_t)stream);
+  if (e != hipSuccess) return fail(nullptr, CDSL_EDEVICE, hipGetErrorString(e));
+  return CDSL_OK;
+}

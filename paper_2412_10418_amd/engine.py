@@ -84,15 +84,26 @@ class Engine:
         prefix, beams, head_lp = self.ctx.cdsl_prefill(prompts, k)
         return DecodeState(prefix, beams, head_lp, [[] for _ in range(prompts.shape[0])])
 
+    def _soft_buffers(self, B: int, k: int, d: int, bf: StepBuffers):
+        key = ("soft", B, k, d)
+        if key not in self._bufs:
+            dev = self.device
+            z = lambda *s, dt=torch.float32: torch.zeros(s, dtype=dt, device=dev)
+            self._bufs[key] = {"draft_logits": z(B, k, d, self.wl.draft.vocab)}
+            bf.verify.update(draft_lp=z(B, k, d), res_ids=z(B, k, d, dt=torch.int32), res_lp=z(B, k, d))
+        return self._bufs[key]
+
     def step(self, st: DecodeState, keywords: Optional[torch.Tensor] = None,
              reward_w: Optional[torch.Tensor] = None, alpha: Optional[float] = None,
              k: Optional[int] = None, d: Optional[int] = None, marks: Optional[list] = None,
-             reward: Optional[str] = None) -> StepBuffers:
+             reward: Optional[str] = None, u: Optional[torch.Tensor] = None,
+             v: Optional[torch.Tensor] = None) -> StepBuffers:
         """One lookahead step.  Updates ``st`` in place; returns the step's
         buffers (valid until the next step with the same shape).  With a list
         ``marks``, timing events are appended before the rollout, after it,
         after the verification and after the commit.  ``reward`` overrides the
-        workload's reward kind."""
+        workload's reward kind.  With uniforms u and v ([B, k, d] device
+        float32) the step uses speculative sampling's soft rejection."""
         def mark():
             if marks is not None:
                 e = torch.cuda.Event(enable_timing=True)
@@ -105,10 +116,22 @@ class Engine:
         B = st.prefix.B
         bf = self.buffers(B, k, d)
         c = self.ctx
+        soft = u is not None
+        if soft:
+            if v is None:
+                raise ValueError("soft rejection takes both u and v")
+            sb = self._soft_buffers(B, k, d, bf)
         mark()
-        c.cdsl_rollout(st.prefix, st.beams, k, d, bf.lookaheads)
+        if soft:
+            c.cdsl_rollout_keep(st.prefix, st.beams, k, d, bf.lookaheads, sb["draft_logits"])
+        else:
+            c.cdsl_rollout(st.prefix, st.beams, k, d, bf.lookaheads)
         mark()
-        c.cdsl_verify(st.prefix, bf.lookaheads, k, d, st.head_lp, out=bf.verify)
+        if soft:
+            c.cdsl_verify_soft(st.prefix, bf.lookaheads, k, d, st.head_lp, sb["draft_logits"], u, v, bf.verify,
+                               want_hidden=bf.verify["hidden"] is not None)
+        else:
+            c.cdsl_verify(st.prefix, bf.lookaheads, k, d, st.head_lp, out=bf.verify)
         mark()
         kind = reward or self.wl.reward
         if kind == "linear":
@@ -118,9 +141,14 @@ class Engine:
                                    normalize=(kind == "keyword_coverage"), reward=bf.reward)
         c.cdsl_select(bf.verify["scores"], bf.reward, alpha, bf.beam)
         # commit writes the next heads into separate buffers, then they swap
-        em, nb, nlp = c.cdsl_commit(st.prefix, bf.lookaheads, bf.beam, bf.verify["n_accept"],
-                                    bf.verify["row_topk_ids"], bf.verify["row_topk_lp"], k, d,
-                                    bf.next_beams, bf.next_head_lp)
+        if soft:
+            em = c.cdsl_commit_soft(st.prefix, bf.lookaheads, bf.beam, bf.verify["n_accept"],
+                                    bf.verify["row_topk_ids"], bf.verify["row_topk_lp"], bf.verify["res_ids"],
+                                    bf.verify["res_lp"], k, d, bf.next_beams, bf.next_head_lp)
+        else:
+            em, _, _ = c.cdsl_commit(st.prefix, bf.lookaheads, bf.beam, bf.verify["n_accept"],
+                                     bf.verify["row_topk_ids"], bf.verify["row_topk_lp"], k, d,
+                                     bf.next_beams, bf.next_head_lp)
         mark()
         for b in range(B):
             st.emitted[b].extend(em[b])

@@ -84,10 +84,22 @@ def _first_diff(a, b):
     return -1
 
 
+def soft_margins(dtype):
+    """(acceptance, residual) margins below which either soft decision is
+    correct, from the log-prob tolerance e: the bound min(1, p/q) moves by up
+    to e^(2e) - 1 ~ 2e; a cumulative boundary of the residual by up to
+    sum |dp| + sum |dq| ~ 2e in probability, i.e. 2e / Z in the units of v."""
+    e = lp_tol(dtype)
+    return 2.0 * e, 2.0 * e
+
+
 def compare_step(rep: Report, wl, k, d, o_step, g_heads, g_head_lp, g_look, g_ver, g_reward, g_beam, g_emit,
-                 tol) -> bool:
+                 tol, g_v=None) -> bool:
     """Compare one prompt's step; returns False when a legal near-tie
-    divergence ends the trajectory comparison (raises on a real mismatch)."""
+    divergence ends the trajectory comparison (raises on a real mismatch).
+    With soft rejection (o_step.soft set), the acceptance counts, the draft
+    log-probs and the residual draw are compared too; g_v is the prompt's
+    v [k, d]."""
     # a1 beam heads: ordered top-k of s_t
     oh = o_step.heads
     u = _first_diff(g_heads, oh)
@@ -112,7 +124,18 @@ def compare_step(rep: Report, wl, k, d, o_step, g_heads, g_head_lp, g_look, g_ve
     rep.max_lp_err = max(rep.max_lp_err, lp_err)
     ok = ve.margin > TOK_MARGIN
     assert np.array_equal(g_ver["target_argmax"][ok], ve.y[ok])
-    if np.all(ok) or np.array_equal(g_ver["target_argmax"], ve.y):
+    so = o_step.soft
+    if so is not None:
+        am, rm = soft_margins(wl.dtype)
+        assert np.max(np.abs(g_ver["draft_lp"] - o_step.roll.lq)) <= tol
+        for i in range(k):
+            gn, on = int(g_ver["n_accept"][i]), int(so.n[i])
+            if gn != on:
+                j = min(gn, on)
+                assert so.accept_margin[i, j] <= am, (i, gn, on, so.accept_margin[i])
+                rep.stopped = f"soft acceptance near tie (beam {i}, j {j}, margin {so.accept_margin[i, j]:.1e})"
+                return False
+    elif np.all(ok) or np.array_equal(g_ver["target_argmax"], ve.y):
         assert np.array_equal(g_ver["n_accept"], ve.n)
     elif not np.array_equal(g_ver["n_accept"], ve.n):
         rep.stopped = "target argmax near tie"
@@ -134,13 +157,28 @@ def compare_step(rep: Report, wl, k, d, o_step, g_heads, g_head_lp, g_look, g_ve
         return False
     # a8 commit
     assert list(g_emit) == list(o_step.emitted)
+    if so is not None and so.lead is not None:
+        i, n = int(g_beam), int(so.n[int(g_beam)])
+        g_res = int(g_ver["res_ids"][i, n])
+        assert abs(float(g_ver["res_lp"][i, n]) - so.lead_lp) <= tol or g_res != so.lead
+        if g_res != so.lead:
+            # a different draw must still sit at v in the oracle's residual
+            # distribution, within the residual margin
+            lo, hi, Z = oracle.residual_interval(o_step.ver.logits[i, n], o_step.roll.logits[i, n], g_res)
+            vv = float(g_v[i, n])
+            win = rm / Z
+            assert hi > lo and lo - win <= vv <= hi + win, (g_res, so.lead, lo, hi, vv, Z)
+            assert so.lead_margin <= win, (g_res, so.lead, so.lead_margin, Z)
+            rep.stopped = f"residual draw near a boundary (margin {so.lead_margin:.1e})"
+            return False
     rep.checks += 1
     return True
 
 
-def run_and_compare(s: Setup, B: int, steps: int, check_prompts, k=None, d=None, alpha=None):
+def run_and_compare(s: Setup, B: int, steps: int, check_prompts, k=None, d=None, alpha=None, soft=False):
     """Run ``steps`` GPU steps on a batch of B prompts and compare the listed
-    prompts step by step with independent oracle runs."""
+    prompts step by step with independent oracle runs.  soft: speculative
+    sampling's rejection with seeded uniforms of the workload."""
     import torch
     wl = s.wl
     k = k or wl.k
@@ -158,17 +196,24 @@ def run_and_compare(s: Setup, B: int, steps: int, check_prompts, k=None, d=None,
     for t in range(steps):
         heads = st.beams.cpu().numpy().copy()
         head_lp = st.head_lp.cpu().numpy().copy()
-        bf = eng.step(st, keywords=kw_t, reward_w=rw_t, alpha=alpha, k=k, d=d)
+        u = v = None
+        if soft:
+            u = ci.uniforms(wl.seed, 0, t, B, k, d)
+            v = ci.uniforms(wl.seed, 1, t, B, k, d)
+        bf = eng.step(st, keywords=kw_t, reward_w=rw_t, alpha=alpha, k=k, d=d,
+                      u=torch.from_numpy(u).cuda() if soft else None, v=torch.from_numpy(v).cuda() if soft else None)
         look = bf.lookaheads.cpu().numpy()
         ver = {kk: (v.cpu().numpy() if v is not None else None) for kk, v in bf.verify.items()}
         rew = bf.reward.cpu().numpy()
         beam = bf.beam.cpu().numpy()
         for b in list(live):
             o = oracle.step(s.odraft, s.otarget, ost[b], k, d, alpha, wl.reward,
-                            kws=s.kws[b] if s.kws is not None else None, w=s.rw)
-            gv = {kk: (v[b] if v is not None else None) for kk, v in ver.items()}
+                            kws=s.kws[b] if s.kws is not None else None, w=s.rw,
+                            rejection="soft" if soft else "hard",
+                            u=u[b] if soft else None, v=v[b] if soft else None)
+            gv = {kk: (x[b] if x is not None else None) for kk, x in ver.items()}
             cont = compare_step(reps[b], wl, k, d, o, heads[b], head_lp[b], look[b], gv, rew[b], beam[b],
-                                eng._last_emitted[b], tol)
+                                eng._last_emitted[b], tol, g_v=v[b] if soft else None)
             if cont:
                 reps[b].steps_compared += 1
                 ost[b] = o.state
