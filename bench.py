@@ -277,9 +277,10 @@ METHOD_A_T, METHOD_R_T, METHOD_B = 0.3, 0.3, 1
 def measure_methods(eng, wl, prompts, k, d, steps):
     """Wall-clock of the paper's decoding methods on the same models and
     prompts, with the concept-coverage reward (4 seeded concepts per prompt):
-    the CDSL step (the timed path above, here with that reward), one
-    iteration of the full controller (Alg. 1), and one token of CDLH-appx.
-    (draft lookaheads) and of CDLH (target lookaheads).  Each method starts
+    the CDSL step (the timed path above, here with that reward), the same
+    step with speculative sampling's soft rejection, one iteration of the
+    full controller (Alg. 1), and one token of CDLH-appx. (draft lookaheads)
+    and of CDLH (target lookaheads).  Each method starts
     from a fresh prefill, runs one untimed iteration, then `steps` timed
     ones.  Tokens per iteration depend on how often the target accepts the
     draft's tokens, which for independent random models is rarely."""
@@ -289,8 +290,19 @@ def measure_methods(eng, wl, prompts, k, d, steps):
     B = prompts.shape[0]
     kws = torch.from_numpy(ci.keywords(wl.seed, B, 4, wl.target.vocab)).cuda()
     p = torch.from_numpy(prompts).cuda()
+    # seeded uniforms of speculative sampling, resident before timing
+    U = [(torch.from_numpy(ci.uniforms(wl.seed, 0, t, B, k, d)).cuda(),
+          torch.from_numpy(ci.uniforms(wl.seed, 1, t, B, k, d)).cuda()) for t in range(steps + 1)]
+    it = [0]
+
+    def soft_step(st):
+        u, v = U[it[0] % len(U)]
+        it[0] += 1
+        return eng.step(st, keywords=kws, k=k, d=d, alpha=math.inf, reward="keyword_coverage", u=u, v=v)
+
     runs = {
         "cdsl_step": lambda st: eng.step(st, keywords=kws, k=k, d=d, alpha=math.inf, reward="keyword_coverage"),
+        "cdsl_step_soft": soft_step,
         "alg1": lambda st: eng.controller_step(st, kws, METHOD_A_T, METHOD_R_T, METHOD_B, k=k, d=d, normalize=True),
         "cdlh_appx": lambda st: eng.head_step(st, kws, 0, k=k, d=d, normalize=True),
         "cdlh": lambda st: eng.head_step(st, kws, 1, k=k, d=d, normalize=True),
