@@ -53,6 +53,23 @@ int cdsl_op_logit_rows(const float* logits, int32_t M, int32_t V,
                        int32_t* amax, int32_t* topk_ids, float* topk_lp,
                        void* stream);
 
+/* The LM head with its row statistics fused into the GEMM epilogue: the
+ * same outputs as cdsl_op_logit_rows on logits = A[M,K] * B[V,K]^T
+ * (cdsl_op_gemm's operands and dtypes; argmax and top-k ids identical, the
+ * log-probs equal up to the summation order of the logsumexp), without the
+ * logits ever reaching memory.  Each column tile of the GEMM reduces its
+ * rows to (max, sum of exp, argmax, its kk best, the gathered value); one
+ * workgroup per row folds the tiles.  amax may be NULL.  The workspace must
+ * hold cdsl_op_lm_head_rows_workspace(M, V, K, dtype, kk) bytes (0 means
+ * the shape is not covered).  Errors: EINVAL. */
+size_t cdsl_op_lm_head_rows_workspace(int32_t M, int32_t V, int32_t K,
+                                      int32_t dtype, int32_t kk);
+int cdsl_op_lm_head_rows(const float* A, const void* B, int32_t M, int32_t V,
+                         int32_t K, int32_t dtype, const int32_t* gather,
+                         int32_t kk, float* lp, int32_t* amax,
+                         int32_t* topk_ids, float* topk_lp, void* workspace,
+                         size_t workspace_bytes, void* stream);
+
 /* Speculative sampling rows (Sec. 3.2.2) over target_logits[M, V] (p) and
  * draft_logits[M, V] (q), fp32, rows ordered (row group g, position j) with
  * M = G * d; the row's draft token is x = lookaheads[g, j + 1] (an int32

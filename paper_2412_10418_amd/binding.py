@@ -22,6 +22,7 @@ ERR_NAMES = {0: "OK", -1: "EINVAL", -2: "ERANGE", -3: "ENOMEM", -4: "EDEVICE", -
 EXPORTS = [
     "cdsl_init", "cdsl_prefill", "cdsl_rollout", "cdsl_rollout_with", "cdsl_rollout_keep", "cdsl_verify",
     "cdsl_verify_kk", "cdsl_verify_soft", "cdsl_commit_soft", "cdsl_op_soft_rows",
+    "cdsl_op_lm_head_rows_workspace", "cdsl_op_lm_head_rows",
     "cdsl_reward_keywords",
     "cdsl_reward_keywords_upto", "cdsl_reward_linear", "cdsl_select", "cdsl_select_first", "cdsl_controller_states",
     "cdsl_commit", "cdsl_commit_kk",
@@ -85,6 +86,8 @@ def lib():
         "cdsl_verify_soft": ([vp, vp, vp, i32, i32] + [vp] * 14, i32),
         "cdsl_commit_soft": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, vp, vp, vp, vp], i32),
         "cdsl_op_soft_rows": ([vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp], i32),
+        "cdsl_op_lm_head_rows_workspace": ([i32, i32, i32, i32, i32], C.c_size_t),
+        "cdsl_op_lm_head_rows": ([vp, vp, i32, i32, i32, i32, vp, i32, vp, vp, vp, vp, vp, C.c_size_t, vp], i32),
         "cdsl_reward_keywords_upto": ([vp, vp, vp, i32, i32, vp, vp, i32, i32, vp], i32),
         "cdsl_commit_heads": ([vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp], i32),
         "cdsl_verify_kk": ([vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp], i32),
@@ -171,6 +174,28 @@ def cdsl_op_logit_rows(logits: torch.Tensor, gather: Optional[torch.Tensor], kk:
     rc = lib().cdsl_op_logit_rows(_ptr(logits, torch.float32, "logits"), M, V,
                                   _ptr(gather, torch.int32, "gather"), kk, lp.data_ptr(),
                                   amax.data_ptr(), tk.data_ptr(), tl.data_ptr(), _stream())
+    _check(rc)
+    return lp, amax, tk[:, :kk], tl[:, :kk]
+
+
+def cdsl_op_lm_head_rows(A: torch.Tensor, B: torch.Tensor, gather: Optional[torch.Tensor], kk: int):
+    """The LM head with the fused row epilogue; returns (lp, amax, topk_ids,
+    topk_lp) as cdsl_op_logit_rows does for the logits A @ B.T."""
+    M, K = A.shape
+    V = B.shape[0]
+    dt = CDSL_BF16 if B.dtype == torch.bfloat16 else CDSL_F32
+    dev = A.device
+    need = lib().cdsl_op_lm_head_rows_workspace(M, V, K, dt, kk)
+    if need == 0:
+        raise ValueError("shape not covered by the fused LM-head epilogue")
+    ws = torch.zeros(need, dtype=torch.uint8, device=dev)
+    lp = torch.zeros(M, dtype=torch.float32, device=dev)
+    amax = torch.zeros(M, dtype=torch.int32, device=dev)
+    tk = torch.zeros((M, max(kk, 1)), dtype=torch.int32, device=dev)
+    tl = torch.zeros((M, max(kk, 1)), dtype=torch.float32, device=dev)
+    rc = lib().cdsl_op_lm_head_rows(_ptr(A, torch.float32, "A"), _ptr(B, B.dtype, "B"), M, V, K, dt,
+                                    _ptr(gather, torch.int32, "gather"), kk, lp.data_ptr(), amax.data_ptr(),
+                                    tk.data_ptr(), tl.data_ptr(), ws.data_ptr(), need, _stream())
     _check(rc)
     return lp, amax, tk[:, :kk], tl[:, :kk]
 

@@ -55,6 +55,48 @@ __host__ __device__ inline int pass_batch(const PassDesc& p, int bi) {
   return p.prompt_ids ? p.prompt_ids[bi] : bi;
 }
 
+// Index of row m of a pass into a [B][kp][stride] token array:
+// (b * kp + i) * stride + off + j.  Disabled: index = m.
+struct RowMap {
+  int enabled;
+  PassDesc p;
+  int stride, off;
+};
+
+__host__ __device__ inline long long rowmap_index(const RowMap& r, int m) {
+  if (!r.enabled) return m;
+  const int j = m % r.p.R;
+  const int t = m / r.p.R;
+  const int i = t % r.p.kp;
+  const int bi = t / r.p.kp;
+  const int b = r.p.prompt_ids ? r.p.prompt_ids[bi] : bi;
+  return (long long)(b * r.p.kp + i) * r.stride + r.off + j;
+}
+
+// Per-row statistics of a logit matrix, kept per column tile so that the
+// logits themselves never reach memory (the LM-head GEMM writes these in
+// its epilogue; a merge kernel folds the tiles).  For row m and tile t:
+//   mx[m * tiles + t]   largest value of the tile's columns
+//   se[m * tiles + t]   sum of exp(v - mx) over them
+//   am[m * tiles + t]   lowest column holding mx
+//   tv/tc[(m * tiles + t) * kk + u]  the tile's kk best (value descending,
+//                        column ascending), kk <= 16; unused slots -inf
+//   zx[m]               the value at column gather_tok[rowmap(gather_map, m)]
+//                        (written by the tile that holds it; gather_tok null:
+//                        no gather)
+struct RowStats {
+  float* mx;
+  float* se;
+  int* am;
+  float* tv;
+  int* tc;
+  int kk;
+  int tiles;
+  float* zx;
+  const int* gather_tok;
+  RowMap gather_map;
+};
+
 // KV pool of one model: per layer, per block, per KV head:
 //   K: [16 tokens][hd]            (key-major, hd contiguous)
 //   V: [hd][16 tokens]            (transposed: token contiguous)

@@ -7,7 +7,7 @@
 
 namespace cdsl {
 
-enum GemmEpilogue { kEpiStore = 0, kEpiResidual = 1, kEpiSwiGLU = 2 };
+enum GemmEpilogue { kEpiStore = 0, kEpiResidual = 1, kEpiSwiGLU = 2, kEpiRowStats = 3 };
 
 // The activation operand: bf16 hi / lo planes [M, K] (bf16-weight models) or
 // one fp32 matrix [M, K] (fp32-weight models).
@@ -33,10 +33,15 @@ struct GemmOut {
 //   kEpiSwiGLU:   (bf16 only) W packs, per group of 32 rows, 16 gate rows
 //                 then the 16 matching up rows; the output (ldc = N/2)
 //                 receives silu(gate) * up as hi / lo planes.
+//   kEpiRowStats: no C; the product's row statistics per column tile go to
+//                 *rs (RowStats in common.h), whose tiles field the launch
+//                 sets.  The K dimension is never split for it.
 size_t gemm_workspace_bytes(int M, int N, int K, int dtype);
 int gemm_check(int M, int N, int K, int dtype);
 // 0: dense bf16 kernel, 1: skinny bf16 kernel, 2: fp32 kernel
 int gemm_kind(int M, int N, int K, int dtype);
+// Column tiles of a kEpiRowStats launch of this shape (0: not supported).
+int gemm_rowstats_tiles(int M, int N, int K, int dtype);
 // Called between the main kernel and the split-K reduce, when there is one
 // (lets the caller time the two kernels separately).
 struct GemmHook {
@@ -50,7 +55,7 @@ struct GemmHook {
 // kEpiSwiGLU is never deferred.
 hipError_t gemm_launch(const GemmOperand& A, const void* B, const GemmOut& out, int M, int N, int K, int dtype,
                        int epi, void* ws, size_t ws_bytes, hipStream_t st, bool prefill = false,
-                       GemmHook* hook = nullptr, int* deferred = nullptr);
+                       GemmHook* hook = nullptr, int* deferred = nullptr, RowStats* rs = nullptr);
 hipError_t swiglu_f32_launch(const float* gu, float* act, int M, int F, hipStream_t st);
 hipError_t split_planes_launch(const float* x, bf16* hi, bf16* lo, long long n, hipStream_t st);
 

@@ -50,6 +50,7 @@ struct GemmArgs {
   int ksplit, kchunk;
   float* partial;   // split planes [ksplit][M][N]
   int tiles_m, tiles_n;
+  RowStats rs;      // kEpiRowStats: per-tile row statistics instead of C
 };
 
 __device__ __forceinline__ float silu(float x) { return x / (1.f + __expf(-x)); }
@@ -77,6 +78,92 @@ __device__ __forceinline__ void epi_swiglu(const GemmArgs& a, int row, int col_g
 __device__ __forceinline__ void part_store(const GemmArgs& a, int row, int col, float v) {
   if (row >= a.M || col >= a.N) return;
   a.partial[((long long)blockIdx.z * a.M + row) * a.N + col] = v;
+}
+
+// kEpiRowStats: statistics of the rows of an fp32 tile [BM][BN] held in LDS
+// (rows m0 + r, columns n0 + c; rows >= M and columns >= N left out), one
+// wave per row at a time, each lane owning columns lane + 64 q.  t is the
+// column tile's index in the RowStats layout.
+template <int NT, int BM, int BN>
+__device__ void tile_row_stats(const float* tile, int m0, int n0, int M, int N, int t, const RowStats& s) {
+  static_assert(BN % 64 == 0, "whole waves of columns");
+  constexpr int NW = NT / 64, Q = BN / 64;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  for (int r = w; r < BM; r += NW) {
+    const int m = m0 + r;
+    if (m >= M) break;
+    float v[Q];
+    bool ok[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      ok[q] = n0 + q * 64 + lane < N;
+      v[q] = ok[q] ? tile[r * BN + q * 64 + lane] : -INFINITY;
+    }
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+      if (ok[q] && vi_better(v[q], n0 + q * 64 + lane, bv, bi)) {
+        bv = v[q];
+        bi = n0 + q * 64 + lane;
+      }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, 64);
+      const int oi = __shfl_xor(bi, o, 64);
+      if (vi_better(ov, oi, bv, bi)) {
+        bv = ov;
+        bi = oi;
+      }
+    }
+    float se = 0.f;
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+      if (ok[q]) se += __expf(v[q] - bv);
+    se = wave_sum(se);
+    const long long o = (long long)m * s.tiles + t;
+    if (lane == 0) {
+      s.mx[o] = bv;
+      s.se[o] = se;
+      s.am[o] = bi;
+    }
+    if (s.gather_tok) {
+      const int x = min(max(s.gather_tok[rowmap_index(s.gather_map, m)], 0), N - 1);
+      const int c = x - n0;
+      if (c >= 0 && c < BN && (c & 63) == lane) {
+        float zv = v[0];
+#pragma unroll
+        for (int q = 1; q < Q; ++q)
+          if ((c >> 6) == q) zv = v[q];
+        s.zx[m] = zv;
+      }
+    }
+    unsigned taken = 0;   // bit q: v[q] already listed
+    for (int u = 0; u < s.kk; ++u) {
+      float cv = -INFINITY;
+      int ci = 0x7fffffff;
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+        if (ok[q] && !((taken >> q) & 1u) && vi_better(v[q], n0 + q * 64 + lane, cv, ci)) {
+          cv = v[q];
+          ci = n0 + q * 64 + lane;
+        }
+#pragma unroll
+      for (int sh = 32; sh > 0; sh >>= 1) {
+        const float ov = __shfl_xor(cv, sh, 64);
+        const int oi = __shfl_xor(ci, sh, 64);
+        if (vi_better(ov, oi, cv, ci)) {
+          cv = ov;
+          ci = oi;
+        }
+      }
+      if (ci != 0x7fffffff && ((ci - n0) & 63) == lane) taken |= 1u << ((ci - n0) >> 6);
+      if (lane == 0) {
+        s.tv[o * s.kk + u] = cv;
+        s.tc[o * s.kk + u] = ci;
+      }
+    }
+  }
 }
 
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
@@ -280,6 +367,23 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dense(GemmArgs a) {
   if (kt < nk) mma(0);   // odd number of stages: the last one is in buffer 0
 
   const int rbase = m0 + wm * TM * 16 + lg * 4, cbase = n0 + wn * TN * 16 + lr;
+  if constexpr ((size_t)BM * BN * sizeof(float) <= sizeof(lds)) {
+    if (a.epi == kEpiRowStats) {
+      // the stages are consumed: the tile goes through LDS for the row pass
+      float* tile = reinterpret_cast<float*>(&lds[0][0]);
+      __syncthreads();
+#pragma unroll
+      for (int t = 0; t < TM; ++t)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            tile[(wm * TM * 16 + t * 16 + lg * 4 + e) * BN + wn * TN * 16 + j * 16 + lr] = acc[t * TN + j][e];
+      __syncthreads();
+      tile_row_stats<C::NT, BM, BN>(tile, m0, n0, a.M, a.N, tn_blk, a.rs);
+      return;
+    }
+  }
   if (a.ksplit > 1) {
 #pragma unroll
     for (int t = 0; t < TM; ++t)
@@ -454,6 +558,20 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_skinny(GemmArgs a) {
         for (int e = 0; e < 4; ++e) part_store(a, i * 16 + lg * 4 + e, n0 + j * 16 + lr, acc[i][j][e]);
     return;
   }
+  if (a.epi == kEpiRowStats) {
+    static_assert((size_t)BM * BN * sizeof(float) <= sizeof(As), "the tile fits the activation buffers");
+    float* tile = reinterpret_cast<float*>(&As[0][0][0]);
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < CT; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) tile[(i * 16 + lg * 4 + e) * BN + wave * CT * 16 + j * 16 + lr] = acc[i][j][e];
+    __syncthreads();
+    tile_row_stats<NT, BM, BN>(tile, 0, blockIdx.x * BN, a.M, a.N, blockIdx.x, a.rs);
+    return;
+  }
   if (a.epi == kEpiSwiGLU) {
     if constexpr (CT % 2 == 0) {
       // column tiles 2t (gate) and 2t + 1 (up) of the packed weight are in
@@ -501,7 +619,7 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_skinny(GemmArgs a) {
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void gemm_f32_tiled(const float* __restrict__ A, const float* __restrict__ B,
                                                        float* __restrict__ C, int M, int N, int K, int ldc,
-                                                       int epi) {
+                                                       int epi, RowStats rs) {
   __shared__ float As[16][64 + 4];
   __shared__ float Bs[16][64 + 4];
   const int tid = threadIdx.x;
@@ -531,6 +649,16 @@ __global__ __launch_bounds__(256) void gemm_f32_tiled(const float* __restrict__ 
         for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
     }
     __syncthreads();
+  }
+  if (epi == kEpiRowStats) {
+    __shared__ float tile[64 * 64];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) tile[(ty * 4 + i) * 64 + tx * 4 + j] = acc[i][j];
+    __syncthreads();
+    tile_row_stats<256, 64, 64>(tile, m0, n0, M, N, blockIdx.x, rs);
+    return;
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -598,7 +726,7 @@ struct Plan {
 
 constexpr int skinny_ring(int ct) { return ct == 1 ? 8 : 4; }
 
-Plan make_plan(int M, int N, int K, int dtype) {
+Plan make_plan(int M, int N, int K, int dtype, bool no_split = false) {
   Plan p{};
   if (dtype == 0) {
     p.kind = 2;
@@ -662,8 +790,22 @@ Plan make_plan(int M, int N, int K, int dtype) {
     p.ksplit = s;
     p.kchunk = per * kc;
   }
+  if (no_split) {
+    p.ksplit = 1;
+    p.kchunk = K;
+  }
   if (p.ksplit > 1) p.ws_bytes = (size_t)p.ksplit * M * N * sizeof(float);
   return p;
+}
+
+// Column tiles of a row-statistics launch (0: the shape's kernel cannot
+// stage its output tile through LDS).
+int rowstats_tiles(const Plan& p, int N) {
+  if (p.kind == 2) return (N + 63) / 64;
+  if (p.kind == 1) return p.tiles_n;
+  const DenseShape& d = kDense[p.cfg];
+  const size_t lds = 2 * 2 * ((size_t)(2 * d.bm + d.bn) * d.kc + 64 * d.wm * d.wn * 8);
+  return (size_t)d.bm * d.bn * sizeof(float) <= lds ? p.tiles_n : 0;
 }
 
 }  // namespace
@@ -676,6 +818,11 @@ size_t gemm_workspace_bytes(int M, int N, int K, int dtype) {
 
 int gemm_kind(int M, int N, int K, int dtype) { return make_plan(M, N, K, dtype).kind; }
 
+int gemm_rowstats_tiles(int M, int N, int K, int dtype) {
+  if (M <= 0) return 0;
+  return rowstats_tiles(make_plan(M, N, K, dtype, true), N);
+}
+
 int gemm_check(int M, int N, int K, int dtype) {
   if (M < 0 || N <= 0 || K <= 0) return -1;
   if (dtype == 1 && K % DBK != 0) return -1;
@@ -685,14 +832,21 @@ int gemm_check(int M, int N, int K, int dtype) {
 
 hipError_t gemm_launch(const GemmOperand& A, const void* B, const GemmOut& out, int M, int N, int K, int dtype,
                        int epi, void* ws, size_t ws_bytes, hipStream_t st, bool prefill, GemmHook* hook,
-                       int* deferred) {
+                       int* deferred, RowStats* rs) {
   if (deferred) *deferred = 1;
   if (M == 0) return hipSuccess;
-  Plan p = make_plan(M, N, K, dtype);
+  const bool stats = epi == kEpiRowStats;
+  if (stats != (rs != nullptr)) return hipErrorInvalidValue;
+  Plan p = make_plan(M, N, K, dtype, stats);
+  if (stats) {
+    rs->tiles = rowstats_tiles(p, N);
+    if (rs->tiles == 0 || rs->kk < 0 || rs->kk > 16) return hipErrorInvalidValue;
+  }
   if (p.kind == 2) {
     if (epi == kEpiSwiGLU) return hipErrorInvalidValue;  // fp32 path: store + swiglu_f32
     dim3 grid((N + 63) / 64, (M + 63) / 64);
-    gemm_f32_tiled<<<grid, 256, 0, st>>>(A.f32, (const float*)B, out.f32, M, N, K, out.ldc, epi);
+    gemm_f32_tiled<<<grid, 256, 0, st>>>(A.f32, (const float*)B, out.f32, M, N, K, out.ldc, epi,
+                                         stats ? *rs : RowStats{});
     return hipGetLastError();
   }
   if (p.ws_bytes > ws_bytes) return hipErrorInvalidValue;
@@ -713,6 +867,7 @@ hipError_t gemm_launch(const GemmOperand& A, const void* B, const GemmOut& out, 
   a.tiles_m = p.tiles_m;
   a.tiles_n = p.tiles_n;
   a.partial = (float*)ws;
+  a.rs = stats ? *rs : RowStats{};
   if (p.kind == 0) {
     dim3 grid(p.tiles_m * p.tiles_n, 1, p.ksplit);
     const DenseShape& d = kDense[p.cfg];

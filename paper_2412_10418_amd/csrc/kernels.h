@@ -4,14 +4,6 @@
 
 namespace cdsl {
 
-// Index of row m of a pass into a [B][kp][stride] token array:
-// (b * kp + i) * stride + off + j.  Disabled: index = m.
-struct RowMap {
-  int enabled;
-  PassDesc p;
-  int stride, off;
-};
-
 struct LogitArgs {
   const float* logits;     // [M][ld] (ld = V when 0)
   int V;
@@ -28,16 +20,6 @@ struct LogitArgs {
   const int* topk_rows;    // destination row of row m (null: m)
 };
 
-__host__ __device__ inline long long rowmap_index(const RowMap& r, int m) {
-  if (!r.enabled) return m;
-  const int j = m % r.p.R;
-  const int t = m / r.p.R;
-  const int i = t % r.p.kp;
-  const int bi = t / r.p.kp;
-  const int b = r.p.prompt_ids ? r.p.prompt_ids[bi] : bi;
-  return (long long)(b * r.p.kp + i) * r.stride + r.off + j;
-}
-
 hipError_t embed_launch(const PassDesc& p, const void* emb, float* h, int D, int V, int dtype, hipStream_t st);
 // S > 0: fold S split planes part[S][rows][D] into x first (written back);
 // g == null then only folds.
@@ -49,6 +31,9 @@ hipError_t rope_kv_launch(const PassDesc& p, const float* qkv, void* qout, const
                           const float* cos_t, const float* sin_t, int H, int Hkv, int hd, int dtype, hipStream_t st,
                           int S = 0);
 hipError_t logit_rows_launch(const LogitArgs& a, int M, hipStream_t st);
+// logit_rows_launch's outputs (a.logits unused) from the per-tile row
+// statistics of the LM-head GEMM (kEpiRowStats); s.kk must equal a.kk.
+hipError_t rowstats_merge_launch(const RowStats& s, const LogitArgs& a, int M, hipStream_t st);
 // lq, u non-null: soft rejection (speculative sampling) instead of the argmax match
 hipError_t beam_scores_launch(int BK, int d, const int* look, const int* y, const float* lp, const float* head_lp,
                               const float* lq, const float* u, int* n_accept, float* scores, hipStream_t st);

@@ -1027,6 +1027,101 @@ hipError_t rope_kv_launch(const PassDesc& p, const float* qkv, void* qout, const
   return hipGetLastError();
 }
 
+// The outputs of logit_rows_kernel from the per-tile row statistics the
+// LM-head GEMM wrote (RowStats) instead of from the logits: argmax, the
+// log-prob of the gathered token, and the top-kk as log-probs.  One
+// workgroup per row.  The top-kk come in kk rounds over the tiles' lists,
+// each taking the best candidate ordered after the previous pick (value
+// descending, id ascending; ids are unique).
+__global__ __launch_bounds__(256) void rowstats_merge_kernel(RowStats s, LogitArgs a) {
+  __shared__ float shv[4];
+  __shared__ int shi[4];
+  __shared__ float shs[4];
+  const int m = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const long long base = (long long)m * s.tiles;
+  auto block_best = [&](float v, int id, float& fv, int& fi) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(v, o, 64);
+      const int oi = __shfl_xor(id, o, 64);
+      if (vi_better(ov, oi, v, id)) {
+        v = ov;
+        id = oi;
+      }
+    }
+    if (lane == 0) {
+      shv[w] = v;
+      shi[w] = id;
+    }
+    __syncthreads();
+    fv = shv[0];
+    fi = shi[0];
+    for (int u = 1; u < 4; ++u)
+      if (vi_better(shv[u], shi[u], fv, fi)) {
+        fv = shv[u];
+        fi = shi[u];
+      }
+    __syncthreads();
+  };
+  float bv = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int t = tid; t < s.tiles; t += 256)
+    if (vi_better(s.mx[base + t], s.am[base + t], bv, bi)) {
+      bv = s.mx[base + t];
+      bi = s.am[base + t];
+    }
+  float G;
+  int amax;
+  block_best(bv, bi, G, amax);
+  if (tid == 0 && a.amax) a.amax[rowmap_index(a.amax_map, m)] = amax;
+  if (!a.want_lse) return;
+  float sv = 0.f;
+  for (int t = tid; t < s.tiles; t += 256) {
+    const float mx = s.mx[base + t];
+    if (mx != -INFINITY) sv += s.se[base + t] * __expf(mx - G);
+  }
+  sv = wave_sum(sv);
+  if (lane == 0) shs[w] = sv;
+  __syncthreads();
+  const float lse = G + __logf(shs[0] + shs[1] + shs[2] + shs[3]);
+  if (a.lp && tid == 0) a.lp[m] = s.zx[m] - lse;
+  if (a.kk == 0) return;
+  const int dst = a.topk_rows ? a.topk_rows[m] : m;
+  const int nc = s.tiles * s.kk;
+  const long long cb = base * s.kk;
+  float pv = INFINITY;
+  int pi = -1;
+  for (int r = 0; r < a.kk; ++r) {
+    float cv = -INFINITY;
+    int ci = 0x7fffffff;
+    for (int q = tid; q < nc; q += 256) {
+      const float v = s.tv[cb + q];
+      const int id = s.tc[cb + q];
+      if ((v < pv || (v == pv && id > pi)) && vi_better(v, id, cv, ci)) {
+        cv = v;
+        ci = id;
+      }
+    }
+    float fv;
+    int fi;
+    block_best(cv, ci, fv, fi);
+    if (tid == 0) {
+      a.topk_ids[(long long)dst * a.kk + r] = fi;
+      a.topk_lp[(long long)dst * a.kk + r] = fv - lse;
+    }
+    pv = fv;
+    pi = fi;
+  }
+}
+
+hipError_t rowstats_merge_launch(const RowStats& s, const LogitArgs& a, int M, hipStream_t st) {
+  if (M == 0) return hipSuccess;
+  if (a.kk != s.kk || a.kk < 0 || a.kk > 16 || s.tiles <= 0) return hipErrorInvalidValue;
+  rowstats_merge_kernel<<<M, 256, 0, st>>>(s, a);
+  return hipGetLastError();
+}
+
 hipError_t logit_rows_launch(const LogitArgs& a, int M, hipStream_t st) {
   if (M == 0) return hipSuccess;
   if (a.kk > 16 || a.kk < 0) return hipErrorInvalidValue;

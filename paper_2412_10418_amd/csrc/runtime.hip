@@ -51,6 +51,11 @@ struct Workspace {
   float *u32 = nullptr, *o32 = nullptr, *act32 = nullptr;
   float* gu32 = nullptr;
   float* logits = nullptr;
+  // LM-head row statistics per column tile (the fused epilogue); rs_cap rows
+  // x tiles, times the top-k width for the candidate lists
+  float *rs_mx = nullptr, *rs_se = nullptr, *rs_tv = nullptr, *rs_zx = nullptr;
+  int *rs_am = nullptr, *rs_tc = nullptr;
+  size_t rs_cap = 0;
   float* part_o = nullptr;
   float* part_ml = nullptr;
   size_t part_rows = 0;     // capacity in (row, head) units for one split
@@ -369,6 +374,15 @@ void alloc_workspace(cdsl_ctx* c) {
     w.gu32 = dev_alloc<float>(c, M * 2 * Fm);
   }
   w.logits = dev_alloc<float>(c, (size_t)w.Mlog * Vm);
+  for (auto& md : c->m)
+    for (int mm = 1; mm <= w.Mlog; ++mm)
+      w.rs_cap = std::max(w.rs_cap, (size_t)mm * gemm_rowstats_tiles(mm, md.c.vocab, md.c.d_model, c->dtype));
+  w.rs_mx = dev_alloc<float>(c, w.rs_cap);
+  w.rs_se = dev_alloc<float>(c, w.rs_cap);
+  w.rs_am = dev_alloc<int>(c, w.rs_cap);
+  w.rs_tv = dev_alloc<float>(c, w.rs_cap * l.max_k);
+  w.rs_tc = dev_alloc<int>(c, w.rs_cap * l.max_k);
+  w.rs_zx = dev_alloc<float>(c, w.Mlog);
   // attention split partials sized for the verification / rollout passes
   w.part_rows = (size_t)std::max(verify_rows, roll_rows) * Hm;
   if (c->dtype == CDSL_BF16) {
@@ -396,12 +410,14 @@ void alloc_workspace(cdsl_ctx* c) {
 // Returns the number of split planes left in the GEMM workspace for the
 // caller to fold (1: none) when defer is set.
 int gemm(cdsl_ctx* c, const GemmOperand& A, const void* W, const GemmOut& out, int M, int N, int K, int epi,
-         bool prefill, bool defer = false) {
+         bool prefill, bool defer = false, RowStats* rs = nullptr) {
   const double wes = c->dtype == CDSL_BF16 ? 2.0 : 4.0;   // weight element size
-  // output bytes: fp32 store, fp32 read-modify-write, or the two bf16 planes
-  // of the half-width SwiGLU output
-  const double outb = epi == kEpiSwiGLU ? (double)M * (N / 2) * 4.0
-                                        : (double)M * N * 4.0 * (epi == kEpiResidual ? 2.0 : 1.0);
+  // output bytes: fp32 store, fp32 read-modify-write, the two bf16 planes
+  // of the half-width SwiGLU output, or the per-tile row statistics
+  const double outb =
+      epi == kEpiSwiGLU     ? (double)M * (N / 2) * 4.0
+      : epi == kEpiRowStats ? (double)M * gemm_rowstats_tiles(M, N, K, c->dtype) * (3.0 + 2.0 * rs->kk) * 4.0
+                            : (double)M * N * 4.0 * (epi == kEpiResidual ? 2.0 : 1.0);
   const int kind = gemm_kind(M, N, K, c->dtype);
   const int cls = kind == 0 ? CDSL_K_GEMM_DENSE : kind == 1 ? CDSL_K_GEMM_SKINNY : CDSL_K_GEMM_F32;
   // with split-K, the main kernel writes fp32 partial planes and the reduce
@@ -428,17 +444,23 @@ int gemm(cdsl_ctx* c, const GemmOperand& A, const void* W, const GemmOut& out, i
   hk.plane = (double)M * N * 4.0;
   int planes = 1;
   CK(gemm_launch(A, W, out, M, N, K, c->dtype, epi, c->ws.gemm_ws, c->ws.gemm_ws_bytes, c->st, prefill,
-                 c->prof ? &hk : nullptr, defer ? &planes : nullptr));
+                 c->prof ? &hk : nullptr, defer ? &planes : nullptr, rs));
   return planes;
 }
 
+void logit_rows(cdsl_ctx* c, const LogitArgs& la, int M);
+
 // Forward pass of one model over the rows of p.  With want_logits, the
 // final-normed rows (all, or the last row of each beam with last_only) go
-// through the LM head into ws.logits; hid receives fp32 final-normed rows of
-// every beam's last row when non-null.
+// through the LM head into ws.logits (or logits_out at row stride
+// logits_ld); hid receives fp32 final-normed rows of every beam's last row
+// when non-null.  With fuse, the LM head instead leaves per-tile row
+// statistics and a merge kernel writes fuse's outputs (argmax, gathered
+// log-prob, top-k), so no logits reach memory; shapes the fused epilogue
+// does not cover take the logits and logit_rows.
 void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, long long sum_prefix_len,
               bool want_logits, bool last_only, float* hid, bool prefill = false, float* logits_out = nullptr,
-              int logits_ld = 0) {
+              int logits_ld = 0, const LogitArgs* fuse = nullptr) {
   Workspace& w = c->ws;
   const auto& k = md.c;
   const int M = p.M();
@@ -543,8 +565,34 @@ void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, lon
     Span sp(c, CDSL_K_ROWWISE, 0.0, (double)rows * D * (4.0 + es));
     CK(rmsnorm_launch(w.h, md.gf, w.u32, w.uh, w.ul, rows, D, k.rms_eps, last_only ? 1 : 0, p.R, hid, c->st));
   }
+  if (fuse) {
+    const int tiles = gemm_rowstats_tiles(rows, k.vocab, D, c->dtype);
+    if (tiles > 0 && (size_t)rows * tiles <= w.rs_cap && fuse->kk <= c->lim.max_k) {
+      RowStats rs{};
+      rs.mx = w.rs_mx;
+      rs.se = w.rs_se;
+      rs.am = w.rs_am;
+      rs.tv = w.rs_tv;
+      rs.tc = w.rs_tc;
+      rs.kk = fuse->kk;
+      rs.zx = w.rs_zx;
+      rs.gather_tok = fuse->lp ? fuse->gather_tok : nullptr;
+      rs.gather_map = fuse->gather_map;
+      gemm(c, Au, md.lm, GemmOut{nullptr, nullptr, nullptr, k.vocab}, rows, k.vocab, D, kEpiRowStats, prefill, false,
+           &rs);
+      Span sp(c, CDSL_K_LOGIT_ROWS, 0.0, (double)rows * rs.tiles * (3.0 + 2.0 * rs.kk) * 4.0);
+      CK(rowstats_merge_launch(rs, *fuse, rows, c->st));
+      return;
+    }
+  }
   gemm(c, Au, md.lm, GemmOut{logits_out ? logits_out : w.logits, nullptr, nullptr, logits_ld ? logits_ld : k.vocab},
        rows, k.vocab, D, kEpiStore, prefill);
+  if (fuse) {
+    LogitArgs la = *fuse;
+    la.logits = w.logits;
+    la.ld = 0;
+    logit_rows(c, la, rows);
+  }
 }
 
 void logit_rows(cdsl_ctx* c, const LogitArgs& la, int M) {
@@ -744,17 +792,15 @@ int cdsl_prefill(cdsl_ctx* c, const int32_t* tokens, int32_t B, int32_t L, int32
       p.tok = tokens;
       p.tok_stride = L;
       p.tok_off = 0;
-      run_pass(c, c->m[0], p, 0, 0, false, false, nullptr, true);
-      run_pass(c, c->m[1], p, 0, 0, true, true, nullptr, true);
       LogitArgs la{};
-      la.logits = c->ws.logits;
       la.V = c->m[1].c.vocab;
       la.want_lse = 1;
       la.kk = k;
       la.topk_ids = beams;
       la.topk_lp = head_lp;
       la.topk_rows = c->iota + b0;
-      logit_rows(c, la, nb);
+      run_pass(c, c->m[0], p, 0, 0, false, false, nullptr, true);
+      run_pass(c, c->m[1], p, 0, 0, true, true, nullptr, true, nullptr, 0, &la);
     }
     CK(add_launch(B, nullptr, px->Lp, L, c->st));
     for (int b = 0; b < B; ++b) px->len[b] = L;
@@ -804,11 +850,8 @@ int rollout_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, 
       p.tok_stride = d + 1;
       p.tok_off = j0;
       float* dst = keep ? keep + (long long)j0 * V : nullptr;
-      run_pass(c, c->m[roller], p, Lmax, sum_len(px), true, false, nullptr, false, dst, keep ? d * V : 0);
       LogitArgs la{};
-      la.logits = dst ? dst : c->ws.logits;
       la.V = V;
-      la.ld = keep ? (long long)d * V : 0;
       la.want_lse = 0;
       la.kk = 0;
       la.amax = lookaheads;
@@ -816,7 +859,15 @@ int rollout_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, 
       la.amax_map.p = p;
       la.amax_map.stride = d + 1;
       la.amax_map.off = j0 + 1;
-      logit_rows(c, la, p.M());
+      if (keep) {
+        // the kept logits are an output: write them, then take the argmax
+        run_pass(c, c->m[roller], p, Lmax, sum_len(px), true, false, nullptr, false, dst, d * V);
+        la.logits = dst;
+        la.ld = (long long)d * V;
+        logit_rows(c, la, p.M());
+      } else {
+        run_pass(c, c->m[roller], p, Lmax, sum_len(px), true, false, nullptr, false, nullptr, 0, &la);
+      }
     }
     px->rolled_k = k;
     px->rolled_d = d;
@@ -886,9 +937,7 @@ int verify_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, in
     p.tok = look;
     p.tok_stride = d + 1;
     p.tok_off = 0;
-    run_pass(c, c->m[1], p, max_len(px), sum_len(px), true, false, hidden);
     LogitArgs la{};
-    la.logits = c->ws.logits;
     la.V = c->m[1].c.vocab;
     la.want_lse = 1;
     la.kk = kk;
@@ -901,7 +950,14 @@ int verify_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, in
     la.gather_map.off = 1;
     la.topk_ids = row_topk_ids;
     la.topk_lp = row_topk_lp;
-    logit_rows(c, la, p.M());
+    if (soft) {
+      // speculative sampling reads the target's logit rows: keep them
+      run_pass(c, c->m[1], p, max_len(px), sum_len(px), true, false, hidden);
+      la.logits = c->ws.logits;
+      logit_rows(c, la, p.M());
+    } else {
+      run_pass(c, c->m[1], p, max_len(px), sum_len(px), true, false, hidden, false, nullptr, 0, &la);
+    }
     if (soft) {
       Span sp(c, CDSL_K_LOGIT_ROWS, 0.0, (double)p.M() * la.V * 4.0 * 2.0);
       CK(soft_rows_launch(c->ws.logits, soft->draft_logits, p.M(), la.V, d, look, soft->v, soft->draft_lp,
@@ -1105,17 +1161,15 @@ int commit_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t
       const int Lmax = max_len(px);
       long long sl = 0;
       for (int u = 0; u < ncatch; ++u) sl += px->len[c->ids_host[u]];
-      run_pass(c, c->m[0], p, Lmax, sl, false, false, nullptr);
-      run_pass(c, c->m[1], p, Lmax, sl, true, false, nullptr);
       LogitArgs la{};
-      la.logits = c->ws.logits;
       la.V = c->m[1].c.vocab;
       la.want_lse = 1;
       la.kk = kk;
       la.topk_ids = next_beams;
       la.topk_lp = next_head_lp;
       la.topk_rows = c->ids_dev;
-      logit_rows(c, la, ncatch);
+      run_pass(c, c->m[0], p, Lmax, sl, false, false, nullptr);
+      run_pass(c, c->m[1], p, Lmax, sl, true, false, nullptr, false, nullptr, 0, &la);
       CK(add_launch(ncatch, c->ids_dev, px->Lp, 1, c->st));
       for (int u = 0; u < ncatch; ++u) px->len[c->ids_host[u]] += 1;
     }
@@ -1188,17 +1242,15 @@ int cdsl_commit_heads(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const i
       const int Lmax = max_len(px);
       long long sl = 0;
       for (int u = 0; u < n; ++u) sl += px->len[c->ids_host[u]];
-      run_pass(c, c->m[0], p, Lmax, sl, false, false, nullptr);
-      run_pass(c, c->m[1], p, Lmax, sl, true, false, nullptr);
       LogitArgs la{};
-      la.logits = c->ws.logits;
       la.V = c->m[1].c.vocab;
       la.want_lse = 1;
       la.kk = kk;
       la.topk_ids = next_beams;
       la.topk_lp = next_head_lp;
       la.topk_rows = c->ids_dev;
-      logit_rows(c, la, n);
+      run_pass(c, c->m[0], p, Lmax, sl, false, false, nullptr);
+      run_pass(c, c->m[1], p, Lmax, sl, true, false, nullptr, false, nullptr, 0, &la);
       CK(add_launch(n, c->ids_dev, px->Lp, 1, c->st));
       for (int u = 0; u < n; ++u) px->len[c->ids_host[u]] += 1;
     }
@@ -1332,3 +1384,80 @@ int cdsl_op_soft_rows(const float* target_logits, const float* draft_logits, int
   if (e != hipSuccess) return fail(nullptr, CDSL_EDEVICE, hipGetErrorString(e));
   return CDSL_OK;
 }
+
+namespace {
+struct LmHeadWs {
+  size_t planes, mx, se, am, tv, tc, zx, total;
+};
+LmHeadWs lm_head_ws(int M, int V, int K, int dtype, int kk, int tiles) {
+  auto al = [](size_t b) { return (b + 255) & ~(size_t)255; };
+  LmHeadWs w{};
+  const size_t mt = (size_t)M * tiles;
+  w.planes = 0;
+  w.mx = al(op_planes_bytes(M, K, dtype));
+  w.se = w.mx + al(mt * 4);
+  w.am = w.se + al(mt * 4);
+  w.tv = w.am + al(mt * 4);
+  w.tc = w.tv + al(mt * kk * 4);
+  w.zx = w.tc + al(mt * kk * 4);
+  w.total = w.zx + al((size_t)M * 4);
+  (void)V;
+  return w;
+}
+}  // namespace
+
+size_t cdsl_op_lm_head_rows_workspace(int32_t M, int32_t V, int32_t K, int32_t dtype, int32_t kk) {
+  if (M <= 0 || V <= 0 || K <= 0 || kk < 0 || kk > 16) return 0;
+  const int tiles = gemm_rowstats_tiles(M, V, K, dtype);
+  return tiles > 0 ? lm_head_ws(M, V, K, dtype, kk, tiles).total : 0;
+}
+
+int cdsl_op_lm_head_rows(const float* A, const void* B, int32_t M, int32_t V, int32_t K, int32_t dtype,
+                         const int32_t* gather, int32_t kk, float* lp, int32_t* amax, int32_t* topk_ids,
+                         float* topk_lp, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!A || !B || !workspace || M < 0 || V <= 0 || kk < 0 || kk > 16 || kk > V)
+    return fail(nullptr, CDSL_EINVAL, "bad argument");
+  if ((gather && !lp) || (kk > 0 && (!topk_ids || !topk_lp))) return fail(nullptr, CDSL_EINVAL, "missing output");
+  if (dtype != CDSL_F32 && dtype != CDSL_BF16) return fail(nullptr, CDSL_EINVAL, "bad dtype");
+  if (gemm_check(M, V, K, dtype) != 0) return fail(nullptr, CDSL_EINVAL, "unsupported shape");
+  if (M == 0) return CDSL_OK;
+  const int tiles = gemm_rowstats_tiles(M, V, K, dtype);
+  if (tiles <= 0) return fail(nullptr, CDSL_EINVAL, "shape not covered by the fused epilogue");
+  const LmHeadWs w = lm_head_ws(M, V, K, dtype, kk, tiles);
+  if (workspace_bytes < w.total) return fail(nullptr, CDSL_EINVAL, "workspace too small");
+  hipStream_t st = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  GemmOperand op{nullptr, nullptr, A};
+  if (dtype == CDSL_BF16) {
+    bf16* hi = (bf16*)ws;
+    bf16* lo = hi + (size_t)M * K;
+    hipError_t e = split_planes_launch(A, hi, lo, (long long)M * K, st);
+    if (e != hipSuccess) return fail(nullptr, CDSL_EDEVICE, hipGetErrorString(e));
+    op = GemmOperand{hi, lo, nullptr};
+  }
+  RowStats rs{};
+  rs.mx = (float*)(ws + w.mx);
+  rs.se = (float*)(ws + w.se);
+  rs.am = (int*)(ws + w.am);
+  rs.tv = (float*)(ws + w.tv);
+  rs.tc = (int*)(ws + w.tc);
+  rs.kk = kk;
+  rs.zx = (float*)(ws + w.zx);
+  rs.gather_tok = gather;
+  hipError_t e = gemm_launch(op, B, GemmOut{nullptr, nullptr, nullptr, V}, M, V, K, dtype, kEpiRowStats, nullptr, 0,
+                             st, false, nullptr, nullptr, &rs);
+  if (e != hipSuccess) return fail(nullptr, CDSL_EDEVICE, hipGetErrorString(e));
+  LogitArgs la{};
+  la.V = V;
+  la.want_lse = (gather || kk > 0) ? 1 : 0;
+  la.kk = kk;
+  la.amax = amax;
+  la.lp = gather ? lp : nullptr;
+  la.gather_tok = gather;
+  la.topk_ids = topk_ids;
+  la.topk_lp = topk_lp;
+  e = rowstats_merge_launch(rs, la, M, st);
+  if (e != hipSuccess) return fail(nullptr, CDSL_EDEVICE, hipGetErrorString(e));
+  return CDSL_OK;
+}
+

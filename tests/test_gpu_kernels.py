@@ -91,3 +91,56 @@ def test_logit_rows_match_oracle(M, V, kk):
         ids = oracle.topk_ids(z[m], kk)
         assert list(tk[m]) == list(ids)
         assert np.max(np.abs(tl[m] - ls[ids])) < 2e-5
+
+
+@pytest.mark.parametrize("M,V,K,dt,kk", [
+    (80, 32000, 2048, "bf16", 0),      # rollout: draft LM head, argmax only (skinny, 128-column tiles)
+    (80, 32000, 2048, "bf16", 5),
+    (800, 32000, 4096, "bf16", 5),     # verification block (dense, 256-column tiles)
+    (333, 1300, 576, "bf16", 8),       # dense, ragged rows and last tile
+    (7, 1000, 256, "bf16", 16),        # skinny, 64-column tiles, ragged last tile
+    (5, 128256, 256, "bf16", 8),       # large vocabulary
+    (37, 997, 64, "f32", 4),           # fp32 kernel, 64-column tiles
+])
+def test_fused_lm_head_rows_match_reference(M, V, K, dt, kk):
+    """The LM head with its row statistics fused into the GEMM epilogue,
+    against float64 logits: argmax and top-k ids exact wherever the
+    reference's deciding gap exceeds 1e-3 (the fp32 product is accurate to
+    ~1e-5 here), log-probs within 1e-4.  Planted exact ties (identical weight
+    rows) must resolve to the lowest id."""
+    from paper_2412_10418_amd.binding import cdsl_op_lm_head_rows
+    rng = np.random.default_rng([M, V, K, kk])
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    if dt == "bf16":
+        Bd, Bt = _bf16_mat(rng, (V, K), scale=0.05)
+    else:
+        Bd = (rng.uniform(-1, 1, (V, K)) * 0.05).astype(np.float32)
+        Bt = torch.from_numpy(Bd).cuda()
+        Bd = Bd.astype(np.float64)
+    # identical weight rows give identical logits in every row: exact ties
+    for a, b in ((3, 700 % V), (V - 2, V - 1)):
+        Bd[b] = Bd[a]
+    Bt[[700 % V, V - 1]] = Bt[[3, V - 2]]
+    g = rng.integers(0, V, M).astype(np.int32)
+    lp, amax, tk, tl = cdsl_op_lm_head_rows(torch.from_numpy(A).cuda(), Bt, torch.from_numpy(g).cuda(), kk)
+    lp, amax, tk, tl = (t.cpu().numpy() for t in (lp, amax, tk, tl))
+    z = A.astype(np.float64) @ Bd.T
+    checked = 0
+    for m in range(M):
+        ls = oracle.log_softmax(z[m])
+        assert abs(lp[m] - ls[g[m]]) < 1e-4
+        srt = np.sort(z[m])[::-1]
+        if srt[0] - srt[1] > 1e-3 or oracle.argmax_lowest(z[m]) in (3, V - 2):
+            assert amax[m] == oracle.argmax_lowest(z[m])
+            checked += 1
+        if kk:
+            ids = oracle.topk_ids(z[m], kk + 1)
+            for u in range(kk):
+                # the order is fixed up to the first place whose gap to the
+                # next value is within the error (exact ties order by id)
+                gap = z[m][ids[u]] - z[m][ids[u + 1]]
+                if 0.0 < gap <= 1e-3:
+                    break
+                assert tk[m, u] == ids[u], (m, u, list(tk[m]), list(ids))
+                assert abs(tl[m, u] - ls[ids[u]]) < 1e-4
+    assert checked >= M // 2

@@ -74,6 +74,10 @@ def test_error_paths_without_device(lib):
     assert L.cdsl_commit_soft(None, None, None, None, None, None, None, None, None, 1, 1, None, None, None,
                               None) == binding.CDSL_EINVAL
     assert L.cdsl_op_soft_rows(None, None, 1, 1, 1, None, None, None, None, None, None) == binding.CDSL_EINVAL
+    assert L.cdsl_op_lm_head_rows(None, None, 1, 1, 1, 1, None, 0, None, None, None, None, None, 0,
+                                  None) == binding.CDSL_EINVAL
+    assert L.cdsl_op_lm_head_rows_workspace(80, 32000, 2048, binding.CDSL_BF16, 5) > 0
+    assert L.cdsl_op_lm_head_rows_workspace(0, 32000, 2048, binding.CDSL_BF16, 5) == 0
     assert L.cdsl_controller_states(None, None, None, 1, 1, 0.5, 0.5, 1, None, None) == binding.CDSL_EINVAL
     assert L.cdsl_op_logit_rows(None, 1, 1, None, 0, None, None, None, None, None) == binding.CDSL_EINVAL
     assert L.cdsl_op_gemm_workspace(80, 3072, 2048, binding.CDSL_BF16) > 0
