@@ -81,87 +81,93 @@ __device__ __forceinline__ void part_store(const GemmArgs& a, int row, int col, 
 }
 
 // kEpiRowStats: statistics of the rows of an fp32 tile [BM][BN] held in LDS
-// (rows m0 + r, columns n0 + c; rows >= M and columns >= N left out), one
-// wave per row at a time, each lane owning columns lane + 64 q.  t is the
-// column tile's index in the RowStats layout.
+// (rows m0 + r, columns n0 + c; rows >= M and columns >= N left out).  P
+// adjacent lanes share a row, each owning CW columns, and every row is
+// handled at once: branch-free passes over the lane's columns (maximum and
+// argmax, then the sum of exp, then one pass per top-k place picking the
+// best entry ordered after the row's previous pick), each followed by a
+// merge over the P lanes with shuffles.  Each lane starts its passes at a
+// row-dependent column so that lanes of different rows hit different LDS
+// banks.  t is the column tile's index in the RowStats layout.
 template <int NT, int BM, int BN>
 __device__ void tile_row_stats(const float* tile, int m0, int n0, int M, int N, int t, const RowStats& s) {
-  static_assert(BN % 64 == 0, "whole waves of columns");
-  constexpr int NW = NT / 64, Q = BN / 64;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  for (int r = w; r < BM; r += NW) {
+  constexpr int P = NT / BM >= 4 ? 4 : (NT / BM >= 2 ? 2 : 1);   // lanes per row, divides 64
+  constexpr int RPP = NT / P;                                     // rows per pass
+  constexpr int CW = BN / P;                                      // columns per lane
+  static_assert(BN % P == 0 && (CW & (CW - 1)) == 0, "power-of-two column runs");
+  const int part = threadIdx.x % P;
+  const int c0 = part * CW;
+  auto row_best = [&](float& v, int& id) {
+#pragma unroll
+    for (int o = 1; o < P; o <<= 1) {
+      const float ov = __shfl_xor(v, o, 64);
+      const int oi = __shfl_xor(id, o, 64);
+      if (vi_better(ov, oi, v, id)) {
+        v = ov;
+        id = oi;
+      }
+    }
+  };
+  for (int r0 = 0; r0 < BM; r0 += RPP) {
+    const int r = min(r0 + (int)threadIdx.x / P, BM - 1);
     const int m = m0 + r;
-    if (m >= M) break;
-    float v[Q];
-    bool ok[Q];
-#pragma unroll
-    for (int q = 0; q < Q; ++q) {
-      ok[q] = n0 + q * 64 + lane < N;
-      v[q] = ok[q] ? tile[r * BN + q * 64 + lane] : -INFINITY;
+    const bool live = r0 + (int)threadIdx.x / P < BM && m < M;
+    const float* row = tile + r * BN + c0;
+    const int rot = (r * 5 + part * 16) & (CW - 1);
+    float av = -INFINITY;
+    int ai = 0x7fffffff;
+#pragma unroll 8
+    for (int i = 0; i < CW; ++i) {
+      const int c = (rot + i) & (CW - 1);
+      const int col = n0 + c0 + c;
+      const float v = col < N ? row[c] : -INFINITY;
+      const bool b = vi_better(v, col, av, ai);
+      av = b ? v : av;
+      ai = b ? col : ai;
     }
-    float bv = -INFINITY;
-    int bi = 0x7fffffff;
-#pragma unroll
-    for (int q = 0; q < Q; ++q)
-      if (ok[q] && vi_better(v[q], n0 + q * 64 + lane, bv, bi)) {
-        bv = v[q];
-        bi = n0 + q * 64 + lane;
-      }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, 64);
-      const int oi = __shfl_xor(bi, o, 64);
-      if (vi_better(ov, oi, bv, bi)) {
-        bv = ov;
-        bi = oi;
-      }
-    }
+    row_best(av, ai);
     float se = 0.f;
+#pragma unroll 8
+    for (int i = 0; i < CW; ++i) {
+      const int c = (rot + i) & (CW - 1);
+      se += n0 + c0 + c < N ? __expf(row[c] - av) : 0.f;
+    }
 #pragma unroll
-    for (int q = 0; q < Q; ++q)
-      if (ok[q]) se += __expf(v[q] - bv);
-    se = wave_sum(se);
+    for (int o = 1; o < P; o <<= 1) se += __shfl_xor(se, o, 64);
     const long long o = (long long)m * s.tiles + t;
-    if (lane == 0) {
-      s.mx[o] = bv;
+    if (live && part == 0) {
+      s.mx[o] = av;
       s.se[o] = se;
-      s.am[o] = bi;
+      s.am[o] = ai;
     }
-    if (s.gather_tok) {
-      const int x = min(max(s.gather_tok[rowmap_index(s.gather_map, m)], 0), N - 1);
-      const int c = x - n0;
-      if (c >= 0 && c < BN && (c & 63) == lane) {
-        float zv = v[0];
-#pragma unroll
-        for (int q = 1; q < Q; ++q)
-          if ((c >> 6) == q) zv = v[q];
-        s.zx[m] = zv;
-      }
-    }
-    unsigned taken = 0;   // bit q: v[q] already listed
+    // top-kk: the u-th pick is the best entry ordered after pick u - 1
+    float pv = INFINITY;
+    int pc = -1;
     for (int u = 0; u < s.kk; ++u) {
       float cv = -INFINITY;
       int ci = 0x7fffffff;
-#pragma unroll
-      for (int q = 0; q < Q; ++q)
-        if (ok[q] && !((taken >> q) & 1u) && vi_better(v[q], n0 + q * 64 + lane, cv, ci)) {
-          cv = v[q];
-          ci = n0 + q * 64 + lane;
-        }
-#pragma unroll
-      for (int sh = 32; sh > 0; sh >>= 1) {
-        const float ov = __shfl_xor(cv, sh, 64);
-        const int oi = __shfl_xor(ci, sh, 64);
-        if (vi_better(ov, oi, cv, ci)) {
-          cv = ov;
-          ci = oi;
-        }
+#pragma unroll 8
+      for (int i = 0; i < CW; ++i) {
+        const int c = (rot + i) & (CW - 1);
+        const int col = n0 + c0 + c;
+        const float v = col < N ? row[c] : -INFINITY;
+        const bool after = v < pv || (v == pv && col > pc);
+        const bool b = after && col < N && vi_better(v, col, cv, ci);
+        cv = b ? v : cv;
+        ci = b ? col : ci;
       }
-      if (ci != 0x7fffffff && ((ci - n0) & 63) == lane) taken |= 1u << ((ci - n0) >> 6);
-      if (lane == 0) {
+      row_best(cv, ci);
+      if (live && part == 0) {
         s.tv[o * s.kk + u] = cv;
         s.tc[o * s.kk + u] = ci;
       }
+      pv = cv;
+      pc = ci;
+    }
+    if (live && s.gather_tok) {
+      const int x = min(max(s.gather_tok[rowmap_index(s.gather_map, m)], 0), N - 1);
+      const int c = x - n0 - c0;
+      if (c >= 0 && c < CW) s.zx[m] = row[c];
     }
   }
 }

@@ -454,10 +454,11 @@ void logit_rows(cdsl_ctx* c, const LogitArgs& la, int M);
 // final-normed rows (all, or the last row of each beam with last_only) go
 // through the LM head into ws.logits (or logits_out at row stride
 // logits_ld); hid receives fp32 final-normed rows of every beam's last row
-// when non-null.  With fuse, the LM head instead leaves per-tile row
-// statistics and a merge kernel writes fuse's outputs (argmax, gathered
-// log-prob, top-k), so no logits reach memory; shapes the fused epilogue
-// does not cover take the logits and logit_rows.
+// when non-null.  fuse names the row outputs wanted from the logits
+// (argmax, gathered log-prob, top-k).  For argmax-only heads and heads of
+// few rows the LM head leaves per-tile row statistics and a merge kernel
+// writes those outputs, so no logits reach memory; other heads write the
+// logits and logit_rows reduces them.
 void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, long long sum_prefix_len,
               bool want_logits, bool last_only, float* hid, bool prefill = false, float* logits_out = nullptr,
               int logits_ld = 0, const LogitArgs* fuse = nullptr) {
@@ -565,7 +566,11 @@ void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, lon
     Span sp(c, CDSL_K_ROWWISE, 0.0, (double)rows * D * (4.0 + es));
     CK(rmsnorm_launch(w.h, md.gf, w.u32, w.uh, w.ul, rows, D, k.rms_eps, last_only ? 1 : 0, p.R, hid, c->st));
   }
-  if (fuse) {
+  // The fused epilogue pays where it only reduces (argmax, logsumexp) or
+  // the rows are few: its per-tile top-k selection costs more vector ALU
+  // time than writing and re-reading the logits once the rows are many
+  // (measured at 800 rows, k = 5: 750 vs 505 us for the 32000-token head).
+  if (fuse && (fuse->kk == 0 || rows <= 32)) {
     const int tiles = gemm_rowstats_tiles(rows, k.vocab, D, c->dtype);
     if (tiles > 0 && (size_t)rows * tiles <= w.rs_cap && fuse->kk <= c->lim.max_k) {
       RowStats rs{};
