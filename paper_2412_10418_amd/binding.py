@@ -267,6 +267,8 @@ class Context:
         self.handle = h
         self.draft_shape, self.target_shape = draft_shape, target_shape
         self.dtype = dtype
+        self.limits = {"max_batch": lim.max_batch, "max_ctx": lim.max_ctx, "max_k": lim.max_k,
+                       "max_d": lim.max_d, "max_prompt": lim.max_prompt, "max_prefixes": lim.max_prefixes}
         del dkeep, tkeep
 
     def close(self):

@@ -203,3 +203,59 @@ def test_small_bf16_verify_on_oracle_lookaheads(small):
     print("bf16 verify max |dlp|", err)
     assert err < 2e-2
     st.prefix.free()
+
+
+def test_largest_k_and_d_match_oracle():
+    """The largest beam count and lookahead depth the library takes (k = 16,
+    d = 32: two suffix blocks per beam, 512 verified rows per prompt, top-16
+    rows), hard and soft rejection, against the oracle."""
+    s = make_setup("tiny")
+    make_engine(s, B=2, max_steps=6, k=16, d=32)
+    try:
+        st, reps = run_and_compare(s, B=2, steps=2, check_prompts=[0, 1], k=16, d=32)
+        for b, r in reps.items():
+            print(f"hard, prompt {b}: {r.steps_compared} steps, max |dlp| {r.max_lp_err:.2e}, stop: {r.stopped or '-'}")
+            assert r.steps_compared >= 1
+        st.prefix.free()
+        st, reps = run_and_compare(s, B=2, steps=2, check_prompts=[0, 1], k=16, d=32, soft=True)
+        for b, r in reps.items():
+            print(f"soft, prompt {b}: {r.steps_compared} steps, stop: {r.stopped or '-'}")
+            assert r.steps_compared >= 1
+        st.prefix.free()
+    finally:
+        s.engine.close()
+
+
+def test_batch_and_context_limits(tiny):
+    """An empty batch, a batch or prompt beyond the limits, and a context
+    that runs out are reported as errors (nothing is launched for them),
+    and the prefix never grows past max_ctx."""
+    from paper_2412_10418_amd.binding import CDSLError, CDSL_ERANGE, CDSL_EINVAL
+    eng = tiny.engine
+    L = tiny.wl.prompt_len
+    with pytest.raises(CDSLError) as e:
+        eng.ctx.cdsl_prefill(torch.zeros((0, L), dtype=torch.int32, device="cuda"), tiny.wl.k)
+    assert e.value.code == CDSL_EINVAL
+    with pytest.raises(CDSLError) as e:
+        eng.ctx.cdsl_prefill(torch.zeros((7, L), dtype=torch.int32, device="cuda"), tiny.wl.k)
+    assert e.value.code == CDSL_ERANGE
+    with pytest.raises(CDSLError) as e:
+        eng.ctx.cdsl_prefill(torch.zeros((1, L + 1), dtype=torch.int32, device="cuda"), tiny.wl.k)
+    assert e.value.code == CDSL_ERANGE
+    # the tiny engine holds prompt + 8 steps of d + 1 tokens: keep stepping
+    # until the next lookahead would not fit
+    st = eng.start(torch.from_numpy(tiny.prompts(1)).cuda())
+    kw = torch.from_numpy(tiny.kws[:1]).cuda()
+    max_ctx = eng.ctx.limits["max_ctx"]
+    raised = False
+    for _ in range(200):
+        try:
+            eng.step(st, keywords=kw)
+        except CDSLError as err:
+            assert err.code == CDSL_ERANGE
+            raised = True
+            break
+        assert max(st.prefix.lengths()) <= max_ctx
+    assert raised
+    assert max(st.prefix.lengths()) + tiny.wl.d + 1 > max_ctx
+    st.prefix.free()
