@@ -96,7 +96,8 @@ def soft_margins(dtype):
 def compare_step(rep: Report, wl, k, d, o_step, g_heads, g_head_lp, g_look, g_ver, g_reward, g_beam, g_emit,
                  tol, g_v=None) -> bool:
     """Compare one prompt's step; returns False when a legal near-tie
-    divergence ends the trajectory comparison (raises on a real mismatch).
+    divergence ends the trajectory comparison (raises on a real mismatch),
+    "last" when the step matched but the trajectories part after it.
     With soft rejection (o_step.soft set), the acceptance counts, the draft
     log-probs and the residual draw are compared too; g_v is the prompt's
     v [k, d]."""
@@ -169,8 +170,10 @@ def compare_step(rep: Report, wl, k, d, o_step, g_heads, g_head_lp, g_look, g_ve
             win = rm / Z
             assert hi > lo and lo - win <= vv <= hi + win, (g_res, so.lead, lo, hi, vv, Z)
             assert so.lead_margin <= win, (g_res, so.lead, so.lead_margin, Z)
-            rep.stopped = f"residual draw near a boundary (margin {so.lead_margin:.1e})"
-            return False
+            # this step matched; the next one starts from another lead token
+            rep.stopped = f"after this step: residual draw near a boundary (margin {so.lead_margin:.1e})"
+            rep.checks += 1
+            return "last"
     rep.checks += 1
     return True
 
@@ -217,6 +220,6 @@ def run_and_compare(s: Setup, B: int, steps: int, check_prompts, k=None, d=None,
             if cont:
                 reps[b].steps_compared += 1
                 ost[b] = o.state
-            else:
+            if cont is not True:
                 live.discard(b)
     return st, reps

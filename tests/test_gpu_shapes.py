@@ -36,16 +36,29 @@ def test_gqa_bf16_steps_match_oracle(k, d, L):
         s.engine.close()
 
 
+@pytest.fixture(scope="module")
+def full7b():
+    s = make_setup("7b1b")
+    make_engine(s, B=16, max_steps=4)
+    yield s
+    s.engine.close()
+
+
 @pytest.mark.timeout(600)
-def test_7b1b_full_size_sampled_parity():
+def test_7b1b_full_size_sampled_parity(full7b):
     """The 7B / 1B pair at its full batch (16 prompts x 256 tokens, k=5,
     d=10) in the launch configuration the benchmark times; prompts 0 and 11
     of the batch are compared with the oracle for two steps."""
-    s = make_setup("7b1b")
-    make_engine(s, B=16, max_steps=3)
-    try:
-        st, reps = run_and_compare(s, B=16, steps=2, check_prompts=[0, 11])
-        _report(reps)
-        st.prefix.free()
-    finally:
-        s.engine.close()
+    st, reps = run_and_compare(full7b, B=16, steps=2, check_prompts=[0, 11])
+    _report(reps)
+    st.prefix.free()
+
+
+@pytest.mark.timeout(600)
+def test_7b1b_full_size_soft_rejection(full7b):
+    """The same configuration with speculative sampling's soft rejection
+    (kept draft logits of 16 x 5 x 10 rows over 32000 tokens, the residual
+    draw): prompts 0 and 11, two steps."""
+    st, reps = run_and_compare(full7b, B=16, steps=2, check_prompts=[0, 11], soft=True)
+    _report(reps)
+    st.prefix.free()
