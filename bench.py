@@ -45,9 +45,11 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (reference for HBM byte counters)")
-    ap.add_argument("--summarize-profile", nargs=4, metavar=("BENCH_JSON", "TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
+    ap.add_argument("--summarize-profile", nargs="+",
+                    metavar="BENCH_JSON TRACE_DIR FETCH_DIR WRITE_DIR [UTIL_DIR]",
                     help="write a markdown summary of rocprofv3 runs of this script (kernel trace, FETCH_SIZE and "
-                         "WRITE_SIZE passes with --calibrate-copy) and exit; no GPU needed")
+                         "WRITE_SIZE passes with --calibrate-copy, optionally a MfmaUtil/LdsUtil pass) and exit; "
+                         "no GPU needed")
     ap.add_argument("--summary-out", default=None)
     ap.add_argument("--commands", default=None, help="text file with the exact profiling commands (for the summary)")
     return ap.parse_args()
@@ -121,7 +123,10 @@ def summarize_profile(args):
     """Markdown summary of the three rocprofv3 runs of this script."""
     import csv
     import re
-    bench_json, trace_dir, fetch_dir, write_dir = args.summarize_profile
+    if len(args.summarize_profile) not in (4, 5):
+        raise SystemExit("--summarize-profile takes BENCH_JSON TRACE_DIR FETCH_DIR WRITE_DIR [UTIL_DIR]")
+    bench_json, trace_dir, fetch_dir, write_dir = args.summarize_profile[:4]
+    util_dir = args.summarize_profile[4] if len(args.summarize_profile) == 5 else None
     with open(bench_json) as fh:
         line = [ln for ln in fh.read().splitlines() if ln.startswith("{")][-1]
     b = json.loads(line)
@@ -192,6 +197,22 @@ def summarize_profile(args):
                      "bytes_per_launch": round(bpl), "rocprof_avg_us": round(avg_us, 2)})
     out += ["", "The bench times each class with HIP events around its launches on the library stream; "
             "its average per launch is expected to agree with the rocprofv3 average of the same kernel.", ""]
+    if util_dir:
+        util = counters(util_dir)
+        out += ["## Matrix-core and LDS utilisation (MfmaUtil / LdsUtil pass)", "",
+                "Per-dispatch averages of rocprofv3's derived metrics (percent of the active time of the CUs "
+                "that ran the kernel).", "",
+                "| class | kernel | dispatches | MfmaUtil % | LdsUtil % |", "|---|---|---:|---:|---:|"]
+        for cls, (pat, _files) in CLASS_KERNEL.items():
+            rx = re.compile(pat)
+            mv = [float(r["Counter_Value"]) for r in util
+                  if rx.search(r["Kernel_Name"]) and r["Counter_Name"] == "MfmaUtil"]
+            lv = [float(r["Counter_Value"]) for r in util
+                  if rx.search(r["Kernel_Name"]) and r["Counter_Name"] == "LdsUtil"]
+            if mv:
+                out.append(f"| {cls} | `{pat}` | {len(mv)} | {sum(mv) / len(mv):.1f} | "
+                           f"{sum(lv) / len(lv) if lv else float('nan'):.1f} |")
+        out.append("")
     out += [TRAFFIC_TAG + json.dumps(r) + " -->" for r in recs]
     text = "\n".join(out) + "\n"
     if args.summary_out:
