@@ -363,6 +363,11 @@ __global__ __launch_bounds__(NT) void rope_kv_write_split(PassDesc p, const floa
 // Logits row statistics, one workgroup per row, one read of the row:
 // online logsumexp, argmax, thread-local top-KK lists merged by KK rounds of
 // block argmax.  Ordering: value descending, then id ascending.
+// A token id that indexes the vocabulary even for a row without a finite
+// logit (all NaN), so that the next pass's embedding never reads out of
+// bounds; the NaN still reaches the scores and makes the selection fail.
+__device__ __forceinline__ int vocab_id(int id, int V) { return (id >= 0 && id < V) ? id : 0; }
+
 template <int KKMAX>
 __global__ __launch_bounds__(256) void logit_rows_kernel(LogitArgs a) {
   __shared__ float shv[4];
@@ -453,7 +458,7 @@ __global__ __launch_bounds__(256) void logit_rows_kernel(LogitArgs a) {
       shv[0] = fv;
     }
     __syncthreads();
-    if (tid == 0 && a.amax) a.amax[rowmap_index(a.amax_map, m)] = shi[0];
+    if (tid == 0 && a.amax) a.amax[rowmap_index(a.amax_map, m)] = vocab_id(shi[0], a.V);
     __syncthreads();
   }
   if (!a.want_lse) return;
@@ -502,7 +507,7 @@ __global__ __launch_bounds__(256) void logit_rows_kernel(LogitArgs a) {
         fi = shi[u];
       }
     if (tid == 0) {
-      a.topk_ids[(long long)dst * a.kk + r] = fi;
+      a.topk_ids[(long long)dst * a.kk + r] = vocab_id(fi, a.V);
       a.topk_lp[(long long)dst * a.kk + r] = fv - lse;
     }
     if (li[0] == fi) {   // ids are unique: exactly one thread pops
@@ -1074,7 +1079,7 @@ __global__ __launch_bounds__(256) void rowstats_merge_kernel(RowStats s, LogitAr
   float G;
   int amax;
   block_best(bv, bi, G, amax);
-  if (tid == 0 && a.amax) a.amax[rowmap_index(a.amax_map, m)] = amax;
+  if (tid == 0 && a.amax) a.amax[rowmap_index(a.amax_map, m)] = vocab_id(amax, a.V);
   if (!a.want_lse) return;
   float sv = 0.f;
   for (int t = tid; t < s.tiles; t += 256) {
@@ -1107,7 +1112,7 @@ __global__ __launch_bounds__(256) void rowstats_merge_kernel(RowStats s, LogitAr
     int fi;
     block_best(cv, ci, fv, fi);
     if (tid == 0) {
-      a.topk_ids[(long long)dst * a.kk + r] = fi;
+      a.topk_ids[(long long)dst * a.kk + r] = vocab_id(fi, a.V);
       a.topk_lp[(long long)dst * a.kk + r] = fv - lse;
     }
     pv = fv;
