@@ -442,9 +442,10 @@ class HeadStep:
 
 def lookahead_heads(roller: Decoder, roller_cache: KVCache, st: PromptState, k: int, d: int):
     """The k candidate tokens of the appendix algorithm -- the top-k of M_p
-    at the prefix end, value descending, lowest id first on ties -- each
+    at the prefix end, value descending, lowest id first on ties (after a
+    soft rejection, the resampled token first: ``beam_heads``) -- each
     followed by d greedy tokens of the roller on its own copy of the cache."""
-    heads = topk_ids(st.s_logits, k)
+    heads = beam_heads(st, k)[0]
     x = np.zeros((k, d), np.int64)
     mg = np.zeros((k, d))
     for i, c in enumerate(heads):
@@ -468,8 +469,9 @@ def cdlh_step(roller_is_target: bool, draft: Decoder, target: Decoder, st: Promp
     the step), and the best candidate is the one token emitted.
 
     prefer_first_at = r_t gives Step-1 of Alg. 1 with b = 1: the first
-    candidate -- M_p's own greedy token -- is taken when its lookahead
-    reaches the reward threshold, else Step-2 picks the best."""
+    candidate -- M_p's own greedy token, or the resampled token after a soft
+    rejection -- is taken when its lookahead reaches the reward threshold,
+    else Step-2 picks the best."""
     roller = target if roller_is_target else draft
     cache = st.target_cache if roller_is_target else st.draft_cache
     heads, x, mg = lookahead_heads(roller, cache, st, k, d)
@@ -480,8 +482,7 @@ def cdlh_step(roller_is_target: bool, draft: Decoder, target: Decoder, st: Promp
     else:
         pick = argmax_first(r)
     tok = int(heads[pick])
-    top = np.sort(st.s_logits)[::-1][:k + 1]
-    hm = float(np.min(-np.diff(top))) if len(top) > 1 else math.inf
+    hm = float(np.min(beam_heads(st, k)[2]))
     return HeadStep(heads, x, mg, r, pick, tok, commit(draft, target, st, [tok]), hm)
 
 
@@ -500,11 +501,17 @@ class ControllerStep:
     extra: Optional[HeadStep]  # the one-token action of S2/S3 and S4
     emitted: List[int]
     after: PromptState
+    soft: Optional[SoftResult] = None   # speculative sampling's test (k = 1)
+    roll: Optional[Rollout] = None
 
 
 def controller_step(draft: Decoder, target: Decoder, st: PromptState, k: int, d: int, a_t: float, r_t: float,
-                    b: int, reward_kind: str, kws: Sequence[int]) -> ControllerStep:
-    """One iteration of Alg. 1 (Sec. 3.2.1-3.2.3) with hard rejection.
+                    b: int, reward_kind: str, kws: Sequence[int], rejection: str = "hard",
+                    u: Optional[np.ndarray] = None, v: Optional[np.ndarray] = None) -> ControllerStep:
+    """One iteration of Alg. 1 (Sec. 3.2.1-3.2.3) with hard rejection, or
+    with speculative sampling's test plugged into the rejection loop
+    (rejection = "soft", uniforms u, v of shape [1, d]; the token drawn at
+    the rejected position then heads the next candidates, as in ``step``).
 
     Readings: the draft starts after M_p's greedy token c (the head of the
     k = 1 step) instead of straight from pfx; that token is emitted in every
@@ -525,16 +532,27 @@ def controller_step(draft: Decoder, target: Decoder, st: PromptState, k: int, d:
     c = int(heads[0])
     ro = rollout(draft, st, [c], d)
     ve = verify(target, st, [c], head_lp, ro.x)
-    n = int(ve.n[0])
+    soft, lead = None, None
+    if rejection == "soft":
+        n = soft_accept_count(ve.logprobs[0], ro.lq[0], u[0])
+        lead_lp, lm = None, math.inf
+        if n < d:
+            lead, lead_lp, lm = residual_sample(ve.logits[0, n], ro.logits[0, n], v[0, n])
+        soft = SoftResult(np.array([n]), soft_accept_margins(ve.logprobs[0], ro.lq[0], u[0])[None], lead, lead_lp,
+                          lm)
+    elif rejection == "hard":
+        n = int(ve.n[0])
+    else:
+        raise ValueError(rejection)
     a = n / d
     acc = [c] + [int(t) for t in ro.x[0, :n]]
     r = keyword_reward(reward_kind, list(st.generated) + acc, kws)
-    st1 = commit(draft, target, st, acc)
+    st1 = commit(draft, target, st, acc, lead)
     if a >= a_t and r >= r_t:
         return ControllerStep(c, float(head_lp[0]), float(hm[0]), ro.x[0], ro.margin[0], ve, n, a, r, "S1", None,
-                              acc, st1)
+                              acc, st1, soft, ro)
     state = "S2/S3" if a < a_t else "S4"
     pref = r_t if (state == "S2/S3" and b == 1) else None
     hs = cdlh_step(False, draft, target, st1, k, d, reward_kind, kws, prefer_first_at=pref)
     return ControllerStep(c, float(head_lp[0]), float(hm[0]), ro.x[0], ro.margin[0], ve, n, a, r, state, hs,
-                          acc + [hs.token], hs.state)
+                          acc + [hs.token], hs.state, soft, ro)

@@ -577,3 +577,38 @@ def test_soft_step_matches_full_recompute(models):
             assert list(nxt) == [r.soft.lead] + rest
         cur = r.state
     assert seen_lead >= 1
+
+
+def test_soft_controller_matches_full_recompute(models):
+    """Alg. 1 with speculative sampling's test in the rejection loop: n from
+    p and q recomputed by the library models; a rejected token is replaced by
+    the residual draw from those logits, which heads the next candidates, so
+    Step-1 (b = 1, r_t = -inf: always taken; a_t = 2 forces S2/S3) emits it
+    right after the accepted tokens."""
+    from hf_ref import hf_logits
+    draft, target, cur = _state(models, n=8)
+    hf_d, hf_t = models["gqa"][3], models["mha"][3]
+    k, d = 3, 3
+    rng = np.random.default_rng(21)
+    seen_lead = 0
+    for _ in range(4):
+        u = rng.random((1, d)).astype(np.float32)
+        v = rng.random((1, d)).astype(np.float32)
+        cs = oracle.controller_step(draft, target, cur, k, d, 2.0, -math.inf, 1, "keyword_count", [1, 2, 3],
+                                    rejection="soft", u=u, v=v)
+        assert cs.state == "S2/S3"
+        seq = list(cur.tokens) + [cs.head] + [int(t) for t in cs.x]
+        L = len(cur.tokens)
+        zt = hf_logits(hf_t, seq[:-1])[L:]
+        zd = hf_logits(hf_d, seq[:-1])[L:]
+        lt = [oracle.log_softmax(zt[j])[cs.x[j]] for j in range(d)]
+        ld = [oracle.log_softmax(zd[j])[cs.x[j]] for j in range(d)]
+        n = oracle.soft_accept_count(lt, ld, u[0])
+        assert n == cs.n
+        if n < d:
+            lead, _, _ = oracle.residual_sample(zt[n], zd[n], v[0, n])
+            assert cs.soft.lead == lead
+            assert cs.emitted == [cs.head] + [int(t) for t in cs.x[:n]] + [lead]
+            seen_lead += 1
+        cur = cs.after
+    assert seen_lead >= 1
