@@ -225,7 +225,9 @@ int cdsl_rollout_keep(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* beams,
                       int32_t k, int32_t d, int32_t* lookaheads,
                       float* draft_logits);
 
-/* cdsl_verify with speculative sampling's test: x_{i,j} is kept while
+/* cdsl_verify_kk with speculative sampling's test (kk: top-k width of the
+ * row_topk outputs and of the next heads; kk = k for the beam step, k = 1
+ * with kk = the beam count for the controller): x_{i,j} is kept while
  * u[b, i, j-1] <= min(1, p_j(x_{i,j}) / q_j(x_{i,j})), and n_accept counts
  * the kept tokens before the first rejection.  u and v are [B, k, d]
  * uniforms in [0, 1) supplied by the caller (the method's random numbers
@@ -239,26 +241,28 @@ int cdsl_rollout_keep(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* beams,
  * prefix with the same k and d (ESTATE otherwise).  Errors as cdsl_verify;
  * EINVAL if the two models' vocabularies differ. */
 int cdsl_verify_soft(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookaheads,
-                     int32_t k, int32_t d, const float* head_lp,
+                     int32_t k, int32_t d, int32_t kk, const float* head_lp,
                      const float* draft_logits, const float* u, const float* v,
                      float* logprobs, float* draft_lp, int32_t* target_argmax,
                      int32_t* n_accept, float* scores, int32_t* row_topk_ids,
                      float* row_topk_lp, int32_t* res_ids, float* res_lp,
                      float* hidden);
 
-/* cdsl_commit after cdsl_verify_soft.  Emits [c_i*, x_i*,1..n] as
- * cdsl_commit does (no bonus token).  When n < d, the next heads are the
- * residual draw res_ids[b, i*, n] (head_lp res_lp) followed by the k - 1
- * best tokens of that row's top-k without it; when n = d they are the
- * target's top-k after the catch-up, as in cdsl_commit.  Errors as
+/* cdsl_commit after cdsl_verify_soft (same k, d, kk).  Emits
+ * [c_i*, x_i*,1..n] as cdsl_commit does (no bonus token).  When n < d, the
+ * next heads ([B, kk]) are the residual draw res_ids[b, i*, n] (head_lp
+ * res_lp) followed by the kk - 1 best tokens of that row's top-kk without
+ * it; when n = d they are the target's top-kk after the catch-up, as in
+ * cdsl_commit.  Errors as
  * cdsl_commit; ESTATE if the last verification was not soft (and
  * cdsl_commit returns ESTATE after a soft one). */
 int cdsl_commit_soft(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookaheads,
                      const int32_t* beam, const int32_t* n_accept,
                      const int32_t* row_topk_ids, const float* row_topk_lp,
                      const int32_t* res_ids, const float* res_lp, int32_t k,
-                     int32_t d, int32_t* emitted_host, int32_t* n_emit_host,
-                     int32_t* next_beams, float* next_head_lp);
+                     int32_t d, int32_t kk, int32_t* emitted_host,
+                     int32_t* n_emit_host, int32_t* next_beams,
+                     float* next_head_lp);
 
 /* Reward-only selection with Step-1 of the controller (Sec. 3.2.3, S2/S3
  * with b = 1): beam[b] = 0 when reward[b, 0] >= first_at[b] (head 0 is the

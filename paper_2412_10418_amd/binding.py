@@ -83,8 +83,8 @@ def lib():
         "cdsl_rollout": ([vp, vp, vp, i32, i32, vp], i32),
         "cdsl_rollout_with": ([vp, vp, vp, i32, i32, i32, vp], i32),
         "cdsl_rollout_keep": ([vp, vp, vp, i32, i32, vp, vp], i32),
-        "cdsl_verify_soft": ([vp, vp, vp, i32, i32] + [vp] * 14, i32),
-        "cdsl_commit_soft": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, vp, vp, vp, vp], i32),
+        "cdsl_verify_soft": ([vp, vp, vp, i32, i32, i32] + [vp] * 14, i32),
+        "cdsl_commit_soft": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp], i32),
         "cdsl_op_soft_rows": ([vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp], i32),
         "cdsl_op_lm_head_rows_workspace": ([i32, i32, i32, i32, i32], C.c_size_t),
         "cdsl_op_lm_head_rows": ([vp, vp, i32, i32, i32, i32, vp, i32, vp, vp, vp, vp, vp, C.c_size_t, vp], i32),
@@ -334,15 +334,23 @@ class Context:
 
     def cdsl_verify_soft(self, prefix: Prefix, lookaheads: torch.Tensor, k: int, d: int, head_lp: torch.Tensor,
                          draft_logits: torch.Tensor, u: torch.Tensor, v: torch.Tensor, out: dict,
-                         want_hidden: bool = False) -> dict:
-        """out: the buffers of cdsl_verify plus draft_lp, res_ids, res_lp ([B, k, d])."""
+                         want_hidden: bool = False, kk: Optional[int] = None) -> dict:
+        """out: the buffers of cdsl_verify plus draft_lp, res_ids, res_lp ([B, k, d]);
+        kk: top-k width of row_topk (default k)."""
         B = prefix.B
+        kk = k if kk is None else kk
         for nm, t in (("u", u), ("v", v)):
             if t.shape != (B, k, d):
                 raise ValueError(f"{nm} must be [B, k, d]")
+        for nm in ("logprobs", "draft_lp", "target_argmax", "res_ids", "res_lp"):
+            if out[nm].numel() != B * k * d:
+                raise ValueError(f"out[{nm!r}] must hold B*k*d values")
+        for nm in ("row_topk_ids", "row_topk_lp"):
+            if out[nm].numel() != B * k * d * kk:
+                raise ValueError(f"out[{nm!r}] must hold B*k*d*kk values")
         hid = out.get("hidden") if want_hidden else None
         rc = lib().cdsl_verify_soft(self.handle, prefix.handle, _ptr(lookaheads, torch.int32, "lookaheads"), k, d,
-                                    _ptr(head_lp, torch.float32, "head_lp"),
+                                    kk, _ptr(head_lp, torch.float32, "head_lp"),
                                     _ptr(draft_logits, torch.float32, "draft_logits"), _ptr(u, torch.float32, "u"),
                                     _ptr(v, torch.float32, "v"), out["logprobs"].data_ptr(),
                                     out["draft_lp"].data_ptr(), out["target_argmax"].data_ptr(),
@@ -355,7 +363,9 @@ class Context:
 
     def cdsl_commit_soft(self, prefix: Prefix, lookaheads, beam, n_accept, row_topk_ids, row_topk_lp, res_ids,
                          res_lp, k, d, next_beams: torch.Tensor, next_head_lp: torch.Tensor):
+        """kk (the next-head width) is next_beams.shape[1]."""
         B = prefix.B
+        kk = next_beams.shape[1]
         emitted = (C.c_int32 * (B * (d + 1)))()
         n_emit = (C.c_int32 * B)()
         rc = lib().cdsl_commit_soft(self.handle, prefix.handle, _ptr(lookaheads, torch.int32, "lookaheads"),
@@ -363,7 +373,7 @@ class Context:
                                     _ptr(row_topk_ids, torch.int32, "row_topk_ids"),
                                     _ptr(row_topk_lp, torch.float32, "row_topk_lp"),
                                     _ptr(res_ids, torch.int32, "res_ids"), _ptr(res_lp, torch.float32, "res_lp"),
-                                    k, d, emitted, n_emit, _ptr(next_beams, torch.int32, "next_beams"),
+                                    k, d, kk, emitted, n_emit, _ptr(next_beams, torch.int32, "next_beams"),
                                     _ptr(next_head_lp, torch.float32, "next_head_lp"))
         _check(rc, self.handle)
         return [[emitted[b * (d + 1) + t] for t in range(n_emit[b])] for b in range(B)]

@@ -990,12 +990,12 @@ int cdsl_verify_kk(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k,
                      row_topk_lp, hidden, nullptr);
 }
 
-int cdsl_verify_soft(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d, const float* head_lp,
-                     const float* draft_logits, const float* u, const float* v, float* logprobs, float* draft_lp,
-                     int32_t* target_argmax, int32_t* n_accept, float* scores, int32_t* row_topk_ids,
-                     float* row_topk_lp, int32_t* res_ids, float* res_lp, float* hidden) {
+int cdsl_verify_soft(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d, int32_t kk,
+                     const float* head_lp, const float* draft_logits, const float* u, const float* v,
+                     float* logprobs, float* draft_lp, int32_t* target_argmax, int32_t* n_accept, float* scores,
+                     int32_t* row_topk_ids, float* row_topk_lp, int32_t* res_ids, float* res_lp, float* hidden) {
   const SoftArgs sa{draft_logits, u, v, draft_lp, res_ids, res_lp};
-  return verify_impl(c, px, look, k, d, k, head_lp, logprobs, target_argmax, n_accept, scores, row_topk_ids,
+  return verify_impl(c, px, look, k, d, kk, head_lp, logprobs, target_argmax, n_accept, scores, row_topk_ids,
                      row_topk_lp, hidden, &sa);
 }
 
@@ -1091,12 +1091,12 @@ int cdsl_commit_kk(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int3
 
 int cdsl_commit_soft(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, const int32_t* n_accept,
                      const int32_t* rtk_ids, const float* rtk_lp, const int32_t* res_ids, const float* res_lp,
-                     int32_t k, int32_t d, int32_t* emitted_host, int32_t* n_emit_host, int32_t* next_beams,
-                     float* next_head_lp) {
+                     int32_t k, int32_t d, int32_t kk, int32_t* emitted_host, int32_t* n_emit_host,
+                     int32_t* next_beams, float* next_head_lp) {
   if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
   if (!res_ids || !res_lp) return fail(c, CDSL_EINVAL, "null argument");
   if (px && !px->verified_soft) return fail(c, CDSL_ESTATE, "cdsl_commit_soft needs a cdsl_verify_soft");
-  return commit_impl(c, px, look, beam, n_accept, rtk_ids, rtk_lp, res_ids, res_lp, k, d, k, emitted_host,
+  return commit_impl(c, px, look, beam, n_accept, rtk_ids, rtk_lp, res_ids, res_lp, k, d, kk, emitted_host,
                      n_emit_host, next_beams, next_head_lp);
 }
 

@@ -182,6 +182,15 @@ class Engine:
                 "state": z(B, dt=i32), "first_at": z(B)}
         return self._bufs[key]
 
+    def _controller_soft_buffers(self, B: int, k: int, d: int, cb: dict):
+        key = ("ctrl_soft", B, k, d)
+        if key not in self._bufs:
+            dev = self.device
+            z = lambda *s, dt=torch.float32: torch.zeros(s, dtype=dt, device=dev)
+            self._bufs[key] = {"draft_logits": z(B, 1, d, self.wl.draft.vocab)}
+            cb["verify"].update(draft_lp=z(B, 1, d), res_ids=z(B, 1, d, dt=torch.int32), res_lp=z(B, 1, d))
+        return self._bufs[key]
+
     def head_step(self, st: DecodeState, keywords: torch.Tensor, roller: int, k: Optional[int] = None,
                   d: Optional[int] = None, mask: Optional[List[bool]] = None,
                   first_at: Optional[torch.Tensor] = None,
@@ -213,13 +222,17 @@ class Engine:
 
     def controller_step(self, st: DecodeState, keywords: torch.Tensor, a_t: float, r_t: float, b: int,
                         k: Optional[int] = None, d: Optional[int] = None,
-                        normalize: Optional[bool] = None) -> dict:
+                        normalize: Optional[bool] = None, u: Optional[torch.Tensor] = None,
+                        v: Optional[torch.Tensor] = None) -> dict:
         """One iteration of Alg. 1 for every prompt, with the readings of the
         oracle's ``controller_step``: draft d tokens after the target's greedy
         head c (k = 1 rollout), verify them (top-k width k for the next
         heads), a = n / d, r = R(generated + c + x_1..x_n); emit [c, x_1..x_n]
         everywhere, then one more token (CDLH-appx., with Step-1 first for
-        b = 1) for the prompts not in S1."""
+        b = 1) for the prompts not in S1.  With uniforms u and v ([B, 1, d]
+        device float32) the rejection loop is speculative sampling's test and
+        the residual draw at the rejected position heads the next candidates
+        (so Step-1 considers it first)."""
         if b not in (0, 1):
             raise ValueError("b must be 0 or 1")
         k = k or self.k
@@ -227,18 +240,33 @@ class Engine:
         B = st.prefix.B
         cb = self._controller_buffers(B, k, d)
         c = self.ctx
+        soft = u is not None
+        if soft and v is None:
+            raise ValueError("soft rejection takes both u and v")
         if normalize is None:
             normalize = self.wl.reward == "keyword_coverage"
         cb["heads"].copy_(st.beams[:, :1])
         cb["head_lp"].copy_(st.head_lp[:, :1])
-        c.cdsl_rollout(st.prefix, cb["heads"], 1, d, cb["look"])
-        c.cdsl_verify(st.prefix, cb["look"], 1, d, cb["head_lp"], out=cb["verify"], kk=k)
+        if soft:
+            sb = self._controller_soft_buffers(B, k, d, cb)
+            c.cdsl_rollout_keep(st.prefix, cb["heads"], 1, d, cb["look"], sb["draft_logits"])
+            c.cdsl_verify_soft(st.prefix, cb["look"], 1, d, cb["head_lp"], sb["draft_logits"], u, v, cb["verify"],
+                               kk=k)
+        else:
+            c.cdsl_rollout(st.prefix, cb["heads"], 1, d, cb["look"])
+            c.cdsl_verify(st.prefix, cb["look"], 1, d, cb["head_lp"], out=cb["verify"], kk=k)
         c.cdsl_reward_keywords_upto(st.prefix, cb["look"], 1, d, cb["verify"]["n_accept"], keywords,
                                     normalize=normalize, reward=cb["reward"])
         c.cdsl_controller_states(cb["verify"]["n_accept"], cb["reward"], d, a_t, r_t, b, cb["state"], cb["first_at"])
-        em, _, _ = c.cdsl_commit(st.prefix, cb["look"], cb["beam"], cb["verify"]["n_accept"],
-                                 cb["verify"]["row_topk_ids"], cb["verify"]["row_topk_lp"], 1, d,
-                                 cb["next_beams"], cb["next_head_lp"], kk=k)
+        if soft:
+            em = c.cdsl_commit_soft(st.prefix, cb["look"], cb["beam"], cb["verify"]["n_accept"],
+                                    cb["verify"]["row_topk_ids"], cb["verify"]["row_topk_lp"],
+                                    cb["verify"]["res_ids"], cb["verify"]["res_lp"], 1, d,
+                                    cb["next_beams"], cb["next_head_lp"])
+        else:
+            em, _, _ = c.cdsl_commit(st.prefix, cb["look"], cb["beam"], cb["verify"]["n_accept"],
+                                     cb["verify"]["row_topk_ids"], cb["verify"]["row_topk_lp"], 1, d,
+                                     cb["next_beams"], cb["next_head_lp"], kk=k)
         # commit has synchronised the stream: these reads only copy
         codes = cb["state"].cpu().tolist()
         n = cb["verify"]["n_accept"][:, 0].cpu().tolist()

@@ -13,8 +13,9 @@ import numpy as np
 import pytest
 import torch
 
+import cdsl_inputs as ci
 import oracle
-from cdsl_harness import TOK_MARGIN, make_engine, make_setup
+from cdsl_harness import TOK_MARGIN, lp_tol, make_engine, make_setup, soft_margins
 
 pytestmark = pytest.mark.gpu
 
@@ -75,9 +76,39 @@ def _cmp_head_step(M, look, rew, tok, hs):
     return ""
 
 
-def _cmp_controller(M, look, y, out, b, cs):
+def _cmp_soft(s, sv, b, cs):
+    """Speculative sampling's part of one prompt's iteration (sv: the
+    verification buffers of prompt b on the host, v: its [d] uniforms):
+    the draft log-probs, the acceptance count and the residual draw.
+    Returns "" when they match, else the near tie that ends the comparison;
+    a different draw must still be a valid one."""
+    am, rm = soft_margins(s.wl.dtype)
+    tol = lp_tol(s.wl.dtype)
+    so = cs.soft
+    assert np.max(np.abs(sv["draft_lp"] - cs.roll.lq[0])) <= tol
+    gn, on = int(sv["n"]), int(so.n[0])
+    if gn != on:
+        j = min(gn, on)
+        assert so.accept_margin[0, j] <= am, (gn, on, so.accept_margin[0])
+        return f"soft acceptance near tie ({so.accept_margin[0, j]:.1e})"
+    if so.lead is None:
+        return ""
+    g_res = int(sv["res_ids"][on])
+    if g_res == so.lead:
+        assert abs(float(sv["res_lp"][on]) - so.lead_lp) <= tol
+        return ""
+    lo, hi, Z = oracle.residual_interval(cs.ver.logits[0, on], cs.roll.logits[0, on], g_res)
+    win = rm / Z
+    vv = float(sv["v"][on])
+    assert hi > lo and lo - win <= vv <= hi + win, (g_res, so.lead, lo, hi, vv, Z)
+    assert so.lead_margin <= win, (g_res, so.lead, so.lead_margin, Z)
+    return f"residual draw near a boundary ({so.lead_margin:.1e})"
+
+
+def _cmp_controller(M, look, y, out, b, cs, s=None, sv=None):
     """One prompt's Alg. 1 iteration: GPU lookahead [d+1], target argmax of
-    the verified rows [d], the engine's outputs, against ControllerStep."""
+    the verified rows [d], the engine's outputs, against ControllerStep.
+    With soft rejection, sv holds prompt b's soft buffers (see _cmp_soft)."""
     got = list(out["emitted"][b])
     if got[0] != cs.head:
         assert cs.head_margin <= M, (got[0], cs.head, cs.head_margin)
@@ -86,11 +117,16 @@ def _cmp_controller(M, look, y, out, b, cs):
     if u >= 0:
         assert cs.draft_margin[u] <= M, (u, list(look), list(cs.x), cs.draft_margin)
         return f"draft near tie ({cs.draft_margin[u]:.1e})"
-    u = _first_diff(y, cs.ver.y[0])
-    if u >= 0:
-        assert cs.ver.margin[0, u] <= M, (u, list(y), list(cs.ver.y[0]), cs.ver.margin[0])
-        if out["n"][b] != cs.n:
-            return f"acceptance near tie ({cs.ver.margin[0, u]:.1e})"
+    if cs.soft is not None:
+        why = _cmp_soft(s, sv, b, cs)
+        if why:
+            return why
+    else:
+        u = _first_diff(y, cs.ver.y[0])
+        if u >= 0:
+            assert cs.ver.margin[0, u] <= M, (u, list(y), list(cs.ver.y[0]), cs.ver.margin[0])
+            if out["n"][b] != cs.n:
+                return f"acceptance near tie ({cs.ver.margin[0, u]:.1e})"
     assert out["n"][b] == cs.n
     assert out["r"][b] == pytest.approx(cs.r, abs=1e-6)
     assert out["states"][b] == cs.state
@@ -140,7 +176,7 @@ def _run_head_steps(s, B, steps, roller):
     return compared
 
 
-def _run_controller(s, B, steps, a_t, r_t, bb):
+def _run_controller(s, B, steps, a_t, r_t, bb, soft=False):
     eng = s.engine
     k, d = s.wl.k, s.wl.d
     st = eng.start(torch.from_numpy(s.prompts(B)).cuda())
@@ -150,15 +186,31 @@ def _run_controller(s, B, steps, a_t, r_t, bb):
     seen = set()
     compared = 0
     cb = eng._controller_buffers(B, k, d)
-    for _ in range(steps):
-        out = eng.controller_step(st, kw, a_t, r_t, bb)
+    for t in range(steps):
+        u = v = None
+        if soft:
+            # uniforms of the k = 1 draft: [B, 1, d]
+            u = ci.uniforms(s.wl.seed, 0, t, B, 1, d)
+            v = ci.uniforms(s.wl.seed, 1, t, B, 1, d)
+        out = eng.controller_step(st, kw, a_t, r_t, bb, u=torch.from_numpy(u).cuda() if soft else None,
+                                  v=torch.from_numpy(v).cuda() if soft else None)
         look = cb["look"][:, 0].cpu().numpy()
         y = cb["verify"]["target_argmax"][:, 0].cpu().numpy()
+        if soft:
+            sv = {nm: cb["verify"][nm][:, 0].cpu().numpy() for nm in ("draft_lp", "res_ids", "res_lp", "n_accept")}
         for b in range(B):
             if not alive[b]:
                 continue
-            cs = oracle.controller_step(s.odraft, s.otarget, ost[b], k, d, a_t, r_t, bb, s.wl.reward, s.kws[b])
-            why = _cmp_controller(_margin(s), look[b], y[b], out, b, cs)
+            cs = oracle.controller_step(s.odraft, s.otarget, ost[b], k, d, a_t, r_t, bb, s.wl.reward, s.kws[b],
+                                        rejection="soft" if soft else "hard",
+                                        u=u[b] if soft else None, v=v[b] if soft else None)
+            svb = None
+            if soft:
+                svb = {"draft_lp": sv["draft_lp"][b], "res_ids": sv["res_ids"][b], "res_lp": sv["res_lp"][b],
+                       "n": sv["n_accept"][b], "v": v[b, 0]}
+                if cs.soft.lead is not None:
+                    seen.add("lead")
+            why = _cmp_controller(_margin(s), look[b], y[b], out, b, cs, s, svb)
             if why:
                 print(f"prompt {b}: stopped after {compared} compared steps: {why}")
                 alive[b] = False
@@ -191,6 +243,22 @@ def test_controller_steps_match_oracle(request, which, a_t, r_t, bb, state):
     compared, seen = _run_controller(request.getfixturevalue(which), 3, 5, a_t, r_t, bb)
     assert compared >= 5
     assert state in seen
+
+
+@pytest.mark.parametrize("which,a_t,r_t,bb,state", [
+    ("tiny", 0.5, 1.0, 1, "S2/S3"), ("tiny", 0.3, 0.0, 0, "S1"),
+    ("tiny_same", 0.5, 0.0, 0, "S1"), ("tiny_same", 0.5, 1.0, 1, "S4")])
+def test_soft_controller_steps_match_oracle(request, which, a_t, r_t, bb, state):
+    """Alg. 1 with speculative sampling's test in the rejection loop, 5
+    iterations for 3 prompts on seeded uniforms: the head (the previous
+    residual draw, when there was one), the draft, its log-probs, the
+    acceptance count, the residual draw, r, the state and the emitted tokens.
+    With draft = target every token is accepted (p = q) and no draw is made."""
+    compared, seen = _run_controller(request.getfixturevalue(which), 3, 5, a_t, r_t, bb, soft=True)
+    assert compared >= 5
+    assert state in seen
+    if which == "tiny":
+        assert "lead" in seen
 
 
 def test_controller_error_paths(tiny):

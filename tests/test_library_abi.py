@@ -70,8 +70,8 @@ def test_error_paths_without_device(lib):
     assert L.cdsl_reward_keywords_upto(None, None, None, 1, 1, None, None, 1, 0, None) == binding.CDSL_EINVAL
     assert L.cdsl_select_first(None, None, None, 1, 1, None) == binding.CDSL_EINVAL
     assert L.cdsl_rollout_keep(None, None, None, 1, 1, None, None) == binding.CDSL_EINVAL
-    assert L.cdsl_verify_soft(None, None, None, 1, 1, *([None] * 14)) == binding.CDSL_EINVAL
-    assert L.cdsl_commit_soft(None, None, None, None, None, None, None, None, None, 1, 1, None, None, None,
+    assert L.cdsl_verify_soft(None, None, None, 1, 1, 1, *([None] * 14)) == binding.CDSL_EINVAL
+    assert L.cdsl_commit_soft(None, None, None, None, None, None, None, None, None, 1, 1, 1, None, None, None,
                               None) == binding.CDSL_EINVAL
     assert L.cdsl_op_soft_rows(None, None, 1, 1, 1, None, None, None, None, None, None) == binding.CDSL_EINVAL
     assert L.cdsl_op_lm_head_rows(None, None, 1, 1, 1, 1, None, 0, None, None, None, None, None, 0,
