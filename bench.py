@@ -300,7 +300,8 @@ def measure_methods(eng, wl, prompts, k, d, steps):
     prompts, with the concept-coverage reward (4 seeded concepts per prompt):
     the CDSL step (the timed path above, here with that reward), the same
     step with speculative sampling's soft rejection, one iteration of the
-    full controller (Alg. 1), and one token of CDLH-appx. (draft lookaheads)
+    full controller (Alg. 1) with hard and with soft rejection, and one token
+    of CDLH-appx. (draft lookaheads)
     and of CDLH (target lookaheads).  Each method starts
     from a fresh prefill, runs one untimed iteration, then `steps` timed
     ones.  Tokens per iteration depend on how often the target accepts the
@@ -314,6 +315,8 @@ def measure_methods(eng, wl, prompts, k, d, steps):
     # seeded uniforms of speculative sampling, resident before timing
     U = [(torch.from_numpy(ci.uniforms(wl.seed, 0, t, B, k, d)).cuda(),
           torch.from_numpy(ci.uniforms(wl.seed, 1, t, B, k, d)).cuda()) for t in range(steps + 1)]
+    U1 = [(torch.from_numpy(ci.uniforms(wl.seed, 0, t, B, 1, d)).cuda(),
+           torch.from_numpy(ci.uniforms(wl.seed, 1, t, B, 1, d)).cuda()) for t in range(steps + 1)]
     it = [0]
 
     def soft_step(st):
@@ -321,15 +324,22 @@ def measure_methods(eng, wl, prompts, k, d, steps):
         it[0] += 1
         return eng.step(st, keywords=kws, k=k, d=d, alpha=math.inf, reward="keyword_coverage", u=u, v=v)
 
+    def alg1_soft(st):
+        u, v = U1[it[0] % len(U1)]
+        it[0] += 1
+        return eng.controller_step(st, kws, METHOD_A_T, METHOD_R_T, METHOD_B, k=k, d=d, normalize=True, u=u, v=v)
+
     runs = {
         "cdsl_step": lambda st: eng.step(st, keywords=kws, k=k, d=d, alpha=math.inf, reward="keyword_coverage"),
         "cdsl_step_soft": soft_step,
         "alg1": lambda st: eng.controller_step(st, kws, METHOD_A_T, METHOD_R_T, METHOD_B, k=k, d=d, normalize=True),
+        "alg1_soft": alg1_soft,
         "cdlh_appx": lambda st: eng.head_step(st, kws, 0, k=k, d=d, normalize=True),
         "cdlh": lambda st: eng.head_step(st, kws, 1, k=k, d=d, normalize=True),
     }
     out = {}
     for name, fn in runs.items():
+        it[0] = 0
         st = eng.start(p, k=k)
         fn(st)
         torch.cuda.synchronize()
