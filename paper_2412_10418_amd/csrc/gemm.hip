@@ -494,22 +494,41 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_skinny(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < CT; ++j) acc[i][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
 
+  // The fragments of a stage (both k-steps when they fit the registers,
+  // else one k-step at a time) are all read before the MFMAs that use them,
+  // and consecutive MFMAs go to different accumulators (the hi planes of
+  // every row tile, then the lo planes).  With one wave per SIMD nothing
+  // else hides an LDS round trip or a dependent MFMA, so reading and
+  // multiplying fragment by fragment would serialise them.
+  constexpr int KB = MT <= 5 ? 2 : 1;          // k-steps per fragment batch
   auto mma = [&](int cur, auto slot_c) __attribute__((always_inline)) {
     constexpr int sl = decltype(slot_c)::value;
 #pragma unroll
-    for (int s = 0; s < 2; ++s)
+    for (int s0 = 0; s0 < 2; s0 += KB) {
+      bf16x8 af[KB][2][MT];
 #pragma unroll
-      for (int i = 0; i < MT; ++i) {
-        const int row = i * 16 + lr;
-        const int off = row * SKC + (((s * 4 + lg) ^ (row & 7)) << 3);
-        const bf16x8 ah = *(const bf16x8*)&As[cur][0][off];
-        const bf16x8 al = *(const bf16x8*)&As[cur][1][off];
+      for (int u = 0; u < KB; ++u)
 #pragma unroll
-        for (int j = 0; j < CT; ++j) {
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, ring[sl][j][s], acc[i][j], 0, 0, 0);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, ring[sl][j][s], acc[i][j], 0, 0, 0);
+        for (int i = 0; i < MT; ++i) {
+          const int row = i * 16 + lr;
+          const int off = row * SKC + ((((s0 + u) * 4 + lg) ^ (row & 7)) << 3);
+          af[u][0][i] = *(const bf16x8*)&As[cur][0][off];
+          af[u][1][i] = *(const bf16x8*)&As[cur][1][off];
         }
-      }
+#pragma unroll
+      for (int u = 0; u < KB; ++u)
+#pragma unroll
+        for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+          for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int j = 0; j < CT; ++j)
+              acc[i][j] =
+                  __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[u][pl][i], ring[sl][j][s0 + u], acc[i][j], 0, 0, 0);
+      // keep the batch's LDS reads ahead of its MFMAs
+      __builtin_amdgcn_sched_group_barrier(0x100, 2 * KB * MT, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2 * KB * MT * CT, 0);
+    }
   };
 
   // stage c (ring slot c % RING, register set c % NA): MFMAs on LDS buffer
