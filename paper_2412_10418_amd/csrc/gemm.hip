@@ -525,9 +525,20 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_skinny(GemmArgs a) {
             for (int j = 0; j < CT; ++j)
               acc[i][j] =
                   __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[u][pl][i], ring[sl][j][s0 + u], acc[i][j], 0, 0, 0);
-      // keep the batch's LDS reads ahead of its MFMAs
-      __builtin_amdgcn_sched_group_barrier(0x100, 2 * KB * MT, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 2 * KB * MT * CT, 0);
+      // the first k-step's reads, then its MFMAs interleaved with the
+      // second k-step's reads, then the second k-step's MFMAs
+      if constexpr (KB == 2) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * MT, 0);
+#pragma unroll
+        for (int q = 0; q < 2 * MT; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, CT, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * MT * CT, 0);
+      } else {
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * KB * MT, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * KB * MT * CT, 0);
+      }
     }
   };
 
