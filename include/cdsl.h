@@ -231,7 +231,8 @@ int cdsl_rollout_keep(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* beams,
  * u[b, i, j-1] <= min(1, p_j(x_{i,j}) / q_j(x_{i,j})), and n_accept counts
  * the kept tokens before the first rejection.  u and v are [B, k, d]
  * uniforms in [0, 1) supplied by the caller (the method's random numbers
- * are inputs).  Outputs, beyond those of cdsl_verify (top-k width k):
+ * are inputs).  Outputs, beyond those of cdsl_verify (row_topk_ids and
+ * row_topk_lp are [B, k, d, kk]):
  *   draft_lp[B, k, d]  log q_j(x_{i,j})
  *   res_ids[B, k, d]   for every fed row, the draw at v from the normalised
  *                      max(0, p_j - q_j) (token ids in ascending order;
@@ -254,8 +255,9 @@ int cdsl_verify_soft(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookahea
  * res_lp) followed by the kk - 1 best tokens of that row's top-kk without
  * it; when n = d they are the target's top-kk after the catch-up, as in
  * cdsl_commit.  Errors as
- * cdsl_commit; ESTATE if the last verification was not soft (and
- * cdsl_commit returns ESTATE after a soft one). */
+ * cdsl_commit; ESTATE if the last verification was not soft or used
+ * another kk (and cdsl_commit / cdsl_commit_kk return ESTATE after a soft
+ * one). */
 int cdsl_commit_soft(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookaheads,
                      const int32_t* beam, const int32_t* n_accept,
                      const int32_t* row_topk_ids, const float* row_topk_lp,

@@ -147,6 +147,18 @@ def test_soft_error_paths(tiny):
         c.cdsl_commit_soft(st.prefix, bf.lookaheads, bf.beam, bf.verify["n_accept"], bf.verify["row_topk_ids"],
                            bf.verify["row_topk_lp"], bf.verify["res_ids"], bf.verify["res_lp"], k, d,
                            bf.next_beams, bf.next_head_lp)
+    # the commit's next-head width must be the soft verification's top-k width
+    c.cdsl_rollout_keep(st.prefix, st.beams, k, d, bf.lookaheads, sb["draft_logits"])
+    c.cdsl_verify_soft(st.prefix, bf.lookaheads, k, d, st.head_lp, sb["draft_logits"], u, u, bf.verify)
+    nb = torch.zeros((1, k - 1), dtype=torch.int32, device="cuda")
+    nl = torch.zeros((1, k - 1), dtype=torch.float32, device="cuda")
+    with pytest.raises(CDSLError):
+        c.cdsl_commit_soft(st.prefix, bf.lookaheads, bf.beam, bf.verify["n_accept"], bf.verify["row_topk_ids"],
+                           bf.verify["row_topk_lp"], bf.verify["res_ids"], bf.verify["res_lp"], k, d, nb, nl)
+    # top-k buffers of another width are refused before any launch
+    with pytest.raises(ValueError):
+        c.cdsl_verify_soft(st.prefix, bf.lookaheads, k, d, st.head_lp, sb["draft_logits"], u, u, bf.verify,
+                           kk=k - 1)
     st.prefix.free()
 
 
