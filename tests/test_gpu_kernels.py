@@ -23,6 +23,8 @@ def _bf16_mat(rng, shape, scale=1.0):
     (1, 192, 256),         # single row
     (37, 640, 1024),       # ragged rows
     (128, 256, 512),       # largest skinny tile
+    (100, 2048, 2048),     # skinny, 7 row tiles (fragments one k-step at a time), split K
+    (112, 25600, 128),     # skinny, 7 row tiles, 32 columns per wave
     (129, 384, 256),       # first dense shape, ragged
     (800, 4096, 4096),     # target o-projection of the verification block (split K)
     (800, 1300, 1024),     # dense, ragged columns of the last tile
