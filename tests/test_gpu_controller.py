@@ -298,3 +298,11 @@ def test_small_bf16_head_steps_match_oracle(small, roller):
 def test_small_bf16_controller_matches_oracle(small):
     compared, _ = _run_controller(small, 2, 2, 0.4, 0.3, 1)
     assert compared >= 1
+
+
+@pytest.mark.timeout(900)
+def test_small_bf16_soft_controller_matches_oracle(small):
+    """Alg. 1 with speculative sampling's test on the bf16 pair: 2
+    iterations for 2 prompts."""
+    compared, _ = _run_controller(small, 2, 2, 0.4, 0.3, 1, soft=True)
+    assert compared >= 1
