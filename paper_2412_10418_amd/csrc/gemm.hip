@@ -463,7 +463,9 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_skinny(GemmArgs a) {
   // discarded).  NA register sets: A(c + NA) is fetched at stage c and
   // written to LDS at stage c + NA - 1, so each activation load has NA - 1
   // stages to arrive.
-  constexpr int NA = NWV == 4 ? 4 : 2;
+  // (the split narrow projections, a ring of 4 at 16 columns per wave:
+  // two sets, which frees the registers those short chunks do not need)
+  constexpr int NA = (NWV == 4 && !(CT == 1 && RING == 4)) ? 4 : 2;
   static_assert(RING % NA == 0, "register sets rotate with the ring");
   u32x4 ar[NA][APT];
   auto aload = [&](int c, auto set_c) __attribute__((always_inline)) {
@@ -755,12 +757,16 @@ struct Plan {
   int kind;          // 0 dense, 1 skinny, 2 f32
   int cfg;           // dense tile configuration
   int mt, ct, nwv;   // skinny row tiles, 16-column tiles per wave, waves
+  bool wide;         // skinny: unsplit wide projection
   int tiles_m, tiles_n;
   int ksplit, kchunk;
   size_t ws_bytes;
 };
 
-constexpr int skinny_ring(int ct) { return ct == 1 ? 8 : 4; }
+// K stages of weights in flight per wave: 8 for the unsplit wide
+// projections at 16 columns per wave, else 4 (which also lets a narrow
+// projection split K into twice as many chunks)
+constexpr int skinny_ring(int ct, bool wide) { return ct == 1 && wide ? 8 : 4; }
 
 Plan make_plan(int M, int N, int K, int dtype, bool no_split = false) {
   Plan p{};
@@ -783,7 +789,8 @@ Plan make_plan(int M, int N, int K, int dtype, bool no_split = false) {
     const bool wide = (N + 63) / 64 >= 200;
     p.ct = (wide && (N + 127) / 128 >= 200) ? 2 : 1;
     p.nwv = 4;
-    const int ring = skinny_ring(p.ct);
+    p.wide = wide;
+    const int ring = skinny_ring(p.ct, wide);
     p.tiles_m = 1;
     p.tiles_n = (N + p.nwv * p.ct * 16 - 1) / (p.nwv * p.ct * 16);
     int s = wide ? 1 : (256 + p.tiles_n - 1) / p.tiles_n;
@@ -924,8 +931,9 @@ hipError_t gemm_launch(const GemmOperand& A, const void* B, const GemmOut& out, 
     dim3 grid(p.tiles_n, 1, p.ksplit);
 #define CDSL_SKINNY(MT)                                                                     \
   case MT:                                                                                  \
-    if (p.ct == 2) gemm_bf16_skinny<MT, 2, skinny_ring(2), 4><<<grid, 256, 0, st>>>(a);       \
-    else gemm_bf16_skinny<MT, 1, skinny_ring(1), 4><<<grid, 256, 0, st>>>(a);                  \
+    if (p.ct == 2) gemm_bf16_skinny<MT, 2, skinny_ring(2, true), 4><<<grid, 256, 0, st>>>(a);  \
+    else if (p.wide) gemm_bf16_skinny<MT, 1, skinny_ring(1, true), 4><<<grid, 256, 0, st>>>(a); \
+    else gemm_bf16_skinny<MT, 1, skinny_ring(1, false), 4><<<grid, 256, 0, st>>>(a);           \
     break;
     switch (p.mt) {
       CDSL_SKINNY(1)
