@@ -129,6 +129,28 @@ def _ptr(t: Optional[torch.Tensor], dtype=None, name="tensor"):
     return t.data_ptr()
 
 
+def _sized(t: Optional[torch.Tensor], n: int, dtype, name="tensor"):
+    """_ptr of a buffer the library reads or writes n elements of: a device
+    tensor of that many elements is required (the C ABI cannot check)."""
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if t.numel() != n:
+        raise ValueError(f"{name} must hold {n} elements, got {tuple(t.shape)}")
+    return _ptr(t, dtype, name)
+
+
+def _verify_out_ptrs(out: dict, B: int, k: int, d: int, kk: int, D: int):
+    """Pointers of cdsl_verify's output buffers, each checked for its size."""
+    hid = out.get("hidden")
+    return (_sized(out["logprobs"], B * k * d, torch.float32, "logprobs"),
+            _sized(out["target_argmax"], B * k * d, torch.int32, "target_argmax"),
+            _sized(out["n_accept"], B * k, torch.int32, "n_accept"),
+            _sized(out["scores"], B * k, torch.float32, "scores"),
+            _sized(out["row_topk_ids"], B * k * d * kk, torch.int32, "row_topk_ids"),
+            _sized(out["row_topk_lp"], B * k * d * kk, torch.float32, "row_topk_lp"),
+            _sized(hid, B * k * D, torch.float32, "hidden") if hid is not None else None)
+
+
 def _stream():
     return torch.cuda.current_stream().cuda_stream
 
@@ -308,8 +330,8 @@ class Context:
                      lookaheads: Optional[torch.Tensor] = None) -> torch.Tensor:
         if lookaheads is None:
             lookaheads = torch.empty((prefix.B, k, d + 1), dtype=torch.int32, device=beams.device)
-        rc = lib().cdsl_rollout(self.handle, prefix.handle, _ptr(beams, torch.int32, "beams"), k, d,
-                                _ptr(lookaheads, torch.int32, "lookaheads"))
+        rc = lib().cdsl_rollout(self.handle, prefix.handle, _sized(beams, prefix.B * k, torch.int32, "beams"), k, d,
+                                _sized(lookaheads, prefix.B * k * (d + 1), torch.int32, "lookaheads"))
         _check(rc, self.handle)
         return lookaheads
 
@@ -317,8 +339,9 @@ class Context:
                           lookaheads: Optional[torch.Tensor] = None) -> torch.Tensor:
         if lookaheads is None:
             lookaheads = torch.empty((prefix.B, k, d + 1), dtype=torch.int32, device=beams.device)
-        rc = lib().cdsl_rollout_with(self.handle, prefix.handle, _ptr(beams, torch.int32, "beams"), k, d,
-                                     int(roller), _ptr(lookaheads, torch.int32, "lookaheads"))
+        rc = lib().cdsl_rollout_with(self.handle, prefix.handle, _sized(beams, prefix.B * k, torch.int32, "beams"),
+                                     k, d, int(roller),
+                                     _sized(lookaheads, prefix.B * k * (d + 1), torch.int32, "lookaheads"))
         _check(rc, self.handle)
         return lookaheads
 
@@ -326,8 +349,8 @@ class Context:
                           draft_logits: torch.Tensor) -> torch.Tensor:
         if draft_logits.numel() != prefix.B * k * d * self.draft_shape.vocab:
             raise ValueError("draft_logits must be [B, k, d, V]")
-        rc = lib().cdsl_rollout_keep(self.handle, prefix.handle, _ptr(beams, torch.int32, "beams"), k, d,
-                                     _ptr(lookaheads, torch.int32, "lookaheads"),
+        rc = lib().cdsl_rollout_keep(self.handle, prefix.handle, _sized(beams, prefix.B * k, torch.int32, "beams"),
+                                     k, d, _sized(lookaheads, prefix.B * k * (d + 1), torch.int32, "lookaheads"),
                                      _ptr(draft_logits, torch.float32, "draft_logits"))
         _check(rc, self.handle)
         return lookaheads
@@ -342,22 +365,19 @@ class Context:
         for nm, t in (("u", u), ("v", v)):
             if t.shape != (B, k, d):
                 raise ValueError(f"{nm} must be [B, k, d]")
-        for nm in ("logprobs", "draft_lp", "target_argmax", "res_ids", "res_lp"):
-            if out[nm].numel() != B * k * d:
-                raise ValueError(f"out[{nm!r}] must hold B*k*d values")
-        for nm in ("row_topk_ids", "row_topk_lp"):
-            if out[nm].numel() != B * k * d * kk:
-                raise ValueError(f"out[{nm!r}] must hold B*k*d*kk values")
-        hid = out.get("hidden") if want_hidden else None
-        rc = lib().cdsl_verify_soft(self.handle, prefix.handle, _ptr(lookaheads, torch.int32, "lookaheads"), k, d,
-                                    kk, _ptr(head_lp, torch.float32, "head_lp"),
-                                    _ptr(draft_logits, torch.float32, "draft_logits"), _ptr(u, torch.float32, "u"),
-                                    _ptr(v, torch.float32, "v"), out["logprobs"].data_ptr(),
-                                    out["draft_lp"].data_ptr(), out["target_argmax"].data_ptr(),
-                                    out["n_accept"].data_ptr(), out["scores"].data_ptr(),
-                                    out["row_topk_ids"].data_ptr(), out["row_topk_lp"].data_ptr(),
-                                    out["res_ids"].data_ptr(), out["res_lp"].data_ptr(),
-                                    hid.data_ptr() if hid is not None else None)
+        o = dict(out)
+        if not want_hidden:
+            o["hidden"] = None
+        lp, y, na, sc, ti, tl, hid = _verify_out_ptrs(o, B, k, d, kk, self.target_shape.d_model)
+        rc = lib().cdsl_verify_soft(self.handle, prefix.handle,
+                                    _sized(lookaheads, B * k * (d + 1), torch.int32, "lookaheads"), k, d, kk,
+                                    _sized(head_lp, B * k, torch.float32, "head_lp"),
+                                    _sized(draft_logits, B * k * d * self.draft_shape.vocab, torch.float32,
+                                           "draft_logits"),
+                                    _ptr(u, torch.float32, "u"), _ptr(v, torch.float32, "v"), lp,
+                                    _sized(out["draft_lp"], B * k * d, torch.float32, "draft_lp"), y, na, sc, ti, tl,
+                                    _sized(out["res_ids"], B * k * d, torch.int32, "res_ids"),
+                                    _sized(out["res_lp"], B * k * d, torch.float32, "res_lp"), hid)
         _check(rc, self.handle)
         return out
 
@@ -368,13 +388,16 @@ class Context:
         kk = next_beams.shape[1]
         emitted = (C.c_int32 * (B * (d + 1)))()
         n_emit = (C.c_int32 * B)()
-        rc = lib().cdsl_commit_soft(self.handle, prefix.handle, _ptr(lookaheads, torch.int32, "lookaheads"),
-                                    _ptr(beam, torch.int32, "beam"), _ptr(n_accept, torch.int32, "n_accept"),
-                                    _ptr(row_topk_ids, torch.int32, "row_topk_ids"),
-                                    _ptr(row_topk_lp, torch.float32, "row_topk_lp"),
-                                    _ptr(res_ids, torch.int32, "res_ids"), _ptr(res_lp, torch.float32, "res_lp"),
-                                    k, d, kk, emitted, n_emit, _ptr(next_beams, torch.int32, "next_beams"),
-                                    _ptr(next_head_lp, torch.float32, "next_head_lp"))
+        rc = lib().cdsl_commit_soft(self.handle, prefix.handle,
+                                    _sized(lookaheads, B * k * (d + 1), torch.int32, "lookaheads"),
+                                    _sized(beam, B, torch.int32, "beam"),
+                                    _sized(n_accept, B * k, torch.int32, "n_accept"),
+                                    _sized(row_topk_ids, B * k * d * kk, torch.int32, "row_topk_ids"),
+                                    _sized(row_topk_lp, B * k * d * kk, torch.float32, "row_topk_lp"),
+                                    _sized(res_ids, B * k * d, torch.int32, "res_ids"),
+                                    _sized(res_lp, B * k * d, torch.float32, "res_lp"),
+                                    k, d, kk, emitted, n_emit, _sized(next_beams, B * kk, torch.int32, "next_beams"),
+                                    _sized(next_head_lp, B * kk, torch.float32, "next_head_lp"))
         _check(rc, self.handle)
         return [[emitted[b * (d + 1) + t] for t in range(n_emit[b])] for b in range(B)]
 
@@ -395,21 +418,14 @@ class Context:
                 "hidden": (torch.empty((B, k, self.target_shape.d_model), dtype=torch.float32, device=dev)
                            if want_hidden else None),
             }
+        outs = _verify_out_ptrs(out, B, k, d, kk, self.target_shape.d_model)
+        look = _sized(lookaheads, B * k * (d + 1), torch.int32, "lookaheads")
+        hl = _sized(head_lp, B * k, torch.float32, "head_lp")
         if kk != k:
-            rc = lib().cdsl_verify_kk(self.handle, prefix.handle, _ptr(lookaheads, torch.int32, "lookaheads"), k,
-                                      d, kk, _ptr(head_lp, torch.float32, "head_lp"), out["logprobs"].data_ptr(),
-                                      out["target_argmax"].data_ptr(), out["n_accept"].data_ptr(),
-                                      out["scores"].data_ptr(), out["row_topk_ids"].data_ptr(),
-                                      out["row_topk_lp"].data_ptr(),
-                                      out["hidden"].data_ptr() if out.get("hidden") is not None else None)
+            rc = lib().cdsl_verify_kk(self.handle, prefix.handle, look, k, d, kk, hl, *outs)
             _check(rc, self.handle)
             return out
-        rc = lib().cdsl_verify(self.handle, prefix.handle, _ptr(lookaheads, torch.int32, "lookaheads"), k, d,
-                               _ptr(head_lp, torch.float32, "head_lp"), out["logprobs"].data_ptr(),
-                               out["target_argmax"].data_ptr(), out["n_accept"].data_ptr(),
-                               out["scores"].data_ptr(), out["row_topk_ids"].data_ptr(),
-                               out["row_topk_lp"].data_ptr(),
-                               out["hidden"].data_ptr() if out.get("hidden") is not None else None)
+        rc = lib().cdsl_verify(self.handle, prefix.handle, look, k, d, hl, *outs)
         _check(rc, self.handle)
         return out
 
@@ -497,15 +513,16 @@ class Context:
             next_head_lp = torch.empty((B, kk), dtype=torch.float32, device=dev)
         emitted = (C.c_int32 * (B * (d + 1)))()
         n_emit = (C.c_int32 * B)()
-        args = (_ptr(lookaheads, torch.int32, "lookaheads"), _ptr(beam, torch.int32, "beam"),
-                _ptr(n_accept, torch.int32, "n_accept"), _ptr(row_topk_ids, torch.int32, "row_topk_ids"),
-                _ptr(row_topk_lp, torch.float32, "row_topk_lp"))
+        args = (_sized(lookaheads, B * k * (d + 1), torch.int32, "lookaheads"),
+                _sized(beam, B, torch.int32, "beam"), _sized(n_accept, B * k, torch.int32, "n_accept"),
+                _sized(row_topk_ids, B * k * d * kk, torch.int32, "row_topk_ids"),
+                _sized(row_topk_lp, B * k * d * kk, torch.float32, "row_topk_lp"))
+        nb = _sized(next_beams, B * kk, torch.int32, "next_beams")
+        nl = _sized(next_head_lp, B * kk, torch.float32, "next_head_lp")
         if kk != k:
-            rc = lib().cdsl_commit_kk(self.handle, prefix.handle, *args, k, d, kk, emitted, n_emit,
-                                      next_beams.data_ptr(), next_head_lp.data_ptr())
+            rc = lib().cdsl_commit_kk(self.handle, prefix.handle, *args, k, d, kk, emitted, n_emit, nb, nl)
         else:
-            rc = lib().cdsl_commit(self.handle, prefix.handle, *args, k, d, emitted, n_emit,
-                                   next_beams.data_ptr(), next_head_lp.data_ptr())
+            rc = lib().cdsl_commit(self.handle, prefix.handle, *args, k, d, emitted, n_emit, nb, nl)
         _check(rc, self.handle)
         em = [[emitted[b * (d + 1) + t] for t in range(n_emit[b])] for b in range(B)]
         return em, next_beams, next_head_lp

@@ -143,9 +143,12 @@ def test_error_paths(tiny):
     eng = tiny.engine
     p = torch.from_numpy(tiny.prompts(1)).cuda()
     st = eng.start(p)
+    wide = torch.zeros((1, tiny.wl.k + 1), dtype=torch.int32, device="cuda")
     with pytest.raises(CDSLError) as e:
-        eng.ctx.cdsl_rollout(st.prefix, st.beams, tiny.wl.k + 1, tiny.wl.d)
+        eng.ctx.cdsl_rollout(st.prefix, wide, tiny.wl.k + 1, tiny.wl.d)
     assert e.value.code == CDSL_ERANGE
+    with pytest.raises(ValueError):       # buffers of the wrong size never reach the library
+        eng.ctx.cdsl_rollout(st.prefix, st.beams, tiny.wl.k + 1, tiny.wl.d)
     bf = eng.buffers(1, tiny.wl.k, tiny.wl.d)
     with pytest.raises(CDSLError) as e:   # commit before rollout/verify
         eng.ctx.cdsl_commit(st.prefix, bf.lookaheads, bf.beam, bf.verify["n_accept"],

@@ -124,6 +124,8 @@ def test_tiny_soft_draft_equal_to_target_accepts_all():
 
 
 def test_soft_error_paths(tiny):
+    import ctypes
+    from paper_2412_10418_amd import binding
     from paper_2412_10418_amd.binding import CDSLError
     s, eng = tiny, tiny.engine
     k, d = s.wl.k, s.wl.d
@@ -147,14 +149,23 @@ def test_soft_error_paths(tiny):
         c.cdsl_commit_soft(st.prefix, bf.lookaheads, bf.beam, bf.verify["n_accept"], bf.verify["row_topk_ids"],
                            bf.verify["row_topk_lp"], bf.verify["res_ids"], bf.verify["res_lp"], k, d,
                            bf.next_beams, bf.next_head_lp)
-    # the commit's next-head width must be the soft verification's top-k width
+    # the commit's next-head width must be the soft verification's top-k
+    # width: the binding refuses buffers of another width, and the library
+    # refuses the call itself (before it reads anything)
     c.cdsl_rollout_keep(st.prefix, st.beams, k, d, bf.lookaheads, sb["draft_logits"])
     c.cdsl_verify_soft(st.prefix, bf.lookaheads, k, d, st.head_lp, sb["draft_logits"], u, u, bf.verify)
     nb = torch.zeros((1, k - 1), dtype=torch.int32, device="cuda")
     nl = torch.zeros((1, k - 1), dtype=torch.float32, device="cuda")
-    with pytest.raises(CDSLError):
+    with pytest.raises(ValueError):
         c.cdsl_commit_soft(st.prefix, bf.lookaheads, bf.beam, bf.verify["n_accept"], bf.verify["row_topk_ids"],
                            bf.verify["row_topk_lp"], bf.verify["res_ids"], bf.verify["res_lp"], k, d, nb, nl)
+    em, ne = (ctypes.c_int32 * (d + 1))(), (ctypes.c_int32 * 1)()
+    vb = bf.verify
+    rc = binding.lib().cdsl_commit_soft(c.handle, st.prefix.handle, bf.lookaheads.data_ptr(), bf.beam.data_ptr(),
+                                        vb["n_accept"].data_ptr(), vb["row_topk_ids"].data_ptr(),
+                                        vb["row_topk_lp"].data_ptr(), vb["res_ids"].data_ptr(),
+                                        vb["res_lp"].data_ptr(), k, d, k - 1, em, ne, nb.data_ptr(), nl.data_ptr())
+    assert rc == binding.CDSL_ESTATE
     # top-k buffers of another width are refused before any launch
     with pytest.raises(ValueError):
         c.cdsl_verify_soft(st.prefix, bf.lookaheads, k, d, st.head_lp, sb["draft_logits"], u, u, bf.verify,
