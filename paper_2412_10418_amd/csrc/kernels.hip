@@ -295,11 +295,13 @@ __global__ __launch_bounds__(NT) void rope_kv_write_split(PassDesc p, const floa
     }
     return;
   }
-  // V of one (beam group, KV head): thread d < hd owns dim row d
-  const int task = blockIdx.x - M;
+  // V of (beam group, KV head) tasks, NT / hd of them per workgroup: thread
+  // d < hd of a task owns dim row d
+  const int per = NT / hd;
+  const int task = ((int)blockIdx.x - M) * per + (int)threadIdx.x / hd;
+  const int d = (int)threadIdx.x % hd;
+  if ((int)threadIdx.x >= per * hd || task >= p.nb * p.kp * Hkv) return;
   const int g = task / Hkv, hh = task % Hkv;
-  const int d = threadIdx.x;
-  if (d >= hd) return;
   const int bi = g / p.kp, i = g % p.kp;
   const int b = pass_batch(p, bi);
   const int Lp = p.Lp[b];
@@ -1016,14 +1018,16 @@ hipError_t rope_kv_launch(const PassDesc& p, const float* qkv, void* qout, const
   if (M == 0) return hipSuccess;
   // q is fp32 for every weight dtype; the KV pool is fp32 or split bf16
   if (dtype == 1) {
-    if (hd > 256) return hipErrorInvalidValue;
-    const int tasks = p.nb * p.kp * Hkv;   // V: one workgroup per (beam group, KV head)
+    if (hd <= 0 || hd > 256) return hipErrorInvalidValue;
+    const int tasks = p.nb * p.kp * Hkv;   // V: (beam group, KV head) tasks, NT / hd per workgroup
     // few rows (the rollout): wider row tasks keep more split planes' loads
     // in flight
     if (M < 256)
-      rope_kv_write_split<512><<<M + tasks, 512, 0, st>>>(p, qkv, (float*)qout, pool, layer, cos_t, sin_t, H, Hkv, hd, S);
+      rope_kv_write_split<512><<<M + (tasks + 512 / hd - 1) / (512 / hd), 512, 0, st>>>(
+          p, qkv, (float*)qout, pool, layer, cos_t, sin_t, H, Hkv, hd, S);
     else
-      rope_kv_write_split<256><<<M + tasks, 256, 0, st>>>(p, qkv, (float*)qout, pool, layer, cos_t, sin_t, H, Hkv, hd, S);
+      rope_kv_write_split<256><<<M + (tasks + 256 / hd - 1) / (256 / hd), 256, 0, st>>>(
+          p, qkv, (float*)qout, pool, layer, cos_t, sin_t, H, Hkv, hd, S);
   }
   else if (S > 1)
     return hipErrorInvalidValue;
