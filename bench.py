@@ -64,6 +64,16 @@ CLASS_KERNEL = {
     "splitk_reduce": (r"splitk_reduce_kernel", ["gemm.hip", "gemm.h", "common.h"]),
 }
 TRAFFIC_TAG = "<!-- traffic "
+# Kernels whose HBM rate the profile summary reports against the peak: the
+# decode (rollout) and verification attention, and the rollout projections
+# by shape family.
+HBM_RATE_KERNELS = [
+    ("rollout attention (draft, hd 64, key groups)", r"attn_split<64, "),
+    ("verification attention (target, hd 128)", r"attn_split<128, "),
+    ("rollout projections, 16 columns per wave, ring 8 (gate/up)", r"gemm_bf16_skinny<\d+, 1, 8, "),
+    ("rollout projections, 16 columns per wave, ring 4 (q/k/v, o, down)", r"gemm_bf16_skinny<\d+, 1, 4, "),
+    ("rollout LM head, 32 columns per wave", r"gemm_bf16_skinny<\d+, 2, 4, "),
+]
 
 
 def source_digest(files):
@@ -197,6 +207,24 @@ def summarize_profile(args):
                      "bytes_per_launch": round(bpl), "rocprof_avg_us": round(avg_us, 2)})
     out += ["", "The bench times each class with HIP events around its launches on the library stream; "
             "its average per launch is expected to agree with the rocprofv3 average of the same kernel.", ""]
+    out += ["## HBM rate of the memory-bound kernels", "",
+            "Measured bytes per dispatch (FETCH_SIZE + WRITE_SIZE, scaled as above) over the rocprofv3 average "
+            f"duration, against the {PEAK_HBM_GBS:.0f} GB/s peak.", "",
+            "| kernel | pattern | dispatches | HBM MB per launch | rocprof avg us | GB/s | % of peak |",
+            "|---|---|---:|---:|---:|---:|---:|"]
+    for label, pat in HBM_RATE_KERNELS:
+        rx = re.compile(pat)
+        fv = [float(r["Counter_Value"]) for r in fetch if rx.search(r["Kernel_Name"])]
+        wv = [float(r["Counter_Value"]) for r in write if rx.search(r["Kernel_Name"])]
+        tv = [r for r in stats if rx.search(r["Name"])]
+        if not fv or not wv or not tv:
+            continue
+        avg_us = sum(float(r["TotalDurationNs"]) for r in tv) / sum(int(r["Calls"]) for r in tv) / 1e3
+        bpl = (sum(fv) / len(fv) * fs + sum(wv) / len(wv) * ws) * 1024.0
+        gbs = bpl / (avg_us * 1e-6) / 1e9
+        out.append(f"| {label} | `{pat}` | {len(fv)} | {bpl / 1e6:.2f} | {avg_us:.2f} | {gbs:.0f} | "
+                   f"{100 * gbs / PEAK_HBM_GBS:.1f}% |")
+    out.append("")
     if util_dir:
         util = counters(util_dir)
         out += ["## Matrix-core and LDS utilisation (MfmaUtil / LdsUtil pass)", "",
