@@ -23,5 +23,6 @@ from .cdsl import (  # noqa: F401
     keyword_hits, keyword_coverage, select_beam, reward_for,
     verify_rows_tree, verify_rows_per_beam,
     keyword_reward, argmax_first, lookahead_heads, cdlh_step, controller_step, HeadStep, ControllerStep,
+    draft_from_prefix, verify_from_prefix, Step1Try,
     soft_accept_count, soft_accept_margins, residual_sample, residual_interval, SoftResult,
 )

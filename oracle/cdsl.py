@@ -117,6 +117,7 @@ class PromptState:
     s: np.ndarray              # log_softmax of M_p at the end of the prefix
     s_logits: np.ndarray       # the raw target logits of that row
     lead: Optional[int] = None  # soft rejection's resampled token: the first next head
+    q_logits: Optional[np.ndarray] = None   # the raw draft logits at the end of the prefix
 
     @property
     def generated(self) -> List[int]:
@@ -129,10 +130,10 @@ class PromptState:
 
 def prefill(draft: Decoder, target: Decoder, prompt: Sequence[int]) -> PromptState:
     prompt = [int(t) for t in prompt]
-    _, dc = draft.extend(draft.empty_cache(), prompt)
+    dout, dc = draft.extend(draft.empty_cache(), prompt)
     out, tc = target.extend(target.empty_cache(), prompt)
     z = out.logits[-1]
-    return PromptState(list(prompt), len(prompt), dc, tc, log_softmax(z), z)
+    return PromptState(list(prompt), len(prompt), dc, tc, log_softmax(z), z, q_logits=dout.logits[-1])
 
 
 @dataclass
@@ -255,11 +256,14 @@ def commit(draft: Decoder, target: Decoder, st: PromptState, emitted: Sequence[i
     next head distribution is read at the last emitted token.  ``lead`` (soft
     rejection) is the token that heads the next beams."""
     emitted = [int(t) for t in emitted]
-    _, dc = draft.extend(st.draft_cache, emitted)
+    if not emitted:      # pfx + [] = pfx (an Alg. 1 iteration that accepted nothing)
+        return PromptState(list(st.tokens), st.n_prompt, st.draft_cache, st.target_cache, st.s, st.s_logits,
+                           None if lead is None else int(lead), st.q_logits)
+    dout, dc = draft.extend(st.draft_cache, emitted)
     out, tc = target.extend(st.target_cache, emitted)
     z = out.logits[-1]
     return PromptState(st.tokens + emitted, st.n_prompt, dc, tc, log_softmax(z), z,
-                       None if lead is None else int(lead))
+                       None if lead is None else int(lead), dout.logits[-1])
 
 
 # ----------------------------------------------------------------------------
@@ -468,10 +472,13 @@ def cdlh_step(roller_is_target: bool, draft: Decoder, target: Decoder, st: Promp
     generated-so-far + candidate + lookahead (the prompt is left out, as in
     the step), and the best candidate is the one token emitted.
 
-    prefer_first_at = r_t gives Step-1 of Alg. 1 with b = 1: the first
-    candidate -- M_p's own greedy token, or the resampled token after a soft
-    rejection -- is taken when its lookahead reaches the reward threshold,
-    else Step-2 picks the best."""
+    prefer_first_at = r_t folds Step-1 of Alg. 1 with b = 1 into the same
+    candidate table: the first candidate (M_p's greedy token; after a soft
+    rejection of the beam step, the resampled token) is taken when its
+    lookahead reaches the threshold, else the best.  With b = 1 Step-1's
+    X_1 and its lookahead are exactly candidate 0 and its lookahead, so this
+    equals Step-1 followed by Step-2 (``controller_step`` computes them
+    apart, in the paper's order)."""
     roller = target if roller_is_target else draft
     cache = st.target_cache if roller_is_target else st.draft_cache
     heads, x, mg = lookahead_heads(roller, cache, st, k, d)
@@ -486,73 +493,149 @@ def cdlh_step(roller_is_target: bool, draft: Decoder, target: Decoder, st: Promp
     return HeadStep(heads, x, mg, r, pick, tok, commit(draft, target, st, [tok]), hm)
 
 
+# ----------------------------------------------------------------------------
+# Alg. 1 itself: lookaheads drafted from the prefix, no beam heads
+# ----------------------------------------------------------------------------
+def draft_from_prefix(draft: Decoder, st: PromptState, d: int) -> Rollout:
+    """Alg. 1, drafting loop: q_1 = M_q(pfx) is the draft's distribution at
+    the end of the prefix, x_j = argmax q_j (lowest id on ties) and
+    q_{j+1} = M_q(pfx + x_1..x_j), for j = 1..d (one sequence: k = 1)."""
+    x = np.zeros((1, d), np.int64)
+    mg = np.zeros((1, d))
+    lq = np.zeros((1, d))
+    zs = np.zeros((1, d, draft.shape.vocab))
+    z = np.asarray(st.q_logits, np.float64)
+    cache = st.draft_cache
+    for j in range(d):
+        x[0, j] = argmax_lowest(z)
+        mg[0, j] = top2_margin(z)
+        lq[0, j] = log_softmax(z)[x[0, j]]
+        zs[0, j] = z
+        if j + 1 < d:
+            out, cache = draft.extend(cache, [int(x[0, j])])
+            z = out.logits[0]
+    return Rollout(x, mg, lq, zs)
+
+
+def verify_from_prefix(target: Decoder, st: PromptState, x: Sequence[int], kk: int) -> Verify:
+    """Alg. 1, verification: p_1 = M_p(pfx) (the target's distribution at
+    the end of the prefix) and p_j = M_p(pfx + x_1..x_{j-1}) for j = 2..d,
+    the last d - 1 in one causal pass over x_1..x_{d-1}; then per row the
+    log-prob of x_j, the argmax y_j, the top-kk (the candidates that Step-2
+    needs after n accepted tokens are those of row n + 1) and the leading
+    matches n (the rejection loop).  One sequence: the outputs are [1, d]."""
+    x = np.asarray(x, np.int64).reshape(-1)
+    d = x.shape[0]
+    rows = [np.asarray(st.s_logits, np.float64)]
+    if d > 1:
+        out, _ = target.extend(st.target_cache, [int(t) for t in x[:d - 1]])
+        rows += list(out.logits)
+    logits = np.stack(rows)[None]                    # [1, d, V]
+    lp = np.zeros((1, d))
+    y = np.zeros((1, d), np.int64)
+    mg = np.zeros((1, d))
+    rtk = np.zeros((1, d, kk), np.int64)
+    rtl = np.zeros((1, d, kk))
+    for j in range(d):
+        z = logits[0, j]
+        ls = log_softmax(z)
+        lp[0, j] = ls[x[j]]
+        y[0, j] = argmax_lowest(z)
+        mg[0, j] = top2_margin(z)
+        rtk[0, j] = topk_ids(z, kk)
+        rtl[0, j] = ls[rtk[0, j]]
+    n = np.array([leading_matches(y[0], x)], np.int64)
+    return Verify(logits, None, lp, y, mg, n, lp.sum(1), rtk, rtl)
+
+
+@dataclass
+class Step1Try:
+    """One round of Step-1 (S2/S3): M_p's greedy token X_i after
+    pfx + x_1..x_n + X_1..X_{i-1}, the draft's d-token lookahead after it, and
+    the reward of the whole window."""
+    X: List[int]               # X_1..X_i
+    x_margin: float            # top-2 margin of M_p's logits at the choice of X_i
+    lh: np.ndarray             # [d] the lookahead
+    lh_margin: np.ndarray      # [d] top-2 margins of its draws
+    reward: float              # R(generated + x_1..x_n + X_1..X_i + lh)
+
+
 @dataclass
 class ControllerStep:
-    head: int                  # c: M_p's greedy token at the prefix end
-    head_lp: float
-    head_margin: float         # gap between the target's top two logits
-    x: np.ndarray              # [d] draft lookahead after c
+    x: np.ndarray              # [d] x_1..x_d drafted from the prefix
     draft_margin: np.ndarray   # [d] top-2 margins of the draft draws
-    ver: Verify                # k = 1 verification of [c, x_1..x_{d-1}]
-    n: int
+    ver: Verify                # p_1..p_d of the verification, [1, d]
+    n: int                     # accepted tokens (hard: leading matches; soft: speculative sampling)
     a: float                   # n / d
-    r: float                   # R(generated + c + x_1..x_n)
+    r: float                   # R(generated + x_1..x_n)
     state: str                 # "S1", "S2/S3" or "S4"
-    extra: Optional[HeadStep]  # the one-token action of S2/S3 and S4
+    step1: List[Step1Try]      # the Step-1 rounds tried (S2/S3 with b > 0)
+    extra: Optional[HeadStep]  # the CDLH-appx. token of Step-2 / S4
     emitted: List[int]
     after: PromptState
-    soft: Optional[SoftResult] = None   # speculative sampling's test (k = 1)
+    soft: Optional[SoftResult] = None   # speculative sampling's test on x_1..x_d
     roll: Optional[Rollout] = None
 
 
 def controller_step(draft: Decoder, target: Decoder, st: PromptState, k: int, d: int, a_t: float, r_t: float,
                     b: int, reward_kind: str, kws: Sequence[int], rejection: str = "hard",
-                    u: Optional[np.ndarray] = None, v: Optional[np.ndarray] = None) -> ControllerStep:
+                    u: Optional[np.ndarray] = None) -> ControllerStep:
     """One iteration of Alg. 1 (Sec. 3.2.1-3.2.3) with hard rejection, or
-    with speculative sampling's test plugged into the rejection loop
-    (rejection = "soft", uniforms u, v of shape [1, d]; the token drawn at
-    the rejected position then heads the next candidates, as in ``step``).
+    with speculative sampling's test in the rejection loop (rejection =
+    "soft", uniforms u of shape [1, d]: x_j is kept while u_j <= min(1,
+    p_j(x_j) / q_j(x_j))).
 
-    Readings: the draft starts after M_p's greedy token c (the head of the
-    k = 1 step) instead of straight from pfx; that token is emitted in every
-    state, like the accepted lookahead tokens.  The acceptance is a = n / d
-    and the reward r = R(generated + c + x_1..x_n), the accepted window.
-      S1 (a >= a_t and r >= r_t): O = [c, x_1..x_n].
-      S2/S3 (a < a_t): O = [c, x_1..x_n] + one token.  Step-1 with b = 1
-          takes M_p's greedy token X_1 after that if its draft lookahead
-          scores R >= r_t; otherwise (and with b = 0) Step-2, i.e. the
-          CDLH-appx. token with k candidates.
-      S4 (a >= a_t, r < r_t): O = [c, x_1..x_n] + the CDLH-appx. token.
-    b > 1 is not taken: it would need M_p tokens appended tentatively and
-    dropped again when the reward stays low (the selected configurations of
-    the paper use b <= 1)."""
-    if b not in (0, 1):
-        raise ValueError("b must be 0 or 1")
-    heads, head_lp, hm = beam_heads(st, 1)
-    c = int(heads[0])
-    ro = rollout(draft, st, [c], d)
-    ve = verify(target, st, [c], head_lp, ro.x)
-    soft, lead = None, None
+    Draft x_1..x_d greedily from pfx; verify them with p_1..p_d; n = the
+    accepted count, a = n / d, r = R(generated + x_1..x_n).  Then:
+      S1 (a >= a_t and r >= r_t): O = [x_1..x_n].
+      S2/S3 (a < a_t): Step-1 tries up to b tokens of M_p: X_i = argmax
+          M_p(pfx + x_1..x_n + X_1..X_{i-1}), a d-token draft lookahead lh
+          after it, and if R(generated + x_1..x_n + X_1..X_i + lh) >= r_t
+          then O = [x_1..x_n] + X_1..X_i.  If no round reaches r_t the X are
+          dropped and Step-2 adds the CDLH-appx. token after x_1..x_n.
+      S4 (a >= a_t, r < r_t): O = [x_1..x_n] + the CDLH-appx. token.
+    The reward windows leave the prompt out, as the step's do.  a_t must be
+    positive: with a_t <= 0 an iteration that accepts nothing would be S1
+    and emit nothing, and the deterministic loop would stand still (the
+    paper's settings use a_t >= 0.3).  With soft rejection only the
+    acceptance count changes: the S1 action emits no token beyond the
+    accepted ones and Step-1 takes M_p's greedy tokens, so the residual
+    draw at the rejected position plays no part."""
+    if not a_t > 0:
+        raise ValueError("a_t must be positive")
+    if b < 0:
+        raise ValueError("b must be >= 0")
+    ro = draft_from_prefix(draft, st, d)
+    x = ro.x[0]
+    ve = verify_from_prefix(target, st, x, k)
+    soft = None
     if rejection == "soft":
         n = soft_accept_count(ve.logprobs[0], ro.lq[0], u[0])
-        lead_lp, lm = None, math.inf
-        if n < d:
-            lead, lead_lp, lm = residual_sample(ve.logits[0, n], ro.logits[0, n], v[0, n])
-        soft = SoftResult(np.array([n]), soft_accept_margins(ve.logprobs[0], ro.lq[0], u[0])[None], lead, lead_lp,
-                          lm)
+        soft = SoftResult(np.array([n]), soft_accept_margins(ve.logprobs[0], ro.lq[0], u[0])[None], None, None,
+                          math.inf)
     elif rejection == "hard":
         n = int(ve.n[0])
     else:
         raise ValueError(rejection)
     a = n / d
-    acc = [c] + [int(t) for t in ro.x[0, :n]]
+    acc = [int(t) for t in x[:n]]
     r = keyword_reward(reward_kind, list(st.generated) + acc, kws)
-    st1 = commit(draft, target, st, acc, lead)
+    st1 = commit(draft, target, st, acc)
     if a >= a_t and r >= r_t:
-        return ControllerStep(c, float(head_lp[0]), float(hm[0]), ro.x[0], ro.margin[0], ve, n, a, r, "S1", None,
-                              acc, st1, soft, ro)
+        return ControllerStep(x, ro.margin[0], ve, n, a, r, "S1", [], None, acc, st1, soft, ro)
     state = "S2/S3" if a < a_t else "S4"
-    pref = r_t if (state == "S2/S3" and b == 1) else None
-    hs = cdlh_step(False, draft, target, st1, k, d, reward_kind, kws, prefer_first_at=pref)
-    return ControllerStep(c, float(head_lp[0]), float(hm[0]), ro.x[0], ro.margin[0], ve, n, a, r, state, hs,
-                          acc + [hs.token], hs.state, soft, ro)
+    tries: List[Step1Try] = []
+    if state == "S2/S3":
+        cur, X = st1, []
+        for _ in range(b):
+            Xi = argmax_lowest(cur.s_logits)
+            xm = top2_margin(cur.s_logits)
+            X.append(Xi)
+            cur = commit(draft, target, cur, [Xi])
+            lh = draft_from_prefix(draft, cur, d)
+            rr = keyword_reward(reward_kind, list(st.generated) + acc + X + [int(t) for t in lh.x[0]], kws)
+            tries.append(Step1Try(list(X), xm, lh.x[0], lh.margin[0], rr))
+            if rr >= r_t:
+                return ControllerStep(x, ro.margin[0], ve, n, a, r, state, tries, None, acc + X, cur, soft, ro)
+    hs = cdlh_step(False, draft, target, st1, k, d, reward_kind, kws)
+    return ControllerStep(x, ro.margin[0], ve, n, a, r, state, tries, hs, acc + [hs.token], hs.state, soft, ro)

@@ -50,3 +50,11 @@ def hf_greedy(model, prompt, n_new):
         z = hf_logits(model, seq)[-1]
         seq.append(int(np.argmax(z)))
     return seq[len(prompt):]
+
+
+def hf_hidden(model, tokens):
+    """Final-normed hidden states [T, D] (the base model's output, after the
+    last RMSNorm)."""
+    with torch.no_grad():
+        out = model.model(torch.tensor([list(map(int, tokens))], dtype=torch.long))
+    return out.last_hidden_state[0].numpy()

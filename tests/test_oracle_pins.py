@@ -93,6 +93,106 @@ def test_plausible_mistakes_fail_the_library_pin(models, monkeypatch):
         assert np.max(np.abs(bad - ref)) > 1e-3, name
 
 
+@pytest.mark.parametrize("which", ["gqa", "mha"])
+def test_hidden_state_matches_library_final_normed_state(models, which, monkeypatch):
+    """The hidden state the linear reward reads is the final-normed one: it
+    matches the library model's last (normed) hidden state; a planted
+    mistake that skips the final norm (the pre-norm residual stream) fails."""
+    from hf_ref import hf_hidden
+    shape, w, dec, hf = models[which]
+    toks = _prompt(15, shape.vocab)
+    ref = hf_hidden(hf, toks)
+    ours = dec.full(toks).hidden
+    assert np.max(np.abs(ours - ref)) < 2e-5 * max(1.0, np.max(np.abs(ref)))
+    calls = {"n": 0}
+    real = odec.rms_norm
+
+    def skip_final(x, g, eps):
+        calls["n"] += 1
+        return x if calls["n"] == 2 * shape.n_layers + 1 else real(x, g, eps)
+
+    monkeypatch.setattr(odec, "rms_norm", skip_final)
+    bad = dec.full(toks).hidden
+    assert np.max(np.abs(bad - ref)) > 1e-2
+
+
+def test_linear_reward_reads_the_last_fed_row(models):
+    """The linear reward of beam i is w . h, h the final-normed state of the
+    last fed row (i, d-1), i.e. after pfx + c_i + x_{i,1..d-1}: checked by a
+    full forward of the library model; the previous row fails."""
+    from hf_ref import hf_hidden
+    draft, target, st = _state(models, n=8)
+    hf_t = models["mha"][3]
+    k, d = 3, 4
+    w = np.random.default_rng(4).standard_normal(models["mha"][0].d_model)
+    r = oracle.step(draft, target, st, k, d, 1.0, "linear", w=w)
+    for i in range(k):
+        seq = list(st.tokens) + [int(r.heads[i])] + [int(t) for t in r.roll.x[i, :d - 1]]
+        hs = hf_hidden(hf_t, seq)
+        # the library's float32 rotary angles bound each state entry's error
+        # to ~2e-5 (see the decoder pin); a wrong row is off by O(1)
+        tol = 2e-5 * float(np.sum(np.abs(w))) * max(1.0, float(np.max(np.abs(hs[-1]))))
+        assert abs(r.reward[i] - float(hs[-1] @ w)) < tol
+        assert abs(float(hs[-2] @ w) - r.reward[i]) > 100 * tol
+
+
+def test_top2_margin_against_sorting_by_hand():
+    """The near-tie gate: the largest value minus the largest of the rest
+    (one copy of the maximum removed), so exact ties give 0."""
+    rng = np.random.default_rng(8)
+    for _ in range(200):
+        V = int(rng.integers(2, 40))
+        z = rng.normal(0.0, 1.0, V)
+        if rng.random() < 0.3:
+            z[rng.integers(0, V)] = z.max()            # planted tie
+        rest = [float(v) for v in z]
+        top = max(rest)
+        rest.remove(top)
+        assert oracle.top2_margin(z) == top - max(rest)
+    assert oracle.top2_margin([1.0, 3.0, 3.0]) == 0.0
+
+
+def test_soft_accept_margins_closed_form():
+    """Distance of u from min(1, p/q), element by element with scalar
+    math; zero exactly at the bound."""
+    rng = np.random.default_rng(9)
+    lt, ld = rng.uniform(-8.0, 0.0, 50), rng.uniform(-8.0, 0.0, 50)
+    u = rng.random(50)
+    got = oracle.soft_accept_margins(lt, ld, u)
+    for j in range(50):
+        bound = min(1.0, math.exp(lt[j] - ld[j]))
+        assert abs(got[j] - abs(u[j] - bound)) < 1e-15
+    assert oracle.soft_accept_margins([-1.0], [-0.5], [math.exp(-0.5)])[0] < 1e-15
+    assert oracle.soft_accept_margins([0.0], [-2.0], [1.0])[0] == 0.0
+
+
+def test_residual_interval_is_the_cumulative_sum():
+    """Token t's interval of v is [sum_{s<t} w_s, sum_{s<=t} w_s] / Z for w =
+    max(0, p - q), summed here with scalar math; the intervals tile [0, 1),
+    and a draw at an interval's midpoint returns its token."""
+    rng = np.random.default_rng(10)
+    for _ in range(20):
+        V = int(rng.integers(3, 30))
+        zp, zq = rng.normal(0, 2, V), rng.normal(0, 2, V)
+        ep = [math.exp(v - max(zp)) for v in zp]
+        eq = [math.exp(v - max(zq)) for v in zq]
+        p = [e / math.fsum(ep) for e in ep]
+        q = [e / math.fsum(eq) for e in eq]
+        w = [max(0.0, a - b) for a, b in zip(p, q)]
+        Z = math.fsum(w)
+        prev_hi = 0.0
+        for t in range(V):
+            lo, hi, Zo = oracle.residual_interval(zp, zq, t)
+            assert abs(Zo - Z) < 1e-12
+            assert abs(lo - math.fsum(w[:t]) / Z) < 1e-12 and abs(hi - math.fsum(w[:t + 1]) / Z) < 1e-12
+            assert abs(lo - prev_hi) < 1e-12
+            prev_hi = hi
+            if w[t] > 0:
+                assert oracle.residual_sample(zp, zq, (lo + hi) / 2)[0] == t
+        assert abs(prev_hi - 1.0) < 1e-12
+    assert oracle.residual_interval([1.0, 2.0], [1.0, 2.0], 1) == (0.0, 0.0, 0.0)
+
+
 # ---------------------------------------------------------------------------
 # caching and verification invariants
 # ---------------------------------------------------------------------------
@@ -361,60 +461,183 @@ def test_lookahead_heuristic_choice_matches_full_recompute(models, roller_is_tar
         assert np.max(np.abs(hs.state.s - oracle.log_softmax(full))) < 1e-10
 
 
-def test_controller_always_s1_is_greedy_decoding(models):
-    """a_t = 0, r_t = -inf: every iteration is S1 (emit the head and the
-    accepted tokens), which is lossless greedy decoding of the target."""
-    draft, target, st0 = _state(models, n=7)
-    st, out = st0, []
-    for _ in range(4):
-        cs = oracle.controller_step(draft, target, st, 3, 3, 0.0, -math.inf, 0, "keyword_count", [4, 5])
-        assert cs.state == "S1" and cs.extra is None
+def _hf_alg1_draft_verify(hf_d, hf_t, tokens, d):
+    """Alg. 1's drafting loop and hard rejection by full recomputation: d
+    greedy draft tokens after the prefix, then the leading matches with the
+    target's argmax after pfx + x_1..x_{j-1}."""
+    from hf_ref import hf_logits
+    x = _hf_greedy_tail(hf_d, tokens, d)
+    zt = hf_logits(hf_t, list(tokens) + x[:-1])[len(tokens) - 1:]
+    n = 0
+    for j in range(d):
+        if int(np.argmax(zt[j])) != x[j]:
+            break
+        n += 1
+    return x, n, zt
+
+
+def _near_draft(models, scale=0.03, seed=5):
+    """A draft that mostly agrees with the "mha" target: its weights plus
+    3% noise, so that 0 < n < d occurs."""
+    shape, w, _, _ = models["mha"]
+    rng = np.random.default_rng(seed)
+    nw = {k: (v + scale * np.std(v) * rng.standard_normal(v.shape) if isinstance(v, np.ndarray) and v.ndim == 2 else v)
+          for k, v in w.items() if k != "layers"}
+    nw["layers"] = [{k: (v + scale * np.std(v) * rng.standard_normal(v.shape) if v.ndim == 2 else v)
+                     for k, v in lw.items()} for lw in w["layers"]]
+    return odec.Decoder(shape, nw)
+
+
+@pytest.mark.parametrize("which,a_t,b", [("random", 2.0, 1), ("random", 1e-9, 1), ("same", 1e-9, 0),
+                                         ("near", 1e-9, 1), ("near", 2.0, 1)])
+def test_controller_greedy_settings_reproduce_greedy_decoding(models, which, a_t, b):
+    """r_t = -inf makes every reward check pass.  Then S1 emits the accepted
+    tokens, which are the target's greedy tokens, and S2/S3's Step-1 (b = 1)
+    emits the target's greedy token after them (a_t = 2 forces S2/S3 every
+    time).  With draft = target every token is accepted (n = d, S1).  Either
+    way Alg. 1 is greedy decoding of the target."""
+    _, _, dt, hf_t = models["mha"]
+    draft = {"random": models["gqa"][2], "same": dt, "near": None}[which] or _near_draft(models)
+    st0 = oracle.prefill(draft, dt, _prompt(7, 64, seed=11))
+    st, out, seen = st0, [], set()
+    for _ in range(5):
+        cs = oracle.controller_step(draft, dt, st, 3, 3, a_t, -math.inf, b, "keyword_count", [4, 5])
+        seen.add((cs.state, cs.n))
         out += cs.emitted
         st = cs.after
-    assert out == _hf_greedy(models["mha"][3], st0.tokens, len(out))
+    assert out == _hf_greedy(hf_t, st0.tokens, len(out))
+    if which == "same":
+        assert seen == {("S1", 3)}
+    if a_t > 1:
+        assert {s for s, _ in seen} == {"S2/S3"}
 
 
-def test_controller_step1_with_low_threshold_takes_target_greedy(models):
-    """a_t above 1 forces S2/S3; with b = 1 and r_t = -inf Step-1 always
-    succeeds on M_p's greedy token, so the output is still greedy decoding
-    of the target."""
-    draft, target, st0 = _state(models, n=7)
-    st, out = st0, []
-    for _ in range(3):
-        cs = oracle.controller_step(draft, target, st, 3, 3, 2.0, -math.inf, 1, "keyword_count", [4, 5])
-        assert cs.state == "S2/S3" and cs.extra.pick == 0
-        out += cs.emitted
-        st = cs.after
-    assert out == _hf_greedy(models["mha"][3], st0.tokens, len(out))
+def test_controller_without_acceptance_emits_exactly_one_token(models):
+    """n = 0 with a_t = 0.3: a = 0 < a_t, so S2/S3, and the iteration emits
+    one token: Step-1's X_1 if its lookahead reaches r_t, else Step-2's."""
+    draft, target, st = _state(models, n=9)
+    hit = 0
+    for b in (0, 1):
+        for r_t in (0.0, 1.0, math.inf):
+            cur = st
+            for _ in range(3):
+                cs = oracle.controller_step(draft, target, cur, 3, 4, 0.3, r_t, b, "keyword_count", [7, 11, 40])
+                if cs.n == 0:
+                    hit += 1
+                    assert cs.state == "S2/S3" and len(cs.emitted) == 1
+                    assert (cs.extra is None) == (b == 1 and cs.step1[0].reward >= r_t)
+                cur = cs.after
+    assert hit >= 6
 
 
-@pytest.mark.parametrize("a_t,r_t,b,state", [(2.0, -math.inf, 0, "S2/S3"), (0.0, math.inf, 1, "S4"),
-                                             (2.0, math.inf, 1, "S2/S3")])
-def test_controller_step2_is_the_cdlh_appx_token(models, a_t, r_t, b, state):
-    """Step-2 (and S4): the token after the accepted ones is CDLH-appx.'s
-    choice, computed here by full recomputation; a and r are checked against
-    their definitions."""
+def test_controller_after_partial_s1_accepts_nothing(models):
+    """A property of the printed algorithm with greedy drafts and hard
+    rejection: after an S1 that accepted n < d tokens the next draft starts
+    with x_{n+1} again, which the target rejected, so that iteration has
+    n = 0."""
+    _, _, dt, _ = models["mha"]
+    draft = _near_draft(models)
+    seen = 0
+    for seed in (11, 12, 13):
+        st = oracle.prefill(draft, dt, _prompt(7, 64, seed=seed))
+        prev = None
+        for _ in range(8):
+            cs = oracle.controller_step(draft, dt, st, 3, 4, 1e-9, -math.inf, 1, "keyword_count", [4])
+            if prev is not None and prev.state == "S1" and prev.n < 4:
+                assert cs.n == 0 and int(cs.x[0]) == int(prev.x[prev.n])
+                seen += 1
+            prev, st = cs, cs.after
+    assert seen >= 2
+
+
+@pytest.mark.parametrize("a_t,r_t,b,state", [(1e-9, -math.inf, 0, "S1"), (2.0, -math.inf, 0, "S2/S3"),
+                                             (2.0, math.inf, 1, "S2/S3"), (2.0, 0.0, 1, "S2/S3"),
+                                             (1e-9, math.inf, 1, "S4")])
+def test_controller_matches_full_recompute(models, a_t, r_t, b, state):
+    """Every quantity of one Alg. 1 iteration by full recomputation with the
+    library models: x drafted from the prefix, n, a, r, the state, Step-1's
+    X_1 and its lookahead reward, and the Step-2 / S4 token (the appendix
+    algorithm after x_1..x_n).  The near draft makes n > 0 for S1 and S4."""
+    from hf_ref import hf_logits
+    _, _, dt, hf_t = models["mha"]
+    draft = _near_draft(models)
+    from hf_ref import hf_llama
+    hf_d = hf_llama(models["mha"][0], draft.w)
+    st = oracle.prefill(draft, dt, _prompt(9, 64, seed=12))
+    k, d, kws = 3, 4, [7, 11, 13, 40]
+    cs = oracle.controller_step(draft, dt, st, k, d, a_t, r_t, b, "keyword_count", kws)
+    assert cs.state == state
+    x, n, _ = _hf_alg1_draft_verify(hf_d, hf_t, st.tokens, d)
+    assert list(cs.x) == x and cs.n == n and cs.a == n / d
+    if state != "S2/S3":
+        assert n > 0
+    acc = x[:n]
+    assert cs.r == float(len(set(acc) & set(kws)))
+    base = list(st.tokens) + acc
+    if state == "S1":
+        assert cs.emitted == acc and cs.extra is None
+        return
+    tail = None
+    if state == "S2/S3" and b == 1:
+        X1 = int(np.argmax(hf_logits(hf_t, base)[-1]))
+        lh = _hf_greedy_tail(hf_d, base + [X1], d)
+        rr = float(len(set(acc + [X1] + lh) & set(kws)))
+        assert cs.step1[0].X == [X1] and list(cs.step1[0].lh) == lh and cs.step1[0].reward == rr
+        if rr >= r_t:
+            tail = [X1]
+    if tail is None:
+        order, scores, best = _brute_cdlh(hf_d, hf_t, base, st.n_prompt, k, d, kws, "keyword_count")
+        tail = [order[best]]
+        assert cs.extra is not None and list(cs.extra.heads) == order
+    assert cs.emitted == acc + tail
+
+
+def test_step1_with_two_rounds(models):
+    """b = 2: when the first M_p token's lookahead misses r_t, Step-1 takes
+    M_p's greedy token after it and tries again; O = x_1..x_n + X_1 + X_2 if
+    that window reaches r_t.  If neither does, both are dropped and Step-2
+    adds the appendix algorithm's token after x_1..x_n."""
     from hf_ref import hf_logits
     draft, target, st = _state(models, n=9)
     hf_d, hf_t = models["gqa"][3], models["mha"][3]
-    k, d, kws = 3, 4, [7, 11, 13, 40]
-    cs = oracle.controller_step(draft, target, st, k, d, a_t, r_t, b, "keyword_count", kws)
-    assert cs.state == state
-    # head, draft lookahead and acceptance by full recomputation
-    c = int(np.argmax(hf_logits(hf_t, st.tokens)[-1]))
-    x = _hf_greedy_tail(hf_d, list(st.tokens) + [c], d)
-    seq = list(st.tokens) + [c]
-    n = 0
-    for j in range(d):
-        if int(np.argmax(hf_logits(hf_t, seq)[-1])) != x[j]:
-            break
-        seq.append(x[j])
-        n += 1
-    assert cs.head == c and list(cs.x) == x and cs.n == n and cs.a == n / d
-    acc = [c] + x[:n]
-    assert cs.r == float(len(set(acc) & set(kws)))
-    order, scores, best = _brute_cdlh(hf_d, hf_t, list(st.tokens) + acc, st.n_prompt, k, d, kws, "keyword_count")
-    assert cs.emitted == acc + [order[best]]
+    d, k = 3, 3
+    x, n, _ = _hf_alg1_draft_verify(hf_d, hf_t, st.tokens, d)
+    acc = x[:n]
+    base = list(st.tokens) + acc
+    X1 = int(np.argmax(hf_logits(hf_t, base)[-1]))
+    lh1 = _hf_greedy_tail(hf_d, base + [X1], d)
+    X2 = int(np.argmax(hf_logits(hf_t, base + [X1])[-1]))
+    lh2 = _hf_greedy_tail(hf_d, base + [X1, X2], d)
+    before = set(st.tokens[st.n_prompt:]) | set(acc) | {X1} | set(lh1)
+    fresh = [t for t in [X2] + lh2 if t not in before]
+    assert fresh, "the seeded prompt has no token that only the second round reaches"
+    cs = oracle.controller_step(draft, target, st, k, d, 2.0, 1.0, 2, "keyword_count", [fresh[0]])
+    assert [t.X for t in cs.step1] == [[X1], [X1, X2]] and list(cs.step1[1].lh) == lh2
+    assert cs.extra is None and cs.emitted == acc + [X1, X2]
+    assert cs.after.tokens == base + [X1, X2]
+    # no round reaches r_t: the X are dropped, Step-2 after x_1..x_n
+    absent = [t for t in range(64) if t not in set(st.tokens) | set(acc) | {X1, X2} | set(lh1) | set(lh2)]
+    cs = oracle.controller_step(draft, target, st, k, d, 2.0, 1.0, 2, "keyword_count", [absent[0]])
+    order, scores, best = _brute_cdlh(hf_d, hf_t, base, st.n_prompt, k, d, [absent[0]], "keyword_count")
+    assert len(cs.step1) == 2 and cs.emitted == acc + [order[best]]
+
+
+@pytest.mark.parametrize("r_t", [0.0, 1.0, 2.0])
+def test_step1_b1_equals_the_first_candidate_rule(models, r_t):
+    """With b = 1, Step-1's token and lookahead are the appendix algorithm's
+    first candidate and its lookahead, so Step-1 then Step-2 equals one
+    candidate table in which candidate 0 wins once it reaches r_t (the form
+    the GPU path computes)."""
+    draft, target, st = _state(models, n=10)
+    kws = [3, 9, 17, 30, 41]
+    cur = st
+    for _ in range(3):
+        cs = oracle.controller_step(draft, target, cur, 4, 3, 2.0, r_t, 1, "keyword_count", kws)
+        acc = [int(t) for t in cs.x[:cs.n]]
+        st1 = oracle.commit(draft, target, cur, acc)
+        hs = oracle.cdlh_step(False, draft, target, st1, 4, 3, "keyword_count", kws, prefer_first_at=r_t)
+        assert cs.emitted == acc + [hs.token]
+        cur = cs.after
 
 
 def test_controller_visits_every_state_on_the_tiny_workload():
@@ -437,6 +660,12 @@ def test_controller_visits_every_state_on_the_tiny_workload():
                 seen[cs.state] = seen.get(cs.state, 0) + 1
                 st = cs.after
     assert set(seen) == {"S1", "S2/S3", "S4"}, seen
+
+
+def test_controller_rejects_non_positive_acceptance_threshold(models):
+    draft, target, st = _state(models, n=6)
+    with pytest.raises(ValueError):
+        oracle.controller_step(draft, target, st, 3, 3, 0.0, 0.0, 1, "keyword_count", [1])
 
 
 # ---------------------------------------------------------------------------
@@ -580,35 +809,36 @@ def test_soft_step_matches_full_recompute(models):
 
 
 def test_soft_controller_matches_full_recompute(models):
-    """Alg. 1 with speculative sampling's test in the rejection loop: n from
-    p and q recomputed by the library models; a rejected token is replaced by
-    the residual draw from those logits, which heads the next candidates, so
-    Step-1 (b = 1, r_t = -inf: always taken; a_t = 2 forces S2/S3) emits it
-    right after the accepted tokens."""
+    """Alg. 1 with speculative sampling's test in the rejection loop: x
+    drafted greedily from the prefix, n from p_j and q_j recomputed by the
+    library models on pfx + x_1..x_{j-1}; the accepted tokens are emitted
+    first (a_t = 2 forces S2/S3, Step-1 with r_t = -inf then adds M_p's
+    greedy token after them)."""
     from hf_ref import hf_logits
-    draft, target, cur = _state(models, n=8)
-    hf_d, hf_t = models["gqa"][3], models["mha"][3]
-    k, d = 3, 3
+    _, _, dt, hf_t = models["mha"]
+    draft = _near_draft(models, scale=0.3)
+    from hf_ref import hf_llama
+    hf_d = hf_llama(models["mha"][0], draft.w)
+    cur = oracle.prefill(draft, dt, _prompt(8, 64, seed=13))
+    d = 3
     rng = np.random.default_rng(21)
-    seen_lead = 0
-    for _ in range(4):
+    ns = []
+    for _ in range(5):
         u = rng.random((1, d)).astype(np.float32)
-        v = rng.random((1, d)).astype(np.float32)
-        cs = oracle.controller_step(draft, target, cur, k, d, 2.0, -math.inf, 1, "keyword_count", [1, 2, 3],
-                                    rejection="soft", u=u, v=v)
+        cs = oracle.controller_step(draft, dt, cur, 3, d, 2.0, -math.inf, 1, "keyword_count", [1, 2, 3],
+                                    rejection="soft", u=u)
         assert cs.state == "S2/S3"
-        seq = list(cur.tokens) + [cs.head] + [int(t) for t in cs.x]
+        x = _hf_greedy_tail(hf_d, cur.tokens, d)
+        assert list(cs.x) == x
         L = len(cur.tokens)
-        zt = hf_logits(hf_t, seq[:-1])[L:]
-        zd = hf_logits(hf_d, seq[:-1])[L:]
-        lt = [oracle.log_softmax(zt[j])[cs.x[j]] for j in range(d)]
-        ld = [oracle.log_softmax(zd[j])[cs.x[j]] for j in range(d)]
+        zt = hf_logits(hf_t, list(cur.tokens) + x[:-1])[L - 1:]
+        zd = hf_logits(hf_d, list(cur.tokens) + x[:-1])[L - 1:]
+        lt = [oracle.log_softmax(zt[j])[x[j]] for j in range(d)]
+        ld = [oracle.log_softmax(zd[j])[x[j]] for j in range(d)]
         n = oracle.soft_accept_count(lt, ld, u[0])
         assert n == cs.n
-        if n < d:
-            lead, _, _ = oracle.residual_sample(zt[n], zd[n], v[0, n])
-            assert cs.soft.lead == lead
-            assert cs.emitted == [cs.head] + [int(t) for t in cs.x[:n]] + [lead]
-            seen_lead += 1
+        ns.append(n)
+        X1 = int(np.argmax(hf_logits(hf_t, list(cur.tokens) + x[:n])[-1]))
+        assert cs.emitted == x[:n] + [X1]
         cur = cs.after
-    assert seen_lead >= 1
+    assert max(ns) > 0
