@@ -327,10 +327,10 @@ def measure_methods(eng, wl, prompts, k, d, steps):
     """Wall-clock of the paper's decoding methods on the same models and
     prompts, with the concept-coverage reward (4 seeded concepts per prompt):
     the CDSL step (the timed path above, here with that reward), the same
-    step with speculative sampling's soft rejection, one iteration of the
-    full controller (Alg. 1) with hard and with soft rejection, and one token
-    of CDLH-appx. (draft lookaheads)
-    and of CDLH (target lookaheads).  Each method starts
+    step with speculative sampling's soft rejection, one iteration of Alg. 1
+    (d tokens drafted from the prefix, the states S1..S4) with hard and with
+    soft rejection, and one token of CDLH-appx. (draft lookaheads) and of
+    CDLH (target lookaheads).  Each method starts
     from a fresh prefill, runs one untimed iteration, then `steps` timed
     ones.  Tokens per iteration depend on how often the target accepts the
     draft's tokens, which for independent random models is rarely."""
@@ -343,8 +343,8 @@ def measure_methods(eng, wl, prompts, k, d, steps):
     # seeded uniforms of speculative sampling, resident before timing
     U = [(torch.from_numpy(ci.uniforms(wl.seed, 0, t, B, k, d)).cuda(),
           torch.from_numpy(ci.uniforms(wl.seed, 1, t, B, k, d)).cuda()) for t in range(steps + 1)]
-    U1 = [(torch.from_numpy(ci.uniforms(wl.seed, 0, t, B, 1, d)).cuda(),
-           torch.from_numpy(ci.uniforms(wl.seed, 1, t, B, 1, d)).cuda()) for t in range(steps + 1)]
+    U1 = [torch.from_numpy(np.ascontiguousarray(ci.uniforms(wl.seed, 0, t, B, 1, d)[:, 0])).cuda()
+          for t in range(steps + 1)]
     it = [0]
 
     def soft_step(st):
@@ -353,9 +353,9 @@ def measure_methods(eng, wl, prompts, k, d, steps):
         return eng.step(st, keywords=kws, k=k, d=d, alpha=math.inf, reward="keyword_coverage", u=u, v=v)
 
     def alg1_soft(st):
-        u, v = U1[it[0] % len(U1)]
+        u = U1[it[0] % len(U1)]
         it[0] += 1
-        return eng.controller_step(st, kws, METHOD_A_T, METHOD_R_T, METHOD_B, k=k, d=d, normalize=True, u=u, v=v)
+        return eng.controller_step(st, kws, METHOD_A_T, METHOD_R_T, METHOD_B, k=k, d=d, normalize=True, u=u)
 
     runs = {
         "cdsl_step": lambda st: eng.step(st, keywords=kws, k=k, d=d, alpha=math.inf, reward="keyword_coverage"),

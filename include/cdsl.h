@@ -22,17 +22,35 @@
  *   cdsl_rollout_keep, cdsl_verify_soft, cdsl_commit_soft
  *                  the same step with speculative sampling's soft rejection
  *                  (Sec. 3.2.2) in place of the argmax test
+ *   cdsl_draft_prefix, cdsl_verify_prefix(_soft), cdsl_reward_keywords_prefix,
+ *   cdsl_commit_prefix
+ *                  one iteration of the paper's Alg. 1 itself: d draft
+ *                  tokens from the prefix (no beam head), their verification
+ *                  p_1..p_d, the reward of the accepted tokens and the commit
+ *                  of x_1..x_n
  *   cdsl_rollout_with, cdsl_reward_keywords_upto, cdsl_controller_states,
  *   cdsl_select_first, cdsl_commit_heads
- *                  the pieces of the paper's full controller (Alg. 1 states
- *                  S1..S4) and of its baselines CDLH (target-rolled
- *                  lookaheads) and CDLH-appx. (draft-rolled, unverified)
+ *                  the rest of Alg. 1 (the state decision between S1..S4 and
+ *                  the one-token actions of Step-1 / Step-2) and its
+ *                  baselines CDLH (target-rolled lookaheads) and CDLH-appx.
+ *                  (draft-rolled, unverified)
  *
  * Conventions
  *   - Every call returns CDSL_OK (0) or a negative CDSL_E* code; the message
  *     of the last failure is available from cdsl_last_error(ctx).  No C++
  *     exception crosses this boundary.  Arguments are checked on the host
- *     before anything is launched; a failed call has launched nothing.
+ *     before anything is launched; a call that fails that check has launched
+ *     nothing.  The commits check the selected beams (and acceptance counts)
+ *     on the device first: a commit that fails with EINVAL or ERANGE leaves
+ *     the prefix, its generated tokens and next_beams as they were.
+ *   - A context that was destroyed, or a prefix handle that was freed, is
+ *     refused with CDSL_ESTATE by every call that takes it (the library
+ *     keeps a registry of live handles).
+ *   - Token ids must lie in [0, V).  Ids that reach the device (prompt
+ *     tokens, lookaheads passed to a verification) are checked there: an id
+ *     outside the range is read as a clamped id and makes the next call that
+ *     synchronises (cdsl_prefill, the commits) fail with CDSL_EINVAL before
+ *     it changes anything; the log-probs gathered at such an id are NaN.
  *   - Pointer arguments are DEVICE pointers unless the name ends in _host.
  *     They are owned by the caller and only read/written during the call
  *     (device work is ordered on the context's stream).
@@ -90,7 +108,10 @@ typedef struct cdsl_model_config {
  *   attn_norm[D], wq[H*hd, D], wk[Hkv*hd, D], wv[Hkv*hd, D], wo[D, H*hd],
  *   mlp_norm[D], w_gate[F, D], w_up[F, D], w_down[D, F]
  * cdsl_init copies (and re-packs) everything into library-owned memory; the
- * caller's buffers are not referenced after cdsl_init returns. */
+ * caller's buffers are not referenced after cdsl_init returns.  The copy is
+ * the packing the kernels want: q/k/v concatenated into one matrix and
+ * gate/up interleaved in groups of 16 rows, so each layer's fused
+ * projections read one contiguous weight. */
 typedef struct cdsl_model {
   cdsl_model_config cfg;
   const void* tok_emb;              /* [V, D]   */
@@ -124,8 +145,12 @@ int cdsl_init(const cdsl_model* draft, const cdsl_model* target,
  * the shared-prefix KV blocks of a new prefix handle (*out, library-owned,
  * released by cdsl_free_prefix).  Writes the first beam heads: beams[B, k]
  * = the k most likely next tokens of the target (log-prob descending, token
- * id ascending on ties) and head_lp[B, k] their log-probs (fp32).
- * Errors: EINVAL, ERANGE (B, L or k beyond limits), ENOMEM (KV pool). */
+ * id ascending on ties) and head_lp[B, k] their log-probs (fp32) -- the
+ * top-k candidates of the lookahead-heuristic algorithm (Sec. 2.1 and the
+ * appendix algorithm; Step-2 of Sec. 3.2.3 takes the same set).
+ * Synchronises the context stream.  Errors: EINVAL (also a prompt token
+ * outside [0, V); no handle is created), ERANGE (B, L or k beyond limits),
+ * ENOMEM (KV pool). */
 int cdsl_prefill(cdsl_ctx* ctx, const int32_t* tokens, int32_t B, int32_t L,
                  int32_t k, cdsl_prefix** out, int32_t* beams, float* head_lp);
 
@@ -266,6 +291,75 @@ int cdsl_commit_soft(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookahea
                      int32_t* n_emit_host, int32_t* next_beams,
                      float* next_head_lp);
 
+/* ---- Alg. 1 itself: a lookahead drafted from the prefix (no beam head) ----
+ * These calls take one lookahead per prompt (k = 1), laid out [B, d+1]:
+ * column 0 is the last token of the prefix (the prompt's last token until
+ * something has been generated) and columns 1..d are x_1..x_d. */
+
+/* Alg. 1, drafting loop: x_j = argmax q_j with q_1 = M_q(pfx) and q_j =
+ * M_q(pfx + x_1..x_{j-1}) (greedy, lowest id on ties), j = 1..d.  Writes
+ * lookaheads[B, d+1] (column 0 as above).  The first of the d draft passes
+ * re-feeds the prefix's last token into the lookahead's first suffix slot,
+ * so q_1 comes from a pass like the others.  draft_logits: NULL, or [B, d, V]
+ * fp32 caller-owned that receives q_1..q_d (for cdsl_verify_prefix_soft;
+ * keep it untouched until then).  Errors as cdsl_rollout. */
+int cdsl_draft_prefix(cdsl_ctx* ctx, cdsl_prefix* prefix, int32_t d,
+                      int32_t* lookaheads, float* draft_logits);
+
+/* Alg. 1, verification (hard rejection): one target pass over the d fed
+ * rows [lookaheads[b, 0], x_1..x_{d-1}] at positions L_b - 1 .. L_b + d - 2,
+ * so row j-1 gives p_j = M_p(pfx + x_1..x_{j-1}), j = 1..d (p_1 = M_p(pfx)).
+ * Outputs (device): logprobs[B, d] = log p_j(x_j), target_argmax[B, d] =
+ * argmax p_j, n_accept[B] = the leading j with argmax p_j = x_j (the
+ * rejection loop), scores[B] = sum_j logprobs, row_topk_ids / row_topk_lp
+ * [B, d, kk] the top-kk of p_1..p_d (row n's are the candidates of Step-2
+ * after n accepted tokens).  lookaheads[b, 0] must be the prefix's last
+ * token, as cdsl_draft_prefix writes it.  Errors as cdsl_verify_kk. */
+int cdsl_verify_prefix(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookaheads,
+                       int32_t d, int32_t kk, float* logprobs, int32_t* target_argmax,
+                       int32_t* n_accept, float* scores, int32_t* row_topk_ids,
+                       float* row_topk_lp);
+
+/* cdsl_verify_prefix with speculative sampling's test in the rejection loop
+ * (Sec. 3.2.2; the paper plugs it into Alg. 1's rejection lines): x_j is
+ * kept while u[b, j-1] <= min(1, p_j(x_j) / q_j(x_j)), with q_j from the
+ * draft_logits of the matching cdsl_draft_prefix.  u, v: [B, d] uniforms in
+ * [0, 1).  Also writes draft_lp[B, d] = log q_j(x_j) and, per row, the draw
+ * at v from the normalised max(0, p_j - q_j) (res_ids, res_lp [B, d]).
+ * Errors as cdsl_verify_soft. */
+int cdsl_verify_prefix_soft(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookaheads,
+                            int32_t d, int32_t kk, const float* draft_logits,
+                            const float* u, const float* v, float* logprobs,
+                            float* draft_lp, int32_t* target_argmax, int32_t* n_accept,
+                            float* scores, int32_t* row_topk_ids, float* row_topk_lp,
+                            int32_t* res_ids, float* res_lp);
+
+/* Alg. 1's reward of the accepted tokens, r = R(x_1..x_n) with the
+ * generated-so-far tokens in front (the prompt is not searched): the number
+ * (normalize: fraction) of distinct keywords present in generated-so-far +
+ * lookaheads[b, 1..upto[b]] (upto [B] device int32, clamped to 0..d; NULL:
+ * all d).  reward [B] fp32.  Errors as cdsl_reward_keywords. */
+int cdsl_reward_keywords_prefix(cdsl_ctx* ctx, cdsl_prefix* prefix,
+                                const int32_t* lookaheads, int32_t d, const int32_t* upto,
+                                const int32_t* keywords, int32_t n_kw, int32_t normalize,
+                                float* reward);
+
+/* Commit of an Alg. 1 iteration's accepted tokens: emits O = [x_1..x_n],
+ * n = n_accept[b] in [0, d] (emitted_host [B, d], n_emit_host [B] = n; n =
+ * 0 emits nothing), as every state of Alg. 1 does before its own action.
+ * The KV of x_1..x_n becomes part of the prefix (both models; when n = d,
+ * x_d is fed through both models as one appended row).  next_beams /
+ * next_head_lp [B, kk] receive the target's top-kk after O: row n of the
+ * verification when n < d, the appended row when n = d.  Synchronises the
+ * context stream once.  Errors: EINVAL (n_accept out of range), ERANGE,
+ * ENOMEM, ESTATE (no cdsl_draft_prefix + cdsl_verify_prefix(_soft) with
+ * this d and kk since the last commit). */
+int cdsl_commit_prefix(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookaheads,
+                       const int32_t* n_accept, int32_t d, int32_t kk,
+                       const int32_t* row_topk_ids, const float* row_topk_lp,
+                       int32_t* emitted_host, int32_t* n_emit_host,
+                       int32_t* next_beams, float* next_head_lp);
+
 /* Reward-only selection with Step-1 of the controller (Sec. 3.2.3, S2/S3
  * with b = 1): beam[b] = 0 when reward[b, 0] >= first_at[b] (head 0 is the
  * target's greedy token), otherwise argmax_i reward[b, i] with the lowest i
@@ -276,14 +370,14 @@ int cdsl_commit_soft(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookahea
 int cdsl_select_first(cdsl_ctx* ctx, const float* reward, const float* first_at,
                       int32_t B, int32_t k, int32_t* beam);
 
-/* The controller's state per prompt after a k = 1 lookahead (Sec. 3.2.3,
+/* The controller's state per prompt after an Alg. 1 lookahead (Sec. 3.2.3,
  * Alg. 1 decision between S1..S4): a = n_accept[b] / d compared in float64
  * with a_t, r = reward[b] (the accepted window's reward, float32 widened to
  * float64) with r_t.  state[b] = 1 (S1: a >= a_t and r >= r_t), 2 (S2/S3:
  * a < a_t) or 4 (S4: a >= a_t, r < r_t).  first_at[b] = r_t for state 2
  * when b = 1 (the input cdsl_select_first takes for Step-1), NaN otherwise.
- * n_accept and reward are [B] (the k = 1 outputs of cdsl_verify and
- * cdsl_reward_keywords_upto), state and first_at [B]; all device.  Errors:
+ * n_accept and reward are [B] (the outputs of cdsl_verify_prefix and
+ * cdsl_reward_keywords_prefix), state and first_at [B]; all device.  Errors:
  * EINVAL for null pointers, B or d <= 0, b not in {0, 1}, NaN thresholds. */
 int cdsl_controller_states(cdsl_ctx* ctx, const int32_t* n_accept, const float* reward,
                            int32_t B, int32_t d, double a_t, double r_t, int32_t b,
@@ -365,7 +459,8 @@ int cdsl_profile_enable(cdsl_ctx* ctx, int32_t enable);
 int cdsl_profile_read(cdsl_ctx* ctx, cdsl_kernel_stats* out);
 
 int cdsl_free_prefix(cdsl_ctx* ctx, cdsl_prefix* prefix);
-int cdsl_destroy(cdsl_ctx* ctx);          /* NULL is accepted */
+/* NULL is accepted; a context already destroyed gives ESTATE. */
+int cdsl_destroy(cdsl_ctx* ctx);
 const char* cdsl_last_error(const cdsl_ctx* ctx);   /* never NULL */
 
 #ifdef __cplusplus

@@ -27,6 +27,8 @@ EXPORTS = [
     "cdsl_reward_keywords_upto", "cdsl_reward_linear", "cdsl_select", "cdsl_select_first", "cdsl_controller_states",
     "cdsl_commit", "cdsl_commit_kk",
     "cdsl_commit_heads",
+    "cdsl_draft_prefix", "cdsl_verify_prefix", "cdsl_verify_prefix_soft", "cdsl_reward_keywords_prefix",
+    "cdsl_commit_prefix",
     "cdsl_prefix_lengths",
     "cdsl_free_prefix", "cdsl_destroy", "cdsl_last_error", "cdsl_profile_enable", "cdsl_profile_read",
     "cdsl_op_gemm_workspace", "cdsl_op_gemm", "cdsl_op_logit_rows",
@@ -90,6 +92,11 @@ def lib():
         "cdsl_op_lm_head_rows": ([vp, vp, i32, i32, i32, i32, vp, i32, vp, vp, vp, vp, vp, C.c_size_t, vp], i32),
         "cdsl_reward_keywords_upto": ([vp, vp, vp, i32, i32, vp, vp, i32, i32, vp], i32),
         "cdsl_commit_heads": ([vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp], i32),
+        "cdsl_draft_prefix": ([vp, vp, i32, vp, vp], i32),
+        "cdsl_verify_prefix": ([vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp], i32),
+        "cdsl_verify_prefix_soft": ([vp, vp, vp, i32, i32] + [vp] * 12, i32),
+        "cdsl_reward_keywords_prefix": ([vp, vp, vp, i32, vp, vp, i32, i32, vp], i32),
+        "cdsl_commit_prefix": ([vp, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp], i32),
         "cdsl_verify_kk": ([vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp], i32),
         "cdsl_commit_kk": ([vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp], i32),
         "cdsl_verify": ([vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp], i32),
@@ -544,6 +551,75 @@ class Context:
                                      _ptr(next_head_lp, torch.float32, "next_head_lp"))
         _check(rc, self.handle)
         return [emitted[b] for b in range(B)]
+
+    # -- Alg. 1 from the prefix (one lookahead per prompt) -------------------
+    def cdsl_draft_prefix(self, prefix: Prefix, d: int, lookaheads: torch.Tensor,
+                          draft_logits: Optional[torch.Tensor] = None) -> torch.Tensor:
+        """lookaheads [B, d+1] (or [B, 1, d+1]); draft_logits [B, d, V] or None."""
+        B = prefix.B
+        dl = None
+        if draft_logits is not None:
+            dl = _sized(draft_logits, B * d * self.draft_shape.vocab, torch.float32, "draft_logits")
+        rc = lib().cdsl_draft_prefix(self.handle, prefix.handle, d,
+                                     _sized(lookaheads, B * (d + 1), torch.int32, "lookaheads"), dl)
+        _check(rc, self.handle)
+        return lookaheads
+
+    def cdsl_verify_prefix(self, prefix: Prefix, lookaheads: torch.Tensor, d: int, kk: int, out: dict,
+                           draft_logits: Optional[torch.Tensor] = None, u: Optional[torch.Tensor] = None,
+                           v: Optional[torch.Tensor] = None) -> dict:
+        """out: logprobs [B, d], target_argmax [B, d], n_accept [B], scores [B],
+        row_topk_ids / row_topk_lp [B, d, kk]; with u (speculative sampling)
+        also draft_lp, res_ids, res_lp [B, d], and draft_logits / v."""
+        B = prefix.B
+        look = _sized(lookaheads, B * (d + 1), torch.int32, "lookaheads")
+        base = (_sized(out["logprobs"], B * d, torch.float32, "logprobs"),
+                _sized(out["target_argmax"], B * d, torch.int32, "target_argmax"),
+                _sized(out["n_accept"], B, torch.int32, "n_accept"),
+                _sized(out["scores"], B, torch.float32, "scores"),
+                _sized(out["row_topk_ids"], B * d * kk, torch.int32, "row_topk_ids"),
+                _sized(out["row_topk_lp"], B * d * kk, torch.float32, "row_topk_lp"))
+        if u is None:
+            rc = lib().cdsl_verify_prefix(self.handle, prefix.handle, look, d, kk, *base)
+        else:
+            lp, y, na, sc, ti, tl = base
+            rc = lib().cdsl_verify_prefix_soft(
+                self.handle, prefix.handle, look, d, kk,
+                _sized(draft_logits, B * d * self.draft_shape.vocab, torch.float32, "draft_logits"),
+                _sized(u, B * d, torch.float32, "u"), _sized(v, B * d, torch.float32, "v"), lp,
+                _sized(out["draft_lp"], B * d, torch.float32, "draft_lp"), y, na, sc, ti, tl,
+                _sized(out["res_ids"], B * d, torch.int32, "res_ids"),
+                _sized(out["res_lp"], B * d, torch.float32, "res_lp"))
+        _check(rc, self.handle)
+        return out
+
+    def cdsl_reward_keywords_prefix(self, prefix: Prefix, lookaheads, d, upto: Optional[torch.Tensor], keywords,
+                                    normalize: bool, reward: torch.Tensor):
+        B = prefix.B
+        rc = lib().cdsl_reward_keywords_prefix(self.handle, prefix.handle,
+                                               _sized(lookaheads, B * (d + 1), torch.int32, "lookaheads"), d,
+                                               _sized(upto, B, torch.int32, "upto") if upto is not None else None,
+                                               _ptr(keywords, torch.int32, "keywords"), keywords.shape[1],
+                                               1 if normalize else 0, _sized(reward, B, torch.float32, "reward"))
+        _check(rc, self.handle)
+        return reward
+
+    def cdsl_commit_prefix(self, prefix: Prefix, lookaheads, n_accept, d, row_topk_ids, row_topk_lp,
+                           next_beams: torch.Tensor, next_head_lp: torch.Tensor) -> List[List[int]]:
+        """Emits x_1..x_n per prompt; kk = next_beams.shape[1]."""
+        B = prefix.B
+        kk = next_beams.shape[1]
+        emitted = (C.c_int32 * (B * d))()
+        n_emit = (C.c_int32 * B)()
+        rc = lib().cdsl_commit_prefix(self.handle, prefix.handle,
+                                      _sized(lookaheads, B * (d + 1), torch.int32, "lookaheads"),
+                                      _sized(n_accept, B, torch.int32, "n_accept"), d, kk,
+                                      _sized(row_topk_ids, B * d * kk, torch.int32, "row_topk_ids"),
+                                      _sized(row_topk_lp, B * d * kk, torch.float32, "row_topk_lp"),
+                                      emitted, n_emit, _sized(next_beams, B * kk, torch.int32, "next_beams"),
+                                      _sized(next_head_lp, B * kk, torch.float32, "next_head_lp"))
+        _check(rc, self.handle)
+        return [[emitted[b * d + t] for t in range(n_emit[b])] for b in range(B)]
 
 
 # ---------------------------------------------------------------------------

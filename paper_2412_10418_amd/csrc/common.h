@@ -48,6 +48,7 @@ struct PassDesc {
   // token of row m: tok[(b * kp + i) * tok_stride + tok_off + j]
   const int* tok;
   int tok_stride, tok_off;
+  int* bad;                // set to 1 when a fed token id lies outside [0, V) (may be null)
   int M() const { return nb * kp * R; }
 };
 

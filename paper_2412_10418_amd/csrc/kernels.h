@@ -18,7 +18,17 @@ struct LogitArgs {
   int* topk_ids;           // [rows][kk]
   float* topk_lp;
   const int* topk_rows;    // destination row of row m (null: m)
+  int* bad;                // set to 1 when a gathered token id lies outside [0, V) (may be null)
 };
+
+// Commit records, one per prompt, stage_stride ints each:
+//   [0] tokens emitted (-1: invalid beam or count)  [1] catch-up: the last
+//   emitted token is fed as one appended row that yields the next heads
+//   [2] selected beam  [3] the record holds the next heads
+//   [kStageHdr, kStageHdr + tcap)               emitted tokens
+//   [kStageHdr + tcap, + kk)                     next head ids
+//   [kStageHdr + tcap + kk, + kk)                next head log-probs (float bits)
+constexpr int kStageHdr = 4;
 
 hipError_t embed_launch(const PassDesc& p, const void* emb, float* h, int D, int V, int dtype, hipStream_t st);
 // S > 0: fold S split planes part[S][rows][D] into x first (written back);
@@ -46,20 +56,25 @@ hipError_t select_launch(int B, int k, const float* scores, const float* reward,
 hipError_t controller_states_launch(int B, int d, const int* n_accept, const float* reward, double a_t, double r_t,
                                     int b1, int* state, float* first_at, hipStream_t st);
 hipError_t reward_keywords_launch(int B, int k, int d, const int* gen, int gen_stride, const int* gen_len,
-                                  const int* look, const int* upto, const int* kws, int n_kw, int normalize,
+                                  const int* look, const int* upto, int head, const int* kws, int n_kw, int normalize,
                                   float* reward, hipStream_t st);
 hipError_t reward_linear_launch(int BK, const float* hidden, const float* w, int D, float* reward, hipStream_t st);
-// head-only commit (mask[b] != 0: emit the head of beam[b]); see kernels.hip
+// the commit kernels write records only; commit_apply_launch carries them out
 hipError_t commit_heads_launch(int B, int k, int d, const int* look, const int* beam, const int* mask, int* stage,
-                               int stage_stride, int* gen, int gen_stride, int* gen_len, int* catch_tok,
-                               hipStream_t st);
+                               int stage_stride, hipStream_t st);
 hipError_t commit_launch(int B, int k, int d, int kk, const int* look, const int* beam, const int* n_accept,
-                         const int* rtk_ids, const float* rtk_lp, const int* res_ids, const float* res_lp,
-                         int* next_beams, float* next_head_lp, int* stage, int stage_stride, int* gen, int gen_stride,
-                         int* gen_len, int* catch_tok, hipStream_t st);
+                         const int* rtk_ids, const float* rtk_lp, const int* res_ids, const float* res_lp, int* stage,
+                         int stage_stride, int tcap, hipStream_t st);
+hipError_t commit_prefix_launch(int B, int d, int kk, const int* look, const int* n_accept, const int* rtk_ids,
+                                const float* rtk_lp, int* stage, int stage_stride, int tcap, hipStream_t st);
+hipError_t commit_apply_launch(int B, const int* stage, int stage_stride, int tcap, int kk, int* gen, int gen_stride,
+                               int* gen_len, int* next_beams, float* next_head_lp, int* catch_tok, hipStream_t st);
+hipError_t prefix_tail_launch(int B, const int* gen, int gen_stride, const int* gen_len, const int* ptail,
+                              const int* Lp, int* Lm1, int* look, int look_stride, hipStream_t st);
+hipError_t last_tokens_launch(int B, const int* tokens, int L, int* out, hipStream_t st);
 hipError_t promote_launch(int B, int k, const KVPool& pool, int n_layers, const int* stage, int stage_stride, int dlim,
-                          const int* Lp, const int* ptable, int ptable_stride, const int* stable, int s_stride_b,
-                          int s_stride_i, int dtype, hipStream_t st);
+                          int soff, const int* Lp, const int* ptable, int ptable_stride, const int* stable,
+                          int s_stride_b, int s_stride_i, int dtype, hipStream_t st);
 hipError_t advance_launch(int B, const int* stage, int stage_stride, int dlim, int* Lp, hipStream_t st);
 hipError_t add_launch(int n, const int* ids, int* v, int delta, hipStream_t st);
 hipError_t fill_int_launch(int* p, int v, long long n, hipStream_t st);

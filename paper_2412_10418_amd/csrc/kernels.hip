@@ -33,15 +33,18 @@ __device__ __forceinline__ float block_sum(float v, float* sh) {
 }
 
 // ---------------------------------------------------------------------------
-// Token ids outside [0, V) are clamped: a bad id gives a wrong row, never
-// an out-of-bounds read.
+// A token id outside [0, V) sets *bad (the library reports it as an invalid
+// argument at its next synchronisation) and is clamped for the read, so it
+// never reads out of bounds.
 template <typename T>
 __global__ __launch_bounds__(256) void embed_rows(PassDesc p, const T* __restrict__ emb, float* __restrict__ h,
-                                                  int D, int V) {
+                                                  int D, int V, int* __restrict__ bad) {
   const int m = blockIdx.x;
   int bi, b, i, j;
   row_decode(p, m, bi, b, i, j);
-  const int tok = min(max(p.tok[(long long)(b * p.kp + i) * p.tok_stride + p.tok_off + j], 0), V - 1);
+  const int raw = p.tok[(long long)(b * p.kp + i) * p.tok_stride + p.tok_off + j];
+  if ((raw < 0 || raw >= V) && threadIdx.x == 0 && bad) *bad = 1;
+  const int tok = min(max(raw, 0), V - 1);
   const T* e = emb + (long long)tok * D;
   float* o = h + (long long)m * D;
   for (int c = threadIdx.x; c < D; c += 256) o[c] = to_f32<T>(e[c]);
@@ -479,8 +482,10 @@ __global__ __launch_bounds__(256) void logit_rows_kernel(LogitArgs a) {
     __syncthreads();
   }
   if (a.lp && tid == 0) {
-    const int tok = min(max(a.gather_tok[rowmap_index(a.gather_map, m)], 0), a.V - 1);
-    a.lp[m] = z[tok] - lse;
+    const int tok = a.gather_tok[rowmap_index(a.gather_map, m)];
+    const bool in = tok >= 0 && tok < a.V;
+    if (!in && a.bad) *a.bad = 1;
+    a.lp[m] = in ? z[tok] - lse : __int_as_float(0x7fc00000);
   }
   if (KKMAX == 0 || a.kk == 0) return;
   const int dst = a.topk_rows ? a.topk_rows[m] : m;
@@ -538,7 +543,7 @@ __global__ void beam_scores_kernel(int BK, int d, const int* __restrict__ look, 
   if (bk >= BK) return;
   int n = 0;
   bool run = true;
-  float s = head_lp[bk];
+  float s = head_lp ? head_lp[bk] : 0.f;
   for (int j = 0; j < d; ++j) {
     const long long r = (long long)bk * d + j;
     bool keep;
@@ -755,12 +760,12 @@ __global__ void controller_states_kernel(int B, int d, const int* __restrict__ n
 }
 
 // Keyword reward, one workgroup per (b, i): distinct keywords present in
-// generated-so-far + the row's head + its first upto[b, i] lookahead tokens
-// (all d when upto is null).
+// generated-so-far + the row's head (when head is set) + its first
+// upto[b, i] lookahead tokens (all d when upto is null).
 __global__ __launch_bounds__(256) void reward_keywords_kernel(int k, int d, const int* __restrict__ gen,
                                                               int gen_stride, const int* __restrict__ gen_len,
                                                               const int* __restrict__ look,
-                                                              const int* __restrict__ upto,
+                                                              const int* __restrict__ upto, int head,
                                                               const int* __restrict__ kws, int n_kw, int normalize,
                                                               float* __restrict__ reward) {
   __shared__ int hit[64];
@@ -772,9 +777,10 @@ __global__ __launch_bounds__(256) void reward_keywords_kernel(int k, int d, cons
   const int* kw = kws + (long long)b * n_kw;
   const int gl = gen_len[b];
   const int nx = upto ? min(max(upto[bk], 0), d) : d;
-  const int total = gl + nx + 1;
+  const int skip = head ? 0 : 1;
+  const int total = gl + nx + 1 - skip;
   for (int t = threadIdx.x; t < total; t += 256) {
-    const int tok = t < gl ? gen[(long long)b * gen_stride + t] : look[(long long)bk * (d + 1) + (t - gl)];
+    const int tok = t < gl ? gen[(long long)b * gen_stride + t] : look[(long long)bk * (d + 1) + skip + (t - gl)];
     for (int u = 0; u < n_kw; ++u)
       if (kw[u] == tok) atomicOr(&hit[u], 1);
   }
@@ -804,72 +810,95 @@ __global__ __launch_bounds__(256) void reward_linear_kernel(const float* __restr
   if (threadIdx.x == 0) reward[bk] = s;
 }
 
-// Commit, one thread per prompt.  stage[b] = {n_emit, catch_up, tokens...}.
-// res_ids / res_lp (soft rejection, [B, k, d]): when n < d the residual draw
-// at the rejected position leads the next heads, followed by the row's top
-// tokens without it.
+// The commit kernels only stage their decisions, one record per prompt (see
+// the layout in kernels.h); commit_apply_kernel carries a record out after
+// the host has checked every prompt's record, so a commit that fails
+// validation changes no generated tokens and no next heads.
+__device__ __forceinline__ void stage_heads(int* st, int tcap, int kk, int u, int id, float lp) {
+  st[kStageHdr + tcap + u] = id;
+  st[kStageHdr + tcap + kk + u] = __float_as_int(lp);
+}
+
+// Beam commit, one thread per prompt: emit [c_i*, x_i*,1..n] of the selected
+// beam.  res_ids / res_lp (soft rejection, [B, k, d]): when n < d the
+// residual draw at the rejected position leads the next heads, followed by
+// the row's top tokens without it.
 __global__ void commit_kernel(int B, int k, int d, int kk, const int* __restrict__ look, const int* __restrict__ beam,
                               const int* __restrict__ n_accept, const int* __restrict__ rtk_ids,
                               const float* __restrict__ rtk_lp, const int* __restrict__ res_ids,
-                              const float* __restrict__ res_lp, int* __restrict__ next_beams,
-                              float* __restrict__ next_head_lp, int* __restrict__ stage, int stage_stride,
-                              int* __restrict__ gen, int gen_stride, int* __restrict__ gen_len,
-                              int* __restrict__ catch_tok) {
+                              const float* __restrict__ res_lp, int* __restrict__ stage, int stage_stride,
+                              int tcap) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= B) return;
   int* st = stage + (long long)b * stage_stride;
   const int i = beam[b];
-  if (i < 0 || i >= k) {
+  const int n = (i >= 0 && i < k) ? n_accept[b * k + i] : -1;
+  if (i < 0 || i >= k || n < 0 || n > d) {
     st[0] = -1;
     return;
   }
   const int bk = b * k + i;
-  const int n = n_accept[bk];
   const int* row = look + (long long)bk * (d + 1);
   st[0] = n + 1;
   st[1] = n == d;
   st[2] = i;
-  const int gl = gen_len[b];
-  for (int t = 0; t <= n; ++t) {
-    st[3 + t] = row[t];
-    gen[(long long)b * gen_stride + gl + t] = row[t];
-  }
-  gen_len[b] = gl + n + 1;
+  st[3] = n < d;
+  for (int t = 0; t <= n; ++t) st[kStageHdr + t] = row[t];
   if (n < d && res_ids) {
     const long long q = (long long)bk * d + n;
     const long long r = q * kk;
     const int lead = res_ids[q];
-    next_beams[b * kk] = lead;
-    next_head_lp[b * kk] = res_lp[q];
+    stage_heads(st, tcap, kk, 0, lead, res_lp[q]);
     int o = 1;
     for (int u = 0; u < kk && o < kk; ++u) {
       if (rtk_ids[r + u] == lead) continue;
-      next_beams[b * kk + o] = rtk_ids[r + u];
-      next_head_lp[b * kk + o] = rtk_lp[r + u];
+      stage_heads(st, tcap, kk, o, rtk_ids[r + u], rtk_lp[r + u]);
       ++o;
     }
   } else if (n < d) {
     const long long r = ((long long)bk * d + n) * kk;
-    for (int u = 0; u < kk; ++u) {
-      next_beams[b * kk + u] = rtk_ids[r + u];
-      next_head_lp[b * kk + u] = rtk_lp[r + u];
-    }
-  } else {
-    catch_tok[b] = row[d];
+    for (int u = 0; u < kk; ++u) stage_heads(st, tcap, kk, u, rtk_ids[r + u], rtk_lp[r + u]);
+  }
+}
+
+// Alg. 1 commit of a lookahead drafted from the prefix (one sequence per
+// prompt, lookahead row [last prefix token, x_1..x_d]): emit x_1..x_n.  The
+// next heads are row n's top-kk (the target after x_1..x_n) when n < d;
+// when n = d, x_d is fed as a catch-up row.  n = 0 emits nothing.
+__global__ void commit_prefix_kernel(int B, int d, int kk, const int* __restrict__ look,
+                                     const int* __restrict__ n_accept, const int* __restrict__ rtk_ids,
+                                     const float* __restrict__ rtk_lp, int* __restrict__ stage, int stage_stride,
+                                     int tcap) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  int* st = stage + (long long)b * stage_stride;
+  const int n = n_accept[b];
+  if (n < 0 || n > d) {
+    st[0] = -1;
+    return;
+  }
+  const int* row = look + (long long)b * (d + 1);
+  st[0] = n;
+  st[1] = n == d;
+  st[2] = 0;
+  st[3] = n < d;
+  for (int t = 0; t < n; ++t) st[kStageHdr + t] = row[1 + t];
+  if (n < d) {
+    const long long r = ((long long)b * d + n) * kk;
+    for (int u = 0; u < kk; ++u) stage_heads(st, tcap, kk, u, rtk_ids[r + u], rtk_lp[r + u]);
   }
 }
 
 // Head-only commit, one thread per prompt: prompts with mask[b] != 0 emit
-// the head of their selected beam (stage = {1, 0, i, token}, appended to
-// the generated tokens and queued in catch_tok for the one-token pass that
-// puts it into both caches); the others emit nothing (stage[0] = 0).
+// the head of their selected beam, fed afterwards as a one-row append pass
+// that yields the next heads; the others emit nothing (n_emit = 0).
 __global__ void commit_heads_kernel(int B, int k, int d, const int* __restrict__ look, const int* __restrict__ beam,
-                                    const int* __restrict__ mask, int* __restrict__ stage, int stage_stride,
-                                    int* __restrict__ gen, int gen_stride, int* __restrict__ gen_len,
-                                    int* __restrict__ catch_tok) {
+                                    const int* __restrict__ mask, int* __restrict__ stage, int stage_stride) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= B) return;
   int* st = stage + (long long)b * stage_stride;
+  st[1] = 0;
+  st[3] = 0;
   if (!mask[b]) {
     st[0] = 0;
     return;
@@ -879,22 +908,63 @@ __global__ void commit_heads_kernel(int B, int k, int d, const int* __restrict__
     st[0] = -1;
     return;
   }
-  const int tok = look[(long long)(b * k + i) * (d + 1)];
   st[0] = 1;
-  st[1] = 0;
+  st[1] = 1;
   st[2] = i;
-  st[3] = tok;
-  const int gl = gen_len[b];
-  gen[(long long)b * gen_stride + gl] = tok;
-  gen_len[b] = gl + 1;
-  catch_tok[b] = tok;
+  st[kStageHdr] = look[(long long)(b * k + i) * (d + 1)];
 }
 
-// Copy the selected beam's first cnt suffix slots into the prefix at
-// positions Lp[b] .. Lp[b] + cnt - 1, for every layer and KV head.
+// Carries out the checked records: append the emitted tokens to the
+// generated tokens, write the staged next heads, and queue the last emitted
+// token of catch-up prompts.
+__global__ void commit_apply_kernel(int B, const int* __restrict__ stage, int stage_stride, int tcap, int kk,
+                                    int* __restrict__ gen, int gen_stride, int* __restrict__ gen_len,
+                                    int* __restrict__ next_beams, float* __restrict__ next_head_lp,
+                                    int* __restrict__ catch_tok) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const int* st = stage + (long long)b * stage_stride;
+  const int ne = st[0];
+  if (ne > 0) {
+    const int gl = gen_len[b];
+    for (int t = 0; t < ne; ++t) gen[(long long)b * gen_stride + gl + t] = st[kStageHdr + t];
+    gen_len[b] = gl + ne;
+    if (st[1]) catch_tok[b] = st[kStageHdr + ne - 1];
+  }
+  if (ne >= 0 && st[3] && !st[1]) {
+    for (int u = 0; u < kk; ++u) {
+      next_beams[b * kk + u] = st[kStageHdr + tcap + u];
+      next_head_lp[b * kk + u] = __int_as_float(st[kStageHdr + tcap + kk + u]);
+    }
+  }
+}
+
+// Alg. 1 passes from the prefix: the lookahead row starts with the last
+// token of the prefix (the prompt's last token until something is
+// generated), and those passes see a prefix one token shorter: Lm1 = Lp - 1.
+__global__ void prefix_tail_kernel(int B, const int* __restrict__ gen, int gen_stride, const int* __restrict__ gen_len,
+                                   const int* __restrict__ ptail, const int* __restrict__ Lp, int* __restrict__ Lm1,
+                                   int* __restrict__ look, int look_stride) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  Lm1[b] = Lp[b] - 1;
+  if (look) {
+    const int gl = gen_len[b];
+    look[(long long)b * look_stride] = gl > 0 ? gen[(long long)b * gen_stride + gl - 1] : ptail[b];
+  }
+}
+
+__global__ void last_tokens_kernel(int B, const int* __restrict__ tokens, int L, int* __restrict__ out) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b < B) out[b] = tokens[(long long)b * L + L - 1];
+}
+
+// Copy cnt suffix slots of the selected beam, from slot soff on, into the
+// prefix at positions Lp[b] .. Lp[b] + cnt - 1, for every layer and KV head
+// (cnt = min(n_emit, dlim)).
 template <typename T>
 __global__ __launch_bounds__(256) void promote_kernel(int k, KVPool pool, int n_layers, const int* __restrict__ stage,
-                                                      int stage_stride, int dlim, const int* __restrict__ Lp,
+                                                      int stage_stride, int dlim, int soff, const int* __restrict__ Lp,
                                                       const int* __restrict__ ptable, int ptable_stride,
                                                       const int* __restrict__ stable, int s_stride_b,
                                                       int s_stride_i) {
@@ -913,8 +983,8 @@ __global__ __launch_bounds__(256) void promote_kernel(int k, KVPool pool, int n_
   for (int u = threadIdx.x; u < cnt * per_tok; u += 256) {
     const int t = u / per_tok, rem = u % per_tok;
     const int hh = rem / hd, dd = rem % hd;
-    const int sblk = stable[(long long)b * s_stride_b + i * s_stride_i + t / kBlock];
-    const int sslot = t % kBlock;
+    const int sblk = stable[(long long)b * s_stride_b + i * s_stride_i + (t + soff) / kBlock];
+    const int sslot = (t + soff) % kBlock;
     const int pos = L0 + t;
     const int pblk = ptable[(long long)b * ptable_stride + pos / kBlock];
     const int pslot = pos % kBlock;
@@ -928,7 +998,8 @@ __global__ __launch_bounds__(256) void promote_kernel(int k, KVPool pool, int n_
 // promote_kernel for the split bf16 pool format
 __global__ __launch_bounds__(256) void promote_split_kernel(int k, KVPool pool, int n_layers,
                                                             const int* __restrict__ stage, int stage_stride, int dlim,
-                                                            const int* __restrict__ Lp, const int* __restrict__ ptable,
+                                                            int soff, const int* __restrict__ Lp,
+                                                            const int* __restrict__ ptable,
                                                             int ptable_stride, const int* __restrict__ stable,
                                                             int s_stride_b, int s_stride_i) {
   const int b = blockIdx.x;
@@ -948,8 +1019,8 @@ __global__ __launch_bounds__(256) void promote_split_kernel(int k, KVPool pool, 
   for (int u = threadIdx.x; u < cnt * per_tok; u += 256) {
     const int t = u / per_tok, rem = u % per_tok;
     const int hh = rem / hd, dd = rem % hd;
-    const int sblk = stable[(long long)b * s_stride_b + i * s_stride_i + t / kBlock];
-    const int sslot = t % kBlock;
+    const int sblk = stable[(long long)b * s_stride_b + i * s_stride_i + (t + soff) / kBlock];
+    const int sslot = (t + soff) % kBlock;
     const int pos = L0 + t;
     const int pblk = ptable[(long long)b * ptable_stride + pos / kBlock];
     const int pslot = pos % kBlock;
@@ -993,8 +1064,8 @@ __global__ void heads_to_lookaheads(int BK, int d, const int* __restrict__ beams
 hipError_t embed_launch(const PassDesc& p, const void* emb, float* h, int D, int V, int dtype, hipStream_t st) {
   const int M = p.M();
   if (M == 0) return hipSuccess;
-  if (dtype == 1) embed_rows<bf16><<<M, 256, 0, st>>>(p, (const bf16*)emb, h, D, V);
-  else embed_rows<float><<<M, 256, 0, st>>>(p, (const float*)emb, h, D, V);
+  if (dtype == 1) embed_rows<bf16><<<M, 256, 0, st>>>(p, (const bf16*)emb, h, D, V, p.bad);
+  else embed_rows<float><<<M, 256, 0, st>>>(p, (const float*)emb, h, D, V, p.bad);
   return hipGetLastError();
 }
 
@@ -1094,7 +1165,12 @@ __global__ __launch_bounds__(256) void rowstats_merge_kernel(RowStats s, LogitAr
   if (lane == 0) shs[w] = sv;
   __syncthreads();
   const float lse = G + __logf(shs[0] + shs[1] + shs[2] + shs[3]);
-  if (a.lp && tid == 0) a.lp[m] = s.zx[m] - lse;
+  if (a.lp && tid == 0) {
+    const int tok = s.gather_tok ? s.gather_tok[rowmap_index(s.gather_map, m)] : 0;
+    const bool in = tok >= 0 && tok < a.V;
+    if (!in && a.bad) *a.bad = 1;
+    a.lp[m] = in ? s.zx[m] - lse : __int_as_float(0x7fc00000);
+  }
   if (a.kk == 0) return;
   const int dst = a.topk_rows ? a.topk_rows[m] : m;
   const int nc = s.tiles * s.kk;
@@ -1170,11 +1246,11 @@ hipError_t controller_states_launch(int B, int d, const int* n_accept, const flo
 }
 
 hipError_t reward_keywords_launch(int B, int k, int d, const int* gen, int gen_stride, const int* gen_len,
-                                  const int* look, const int* upto, const int* kws, int n_kw, int normalize,
+                                  const int* look, const int* upto, int head, const int* kws, int n_kw, int normalize,
                                   float* reward, hipStream_t st) {
   if (B * k == 0) return hipSuccess;
-  reward_keywords_kernel<<<B * k, 256, 0, st>>>(k, d, gen, gen_stride, gen_len, look, upto, kws, n_kw, normalize,
-                                                reward);
+  reward_keywords_kernel<<<B * k, 256, 0, st>>>(k, d, gen, gen_stride, gen_len, look, upto, head, kws, n_kw,
+                                                normalize, reward);
   return hipGetLastError();
 }
 
@@ -1185,32 +1261,53 @@ hipError_t reward_linear_launch(int BK, const float* hidden, const float* w, int
 }
 
 hipError_t commit_heads_launch(int B, int k, int d, const int* look, const int* beam, const int* mask, int* stage,
-                               int stage_stride, int* gen, int gen_stride, int* gen_len, int* catch_tok,
-                               hipStream_t st) {
-  commit_heads_kernel<<<(B + 63) / 64, 64, 0, st>>>(B, k, d, look, beam, mask, stage, stage_stride, gen, gen_stride,
-                                                    gen_len, catch_tok);
+                               int stage_stride, hipStream_t st) {
+  commit_heads_kernel<<<(B + 63) / 64, 64, 0, st>>>(B, k, d, look, beam, mask, stage, stage_stride);
   return hipGetLastError();
 }
 
 hipError_t commit_launch(int B, int k, int d, int kk, const int* look, const int* beam, const int* n_accept,
-                         const int* rtk_ids, const float* rtk_lp, const int* res_ids, const float* res_lp,
-                         int* next_beams, float* next_head_lp, int* stage, int stage_stride, int* gen, int gen_stride,
-                         int* gen_len, int* catch_tok, hipStream_t st) {
+                         const int* rtk_ids, const float* rtk_lp, const int* res_ids, const float* res_lp, int* stage,
+                         int stage_stride, int tcap, hipStream_t st) {
   commit_kernel<<<(B + 63) / 64, 64, 0, st>>>(B, k, d, kk, look, beam, n_accept, rtk_ids, rtk_lp, res_ids, res_lp,
-                                              next_beams, next_head_lp, stage, stage_stride, gen, gen_stride, gen_len,
-                                              catch_tok);
+                                              stage, stage_stride, tcap);
+  return hipGetLastError();
+}
+
+hipError_t commit_prefix_launch(int B, int d, int kk, const int* look, const int* n_accept, const int* rtk_ids,
+                                const float* rtk_lp, int* stage, int stage_stride, int tcap, hipStream_t st) {
+  commit_prefix_kernel<<<(B + 63) / 64, 64, 0, st>>>(B, d, kk, look, n_accept, rtk_ids, rtk_lp, stage, stage_stride,
+                                                     tcap);
+  return hipGetLastError();
+}
+
+hipError_t commit_apply_launch(int B, const int* stage, int stage_stride, int tcap, int kk, int* gen, int gen_stride,
+                               int* gen_len, int* next_beams, float* next_head_lp, int* catch_tok, hipStream_t st) {
+  commit_apply_kernel<<<(B + 63) / 64, 64, 0, st>>>(B, stage, stage_stride, tcap, kk, gen, gen_stride, gen_len,
+                                                    next_beams, next_head_lp, catch_tok);
+  return hipGetLastError();
+}
+
+hipError_t prefix_tail_launch(int B, const int* gen, int gen_stride, const int* gen_len, const int* ptail,
+                              const int* Lp, int* Lm1, int* look, int look_stride, hipStream_t st) {
+  prefix_tail_kernel<<<(B + 63) / 64, 64, 0, st>>>(B, gen, gen_stride, gen_len, ptail, Lp, Lm1, look, look_stride);
+  return hipGetLastError();
+}
+
+hipError_t last_tokens_launch(int B, const int* tokens, int L, int* out, hipStream_t st) {
+  last_tokens_kernel<<<(B + 63) / 64, 64, 0, st>>>(B, tokens, L, out);
   return hipGetLastError();
 }
 
 hipError_t promote_launch(int B, int k, const KVPool& pool, int n_layers, const int* stage, int stage_stride, int dlim,
-                          const int* Lp, const int* ptable, int ptable_stride, const int* stable, int s_stride_b,
-                          int s_stride_i, int dtype, hipStream_t st) {
+                          int soff, const int* Lp, const int* ptable, int ptable_stride, const int* stable,
+                          int s_stride_b, int s_stride_i, int dtype, hipStream_t st) {
   dim3 grid(B, n_layers);
   if (dtype == 1)
-    promote_split_kernel<<<grid, 256, 0, st>>>(k, pool, n_layers, stage, stage_stride, dlim, Lp, ptable,
+    promote_split_kernel<<<grid, 256, 0, st>>>(k, pool, n_layers, stage, stage_stride, dlim, soff, Lp, ptable,
                                                 ptable_stride, stable, s_stride_b, s_stride_i);
   else
-    promote_kernel<float><<<grid, 256, 0, st>>>(k, pool, n_layers, stage, stage_stride, dlim, Lp, ptable,
+    promote_kernel<float><<<grid, 256, 0, st>>>(k, pool, n_layers, stage, stage_stride, dlim, soff, Lp, ptable,
                                                 ptable_stride, stable, s_stride_b, s_stride_i);
   return hipGetLastError();
 }

@@ -6,8 +6,10 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 #include <string>
+#include <unordered_set>
 #include <vector>
 
 #include "../../include/cdsl.h"
@@ -74,7 +76,10 @@ struct cdsl_prefix {
   int* table_dev = nullptr;    // device [B][pstride]
   int* gen = nullptr;          // device [B][gen_stride] emitted tokens
   int* gen_len = nullptr;      // device [B]
+  int* ptail = nullptr;        // device [B] last prompt token
+  int* Lm1 = nullptr;          // device [B] Lp - 1 (the passes that re-feed the last prefix token)
   int rolled_k = 0, rolled_d = 0;
+  int rolled_pfx = 0, verified_pfx = 0;   // the last rollout / verify started from the prefix itself
   int verified_k = 0, verified_d = 0, verified_kk = 0;
   const float* kept_logits = nullptr;   // draft logits of the last rollout (cdsl_rollout_keep)
   int verified_soft = 0;
@@ -100,6 +105,10 @@ struct cdsl_ctx {
   int* ids_dev = nullptr;      // device [max_B]
   int* catch_tok = nullptr;    // device [max_B]
   int* mask_dev = nullptr;     // device [max_B] (head-only commit mask)
+  int* bad = nullptr;          // device flag: a token id outside [0, V) was fed or gathered
+  int* bad_host = nullptr;     // pinned copy of it
+  int stage_tcap = 0;          // token capacity of a commit record
+  std::unordered_set<cdsl_prefix*> prefixes;
   int live_prefixes = 0;
   std::vector<void*> allocs;
   std::string err;
@@ -123,6 +132,27 @@ int fail(cdsl_ctx* c, int code, const std::string& msg) {
   g_err = msg;
   return code;
 }
+
+// Contexts and prefix handles alive, so that a call with a destroyed
+// context or a freed prefix is refused instead of touching freed memory.
+std::mutex g_live_mu;
+std::unordered_set<const cdsl_ctx*> g_live;
+
+bool ctx_live(const cdsl_ctx* c) {
+  std::lock_guard<std::mutex> g(g_live_mu);
+  return g_live.count(c) != 0;
+}
+
+#define CTX_CHECK(c)                                                                         \
+  do {                                                                                       \
+    if (!(c)) return fail(nullptr, CDSL_EINVAL, "null context");                             \
+    if (!ctx_live(c)) return fail(nullptr, CDSL_ESTATE, "unknown or destroyed context");     \
+  } while (0)
+
+#define PX_CHECK(c, px)                                                                      \
+  do {                                                                                       \
+    if ((px) && !(c)->prefixes.count(px)) return fail((c), CDSL_ESTATE, "unknown or freed prefix handle"); \
+  } while (0)
 
 #define CK(call)                                                                             \
   do {                                                                                       \
@@ -620,6 +650,7 @@ PassDesc base_pass(cdsl_ctx* c, cdsl_prefix* px) {
   p.sblocks = c->sblocks;
   p.s_stride_i = c->sblocks;
   p.s_stride_b = c->lim.max_k * c->sblocks;
+  p.bad = c->bad;
   return p;
 }
 
@@ -671,6 +702,39 @@ int guarded(cdsl_ctx* c, F&& f) {
 
 }  // namespace
 
+void destroy_ctx(cdsl_ctx* c);
+
+namespace {
+
+// Queue the read-back of the token-range flag; after the stream has been
+// synchronised, check_bad reports a token id outside [0, V) fed or gathered
+// since the last check as an invalid argument (and clears the flag).
+void queue_bad(cdsl_ctx* c) {
+  CK(hipMemcpyAsync(c->bad_host, c->bad, sizeof(int), hipMemcpyDeviceToHost, c->st));
+}
+
+void check_bad(cdsl_ctx* c) {
+  if (!*c->bad_host) return;
+  *c->bad_host = 0;
+  CK(fill_int_launch(c->bad, 0, 1, c->st));
+  g_err = "a token id outside [0, vocab) was passed since the last synchronising call";
+  throw Fail{CDSL_EINVAL};
+}
+
+// device buffers of a prefix handle (allocated by cdsl_prefill)
+void free_px_buffers(cdsl_ctx* c, cdsl_prefix* px) {
+  for (void* p : {(void*)px->Lp, (void*)px->table_dev, (void*)px->gen, (void*)px->gen_len, (void*)px->ptail,
+                  (void*)px->Lm1}) {
+    auto it = std::find(c->allocs.begin(), c->allocs.end(), p);
+    if (p && it != c->allocs.end()) {
+      (void)hipFree(p);
+      c->allocs.erase(it);
+    }
+  }
+}
+
+}  // namespace
+
 // ===========================================================================
 // C ABI
 // ===========================================================================
@@ -716,22 +780,30 @@ int cdsl_init(const cdsl_model* draft, const cdsl_model* target, const cdsl_limi
     for (int u = 0; u < l.max_batch; ++u) io[u] = u;
     c->iota = dev_alloc<int>(c, l.max_batch);
     CK(hipMemcpy(c->iota, io.data(), io.size() * sizeof(int), hipMemcpyHostToDevice));
-    c->stage_stride = 3 + l.max_d + 1;
+    c->stage_tcap = l.max_d + 1;
+    c->stage_stride = kStageHdr + c->stage_tcap + 2 * l.max_k;
     c->stage = dev_alloc<int>(c, (size_t)l.max_batch * c->stage_stride);
+    c->bad = dev_alloc<int>(c, 1);
+    CK(fill_int_launch(c->bad, 0, 1, c->st));
     c->ids_dev = dev_alloc<int>(c, l.max_batch);
     c->catch_tok = dev_alloc<int>(c, l.max_batch);
     c->mask_dev = dev_alloc<int>(c, l.max_batch);
     CK(hipHostMalloc((void**)&c->stage_host, (size_t)l.max_batch * c->stage_stride * sizeof(int), 0));
     CK(hipHostMalloc((void**)&c->table_host, (size_t)l.max_batch * c->pstride * sizeof(int), 0));
     CK(hipHostMalloc((void**)&c->ids_host, (size_t)l.max_batch * sizeof(int), 0));
+    CK(hipHostMalloc((void**)&c->bad_host, sizeof(int), 0));
     alloc_workspace(c);
     CK(hipStreamSynchronize(c->st));
     return CDSL_OK;
   });
   if (rc != CDSL_OK) {
     std::string msg = c->err;
-    cdsl_destroy(c);
+    destroy_ctx(c);
     return fail(nullptr, rc, msg);
+  }
+  {
+    std::lock_guard<std::mutex> g(g_live_mu);
+    g_live.insert(c);
   }
   *out = c;
   return CDSL_OK;
@@ -739,6 +811,17 @@ int cdsl_init(const cdsl_model* draft, const cdsl_model* target, const cdsl_limi
 
 int cdsl_destroy(cdsl_ctx* c) {
   if (!c) return CDSL_OK;
+  {
+    std::lock_guard<std::mutex> g(g_live_mu);
+    if (!g_live.erase(c)) return fail(nullptr, CDSL_ESTATE, "unknown or destroyed context");
+  }
+  destroy_ctx(c);
+  return CDSL_OK;
+}
+
+}  // extern "C"
+
+void destroy_ctx(cdsl_ctx* c) {
   if (c->st) (void)hipStreamSynchronize(c->st);
   else (void)hipDeviceSynchronize();
   for (auto& p : c->pend) {
@@ -750,18 +833,21 @@ int cdsl_destroy(cdsl_ctx* c) {
   if (c->stage_host) (void)hipHostFree(c->stage_host);
   if (c->table_host) (void)hipHostFree(c->table_host);
   if (c->ids_host) (void)hipHostFree(c->ids_host);
+  if (c->bad_host) (void)hipHostFree(c->bad_host);
+  for (cdsl_prefix* px : c->prefixes) delete px;
   delete c;
-  return CDSL_OK;
 }
 
+extern "C" {
+
 const char* cdsl_last_error(const cdsl_ctx* c) {
-  if (c) return c->err.c_str();
+  if (c && ctx_live(c)) return c->err.c_str();
   return g_err.c_str();
 }
 
 int cdsl_prefill(cdsl_ctx* c, const int32_t* tokens, int32_t B, int32_t L, int32_t k, cdsl_prefix** out,
                  int32_t* beams, float* head_lp) {
-  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  CTX_CHECK(c);
   if (!tokens || !out || !beams || !head_lp) return fail(c, CDSL_EINVAL, "null argument");
   if (B <= 0 || L <= 0 || k <= 0) return fail(c, CDSL_EINVAL, "B, L and k must be positive");
   if (B > c->lim.max_batch || L > c->lim.max_prompt || k > c->lim.max_k)
@@ -780,6 +866,8 @@ int cdsl_prefill(cdsl_ctx* c, const int32_t* tokens, int32_t B, int32_t L, int32
     px->table_dev = dev_alloc<int>(c, (size_t)B * c->pstride);
     px->gen = dev_alloc<int>(c, (size_t)B * c->lim.max_ctx);
     px->gen_len = dev_alloc<int>(c, B);
+    px->ptail = dev_alloc<int>(c, B);
+    px->Lm1 = dev_alloc<int>(c, B);
     for (int b = 0; b < B; ++b) ensure_blocks(c, px, b, L);
     upload_table(c, px);
     CK(fill_int_launch(px->Lp, 0, B, c->st));
@@ -798,6 +886,7 @@ int cdsl_prefill(cdsl_ctx* c, const int32_t* tokens, int32_t B, int32_t L, int32
       p.tok_stride = L;
       p.tok_off = 0;
       LogitArgs la{};
+      la.bad = c->bad;
       la.V = c->m[1].c.vocab;
       la.want_lse = 1;
       la.kk = k;
@@ -808,16 +897,22 @@ int cdsl_prefill(cdsl_ctx* c, const int32_t* tokens, int32_t B, int32_t L, int32
       run_pass(c, c->m[1], p, 0, 0, true, true, nullptr, true, nullptr, 0, &la);
     }
     CK(add_launch(B, nullptr, px->Lp, L, c->st));
+    CK(last_tokens_launch(B, tokens, L, px->ptail, c->st));
     for (int b = 0; b < B; ++b) px->len[b] = L;
+    queue_bad(c);
     CK(hipStreamSynchronize(c->st));
+    check_bad(c);
     return CDSL_OK;
   });
   if (rc != CDSL_OK) {
+    (void)hipStreamSynchronize(c->st);
     for (int blk : px->owned) c->free_blocks.push_back(blk);
+    free_px_buffers(c, px);
     delete px;
     return rc;
   }
   c->live_prefixes++;
+  c->prefixes.insert(px);
   *out = px;
   return CDSL_OK;
 }
@@ -830,11 +925,16 @@ namespace {
 
 // d sequential passes of the roller over all B*k beams; with keep, the
 // logits of pass j land in keep[(b*k + i)*d + j][V] instead of the workspace
+// pfx: Alg. 1's drafting loop from the prefix itself (k = 1, no beams):
+// pass 0 re-feeds the last prefix token at position Lp - 1 into suffix slot 0
+// (the pass sees the prefix minus that token), so its argmax is the draft's
+// greedy token at the end of the prefix.
 int rollout_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, int32_t d, int32_t roller,
-                 int32_t* lookaheads, float* keep) {
-  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+                 int32_t* lookaheads, float* keep, bool pfx = false) {
+  CTX_CHECK(c);
+  PX_CHECK(c, px);
   if (roller != 0 && roller != 1) return fail(c, CDSL_EINVAL, "roller must be 0 (draft) or 1 (target)");
-  if (!px || !beams || !lookaheads) return fail(c, CDSL_EINVAL, "null argument");
+  if (!px || (!beams && !pfx) || !lookaheads) return fail(c, CDSL_EINVAL, "null argument");
   if (k <= 0 || d <= 0) return fail(c, CDSL_EINVAL, "k and d must be positive");
   if (k > c->lim.max_k || d > c->lim.max_d) return fail(c, CDSL_ERANGE, "k or d beyond the limits");
   if (max_len(px) + d + 1 > c->lim.max_ctx) return fail(c, CDSL_ERANGE, "context would exceed max_ctx");
@@ -842,10 +942,15 @@ int rollout_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, 
   if (keep && (long long)d * V > INT32_MAX) return fail(c, CDSL_ERANGE, "d * vocab too large for the kept logits");
   return guarded(c, [&]() {
     const int B = px->B;
-    CK(heads_to_lookaheads_launch(B * k, d, beams, lookaheads, c->st));
+    if (pfx)
+      CK(prefix_tail_launch(B, px->gen, c->lim.max_ctx, px->gen_len, px->ptail, px->Lp, px->Lm1, lookaheads, d + 1,
+                            c->st));
+    else
+      CK(heads_to_lookaheads_launch(B * k, d, beams, lookaheads, c->st));
     const int Lmax = max_len(px);
     for (int j0 = 0; j0 < d; ++j0) {
       PassDesc p = base_pass(c, px);
+      if (pfx) p.Lp = px->Lm1;
       p.mode = kSuffix;
       p.nb = B;
       p.kp = k;
@@ -856,6 +961,7 @@ int rollout_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, 
       p.tok_off = j0;
       float* dst = keep ? keep + (long long)j0 * V : nullptr;
       LogitArgs la{};
+      la.bad = c->bad;
       la.V = V;
       la.want_lse = 0;
       la.kk = 0;
@@ -876,7 +982,9 @@ int rollout_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, 
     }
     px->rolled_k = k;
     px->rolled_d = d;
+    px->rolled_pfx = pfx ? 1 : 0;
     px->verified_k = px->verified_d = 0;
+    px->verified_pfx = 0;
     px->kept_logits = keep;
     return CDSL_OK;
   });
@@ -891,8 +999,13 @@ int cdsl_rollout_with(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_
 
 int cdsl_rollout_keep(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, int32_t d, int32_t* lookaheads,
                       float* draft_logits) {
-  if (c && !draft_logits) return fail(c, CDSL_EINVAL, "null argument");
+  CTX_CHECK(c);
+  if (!draft_logits) return fail(c, CDSL_EINVAL, "null argument");
   return rollout_impl(c, px, beams, k, d, 0, lookaheads, draft_logits);
+}
+
+int cdsl_draft_prefix(cdsl_ctx* c, cdsl_prefix* px, int32_t d, int32_t* lookaheads, float* draft_logits) {
+  return rollout_impl(c, px, nullptr, 1, d, 0, lookaheads, draft_logits, true);
 }
 
 int cdsl_verify(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d, const float* head_lp,
@@ -913,12 +1026,16 @@ struct SoftArgs {
   float* res_lp;               // [B, k, d]
 };
 
+// pfx: Alg. 1's verification of a lookahead drafted from the prefix (k = 1):
+// row 0 re-feeds the last prefix token at position Lp - 1, so row j gives
+// p_{j+1} = M_p(pfx + x_1..x_j); no head log-prob enters the score.
 int verify_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d, int32_t kk,
                 const float* head_lp, float* logprobs, int32_t* target_argmax, int32_t* n_accept, float* scores,
-                int32_t* row_topk_ids, float* row_topk_lp, float* hidden, const SoftArgs* soft) {
-  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+                int32_t* row_topk_ids, float* row_topk_lp, float* hidden, const SoftArgs* soft, bool pfx = false) {
+  CTX_CHECK(c);
+  PX_CHECK(c, px);
   if (kk <= 0 || kk > c->lim.max_k) return fail(c, CDSL_ERANGE, "top-k width beyond the limits");
-  if (!px || !look || !head_lp || !logprobs || !target_argmax || !n_accept || !scores || !row_topk_ids ||
+  if (!px || !look || (!head_lp && !pfx) || !logprobs || !target_argmax || !n_accept || !scores || !row_topk_ids ||
       !row_topk_lp)
     return fail(c, CDSL_EINVAL, "null argument");
   if (k <= 0 || d <= 0) return fail(c, CDSL_EINVAL, "k and d must be positive");
@@ -928,12 +1045,15 @@ int verify_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, in
     if (!soft->draft_logits || !soft->u || !soft->v || !soft->draft_lp || !soft->res_ids || !soft->res_lp)
       return fail(c, CDSL_EINVAL, "null argument");
     if (c->m[0].c.vocab != c->m[1].c.vocab) return fail(c, CDSL_EINVAL, "soft rejection needs one vocabulary");
-    if (soft->draft_logits != px->kept_logits || px->rolled_k != k || px->rolled_d != d)
-      return fail(c, CDSL_ESTATE, "soft verification needs the logits of a cdsl_rollout_keep with the same k, d");
+    if (soft->draft_logits != px->kept_logits || px->rolled_k != k || px->rolled_d != d || px->rolled_pfx != (pfx ? 1 : 0))
+      return fail(c, CDSL_ESTATE, "soft verification needs the kept draft logits of the matching rollout (same k, d)");
   }
   return guarded(c, [&]() {
     const int B = px->B;
+    if (pfx)
+      CK(prefix_tail_launch(B, px->gen, c->lim.max_ctx, px->gen_len, px->ptail, px->Lp, px->Lm1, nullptr, 0, c->st));
     PassDesc p = base_pass(c, px);
+    if (pfx) p.Lp = px->Lm1;
     p.mode = kSuffix;
     p.nb = B;
     p.kp = k;
@@ -943,6 +1063,7 @@ int verify_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, in
     p.tok_stride = d + 1;
     p.tok_off = 0;
     LogitArgs la{};
+    la.bad = c->bad;
     la.V = c->m[1].c.vocab;
     la.want_lse = 1;
     la.kk = kk;
@@ -977,6 +1098,7 @@ int verify_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, in
     px->verified_d = d;
     px->verified_kk = kk;
     px->verified_soft = soft ? 1 : 0;
+    px->verified_pfx = pfx ? 1 : 0;
     return CDSL_OK;
   });
 }
@@ -999,28 +1121,57 @@ int cdsl_verify_soft(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t 
                      row_topk_lp, hidden, &sa);
 }
 
+int cdsl_verify_prefix(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t d, int32_t kk, float* logprobs,
+                       int32_t* target_argmax, int32_t* n_accept, float* scores, int32_t* row_topk_ids,
+                       float* row_topk_lp) {
+  return verify_impl(c, px, look, 1, d, kk, nullptr, logprobs, target_argmax, n_accept, scores, row_topk_ids,
+                     row_topk_lp, nullptr, nullptr, true);
+}
+
+int cdsl_verify_prefix_soft(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t d, int32_t kk,
+                            const float* draft_logits, const float* u, const float* v, float* logprobs,
+                            float* draft_lp, int32_t* target_argmax, int32_t* n_accept, float* scores,
+                            int32_t* row_topk_ids, float* row_topk_lp, int32_t* res_ids, float* res_lp) {
+  const SoftArgs sa{draft_logits, u, v, draft_lp, res_ids, res_lp};
+  return verify_impl(c, px, look, 1, d, kk, nullptr, logprobs, target_argmax, n_accept, scores, row_topk_ids,
+                     row_topk_lp, nullptr, &sa, true);
+}
+
 int cdsl_reward_keywords(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d,
                          const int32_t* keywords, int32_t n_kw, int32_t normalize, float* reward) {
   return cdsl_reward_keywords_upto(c, px, look, k, d, nullptr, keywords, n_kw, normalize, reward);
 }
 
-int cdsl_reward_keywords_upto(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d,
-                              const int32_t* upto, const int32_t* keywords, int32_t n_kw, int32_t normalize,
-                              float* reward) {
-  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+namespace {
+int reward_kw_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d, const int32_t* upto,
+                   int head, const int32_t* keywords, int32_t n_kw, int32_t normalize, float* reward) {
+  CTX_CHECK(c);
+  PX_CHECK(c, px);
   if (!px || !look || !keywords || !reward) return fail(c, CDSL_EINVAL, "null argument");
   if (k <= 0 || d <= 0 || n_kw <= 0 || n_kw > 64) return fail(c, CDSL_EINVAL, "bad k, d or n_kw (1..64)");
   return guarded(c, [&]() {
     Span sp(c, CDSL_K_STEP, 0.0, (double)px->B * k * (d + 1) * 4.0);
-    CK(reward_keywords_launch(px->B, k, d, px->gen, c->lim.max_ctx, px->gen_len, look, upto, keywords, n_kw, normalize,
-                              reward, c->st));
+    CK(reward_keywords_launch(px->B, k, d, px->gen, c->lim.max_ctx, px->gen_len, look, upto, head, keywords, n_kw,
+                              normalize, reward, c->st));
     return CDSL_OK;
   });
+}
+}  // namespace
+
+int cdsl_reward_keywords_upto(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d,
+                              const int32_t* upto, const int32_t* keywords, int32_t n_kw, int32_t normalize,
+                              float* reward) {
+  return reward_kw_impl(c, px, look, k, d, upto, 1, keywords, n_kw, normalize, reward);
+}
+
+int cdsl_reward_keywords_prefix(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t d, const int32_t* upto,
+                                const int32_t* keywords, int32_t n_kw, int32_t normalize, float* reward) {
+  return reward_kw_impl(c, px, look, 1, d, upto, 0, keywords, n_kw, normalize, reward);
 }
 
 int cdsl_reward_linear(cdsl_ctx* c, const float* hidden, const float* w, int32_t B, int32_t k, int32_t D,
                        float* reward) {
-  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  CTX_CHECK(c);
   if (!hidden || !w || !reward || B <= 0 || k <= 0 || D <= 0) return fail(c, CDSL_EINVAL, "bad argument");
   return guarded(c, [&]() {
     Span sp(c, CDSL_K_STEP, 2.0 * B * k * D, (double)B * k * D * 4.0);
@@ -1031,7 +1182,7 @@ int cdsl_reward_linear(cdsl_ctx* c, const float* hidden, const float* w, int32_t
 
 int cdsl_select(cdsl_ctx* c, const float* scores, const float* reward, float alpha, int32_t B, int32_t k,
                 int32_t* beam) {
-  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  CTX_CHECK(c);
   if (!scores || !reward || !beam || B <= 0 || k <= 0) return fail(c, CDSL_EINVAL, "bad argument");
   if (isnan(alpha) || (isinf(alpha) && alpha < 0)) return fail(c, CDSL_EINVAL, "alpha must be finite or +inf");
   return guarded(c, [&]() {
@@ -1044,7 +1195,7 @@ int cdsl_select(cdsl_ctx* c, const float* scores, const float* reward, float alp
 
 int cdsl_select_first(cdsl_ctx* c, const float* reward, const float* first_at, int32_t B, int32_t k,
                       int32_t* beam) {
-  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  CTX_CHECK(c);
   if (!reward || !first_at || !beam || B <= 0 || k <= 0) return fail(c, CDSL_EINVAL, "bad argument");
   return guarded(c, [&]() {
     Span sp(c, CDSL_K_STEP, 0.0, (double)B * (k * 4.0 + 8.0));
@@ -1055,7 +1206,7 @@ int cdsl_select_first(cdsl_ctx* c, const float* reward, const float* first_at, i
 
 int cdsl_controller_states(cdsl_ctx* c, const int32_t* n_accept, const float* reward, int32_t B, int32_t d,
                            double a_t, double r_t, int32_t b, int32_t* state, float* first_at) {
-  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  CTX_CHECK(c);
   if (!n_accept || !reward || !state || !first_at || B <= 0 || d <= 0) return fail(c, CDSL_EINVAL, "bad argument");
   if (b != 0 && b != 1) return fail(c, CDSL_EINVAL, "b must be 0 or 1");
   if (isnan(a_t) || isnan(r_t)) return fail(c, CDSL_EINVAL, "thresholds must not be NaN");
@@ -1077,80 +1228,115 @@ namespace {
 int commit_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, const int32_t* n_accept,
                 const int32_t* rtk_ids, const float* rtk_lp, const int32_t* res_ids, const float* res_lp, int32_t k,
                 int32_t d, int32_t kk, int32_t* emitted_host, int32_t* n_emit_host, int32_t* next_beams,
-                float* next_head_lp);
+                float* next_head_lp, bool pfx);
 }  // namespace
 
 int cdsl_commit_kk(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, const int32_t* n_accept,
                    const int32_t* rtk_ids, const float* rtk_lp, int32_t k, int32_t d, int32_t kk,
                    int32_t* emitted_host, int32_t* n_emit_host, int32_t* next_beams, float* next_head_lp) {
-  if (c && px && px->verified_soft)
+  CTX_CHECK(c);
+  PX_CHECK(c, px);
+  if (px && px->verified_soft)
     return fail(c, CDSL_ESTATE, "the last verification was soft: commit it with cdsl_commit_soft");
   return commit_impl(c, px, look, beam, n_accept, rtk_ids, rtk_lp, nullptr, nullptr, k, d, kk, emitted_host,
-                     n_emit_host, next_beams, next_head_lp);
+                     n_emit_host, next_beams, next_head_lp, false);
 }
 
 int cdsl_commit_soft(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, const int32_t* n_accept,
                      const int32_t* rtk_ids, const float* rtk_lp, const int32_t* res_ids, const float* res_lp,
                      int32_t k, int32_t d, int32_t kk, int32_t* emitted_host, int32_t* n_emit_host,
                      int32_t* next_beams, float* next_head_lp) {
-  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  CTX_CHECK(c);
+  PX_CHECK(c, px);
   if (!res_ids || !res_lp) return fail(c, CDSL_EINVAL, "null argument");
   if (px && !px->verified_soft) return fail(c, CDSL_ESTATE, "cdsl_commit_soft needs a cdsl_verify_soft");
   return commit_impl(c, px, look, beam, n_accept, rtk_ids, rtk_lp, res_ids, res_lp, k, d, kk, emitted_host,
-                     n_emit_host, next_beams, next_head_lp);
+                     n_emit_host, next_beams, next_head_lp, false);
+}
+
+int cdsl_commit_prefix(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* n_accept, int32_t d,
+                       int32_t kk, const int32_t* rtk_ids, const float* rtk_lp, int32_t* emitted_host,
+                       int32_t* n_emit_host, int32_t* next_beams, float* next_head_lp) {
+  CTX_CHECK(c);
+  PX_CHECK(c, px);
+  return commit_impl(c, px, look, nullptr, n_accept, rtk_ids, rtk_lp, nullptr, nullptr, 1, d, kk, emitted_host,
+                     n_emit_host, next_beams, next_head_lp, true);
 }
 
 namespace {
+// Beam commit (pfx false: emit [c_i*, x_i*,1..n], suffix slots 0..n hold
+// their KV) or Alg. 1 commit (pfx: emit x_1..x_n, slots 1..n hold their KV;
+// slot 0 re-fed the last prefix token).  The kernel only stages the
+// decisions; they are carried out once every prompt's record has passed the
+// host checks.  When the emitted tokens run past the rows the passes fed,
+// the last one is fed through both models as a catch-up row that yields the
+// next heads.
 int commit_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, const int32_t* n_accept,
                 const int32_t* rtk_ids, const float* rtk_lp, const int32_t* res_ids, const float* res_lp, int32_t k,
                 int32_t d, int32_t kk, int32_t* emitted_host, int32_t* n_emit_host, int32_t* next_beams,
-                float* next_head_lp) {
-  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
-  if (!px || !look || !beam || !n_accept || !rtk_ids || !rtk_lp || !emitted_host || !n_emit_host || !next_beams ||
-      !next_head_lp)
+                float* next_head_lp, bool pfx) {
+  if (!px || !look || (!beam && !pfx) || !n_accept || !rtk_ids || !rtk_lp || !emitted_host || !n_emit_host ||
+      !next_beams || !next_head_lp)
     return fail(c, CDSL_EINVAL, "null argument");
   if (px->rolled_k != k || px->rolled_d != d || px->verified_k != k || px->verified_d != d)
     return fail(c, CDSL_ESTATE, "commit needs a rollout and a verify with the same k and d");
+  if (px->rolled_pfx != (pfx ? 1 : 0) || px->verified_pfx != (pfx ? 1 : 0))
+    return fail(c, CDSL_ESTATE,
+                pfx ? "cdsl_commit_prefix needs cdsl_draft_prefix and a prefix verification"
+                    : "a beam commit needs a beam rollout and verification");
   if (px->verified_kk != kk) return fail(c, CDSL_ESTATE, "commit needs a verify with the same top-k width");
   return guarded(c, [&]() {
     const int B = px->B;
     {
-      Span sp(c, CDSL_K_STEP, 0.0, (double)B * (d + 1 + 2 * k) * 4.0);
-      CK(commit_launch(B, k, d, kk, look, beam, n_accept, rtk_ids, rtk_lp, res_ids, res_lp, next_beams, next_head_lp,
-                       c->stage, c->stage_stride, px->gen, c->lim.max_ctx, px->gen_len, c->catch_tok, c->st));
+      Span sp(c, CDSL_K_STEP, 0.0, (double)B * (d + 1 + 2 * kk) * 4.0);
+      if (pfx)
+        CK(commit_prefix_launch(B, d, kk, look, n_accept, rtk_ids, rtk_lp, c->stage, c->stage_stride, c->stage_tcap,
+                                c->st));
+      else
+        CK(commit_launch(B, k, d, kk, look, beam, n_accept, rtk_ids, rtk_lp, res_ids, res_lp, c->stage,
+                         c->stage_stride, c->stage_tcap, c->st));
     }
     CK(hipMemcpyAsync(c->stage_host, c->stage, (size_t)B * c->stage_stride * sizeof(int), hipMemcpyDeviceToHost,
                       c->st));
+    queue_bad(c);
     CK(hipStreamSynchronize(c->st));
     if (c->prof) harvest(c);
-    for (int b = 0; b < B; ++b)
-      if (c->stage_host[(size_t)b * c->stage_stride] < 0) {
-        g_err = "invalid beam index (NaN score or reward?) for prompt " + std::to_string(b);
+    check_bad(c);
+    const int dlim = pfx ? d - 1 : d;      // emitted tokens whose KV the passes wrote
+    for (int b = 0; b < B; ++b) {
+      const int ne = c->stage_host[(size_t)b * c->stage_stride];
+      if (ne < 0) {
+        g_err = pfx ? "n_accept out of [0, d] for prompt " + std::to_string(b)
+                    : "invalid beam index (NaN score or reward?) for prompt " + std::to_string(b);
         throw Fail{CDSL_EINVAL};
       }
-    int ncatch = 0;
-    for (int b = 0; b < B; ++b) {
-      const int* stg = c->stage_host + (size_t)b * c->stage_stride;
-      const int ne = stg[0];
-      const int cnt = std::min(ne, d);
-      const int newlen = px->len[b] + ne;
-      if (newlen > c->lim.max_ctx) {
+      if (px->len[b] + ne > c->lim.max_ctx) {
         g_err = "prompt " + std::to_string(b) + " exceeds max_ctx";
         throw Fail{CDSL_ERANGE};
       }
-      ensure_blocks(c, px, b, newlen);
-      (void)cnt;
+    }
+    int ncatch = 0;
+    for (int b = 0; b < B; ++b) {
+      const int* stg = c->stage_host + (size_t)b * c->stage_stride;
+      ensure_blocks(c, px, b, px->len[b] + stg[0]);
       if (stg[1]) c->ids_host[ncatch++] = b;
     }
     upload_table(c, px);
-    for (int mi = 0; mi < 2; ++mi) {
-      Model& md = c->m[mi];
-      Span sp(c, CDSL_K_STEP, 0.0, 0.0);
-      CK(promote_launch(B, k, md.pool, md.c.n_layers, c->stage, c->stage_stride, d, px->Lp, px->table_dev,
-                        c->pstride, c->stable, c->lim.max_k * c->sblocks, c->sblocks, md.c.dtype, c->st));
+    {
+      Span sp(c, CDSL_K_STEP, 0.0, (double)B * (d + 1 + 2 * kk) * 8.0);
+      CK(commit_apply_launch(B, c->stage, c->stage_stride, c->stage_tcap, kk, px->gen, c->lim.max_ctx, px->gen_len,
+                             next_beams, next_head_lp, c->catch_tok, c->st));
     }
-    CK(advance_launch(B, c->stage, c->stage_stride, d, px->Lp, c->st));
-    for (int b = 0; b < B; ++b) px->len[b] += std::min(c->stage_host[(size_t)b * c->stage_stride], d);
+    if (dlim > 0)
+      for (int mi = 0; mi < 2; ++mi) {
+        Model& md = c->m[mi];
+        Span sp(c, CDSL_K_STEP, 0.0, 0.0);
+        CK(promote_launch(B, k, md.pool, md.c.n_layers, c->stage, c->stage_stride, dlim, pfx ? 1 : 0, px->Lp,
+                          px->table_dev, c->pstride, c->stable, c->lim.max_k * c->sblocks, c->sblocks, md.c.dtype,
+                          c->st));
+      }
+    CK(advance_launch(B, c->stage, c->stage_stride, dlim, px->Lp, c->st));
+    for (int b = 0; b < B; ++b) px->len[b] += std::min(c->stage_host[(size_t)b * c->stage_stride], dlim);
     if (ncatch > 0) {
       CK(hipMemcpyAsync(c->ids_dev, c->ids_host, ncatch * sizeof(int), hipMemcpyHostToDevice, c->st));
       PassDesc p = base_pass(c, px);
@@ -1167,6 +1353,7 @@ int commit_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t
       long long sl = 0;
       for (int u = 0; u < ncatch; ++u) sl += px->len[c->ids_host[u]];
       LogitArgs la{};
+      la.bad = c->bad;
       la.V = c->m[1].c.vocab;
       la.want_lse = 1;
       la.kk = kk;
@@ -1178,12 +1365,14 @@ int commit_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t
       CK(add_launch(ncatch, c->ids_dev, px->Lp, 1, c->st));
       for (int u = 0; u < ncatch; ++u) px->len[c->ids_host[u]] += 1;
     }
+    const int width = pfx ? d : d + 1;
     for (int b = 0; b < B; ++b) {
       const int* stg = c->stage_host + (size_t)b * c->stage_stride;
       n_emit_host[b] = stg[0];
-      for (int t = 0; t <= d; ++t) emitted_host[(size_t)b * (d + 1) + t] = t < stg[0] ? stg[3 + t] : -1;
+      for (int t = 0; t < width; ++t) emitted_host[(size_t)b * width + t] = t < stg[0] ? stg[kStageHdr + t] : -1;
     }
     px->rolled_k = px->rolled_d = px->verified_k = px->verified_d = 0;
+    px->rolled_pfx = px->verified_pfx = 0;
     px->verified_soft = 0;
     px->kept_logits = nullptr;
     return CDSL_OK;
@@ -1194,37 +1383,41 @@ int commit_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t
 int cdsl_commit_heads(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, int32_t k, int32_t d,
                       int32_t kk, const int32_t* mask_host, int32_t* emitted_host, int32_t* next_beams,
                       float* next_head_lp) {
-  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  CTX_CHECK(c);
+  PX_CHECK(c, px);
   if (kk <= 0 || kk > c->lim.max_k) return fail(c, CDSL_ERANGE, "top-k width beyond the limits");
   if (!px || !look || !beam || !emitted_host || !next_beams || !next_head_lp)
     return fail(c, CDSL_EINVAL, "null argument");
-  if (px->rolled_k != k || px->rolled_d != d)
-    return fail(c, CDSL_ESTATE, "commit_heads needs a rollout with the same k and d");
+  if (px->rolled_k != k || px->rolled_d != d || px->rolled_pfx)
+    return fail(c, CDSL_ESTATE, "commit_heads needs a beam rollout with the same k and d");
   return guarded(c, [&]() {
     const int B = px->B;
     for (int b = 0; b < B; ++b) c->ids_host[b] = mask_host ? (mask_host[b] != 0) : 1;
     CK(hipMemcpyAsync(c->mask_dev, c->ids_host, (size_t)B * sizeof(int), hipMemcpyHostToDevice, c->st));
     {
       Span sp(c, CDSL_K_STEP, 0.0, (double)B * 16.0);
-      CK(commit_heads_launch(B, k, d, look, beam, c->mask_dev, c->stage, c->stage_stride, px->gen, c->lim.max_ctx,
-                             px->gen_len, c->catch_tok, c->st));
+      CK(commit_heads_launch(B, k, d, look, beam, c->mask_dev, c->stage, c->stage_stride, c->st));
     }
     CK(hipMemcpyAsync(c->stage_host, c->stage, (size_t)B * c->stage_stride * sizeof(int), hipMemcpyDeviceToHost,
                       c->st));
+    queue_bad(c);
     CK(hipStreamSynchronize(c->st));
     if (c->prof) harvest(c);
-    int n = 0;
+    check_bad(c);
     for (int b = 0; b < B; ++b) {
       const int* stg = c->stage_host + (size_t)b * c->stage_stride;
       if (stg[0] < 0) {
         g_err = "invalid beam index (NaN reward?) for prompt " + std::to_string(b);
         throw Fail{CDSL_EINVAL};
       }
-      if (stg[0] == 0) continue;
-      if (px->len[b] + 1 > c->lim.max_ctx) {
+      if (stg[0] > 0 && px->len[b] + 1 > c->lim.max_ctx) {
         g_err = "prompt " + std::to_string(b) + " exceeds max_ctx";
         throw Fail{CDSL_ERANGE};
       }
+    }
+    int n = 0;
+    for (int b = 0; b < B; ++b) {
+      if (c->stage_host[(size_t)b * c->stage_stride] == 0) continue;
       ensure_blocks(c, px, b, px->len[b] + 1);
       c->ids_host[n++] = b;
     }
@@ -1233,6 +1426,8 @@ int cdsl_commit_heads(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const i
       // (the rolled suffixes are dropped), and the target row gives the
       // next heads
       upload_table(c, px);
+      CK(commit_apply_launch(B, c->stage, c->stage_stride, c->stage_tcap, kk, px->gen, c->lim.max_ctx, px->gen_len,
+                             next_beams, next_head_lp, c->catch_tok, c->st));
       CK(hipMemcpyAsync(c->ids_dev, c->ids_host, n * sizeof(int), hipMemcpyHostToDevice, c->st));
       PassDesc p = base_pass(c, px);
       p.mode = kAppend;
@@ -1248,6 +1443,7 @@ int cdsl_commit_heads(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const i
       long long sl = 0;
       for (int u = 0; u < n; ++u) sl += px->len[c->ids_host[u]];
       LogitArgs la{};
+      la.bad = c->bad;
       la.V = c->m[1].c.vocab;
       la.want_lse = 1;
       la.kk = kk;
@@ -1261,9 +1457,10 @@ int cdsl_commit_heads(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const i
     }
     for (int b = 0; b < B; ++b) {
       const int* stg = c->stage_host + (size_t)b * c->stage_stride;
-      emitted_host[b] = stg[0] > 0 ? stg[3] : -1;
+      emitted_host[b] = stg[0] > 0 ? stg[kStageHdr] : -1;
     }
     px->rolled_k = px->rolled_d = px->verified_k = px->verified_d = 0;
+    px->rolled_pfx = px->verified_pfx = 0;
     px->verified_soft = 0;
     px->kept_logits = nullptr;
     return CDSL_OK;
@@ -1271,14 +1468,15 @@ int cdsl_commit_heads(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const i
 }
 
 int cdsl_prefix_lengths(cdsl_ctx* c, const cdsl_prefix* px, int32_t* lengths_host) {
-  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  CTX_CHECK(c);
   if (!px || !lengths_host) return fail(c, CDSL_EINVAL, "null argument");
+  PX_CHECK(c, const_cast<cdsl_prefix*>(px));
   for (int b = 0; b < px->B; ++b) lengths_host[b] = px->len[b];
   return CDSL_OK;
 }
 
 int cdsl_profile_enable(cdsl_ctx* c, int32_t enable) {
-  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  CTX_CHECK(c);
   return guarded(c, [&]() {
     CK(hipStreamSynchronize(c->st));
     harvest(c);
@@ -1289,7 +1487,7 @@ int cdsl_profile_enable(cdsl_ctx* c, int32_t enable) {
 }
 
 int cdsl_profile_read(cdsl_ctx* c, cdsl_kernel_stats* out) {
-  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  CTX_CHECK(c);
   if (!out) return fail(c, CDSL_EINVAL, "null argument");
   return guarded(c, [&]() {
     CK(hipStreamSynchronize(c->st));
@@ -1300,18 +1498,14 @@ int cdsl_profile_read(cdsl_ctx* c, cdsl_kernel_stats* out) {
 }
 
 int cdsl_free_prefix(cdsl_ctx* c, cdsl_prefix* px) {
-  if (!c) return fail(nullptr, CDSL_EINVAL, "null context");
+  CTX_CHECK(c);
   if (!px) return CDSL_OK;
+  PX_CHECK(c, px);
   return guarded(c, [&]() {
     CK(hipStreamSynchronize(c->st));
     for (int blk : px->owned) c->free_blocks.push_back(blk);
-    for (void* p : {(void*)px->Lp, (void*)px->table_dev, (void*)px->gen, (void*)px->gen_len}) {
-      auto it = std::find(c->allocs.begin(), c->allocs.end(), p);
-      if (it != c->allocs.end()) {
-        (void)hipFree(p);
-        c->allocs.erase(it);
-      }
-    }
+    free_px_buffers(c, px);
+    c->prefixes.erase(px);
     delete px;
     c->live_prefixes--;
     return CDSL_OK;

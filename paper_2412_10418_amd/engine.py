@@ -7,8 +7,9 @@ steady-state loop allocates nothing.
 Also the paper's baselines and its full controller on the same calls:
 ``head_step`` emits one token of lookahead-heuristic decoding (CDLH with the
 target as the roller, CDLH-appx. with the draft; Sec. 2.1, 3.1 and the
-appendix algorithm), and ``controller_step`` runs one iteration of Alg. 1
-(states S1 .. S4 of Sec. 3.2.3 with thresholds a_t, r_t and b <= 1).
+appendix algorithm), and ``controller_step`` runs one iteration of Alg. 1:
+lookaheads drafted from the prefix, then states S1 .. S4 of Sec. 3.2.3 with
+thresholds a_t, r_t and b <= 1.
 """
 from __future__ import annotations
 
@@ -174,11 +175,10 @@ class Engine:
             z = lambda *s, dt=torch.float32: torch.zeros(s, dtype=dt, device=dev)
             i32 = torch.int32
             self._bufs[key] = {
-                "look": z(B, 1, d + 1, dt=i32), "heads": z(B, 1, dt=i32), "head_lp": z(B, 1),
-                "verify": {"logprobs": z(B, 1, d), "target_argmax": z(B, 1, d, dt=i32),
-                           "n_accept": z(B, 1, dt=i32), "scores": z(B, 1),
-                           "row_topk_ids": z(B, 1, d, k, dt=i32), "row_topk_lp": z(B, 1, d, k), "hidden": None},
-                "reward": z(B, 1), "beam": z(B, dt=i32), "next_beams": z(B, k, dt=i32), "next_head_lp": z(B, k),
+                "look": z(B, d + 1, dt=i32),
+                "verify": {"logprobs": z(B, d), "target_argmax": z(B, d, dt=i32), "n_accept": z(B, dt=i32),
+                           "scores": z(B), "row_topk_ids": z(B, d, k, dt=i32), "row_topk_lp": z(B, d, k)},
+                "reward": z(B), "next_beams": z(B, k, dt=i32), "next_head_lp": z(B, k),
                 "state": z(B, dt=i32), "first_at": z(B)}
         return self._bufs[key]
 
@@ -187,8 +187,8 @@ class Engine:
         if key not in self._bufs:
             dev = self.device
             z = lambda *s, dt=torch.float32: torch.zeros(s, dtype=dt, device=dev)
-            self._bufs[key] = {"draft_logits": z(B, 1, d, self.wl.draft.vocab)}
-            cb["verify"].update(draft_lp=z(B, 1, d), res_ids=z(B, 1, d, dt=torch.int32), res_lp=z(B, 1, d))
+            self._bufs[key] = {"draft_logits": z(B, d, self.wl.draft.vocab)}
+            cb["verify"].update(draft_lp=z(B, d), res_ids=z(B, d, dt=torch.int32), res_lp=z(B, d))
         return self._bufs[key]
 
     def head_step(self, st: DecodeState, keywords: torch.Tensor, roller: int, k: Optional[int] = None,
@@ -222,17 +222,18 @@ class Engine:
 
     def controller_step(self, st: DecodeState, keywords: torch.Tensor, a_t: float, r_t: float, b: int,
                         k: Optional[int] = None, d: Optional[int] = None,
-                        normalize: Optional[bool] = None, u: Optional[torch.Tensor] = None,
-                        v: Optional[torch.Tensor] = None) -> dict:
-        """One iteration of Alg. 1 for every prompt, with the readings of the
-        oracle's ``controller_step``: draft d tokens after the target's greedy
-        head c (k = 1 rollout), verify them (top-k width k for the next
-        heads), a = n / d, r = R(generated + c + x_1..x_n); emit [c, x_1..x_n]
-        everywhere, then one more token (CDLH-appx., with Step-1 first for
-        b = 1) for the prompts not in S1.  With uniforms u and v ([B, 1, d]
-        device float32) the rejection loop is speculative sampling's test and
-        the residual draw at the rejected position heads the next candidates
-        (so Step-1 considers it first)."""
+                        normalize: Optional[bool] = None, u: Optional[torch.Tensor] = None) -> dict:
+        """One iteration of Alg. 1 for every prompt, as the oracle's
+        ``controller_step`` computes it: d draft tokens from the prefix
+        (cdsl_draft_prefix), their verification p_1..p_d, n accepted (hard
+        rejection, or speculative sampling's test with uniforms u [B, d]),
+        a = n / d, r = R(generated + x_1..x_n), the state, and the commit of
+        x_1..x_n.  Prompts not in S1 then take one more token with the k
+        candidates after x_1..x_n: Step-1's M_p greedy token when its draft
+        lookahead reaches r_t (S2/S3 with b = 1), else the CDLH-appx. token
+        (Step-2, S4).  b is 0 or 1 here."""
+        if not a_t > 0:
+            raise ValueError("a_t must be positive")
         if b not in (0, 1):
             raise ValueError("b must be 0 or 1")
         k = k or self.k
@@ -241,36 +242,26 @@ class Engine:
         cb = self._controller_buffers(B, k, d)
         c = self.ctx
         soft = u is not None
-        if soft and v is None:
-            raise ValueError("soft rejection takes both u and v")
         if normalize is None:
             normalize = self.wl.reward == "keyword_coverage"
-        cb["heads"].copy_(st.beams[:, :1])
-        cb["head_lp"].copy_(st.head_lp[:, :1])
+        ver = cb["verify"]
         if soft:
             sb = self._controller_soft_buffers(B, k, d, cb)
-            c.cdsl_rollout_keep(st.prefix, cb["heads"], 1, d, cb["look"], sb["draft_logits"])
-            c.cdsl_verify_soft(st.prefix, cb["look"], 1, d, cb["head_lp"], sb["draft_logits"], u, v, cb["verify"],
-                               kk=k)
+            c.cdsl_draft_prefix(st.prefix, d, cb["look"], sb["draft_logits"])
+            # the residual draws (at v = u) are computed by the soft test but
+            # play no part in Alg. 1
+            c.cdsl_verify_prefix(st.prefix, cb["look"], d, k, ver, sb["draft_logits"], u, u)
         else:
-            c.cdsl_rollout(st.prefix, cb["heads"], 1, d, cb["look"])
-            c.cdsl_verify(st.prefix, cb["look"], 1, d, cb["head_lp"], out=cb["verify"], kk=k)
-        c.cdsl_reward_keywords_upto(st.prefix, cb["look"], 1, d, cb["verify"]["n_accept"], keywords,
-                                    normalize=normalize, reward=cb["reward"])
-        c.cdsl_controller_states(cb["verify"]["n_accept"], cb["reward"], d, a_t, r_t, b, cb["state"], cb["first_at"])
-        if soft:
-            em = c.cdsl_commit_soft(st.prefix, cb["look"], cb["beam"], cb["verify"]["n_accept"],
-                                    cb["verify"]["row_topk_ids"], cb["verify"]["row_topk_lp"],
-                                    cb["verify"]["res_ids"], cb["verify"]["res_lp"], 1, d,
-                                    cb["next_beams"], cb["next_head_lp"])
-        else:
-            em, _, _ = c.cdsl_commit(st.prefix, cb["look"], cb["beam"], cb["verify"]["n_accept"],
-                                     cb["verify"]["row_topk_ids"], cb["verify"]["row_topk_lp"], 1, d,
-                                     cb["next_beams"], cb["next_head_lp"], kk=k)
-        # commit has synchronised the stream: these reads only copy
+            c.cdsl_draft_prefix(st.prefix, d, cb["look"])
+            c.cdsl_verify_prefix(st.prefix, cb["look"], d, k, ver)
+        c.cdsl_reward_keywords_prefix(st.prefix, cb["look"], d, ver["n_accept"], keywords, normalize, cb["reward"])
+        c.cdsl_controller_states(ver["n_accept"], cb["reward"], d, a_t, r_t, b, cb["state"], cb["first_at"])
+        em = c.cdsl_commit_prefix(st.prefix, cb["look"], ver["n_accept"], d, ver["row_topk_ids"],
+                                  ver["row_topk_lp"], cb["next_beams"], cb["next_head_lp"])
+        # the commit has synchronised the stream: these reads only copy
         codes = cb["state"].cpu().tolist()
-        n = cb["verify"]["n_accept"][:, 0].cpu().tolist()
-        r = cb["reward"][:, 0].cpu().tolist()
+        n = ver["n_accept"].cpu().tolist()
+        r = cb["reward"].cpu().tolist()
         states = [STATE_NAMES[x] for x in codes]
         for i in range(B):
             st.emitted[i].extend(em[i])
