@@ -21,8 +21,9 @@ enum {
   CDSL_EPI_RESIDUAL = 1   /* C[M,N] (fp32) += A * B^T  (residual add)   */
 };
 
-/* Bytes of workspace cdsl_op_gemm needs for this shape (split-K partial
- * tiles and their arrival counters); 0 if none. */
+/* Bytes of workspace cdsl_op_gemm needs for this shape: for bf16 weights
+ * the hi / lo planes of A, then the fp32 partial planes of a split K; 0 if
+ * none. */
 size_t cdsl_op_gemm_workspace(int32_t M, int32_t N, int32_t K, int32_t dtype);
 
 /* Dense projection C = A[M,K] * B[N,K]^T with fp32 accumulation: the
@@ -30,13 +31,29 @@ size_t cdsl_op_gemm_workspace(int32_t M, int32_t N, int32_t K, int32_t dtype);
  * LM head).  A (activations) is fp32; B (weights) is bf16 (dtype
  * CDSL_BF16: A is split into bf16 hi + lo halves, two MFMA products, so the
  * result keeps fp32-level accuracy) or fp32 (CDSL_F32); C is fp32.  K must
- * be a multiple of 32 for bf16 (16 for fp32).  The workspace
- * must hold cdsl_op_gemm_workspace(M, N, K, dtype) bytes and be zeroed once
- * before first use (its counters return to zero after every call).
- * Errors: EINVAL. */
+ * be a multiple of 32 for bf16 (16 for fp32).  The workspace must hold
+ * cdsl_op_gemm_workspace(M, N, K, dtype) bytes; every call writes what it
+ * reads there, so it needs no initial contents.  Errors: EINVAL. */
 int cdsl_op_gemm(const void* A, const void* B, float* C, int32_t M, int32_t N,
                  int32_t K, int32_t dtype, int32_t epilogue, void* workspace,
                  size_t workspace_bytes, void* stream);
+
+/* cdsl_op_gemm for callers that cannot allocate device memory (code under
+ * HIP graph capture, serving loops, harnesses that forbid allocation): the
+ * same kernels, with the workspace taken from a scratch array the library
+ * holds in device memory, CDSL_OP_GEMM_STATIC_BYTES (64 MiB) on each GPU it
+ * runs on, until the process ends.  No allocation happens in the call.
+ * Shapes whose cdsl_op_gemm_workspace exceeds that size are refused with
+ * ERANGE (for bf16 weights: 4 M K bytes of planes plus 4 S M N bytes of S
+ * K-split planes; e.g. M = 800 at N = K = 4096 needs 52 MB).  Every call on
+ * one GPU shares that GPU's array: calls that overlap on one GPU (two
+ * streams, two threads) race and must be serialised by the caller.  The
+ * first call on a device looks up that device's copy of the array.  Errors:
+ * EINVAL, ERANGE, EDEVICE. */
+#define CDSL_OP_GEMM_STATIC_BYTES (64u << 20)
+int cdsl_op_gemm_static(const void* A, const void* B, float* C, int32_t M,
+                        int32_t N, int32_t K, int32_t dtype, int32_t epilogue,
+                        void* stream);
 
 /* Row statistics of logits[M, V] (fp32), one pass per row, never writing
  * probabilities: for row m,

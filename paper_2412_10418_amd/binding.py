@@ -31,7 +31,7 @@ EXPORTS = [
     "cdsl_commit_prefix",
     "cdsl_prefix_lengths",
     "cdsl_free_prefix", "cdsl_destroy", "cdsl_last_error", "cdsl_profile_enable", "cdsl_profile_read",
-    "cdsl_op_gemm_workspace", "cdsl_op_gemm", "cdsl_op_logit_rows",
+    "cdsl_op_gemm_workspace", "cdsl_op_gemm", "cdsl_op_gemm_static", "cdsl_op_logit_rows",
 ]
 
 
@@ -114,6 +114,7 @@ def lib():
         "cdsl_profile_read": ([vp, C.POINTER(KernelStats)], i32),
         "cdsl_op_gemm_workspace": ([i32, i32, i32, i32], C.c_size_t),
         "cdsl_op_gemm": ([vp, vp, vp, i32, i32, i32, i32, i32, vp, C.c_size_t, vp], i32),
+        "cdsl_op_gemm_static": ([vp, vp, vp, i32, i32, i32, i32, i32, vp], i32),
         "cdsl_op_logit_rows": ([vp, i32, i32, vp, i32, vp, vp, vp, vp, vp], i32),
     }
     for name, (args, res) in sig.items():

@@ -1551,6 +1551,48 @@ int cdsl_op_gemm(const void* A, const void* B, float* C, int32_t M, int32_t N, i
   return CDSL_OK;
 }
 
+}  // extern "C"
+
+// The workspace of cdsl_op_gemm_static.  In host code `scratch` names a
+// host-side stand-in, not the device memory: its device address (one per
+// GPU) comes from hipGetSymbolAddress and only that address is passed on.
+namespace {
+static __device__ __align__(256) unsigned char scratch[CDSL_OP_GEMM_STATIC_BYTES];
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kScratchDevices] = {};
+}  // namespace
+
+extern "C" {
+
+int cdsl_op_gemm_static(const void* A, const void* B, float* C, int32_t M, int32_t N, int32_t K, int32_t dtype,
+                        int32_t epilogue, void* stream) {
+  if (!A || !B || !C) return fail(nullptr, CDSL_EINVAL, "null argument");
+  if (dtype != CDSL_F32 && dtype != CDSL_BF16) return fail(nullptr, CDSL_EINVAL, "bad dtype");
+  if (gemm_check(M, N, K, dtype) != 0) return fail(nullptr, CDSL_EINVAL, "unsupported shape");
+  const size_t need = cdsl_op_gemm_workspace(M, N, K, dtype);
+  if (need > CDSL_OP_GEMM_STATIC_BYTES)
+    return fail(nullptr, CDSL_ERANGE,
+                "shape needs " + std::to_string(need) + " bytes of workspace; the static scratch holds " +
+                    std::to_string((size_t)CDSL_OP_GEMM_STATIC_BYTES));
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(nullptr, CDSL_EDEVICE, hipGetErrorString(e));
+  if (dev < 0 || dev >= kScratchDevices) return fail(nullptr, CDSL_EDEVICE, "device index beyond the scratch table");
+  void* ws = nullptr;
+  {
+    std::lock_guard<std::mutex> g(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+      void* p = nullptr;
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (e != hipSuccess || !p) return fail(nullptr, CDSL_EDEVICE, "hipGetSymbolAddress of the scratch array failed");
+      g_scratch_dev[dev] = p;
+    }
+    ws = g_scratch_dev[dev];
+  }
+  return cdsl_op_gemm(A, B, C, M, N, K, dtype, epilogue, ws, CDSL_OP_GEMM_STATIC_BYTES, stream);
+}
+
 int cdsl_op_logit_rows(const float* logits, int32_t M, int32_t V, const int32_t* gather, int32_t kk, float* lp,
                        int32_t* amax, int32_t* topk_ids, float* topk_lp, void* stream) {
   if (!logits || M < 0 || V <= 0 || kk < 0 || kk > 16 || kk > V) return fail(nullptr, CDSL_EINVAL, "bad argument");
