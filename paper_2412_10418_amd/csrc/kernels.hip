@@ -4,6 +4,7 @@
 // the commit (emit, next beams, prefix promotion).
 #include <float.h>
 
+#include "block_pool.h"
 #include "common.h"
 #include "kernels.h"
 
@@ -983,11 +984,9 @@ __global__ __launch_bounds__(256) void promote_kernel(int k, KVPool pool, int n_
   for (int u = threadIdx.x; u < cnt * per_tok; u += 256) {
     const int t = u / per_tok, rem = u % per_tok;
     const int hh = rem / hd, dd = rem % hd;
-    const int sblk = stable[(long long)b * s_stride_b + i * s_stride_i + (t + soff) / kBlock];
-    const int sslot = (t + soff) % kBlock;
-    const int pos = L0 + t;
-    const int pblk = ptable[(long long)b * ptable_stride + pos / kBlock];
-    const int pslot = pos % kBlock;
+    const PromoteIndex ix = promote_index(stable + (long long)b * s_stride_b + i * s_stride_i,
+                                          ptable + (long long)b * ptable_stride, L0, t, soff);
+    const int sblk = ix.sblk, sslot = ix.sslot, pblk = ix.pblk, pslot = ix.pslot;
     kl[(((long long)pblk * Hkv + hh) * kBlock + pslot) * hd + dd] =
         kl[(((long long)sblk * Hkv + hh) * kBlock + sslot) * hd + dd];
     vl[(((long long)pblk * Hkv + hh) * hd + dd) * kBlock + pslot] =
@@ -1019,11 +1018,9 @@ __global__ __launch_bounds__(256) void promote_split_kernel(int k, KVPool pool, 
   for (int u = threadIdx.x; u < cnt * per_tok; u += 256) {
     const int t = u / per_tok, rem = u % per_tok;
     const int hh = rem / hd, dd = rem % hd;
-    const int sblk = stable[(long long)b * s_stride_b + i * s_stride_i + (t + soff) / kBlock];
-    const int sslot = (t + soff) % kBlock;
-    const int pos = L0 + t;
-    const int pblk = ptable[(long long)b * ptable_stride + pos / kBlock];
-    const int pslot = pos % kBlock;
+    const PromoteIndex ix = promote_index(stable + (long long)b * s_stride_b + i * s_stride_i,
+                                          ptable + (long long)b * ptable_stride, L0, t, soff);
+    const int sblk = ix.sblk, sslot = ix.sslot, pblk = ix.pblk, pslot = ix.pslot;
     const bf16* ks = kl + ((long long)sblk * Hkv + hh) * unit + (long long)sslot * hd + dd;
     bf16* kd = kl + ((long long)pblk * Hkv + hh) * unit + (long long)pslot * hd + dd;
     kd[0] = ks[0];

@@ -15,11 +15,14 @@
 #include "../../include/cdsl.h"
 #include "../../include/cdsl_ops.h"
 #include "attention.h"
+#include "block_pool.h"
 #include "common.h"
 #include "gemm.h"
 #include "kernels.h"
 
 using namespace cdsl;
+
+static_assert(kBlock == kPoolBlock, "KV blocks and the pool bookkeeping agree on the block size");
 
 namespace {
 
@@ -94,7 +97,7 @@ struct cdsl_ctx {
   int nblocks = 0;
   int pstride = 0;             // prefix blocks per prompt
   int sblocks = 0;             // suffix blocks per beam
-  std::vector<int> free_blocks;
+  BlockPool pool_blocks;       // free list of the prefix blocks
   int* stable = nullptr;       // device [max_B][max_k][sblocks]
   int* iota = nullptr;         // device [max_B] = 0..max_B-1
   int* stage = nullptr;        // device [max_B][stage_stride]
@@ -356,6 +359,13 @@ void alloc_pool(cdsl_ctx* c, Model& md) {
   md.pool.hd = md.hd;
   md.pool.layer_elems = per_layer;
   const size_t bytes = (size_t)per_layer * md.c.n_layers * sizeof(float);   // fp32 KV
+  size_t free_b = 0, total_b = 0;
+  CK(hipMemGetInfo(&free_b, &total_b));
+  if (2 * bytes > free_b) {
+    g_err = "the KV pool the limits ask for (" + std::to_string(2 * bytes) + " bytes) exceeds free device memory (" +
+            std::to_string(free_b) + " bytes)";
+    throw Fail{CDSL_ENOMEM};
+  }
   md.pool.k = dev_alloc_bytes(c, bytes);
   md.pool.v = dev_alloc_bytes(c, bytes);
   // zero once: stale slots are then always finite (masked weights are 0)
@@ -662,21 +672,14 @@ int max_len(const cdsl_prefix* px) {
 
 // make sure prompt b owns blocks for positions [0, new_len)
 void ensure_blocks(cdsl_ctx* c, cdsl_prefix* px, int b, int new_len) {
-  const int need = (new_len + kBlock - 1) / kBlock;
-  if (need > c->pstride) {
+  const int r = c->pool_blocks.ensure(px->table, px->owned, c->pstride, b, new_len);
+  if (r == BlockPool::kRange) {
     g_err = "prompt " + std::to_string(b) + " exceeds max_ctx";
     throw Fail{CDSL_ERANGE};
   }
-  for (int q = 0; q < need; ++q) {
-    int& slot = px->table[(size_t)b * c->pstride + q];
-    if (slot >= 0) continue;
-    if (c->free_blocks.empty()) {
-      g_err = "KV pool exhausted";
-      throw Fail{CDSL_ENOMEM};
-    }
-    slot = c->free_blocks.back();
-    c->free_blocks.pop_back();
-    px->owned.push_back(slot);
+  if (r == BlockPool::kExhausted) {
+    g_err = "KV pool exhausted";
+    throw Fail{CDSL_ENOMEM};
   }
 }
 
@@ -774,8 +777,7 @@ int cdsl_init(const cdsl_model* draft, const cdsl_model* target, const cdsl_limi
     for (int u = 0; u < suffix_blocks; ++u) st_ids[u] = u;
     c->stable = dev_alloc<int>(c, suffix_blocks);
     CK(hipMemcpy(c->stable, st_ids.data(), suffix_blocks * sizeof(int), hipMemcpyHostToDevice));
-    c->free_blocks.reserve(prefix_blocks);
-    for (int u = c->nblocks - 1; u >= suffix_blocks; --u) c->free_blocks.push_back(u);
+    c->pool_blocks.reset(suffix_blocks, c->nblocks);
     std::vector<int> io(l.max_batch);
     for (int u = 0; u < l.max_batch; ++u) io[u] = u;
     c->iota = dev_alloc<int>(c, l.max_batch);
@@ -906,7 +908,7 @@ int cdsl_prefill(cdsl_ctx* c, const int32_t* tokens, int32_t B, int32_t L, int32
   });
   if (rc != CDSL_OK) {
     (void)hipStreamSynchronize(c->st);
-    for (int blk : px->owned) c->free_blocks.push_back(blk);
+    c->pool_blocks.release(px->owned);
     free_px_buffers(c, px);
     delete px;
     return rc;
@@ -1503,7 +1505,7 @@ int cdsl_free_prefix(cdsl_ctx* c, cdsl_prefix* px) {
   PX_CHECK(c, px);
   return guarded(c, [&]() {
     CK(hipStreamSynchronize(c->st));
-    for (int blk : px->owned) c->free_blocks.push_back(blk);
+    c->pool_blocks.release(px->owned);
     free_px_buffers(c, px);
     c->prefixes.erase(px);
     delete px;

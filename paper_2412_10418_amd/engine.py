@@ -45,16 +45,18 @@ class DecodeState:
 
 class Engine:
     def __init__(self, workload, draft_w, target_w, max_steps: int, device="cuda",
-                 max_batch: Optional[int] = None, k: Optional[int] = None, d: Optional[int] = None):
+                 max_batch: Optional[int] = None, k: Optional[int] = None, d: Optional[int] = None,
+                 max_prompt: Optional[int] = None, max_prefixes: int = 1):
         wl = workload
         self.wl = wl
         self.k = k or wl.k
         self.d = d or wl.d
         self.device = device
         B = max_batch or wl.batch
-        limits = dict(max_batch=B, max_prompt=wl.prompt_len,
-                      max_ctx=wl.prompt_len + max_steps * (self.d + 1) + 2,
-                      max_k=self.k, max_d=self.d, max_prefixes=1)
+        mp = max_prompt or wl.prompt_len
+        limits = dict(max_batch=B, max_prompt=mp,
+                      max_ctx=max(mp, wl.prompt_len + max_steps * (self.d + 1) + 2),
+                      max_k=self.k, max_d=self.d, max_prefixes=max_prefixes)
         self.ctx = Context(wl.draft, draft_w, wl.target, target_w, wl.dtype, limits)
         self._bufs: Dict[tuple, StepBuffers] = {}
 

@@ -8,7 +8,7 @@ import torch
 
 import cdsl_inputs as ci
 import oracle
-from cdsl_harness import TOK_MARGIN, lp_tol, make_engine, make_setup, run_and_compare
+from cdsl_harness import TOK_MARGIN, assert_full_or_tie, lp_tol, make_engine, make_setup, run_and_compare
 
 pytestmark = pytest.mark.gpu
 
@@ -27,7 +27,7 @@ def test_tiny_fp32_eight_steps_match_oracle(tiny):
     st, reps = run_and_compare(tiny, B=3, steps=8, check_prompts=[0, 1, 2])
     for b, r in reps.items():
         print(f"prompt {b}: {r.steps_compared} steps, max |dlp| {r.max_lp_err:.2e}, stop: {r.stopped or '-'}")
-        assert r.steps_compared >= 6
+    assert_full_or_tie(reps, 8)
     lens = st.prefix.lengths()
     assert lens == [tiny.wl.prompt_len + len(e) for e in st.emitted]
     st.prefix.free()
@@ -36,7 +36,7 @@ def test_tiny_fp32_eight_steps_match_oracle(tiny):
 def test_tiny_alpha_infinity_and_zero(tiny):
     for alpha in (math.inf, 0.0):
         st, reps = run_and_compare(tiny, B=2, steps=3, check_prompts=[0, 1], alpha=alpha)
-        assert all(r.steps_compared >= 2 for r in reps.values())
+        assert_full_or_tie(reps, 3)
         st.prefix.free()
 
 
@@ -110,8 +110,7 @@ def test_draft_equal_to_target_accepts_all_and_catches_up():
     make_engine(s, B=2, max_steps=6)
     try:
         st, reps = run_and_compare(s, B=2, steps=4, check_prompts=[0, 1])
-        for r in reps.values():
-            assert r.steps_compared >= 3, r.stopped
+        assert_full_or_tie(reps, 4)
         assert all(len(e) >= 3 * (s.wl.d + 1) for e in st.emitted)
         st.prefix.free()
     finally:
@@ -123,7 +122,7 @@ def test_k1_is_greedy_decoding_of_target():
     make_engine(s, B=1, max_steps=10, k=1, d=3)
     try:
         st, reps = run_and_compare(s, B=1, steps=5, check_prompts=[0], k=1, d=3)
-        assert reps[0].steps_compared >= 4
+        assert_full_or_tie(reps, 5)
         # the oracle's k=1 result is itself pinned to greedy decoding
         seq = list(s.prompts(1)[0])
         from oracle.decoder import Decoder
@@ -184,7 +183,7 @@ def test_small_bf16_steps_match_oracle(small):
     st, reps = run_and_compare(small, B=8, steps=3, check_prompts=[0, 5])
     for b, r in reps.items():
         print(f"prompt {b}: {r.steps_compared} steps, max |dlp| {r.max_lp_err:.2e}, stop: {r.stopped or '-'}")
-        assert r.steps_compared >= 1
+    assert_full_or_tie(reps, 3)
     st.prefix.free()
 
 
@@ -208,6 +207,39 @@ def test_small_bf16_verify_on_oracle_lookaheads(small):
     st.prefix.free()
 
 
+@pytest.mark.timeout(900)
+def test_small_bf16_draft_equal_to_target_catches_up():
+    """bf16 with the 24-layer target as its own draft: the lookaheads are
+    accepted (n = d up to near ties between the rollout's and the
+    verification's rounding), so the commit promotes d rows of the hi / lo
+    KV planes and feeds x_d as the catch-up row through both models."""
+    s = make_setup("small", draft_is_target=True)
+    make_engine(s, B=2, max_steps=4)
+    try:
+        st, reps = run_and_compare(s, B=2, steps=2, check_prompts=[0])
+        for b, r in reps.items():
+            print(f"prompt {b}: {r.steps_compared} steps, max |dlp| {r.max_lp_err:.2e}, stop: {r.stopped or '-'}")
+        assert_full_or_tie(reps, 2)
+        assert len(st.emitted[0]) == 2 * (s.wl.d + 1) or reps[0].stopped
+        st.prefix.free()
+    finally:
+        s.engine.close()
+
+
+@pytest.mark.timeout(900)
+def test_small_bf16_k1_matches_oracle():
+    """bf16, one beam (k = 1): the step is greedy speculative decoding of the
+    target with no bonus token, compared with the oracle for 3 steps."""
+    s = make_setup("small")
+    make_engine(s, B=2, max_steps=4, k=1, d=5)
+    try:
+        st, reps = run_and_compare(s, B=2, steps=3, check_prompts=[1], k=1, d=5)
+        assert_full_or_tie(reps, 3)
+        st.prefix.free()
+    finally:
+        s.engine.close()
+
+
 def test_largest_k_and_d_match_oracle():
     """The largest beam count and lookahead depth the library takes (k = 16,
     d = 32: two suffix blocks per beam, 512 verified rows per prompt, top-16
@@ -218,12 +250,12 @@ def test_largest_k_and_d_match_oracle():
         st, reps = run_and_compare(s, B=2, steps=2, check_prompts=[0, 1], k=16, d=32)
         for b, r in reps.items():
             print(f"hard, prompt {b}: {r.steps_compared} steps, max |dlp| {r.max_lp_err:.2e}, stop: {r.stopped or '-'}")
-            assert r.steps_compared >= 1
+        assert_full_or_tie(reps, 2)
         st.prefix.free()
         st, reps = run_and_compare(s, B=2, steps=2, check_prompts=[0, 1], k=16, d=32, soft=True)
         for b, r in reps.items():
             print(f"soft, prompt {b}: {r.steps_compared} steps, stop: {r.stopped or '-'}")
-            assert r.steps_compared >= 1
+        assert_full_or_tie(reps, 2)
         st.prefix.free()
     finally:
         s.engine.close()
