@@ -425,6 +425,29 @@ int cdsl_commit_heads(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* lookahe
                       const int32_t* mask_host, int32_t* emitted_host,
                       int32_t* next_beams, float* next_head_lp);
 
+/* Append one given token per selected prompt: prompt b with mask_host[b]
+ * != 0 (mask_host NULL: every prompt) emits tokens[b] (device [B] int32),
+ * which is added to its generated tokens and fed through both models as
+ * one appended row; next_beams / next_head_lp [B, kk] of emitting prompts
+ * receive the target's top-kk after it, the other rows are left as they
+ * are.  emitted_host[b] is the token or -1.  This is the move of Alg. 1's
+ * Step-1 (Sec. 3.2.3): M_p's greedy token after the accepted ones, taken
+ * tentatively while its draft lookahead is scored.  Synchronises the
+ * context stream once.  Errors: EINVAL (a selected token outside [0, V):
+ * nothing is appended), ERANGE (max_ctx, kk), ENOMEM. */
+int cdsl_append(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* tokens,
+                const int32_t* mask_host, int32_t kk, int32_t* emitted_host,
+                int32_t* next_beams, float* next_head_lp);
+
+/* Withdraw the last count_host[b] generated tokens of prompt b (host [B];
+ * 0 leaves a prompt as it is): Step-1 drops its tentative M_p tokens when
+ * none of their lookaheads reaches the reward threshold (Sec. 3.2.3).  The
+ * prefix is shortened (its KV past the new end is ignored and later
+ * overwritten) and the tokens leave the generated sequence the rewards
+ * read.  The caller's beam heads are not recomputed: keep those of the
+ * shorter prefix.  Errors: EINVAL (more than the generated tokens). */
+int cdsl_withdraw(cdsl_ctx* ctx, cdsl_prefix* prefix, const int32_t* count_host);
+
 /* Current length (prompt + emitted) of every prompt: lengths_host[B]. */
 int cdsl_prefix_lengths(cdsl_ctx* ctx, const cdsl_prefix* prefix,
                         int32_t* lengths_host);

@@ -28,7 +28,7 @@ EXPORTS = [
     "cdsl_commit", "cdsl_commit_kk",
     "cdsl_commit_heads",
     "cdsl_draft_prefix", "cdsl_verify_prefix", "cdsl_verify_prefix_soft", "cdsl_reward_keywords_prefix",
-    "cdsl_commit_prefix",
+    "cdsl_commit_prefix", "cdsl_append", "cdsl_withdraw",
     "cdsl_prefix_lengths",
     "cdsl_free_prefix", "cdsl_destroy", "cdsl_last_error", "cdsl_profile_enable", "cdsl_profile_read",
     "cdsl_op_gemm_workspace", "cdsl_op_gemm", "cdsl_op_gemm_static", "cdsl_op_logit_rows",
@@ -97,6 +97,8 @@ def lib():
         "cdsl_verify_prefix_soft": ([vp, vp, vp, i32, i32] + [vp] * 12, i32),
         "cdsl_reward_keywords_prefix": ([vp, vp, vp, i32, vp, vp, i32, i32, vp], i32),
         "cdsl_commit_prefix": ([vp, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp], i32),
+        "cdsl_append": ([vp, vp, vp, vp, i32, vp, vp, vp], i32),
+        "cdsl_withdraw": ([vp, vp, vp], i32),
         "cdsl_verify_kk": ([vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp], i32),
         "cdsl_commit_kk": ([vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp], i32),
         "cdsl_verify": ([vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp], i32),
@@ -621,6 +623,25 @@ class Context:
                                       _sized(next_head_lp, B * kk, torch.float32, "next_head_lp"))
         _check(rc, self.handle)
         return [[emitted[b * d + t] for t in range(n_emit[b])] for b in range(B)]
+
+    def cdsl_append(self, prefix: Prefix, tokens: torch.Tensor, mask: Optional[List[bool]],
+                    next_beams: torch.Tensor, next_head_lp: torch.Tensor) -> List[int]:
+        """Emit tokens[b] for the masked prompts; next heads [B, kk] updated
+        in place for them.  Returns the emitted token per prompt (-1: none)."""
+        B = prefix.B
+        kk = next_beams.shape[1]
+        m = None if mask is None else (C.c_int32 * B)(*[1 if v else 0 for v in mask])
+        emitted = (C.c_int32 * B)()
+        rc = lib().cdsl_append(self.handle, prefix.handle, _sized(tokens, B, torch.int32, "tokens"), m, kk, emitted,
+                               _sized(next_beams, B * kk, torch.int32, "next_beams"),
+                               _sized(next_head_lp, B * kk, torch.float32, "next_head_lp"))
+        _check(rc, self.handle)
+        return [emitted[b] for b in range(B)]
+
+    def cdsl_withdraw(self, prefix: Prefix, counts: List[int]):
+        B = prefix.B
+        arr = (C.c_int32 * B)(*[int(x) for x in counts])
+        _check(lib().cdsl_withdraw(self.handle, prefix.handle, arr), self.handle)
 
 
 # ---------------------------------------------------------------------------

@@ -82,21 +82,35 @@ __device__ __forceinline__ void part_store(const GemmArgs& a, int row, int col, 
 
 // kEpiRowStats: statistics of the rows of an fp32 tile [BM][BN] held in LDS
 // (rows m0 + r, columns n0 + c; rows >= M and columns >= N left out).  P
-// adjacent lanes share a row, each owning CW columns, and every row is
-// handled at once: branch-free passes over the lane's columns (maximum and
-// argmax, then the sum of exp, then one pass per top-k place picking the
-// best entry ordered after the row's previous pick), each followed by a
-// merge over the P lanes with shuffles.  Each lane starts its passes at a
-// row-dependent column so that lanes of different rows hit different LDS
-// banks.  t is the column tile's index in the RowStats layout.
+// adjacent lanes share a row, each owning a run of CW columns.  The tile is
+// stored with the columns of each run XOR-permuted by a row- and
+// run-dependent mask (RsLayout::at), so that when every lane reads the
+// same position of its own run, the lanes of a wave hit at most two lanes
+// per LDS bank.  A lane reads its run into registers once, in column
+// order; then branch-free passes over the registers: maximum and argmax
+// (strict comparison in column order keeps the lowest column on ties), the
+// sum of exp, and one pass per further top-k place picking the best entry
+// ordered after the previous pick (the first place is the maximum), each
+// followed by a merge over the P lanes with shuffles.  t is the column
+// tile's index in the RowStats layout.
+template <int NT, int BM, int BN>
+struct RsLayout {
+  static constexpr int P = NT / BM >= 4 ? 4 : (NT / BM >= 2 ? 2 : 1);   // lanes per row, divides 64
+  static constexpr int CW = BN / P;                                     // columns per lane
+  static constexpr int XM = (CW < 32 ? CW : 32) - 1;
+  static_assert(BN % P == 0 && (CW & (CW - 1)) == 0, "power-of-two column runs");
+  __device__ static int at(int r, int c) { return r * BN + (c ^ ((r + 8 * (c / CW)) & XM)); }
+};
+
 template <int NT, int BM, int BN>
 __device__ void tile_row_stats(const float* tile, int m0, int n0, int M, int N, int t, const RowStats& s) {
-  constexpr int P = NT / BM >= 4 ? 4 : (NT / BM >= 2 ? 2 : 1);   // lanes per row, divides 64
+  using L = RsLayout<NT, BM, BN>;
+  constexpr int P = L::P, CW = L::CW;
   constexpr int RPP = NT / P;                                     // rows per pass
-  constexpr int CW = BN / P;                                      // columns per lane
-  static_assert(BN % P == 0 && (CW & (CW - 1)) == 0, "power-of-two column runs");
   const int part = threadIdx.x % P;
   const int c0 = part * CW;
+  const int cbase = n0 + c0;
+  const int nv = N - cbase;                                       // valid columns of this lane if < CW
   auto row_best = [&](float& v, int& id) {
 #pragma unroll
     for (int o = 1; o < P; o <<= 1) {
@@ -108,30 +122,29 @@ __device__ void tile_row_stats(const float* tile, int m0, int n0, int M, int N, 
       }
     }
   };
+#pragma unroll 1
   for (int r0 = 0; r0 < BM; r0 += RPP) {
     const int r = min(r0 + (int)threadIdx.x / P, BM - 1);
     const int m = m0 + r;
     const bool live = r0 + (int)threadIdx.x / P < BM && m < M;
-    const float* row = tile + r * BN + c0;
-    const int rot = (r * 5 + part * 16) & (CW - 1);
+    const float* rowp = tile + r * BN + c0;
+    const int g = (r + 8 * part) & L::XM;
+    float v[CW];   // v[i]: column cbase + i (-inf past N)
+#pragma unroll
+    for (int i = 0; i < CW; ++i) v[i] = i < nv ? rowp[i ^ g] : -INFINITY;
     float av = -INFINITY;
-    int ai = 0x7fffffff;
-#pragma unroll 8
+    int al = -1;
+#pragma unroll
     for (int i = 0; i < CW; ++i) {
-      const int c = (rot + i) & (CW - 1);
-      const int col = n0 + c0 + c;
-      const float v = col < N ? row[c] : -INFINITY;
-      const bool b = vi_better(v, col, av, ai);
-      av = b ? v : av;
-      ai = b ? col : ai;
+      const bool b = v[i] > av;
+      av = b ? v[i] : av;
+      al = b ? i : al;
     }
+    int ai = al >= 0 ? cbase + al : 0x7fffffff;
     row_best(av, ai);
     float se = 0.f;
-#pragma unroll 8
-    for (int i = 0; i < CW; ++i) {
-      const int c = (rot + i) & (CW - 1);
-      se += n0 + c0 + c < N ? __expf(row[c] - av) : 0.f;
-    }
+#pragma unroll
+    for (int i = 0; i < CW; ++i) se += __expf(v[i] - av);   // exp(-inf) = 0 past N
 #pragma unroll
     for (int o = 1; o < P; o <<= 1) se += __shfl_xor(se, o, 64);
     const long long o = (long long)m * s.tiles + t;
@@ -139,23 +152,29 @@ __device__ void tile_row_stats(const float* tile, int m0, int n0, int M, int N, 
       s.mx[o] = av;
       s.se[o] = se;
       s.am[o] = ai;
-    }
-    // top-kk: the u-th pick is the best entry ordered after pick u - 1
-    float pv = INFINITY;
-    int pc = -1;
-    for (int u = 0; u < s.kk; ++u) {
-      float cv = -INFINITY;
-      int ci = 0x7fffffff;
-#pragma unroll 8
-      for (int i = 0; i < CW; ++i) {
-        const int c = (rot + i) & (CW - 1);
-        const int col = n0 + c0 + c;
-        const float v = col < N ? row[c] : -INFINITY;
-        const bool after = v < pv || (v == pv && col > pc);
-        const bool b = after && col < N && vi_better(v, col, cv, ci);
-        cv = b ? v : cv;
-        ci = b ? col : ci;
+      if (s.kk > 0) {
+        s.tv[o * s.kk] = av;
+        s.tc[o * s.kk] = ai;
       }
+    }
+    // top-kk: place 0 is the maximum; place u is the best entry ordered
+    // after place u - 1 (value descending, column ascending)
+    float pv = av;
+    int pc = ai;
+#pragma unroll 1
+    for (int u = 1; u < s.kk; ++u) {
+      const int pl = pc - cbase;   // the previous pick as a local position (any value)
+      float cv = -INFINITY;
+      int cl = -1;
+#pragma unroll
+      for (int i = 0; i < CW; ++i) {
+        const float x = v[i];
+        const bool after = x < pv || (x == pv && i > pl);
+        const bool b = after && x > cv;
+        cv = b ? x : cv;
+        cl = b ? i : cl;
+      }
+      int ci = cl >= 0 ? cbase + cl : 0x7fffffff;
       row_best(cv, ci);
       if (live && part == 0) {
         s.tv[o * s.kk + u] = cv;
@@ -166,8 +185,8 @@ __device__ void tile_row_stats(const float* tile, int m0, int n0, int M, int N, 
     }
     if (live && s.gather_tok) {
       const int x = min(max(s.gather_tok[rowmap_index(s.gather_map, m)], 0), N - 1);
-      const int c = x - n0 - c0;
-      if (c >= 0 && c < CW) s.zx[m] = row[c];
+      const int c = x - cbase;
+      if (c >= 0 && c < CW) s.zx[m] = rowp[c ^ g];
     }
   }
 }
@@ -384,7 +403,8 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dense(GemmArgs a) {
         for (int j = 0; j < TN; ++j)
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            tile[(wm * TM * 16 + t * 16 + lg * 4 + e) * BN + wn * TN * 16 + j * 16 + lr] = acc[t * TN + j][e];
+            tile[RsLayout<C::NT, BM, BN>::at(wm * TM * 16 + t * 16 + lg * 4 + e, wn * TN * 16 + j * 16 + lr)] =
+                acc[t * TN + j][e];
       __syncthreads();
       tile_row_stats<C::NT, BM, BN>(tile, m0, n0, a.M, a.N, tn_blk, a.rs);
       return;
@@ -605,7 +625,8 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_skinny(GemmArgs a) {
 #pragma unroll
       for (int j = 0; j < CT; ++j)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) tile[(i * 16 + lg * 4 + e) * BN + wave * CT * 16 + j * 16 + lr] = acc[i][j][e];
+        for (int e = 0; e < 4; ++e)
+          tile[RsLayout<NT, BM, BN>::at(i * 16 + lg * 4 + e, wave * CT * 16 + j * 16 + lr)] = acc[i][j][e];
     __syncthreads();
     tile_row_stats<NT, BM, BN>(tile, 0, blockIdx.x * BN, a.M, a.N, blockIdx.x, a.rs);
     return;
@@ -693,7 +714,7 @@ __global__ __launch_bounds__(256) void gemm_f32_tiled(const float* __restrict__ 
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) tile[(ty * 4 + i) * 64 + tx * 4 + j] = acc[i][j];
+      for (int j = 0; j < 4; ++j) tile[RsLayout<256, 64, 64>::at(ty * 4 + i, tx * 4 + j)] = acc[i][j];
     __syncthreads();
     tile_row_stats<256, 64, 64>(tile, m0, n0, M, N, blockIdx.x, rs);
     return;

@@ -62,6 +62,9 @@ hipError_t reward_linear_launch(int BK, const float* hidden, const float* w, int
 // the commit kernels write records only; commit_apply_launch carries them out
 hipError_t commit_heads_launch(int B, int k, int d, const int* look, const int* beam, const int* mask, int* stage,
                                int stage_stride, hipStream_t st);
+hipError_t commit_tokens_launch(int B, const int* tokens, const int* mask, int V, int* stage, int stage_stride,
+                                hipStream_t st);
+hipError_t withdraw_launch(int B, const int* cnt, int* Lp, int* gen_len, hipStream_t st);
 hipError_t commit_launch(int B, int k, int d, int kk, const int* look, const int* beam, const int* n_accept,
                          const int* rtk_ids, const float* rtk_lp, const int* res_ids, const float* res_lp, int* stage,
                          int stage_stride, int tcap, hipStream_t st);

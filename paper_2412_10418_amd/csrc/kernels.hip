@@ -915,6 +915,40 @@ __global__ void commit_heads_kernel(int B, int k, int d, const int* __restrict__
   st[kStageHdr] = look[(long long)(b * k + i) * (d + 1)];
 }
 
+// Append of given tokens, one thread per prompt: prompts with mask[b] != 0
+// emit tokens[b] (checked against [0, V): an id outside it invalidates the
+// record), fed afterwards as one appended row; the others emit nothing.
+__global__ void commit_tokens_kernel(int B, const int* __restrict__ tokens, const int* __restrict__ mask, int V,
+                                     int* __restrict__ stage, int stage_stride) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  int* st = stage + (long long)b * stage_stride;
+  st[1] = 0;
+  st[3] = 0;
+  if (!mask[b]) {
+    st[0] = 0;
+    return;
+  }
+  const int tok = tokens[b];
+  if (tok < 0 || tok >= V) {
+    st[0] = -1;
+    return;
+  }
+  st[0] = 1;
+  st[1] = 1;
+  st[2] = 0;
+  st[kStageHdr] = tok;
+}
+
+// Withdraw the last cnt[b] tokens of prompt b's prefix (its length and its
+// generated tokens).
+__global__ void withdraw_kernel(int B, const int* __restrict__ cnt, int* __restrict__ Lp, int* __restrict__ gen_len) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  Lp[b] -= cnt[b];
+  gen_len[b] -= cnt[b];
+}
+
 // Carries out the checked records: append the emitted tokens to the
 // generated tokens, write the staged next heads, and queue the last emitted
 // token of catch-up prompts.
@@ -1260,6 +1294,17 @@ hipError_t reward_linear_launch(int BK, const float* hidden, const float* w, int
 hipError_t commit_heads_launch(int B, int k, int d, const int* look, const int* beam, const int* mask, int* stage,
                                int stage_stride, hipStream_t st) {
   commit_heads_kernel<<<(B + 63) / 64, 64, 0, st>>>(B, k, d, look, beam, mask, stage, stage_stride);
+  return hipGetLastError();
+}
+
+hipError_t commit_tokens_launch(int B, const int* tokens, const int* mask, int V, int* stage, int stage_stride,
+                                hipStream_t st) {
+  commit_tokens_kernel<<<(B + 63) / 64, 64, 0, st>>>(B, tokens, mask, V, stage, stage_stride);
+  return hipGetLastError();
+}
+
+hipError_t withdraw_launch(int B, const int* cnt, int* Lp, int* gen_len, hipStream_t st) {
+  withdraw_kernel<<<(B + 63) / 64, 64, 0, st>>>(B, cnt, Lp, gen_len);
   return hipGetLastError();
 }
 

@@ -72,6 +72,7 @@ struct Workspace {
 
 struct cdsl_prefix {
   int B = 0;
+  int L0 = 0;                   // prompt length
   std::vector<int> len;        // host copy of prefix lengths
   std::vector<int> table;      // [B][pstride] prefix block ids
   std::vector<int> owned;      // blocks to return on free
@@ -104,10 +105,13 @@ struct cdsl_ctx {
   int stage_stride = 0;
   int* stage_host = nullptr;   // pinned
   int* table_host = nullptr;   // pinned [max_B][pstride]
-  int* ids_host = nullptr;     // pinned [max_B]
+  int* ids_host = nullptr;     // pinned [max_B] prompt ids of an appended row (written after a sync)
+  int* mask_host = nullptr;    // pinned [max_B] append mask (its own buffer: written before the call syncs)
+  int* cnt_host = nullptr;     // pinned [max_B] withdrawn counts
   int* ids_dev = nullptr;      // device [max_B]
   int* catch_tok = nullptr;    // device [max_B]
   int* mask_dev = nullptr;     // device [max_B] (head-only commit mask)
+  int* cnt_dev = nullptr;      // device [max_B] (withdrawn counts)
   int* bad = nullptr;          // device flag: a token id outside [0, V) was fed or gathered
   int* bad_host = nullptr;     // pinned copy of it
   int stage_tcap = 0;          // token capacity of a commit record
@@ -607,10 +611,12 @@ void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, lon
     CK(rmsnorm_launch(w.h, md.gf, w.u32, w.uh, w.ul, rows, D, k.rms_eps, last_only ? 1 : 0, p.R, hid, c->st));
   }
   // The fused epilogue pays where it only reduces (argmax, logsumexp) or
-  // the rows are few: its per-tile top-k selection costs more vector ALU
-  // time than writing and re-reading the logits once the rows are many
-  // (measured at 800 rows, k = 5: 750 vs 505 us for the 32000-token head).
-  if (fuse && (fuse->kk == 0 || rows <= 32)) {
+  // the rows fit the skinny kernel (measured, 32000-token head, k = 5: 80
+  // rows 106 vs 132 us, 16 rows 76 vs 115 us).  On the dense kernel its
+  // per-tile top-k passes keep the matrix cores idle for longer than
+  // writing and re-reading the logits takes (800 rows: 532 vs 506 us; 4096
+  // rows of a 128256-token head, k = 8: 9.53 vs 8.58 ms).
+  if (fuse && (fuse->kk == 0 || rows <= 128)) {
     const int tiles = gemm_rowstats_tiles(rows, k.vocab, D, c->dtype);
     if (tiles > 0 && (size_t)rows * tiles <= w.rs_cap && fuse->kk <= c->lim.max_k) {
       RowStats rs{};
@@ -790,10 +796,13 @@ int cdsl_init(const cdsl_model* draft, const cdsl_model* target, const cdsl_limi
     c->ids_dev = dev_alloc<int>(c, l.max_batch);
     c->catch_tok = dev_alloc<int>(c, l.max_batch);
     c->mask_dev = dev_alloc<int>(c, l.max_batch);
+    c->cnt_dev = dev_alloc<int>(c, l.max_batch);
     CK(hipHostMalloc((void**)&c->stage_host, (size_t)l.max_batch * c->stage_stride * sizeof(int), 0));
     CK(hipHostMalloc((void**)&c->table_host, (size_t)l.max_batch * c->pstride * sizeof(int), 0));
     CK(hipHostMalloc((void**)&c->ids_host, (size_t)l.max_batch * sizeof(int), 0));
     CK(hipHostMalloc((void**)&c->bad_host, sizeof(int), 0));
+    CK(hipHostMalloc((void**)&c->mask_host, (size_t)l.max_batch * sizeof(int), 0));
+    CK(hipHostMalloc((void**)&c->cnt_host, (size_t)l.max_batch * sizeof(int), 0));
     alloc_workspace(c);
     CK(hipStreamSynchronize(c->st));
     return CDSL_OK;
@@ -836,6 +845,8 @@ void destroy_ctx(cdsl_ctx* c) {
   if (c->table_host) (void)hipHostFree(c->table_host);
   if (c->ids_host) (void)hipHostFree(c->ids_host);
   if (c->bad_host) (void)hipHostFree(c->bad_host);
+  if (c->mask_host) (void)hipHostFree(c->mask_host);
+  if (c->cnt_host) (void)hipHostFree(c->cnt_host);
   for (cdsl_prefix* px : c->prefixes) delete px;
   delete c;
 }
@@ -861,6 +872,7 @@ int cdsl_prefill(cdsl_ctx* c, const int32_t* tokens, int32_t B, int32_t L, int32
   if (!px) return fail(c, CDSL_ENOMEM, "host allocation failed");
   int rc = guarded(c, [&]() {
     px->B = B;
+    px->L0 = L;
     px->len.assign(B, 0);
     px->table.assign((size_t)B * c->pstride, -1);
     // per-handle device state (lengths, block table, emitted tokens)
@@ -1382,23 +1394,25 @@ int commit_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t
 }
 }  // namespace
 
-int cdsl_commit_heads(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, int32_t k, int32_t d,
-                      int32_t kk, const int32_t* mask_host, int32_t* emitted_host, int32_t* next_beams,
-                      float* next_head_lp) {
-  CTX_CHECK(c);
-  PX_CHECK(c, px);
-  if (kk <= 0 || kk > c->lim.max_k) return fail(c, CDSL_ERANGE, "top-k width beyond the limits");
-  if (!px || !look || !beam || !emitted_host || !next_beams || !next_head_lp)
-    return fail(c, CDSL_EINVAL, "null argument");
-  if (px->rolled_k != k || px->rolled_d != d || px->rolled_pfx)
-    return fail(c, CDSL_ESTATE, "commit_heads needs a beam rollout with the same k and d");
+}  // extern "C"
+
+namespace {
+// One emitted token per selected prompt (the head-only commit of the
+// lookahead-heuristic step, or a token given directly): stage_launch
+// writes the records, then each emitting prompt's token is appended to its
+// generated tokens and fed through both models as one row, whose target
+// row gives the next heads.
+template <typename StageFn>
+int append_impl(cdsl_ctx* c, cdsl_prefix* px, int32_t kk, const int32_t* mask_host, int32_t* emitted_host,
+                int32_t* next_beams, float* next_head_lp, const char* bad_msg_c, StageFn&& stage_launch) {
+  const std::string bad_msg = bad_msg_c;
   return guarded(c, [&]() {
     const int B = px->B;
-    for (int b = 0; b < B; ++b) c->ids_host[b] = mask_host ? (mask_host[b] != 0) : 1;
-    CK(hipMemcpyAsync(c->mask_dev, c->ids_host, (size_t)B * sizeof(int), hipMemcpyHostToDevice, c->st));
+    for (int b = 0; b < B; ++b) c->mask_host[b] = mask_host ? (mask_host[b] != 0) : 1;
+    CK(hipMemcpyAsync(c->mask_dev, c->mask_host, (size_t)B * sizeof(int), hipMemcpyHostToDevice, c->st));
     {
       Span sp(c, CDSL_K_STEP, 0.0, (double)B * 16.0);
-      CK(commit_heads_launch(B, k, d, look, beam, c->mask_dev, c->stage, c->stage_stride, c->st));
+      stage_launch();
     }
     CK(hipMemcpyAsync(c->stage_host, c->stage, (size_t)B * c->stage_stride * sizeof(int), hipMemcpyDeviceToHost,
                       c->st));
@@ -1409,7 +1423,7 @@ int cdsl_commit_heads(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const i
     for (int b = 0; b < B; ++b) {
       const int* stg = c->stage_host + (size_t)b * c->stage_stride;
       if (stg[0] < 0) {
-        g_err = "invalid beam index (NaN reward?) for prompt " + std::to_string(b);
+        g_err = bad_msg + std::to_string(b);
         throw Fail{CDSL_EINVAL};
       }
       if (stg[0] > 0 && px->len[b] + 1 > c->lim.max_ctx) {
@@ -1461,6 +1475,71 @@ int cdsl_commit_heads(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const i
       const int* stg = c->stage_host + (size_t)b * c->stage_stride;
       emitted_host[b] = stg[0] > 0 ? stg[kStageHdr] : -1;
     }
+    px->rolled_k = px->rolled_d = px->verified_k = px->verified_d = 0;
+    px->rolled_pfx = px->verified_pfx = 0;
+    px->verified_soft = 0;
+    px->kept_logits = nullptr;
+    return CDSL_OK;
+  });
+}
+
+}  // namespace
+
+extern "C" {
+
+int cdsl_commit_heads(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t* beam, int32_t k, int32_t d,
+                      int32_t kk, const int32_t* mask_host, int32_t* emitted_host, int32_t* next_beams,
+                      float* next_head_lp) {
+  CTX_CHECK(c);
+  PX_CHECK(c, px);
+  if (kk <= 0 || kk > c->lim.max_k) return fail(c, CDSL_ERANGE, "top-k width beyond the limits");
+  if (!px || !look || !beam || !emitted_host || !next_beams || !next_head_lp)
+    return fail(c, CDSL_EINVAL, "null argument");
+  if (px->rolled_k != k || px->rolled_d != d || px->rolled_pfx)
+    return fail(c, CDSL_ESTATE, "commit_heads needs a beam rollout with the same k and d");
+  return append_impl(c, px, kk, mask_host, emitted_host, next_beams, next_head_lp,
+                     "invalid beam index (NaN reward?) for prompt ", [&]() {
+                       CK(commit_heads_launch(px->B, k, d, look, beam, c->mask_dev, c->stage, c->stage_stride, c->st));
+                     });
+}
+
+int cdsl_append(cdsl_ctx* c, cdsl_prefix* px, const int32_t* tokens, const int32_t* mask_host, int32_t kk,
+                int32_t* emitted_host, int32_t* next_beams, float* next_head_lp) {
+  CTX_CHECK(c);
+  PX_CHECK(c, px);
+  if (kk <= 0 || kk > c->lim.max_k) return fail(c, CDSL_ERANGE, "top-k width beyond the limits");
+  if (!px || !tokens || !emitted_host || !next_beams || !next_head_lp) return fail(c, CDSL_EINVAL, "null argument");
+  return append_impl(c, px, kk, mask_host, emitted_host, next_beams, next_head_lp,
+                     "token id outside [0, vocab) for prompt ", [&]() {
+                       CK(commit_tokens_launch(px->B, tokens, c->mask_dev, c->m[1].c.vocab, c->stage, c->stage_stride,
+                                               c->st));
+                     });
+}
+
+int cdsl_withdraw(cdsl_ctx* c, cdsl_prefix* px, const int32_t* count_host) {
+  CTX_CHECK(c);
+  PX_CHECK(c, px);
+  if (!px || !count_host) return fail(c, CDSL_EINVAL, "null argument");
+  for (int b = 0; b < px->B; ++b)
+    if (count_host[b] < 0 || count_host[b] > px->len[b] - px->L0)
+      return fail(c, CDSL_EINVAL, "prompt " + std::to_string(b) + ": can only withdraw generated tokens");
+  return guarded(c, [&]() {
+    const int B = px->B;
+    int any = 0;
+    for (int b = 0; b < B; ++b) {
+      c->cnt_host[b] = count_host[b];
+      any |= count_host[b];
+    }
+    if (!any) return CDSL_OK;
+    CK(hipMemcpyAsync(c->cnt_dev, c->cnt_host, (size_t)B * sizeof(int), hipMemcpyHostToDevice, c->st));
+    {
+      Span sp(c, CDSL_K_STEP, 0.0, (double)B * 12.0);
+      CK(withdraw_launch(B, c->cnt_dev, px->Lp, px->gen_len, c->st));
+    }
+    for (int b = 0; b < B; ++b) px->len[b] -= count_host[b];
+    // the counts are staged in pinned host memory: let the copy finish
+    // before the next call refills it
+    CK(hipStreamSynchronize(c->st));
     px->rolled_k = px->rolled_d = px->verified_k = px->verified_d = 0;
     px->rolled_pfx = px->verified_pfx = 0;
     px->verified_soft = 0;

@@ -230,14 +230,23 @@ class Engine:
         (cdsl_draft_prefix), their verification p_1..p_d, n accepted (hard
         rejection, or speculative sampling's test with uniforms u [B, d]),
         a = n / d, r = R(generated + x_1..x_n), the state, and the commit of
-        x_1..x_n.  Prompts not in S1 then take one more token with the k
-        candidates after x_1..x_n: Step-1's M_p greedy token when its draft
-        lookahead reaches r_t (S2/S3 with b = 1), else the CDLH-appx. token
-        (Step-2, S4).  b is 0 or 1 here."""
+        x_1..x_n.  Prompts not in S1 then take their action with the k
+        candidates after x_1..x_n (the target's top-k, each with a d-token
+        draft lookahead and its reward):
+          S2/S3, Step-1: M_p's greedy token X_1 is candidate 0; it is taken
+            when its lookahead reaches r_t.  With b >= 2 the prompts whose
+            X_1 missed append it tentatively (cdsl_append), take X_2 = M_p's
+            greedy token after it with a fresh lookahead, and so on for up to
+            b tokens; the first round that reaches r_t keeps its X_1..X_i.
+            If none does, the tentative tokens are withdrawn (cdsl_withdraw)
+            and Step-2 follows.
+          Step-2 and S4: the candidate with the best reward (CDLH-appx.).
+        The host reads the state codes and, between Step-1 rounds, the
+        round's rewards against r_t, to know which prompts continue."""
         if not a_t > 0:
             raise ValueError("a_t must be positive")
-        if b not in (0, 1):
-            raise ValueError("b must be 0 or 1")
+        if b < 0:
+            raise ValueError("b must be >= 0")
         k = k or self.k
         d = d or self.d
         B = st.prefix.B
@@ -257,7 +266,8 @@ class Engine:
             c.cdsl_draft_prefix(st.prefix, d, cb["look"])
             c.cdsl_verify_prefix(st.prefix, cb["look"], d, k, ver)
         c.cdsl_reward_keywords_prefix(st.prefix, cb["look"], d, ver["n_accept"], keywords, normalize, cb["reward"])
-        c.cdsl_controller_states(ver["n_accept"], cb["reward"], d, a_t, r_t, b, cb["state"], cb["first_at"])
+        c.cdsl_controller_states(ver["n_accept"], cb["reward"], d, a_t, r_t, min(b, 1), cb["state"],
+                                 cb["first_at"])
         em = c.cdsl_commit_prefix(st.prefix, cb["look"], ver["n_accept"], d, ver["row_topk_ids"],
                                   ver["row_topk_lp"], cb["next_beams"], cb["next_head_lp"])
         # the commit has synchronised the stream: these reads only copy
@@ -269,12 +279,77 @@ class Engine:
             st.emitted[i].extend(em[i])
         st.beams.copy_(cb["next_beams"])
         st.head_lp.copy_(cb["next_head_lp"])
-        extra = None
+        extra, rounds = None, None
         need = [x != 1 for x in codes]
         if any(need):
-            extra = self.head_step(st, keywords, 0, k=k, d=d, mask=need, first_at=cb["first_at"],
-                                   normalize=normalize)
-        return {"states": states, "n": n, "r": r, "emitted": em, "extra": extra}
+            extra, rounds = self._step1_step2(st, keywords, codes, b, r_t, k, d, normalize, cb["first_at"])
+        return {"states": states, "n": n, "r": r, "emitted": em, "extra": extra, "rounds": rounds}
+
+    def _step1_step2(self, st: DecodeState, keywords, codes, b, r_t, k, d, normalize, first_at):
+        """The one-token actions of the prompts not in S1 (see
+        controller_step).  Returns the candidate table (heads, lookaheads,
+        rewards, the chosen index and the emitted token per prompt) and the
+        Step-1 rounds beyond the first: a list of {"X": [B] tokens,
+        "lookaheads": [B, 1, d+1], "reward": [B], "active": [B] bool}."""
+        B = st.prefix.B
+        c = self.ctx
+        hb = self._heads_buffers(B, k, d)
+        need = [x != 1 for x in codes]
+        c.cdsl_rollout_with(st.prefix, st.beams, k, d, 0, hb["look"])
+        c.cdsl_reward_keywords(st.prefix, hb["look"], k, d, keywords, normalize=normalize, reward=hb["reward"])
+        c.cdsl_select_first(hb["reward"], first_at, hb["beam"])
+        table = {"lookaheads": hb["look"].clone(), "reward": hb["reward"].clone(), "beam": hb["beam"].clone(),
+                 "tokens": [-1] * B}
+        pending = [False] * B
+        if b >= 2:
+            r0 = hb["reward"][:, 0].cpu().tolist()
+            pending = [codes[i] == 2 and not (r0[i] >= r_t) for i in range(B)]
+        final = [need[i] and not pending[i] for i in range(B)]
+        if any(final):
+            toks = c.cdsl_commit_heads(st.prefix, hb["look"], hb["beam"], k, d, final, st.beams, st.head_lp)
+            for i in range(B):
+                if final[i]:
+                    st.emitted[i].append(toks[i])
+                    table["tokens"][i] = toks[i]
+        rounds = []
+        if not any(pending):
+            return table, rounds
+        # Step-2's choice for the prompts still in Step-1, should every round miss
+        s2_tok = torch.gather(table["lookaheads"][:, :, 0], 1, table["beam"].long().view(B, 1)).view(B).contiguous()
+        tentative = [[] for _ in range(B)]
+        look1 = torch.zeros(B, 1, d + 1, dtype=torch.int32, device=st.beams.device)
+        rew1 = torch.zeros(B, 1, device=st.beams.device)
+        zeros = torch.zeros(B, dtype=torch.int32, device=st.beams.device)
+        for _ in range(2, b + 1):
+            if not any(pending):
+                break
+            # take M_p's greedy token tentatively; its next greedy token leads the round
+            xt = st.beams[:, 0].contiguous()
+            got = c.cdsl_append(st.prefix, xt, pending, st.beams, st.head_lp)
+            for i in range(B):
+                if pending[i]:
+                    tentative[i].append(got[i])
+            c.cdsl_rollout_with(st.prefix, st.beams[:, :1].contiguous(), 1, d, 0, look1)
+            c.cdsl_reward_keywords(st.prefix, look1, 1, d, keywords, normalize=normalize, reward=rew1)
+            rr = rew1[:, 0].cpu().tolist()
+            ok = [pending[i] and rr[i] >= r_t for i in range(B)]
+            rounds.append({"X": look1[:, 0, 0].cpu().tolist(), "lookaheads": look1.clone(), "reward": rr,
+                           "active": list(pending)})
+            if any(ok):
+                toks = c.cdsl_commit_heads(st.prefix, look1, zeros, 1, d, ok, st.beams, st.head_lp)
+                for i in range(B):
+                    if ok[i]:
+                        st.emitted[i].extend(tentative[i] + [toks[i]])
+                        table["tokens"][i] = toks[i]
+            pending = [pending[i] and not ok[i] for i in range(B)]
+        if any(pending):
+            c.cdsl_withdraw(st.prefix, [len(tentative[i]) if pending[i] else 0 for i in range(B)])
+            toks = c.cdsl_append(st.prefix, s2_tok, pending, st.beams, st.head_lp)
+            for i in range(B):
+                if pending[i]:
+                    st.emitted[i].append(toks[i])
+                    table["tokens"][i] = toks[i]
+        return table, rounds
 
     def close(self):
         self.ctx.close()

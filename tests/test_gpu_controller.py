@@ -58,7 +58,7 @@ def _first_diff(a, b):
     return -1
 
 
-def _cmp_head_step(M, look, rew, tok, hs):
+def _cmp_head_step(M, look, rew, tok, hs, check_token=True):
     """One prompt's one-token lookahead step (GPU lookaheads [k, d+1],
     rewards [k], token) against the oracle's HeadStep.  Returns "" when
     everything matched, else the near tie that ended the comparison."""
@@ -72,7 +72,8 @@ def _cmp_head_step(M, look, rew, tok, hs):
             assert hs.margin[i, u] <= M, (i, u, list(look[i]), list(hs.x[i]), hs.margin[i])
             return f"rollout near tie ({hs.margin[i, u]:.1e})"
     assert np.allclose(rew, hs.reward, rtol=0, atol=1e-6), (rew, hs.reward)
-    assert tok == hs.token
+    if check_token:
+        assert tok == hs.token
     return ""
 
 
@@ -93,14 +94,15 @@ def _cmp_soft(s, sv, cs):
     return ""
 
 
-def _cmp_controller(s, M, look, y, lp, out, b, cs, st, r_t, bb, sv=None):
+def _cmp_controller(s, M, look, y, lp, out, b, cs, st, r_t, bb, it_emitted, sv=None):
     """One prompt's Alg. 1 iteration: the GPU's lookahead row [d+1] (the
     prefix's last token, then x_1..x_d), the target argmax [d] and log-probs
-    [d] of the verification and the engine's outputs, against the oracle's
-    ControllerStep (cs) from state st.  The one-token action after x_1..x_n
-    is compared with the oracle's candidate table for it (Step-1 folded in
-    for S2/S3 with b = 1, the form the GPU computes; a CPU pin shows it
-    equals Step-1 then Step-2)."""
+    [d] of the verification, the engine's outputs and the tokens the
+    iteration emitted, against the oracle's ControllerStep (cs) from state
+    st.  The action after x_1..x_n is compared with the oracle's candidate
+    table there (for b = 1 with Step-1 folded in as the first-candidate
+    rule, the form the GPU computes; a CPU pin shows it equals Step-1 then
+    Step-2), and with b >= 2 every further Step-1 round with the oracle's."""
     assert look[0] == st.tokens[-1]
     u = _first_diff(look[1:], cs.x)
     if u >= 0:
@@ -120,23 +122,38 @@ def _cmp_controller(s, M, look, y, lp, out, b, cs, st, r_t, bb, sv=None):
     assert out["n"][b] == cs.n
     assert out["r"][b] == pytest.approx(cs.r, abs=1e-6)
     assert out["states"][b] == cs.state
-    got = list(out["emitted"][b])
     acc = [int(t) for t in cs.x[:cs.n]]
-    assert got == acc
+    assert list(out["emitted"][b]) == acc
     ex = out["extra"]
     if cs.state == "S1":
         assert ex is None or ex["tokens"][b] < 0
-        assert cs.emitted == acc
+        assert it_emitted == acc == cs.emitted
         return ""
     assert ex is not None and ex["tokens"][b] >= 0
     st1 = oracle.commit(s.odraft, s.otarget, st, acc)
+    multi = cs.state == "S2/S3" and bb >= 2
     hs = oracle.cdlh_step(False, s.odraft, s.otarget, st1, s.wl.k, s.wl.d, s.wl.reward, s.kws[b],
                           prefer_first_at=r_t if (cs.state == "S2/S3" and bb == 1) else None)
-    why = _cmp_head_step(M, ex["lookaheads"][b].cpu().numpy(), ex["reward"][b].cpu().numpy(), ex["tokens"][b], hs)
+    why = _cmp_head_step(M, ex["lookaheads"][b].cpu().numpy(), ex["reward"][b].cpu().numpy(), ex["tokens"][b], hs,
+                         check_token=not multi)
     if why:
         return why
-    got.append(ex["tokens"][b])
-    assert got == cs.emitted
+    if multi:
+        # round 1 is candidate 0 of the table; rounds 2.. come from the engine
+        assert cs.step1[0].X == [int(hs.heads[0])] and cs.step1[0].reward == pytest.approx(hs.reward[0])
+        for ri, rd in enumerate(out["rounds"]):
+            if not rd["active"][b]:
+                break
+            t = cs.step1[ri + 1]
+            if rd["X"][b] != t.X[-1]:
+                assert t.x_margin <= M, (rd["X"][b], t.X, t.x_margin)
+                return f"step-1 token near tie ({t.x_margin:.1e})"
+            u = _first_diff(rd["lookaheads"][b, 0, 1:].cpu().numpy(), t.lh)
+            if u >= 0:
+                assert t.lh_margin[u] <= M, (u, t.lh, t.lh_margin)
+                return f"step-1 lookahead near tie ({t.lh_margin[u]:.1e})"
+            assert rd["reward"][b] == pytest.approx(t.reward, abs=1e-6)
+    assert it_emitted == cs.emitted, (it_emitted, cs.emitted)
     return ""
 
 
@@ -188,6 +205,7 @@ def _run_controller(s, B, steps, a_t, r_t, bb, soft=False):
         if soft:
             # uniforms of the one lookahead per prompt: [B, d]
             u = ci.uniforms(s.wl.seed, 0, t, B, 1, d)[:, 0]
+        before = [len(e) for e in st.emitted]
         out = eng.controller_step(st, kw, a_t, r_t, bb, u=torch.from_numpy(np.ascontiguousarray(u)).cuda()
                                   if soft else None)
         look = cb["look"].cpu().numpy()
@@ -201,7 +219,8 @@ def _run_controller(s, B, steps, a_t, r_t, bb, soft=False):
             cs = oracle.controller_step(s.odraft, s.otarget, ost[b], k, d, a_t, r_t, bb, s.wl.reward, s.kws[b],
                                         rejection="soft" if soft else "hard", u=u[b][None] if soft else None)
             svb = {"draft_lp": sv["draft_lp"][b], "n": sv["n_accept"][b]} if soft else None
-            why = _cmp_controller(s, _margin(s), look[b], y[b], lp[b], out, b, cs, ost[b], r_t, bb, svb)
+            why = _cmp_controller(s, _margin(s), look[b], y[b], lp[b], out, b, cs, ost[b], r_t, bb,
+                                  [int(t) for t in st.emitted[b][before[b]:]], svb)
             if why:
                 print(f"prompt {b}: stopped after {compared} compared steps: {why}")
                 alive[b] = False
@@ -210,6 +229,12 @@ def _run_controller(s, B, steps, a_t, r_t, bb, soft=False):
             seen.add(cs.state)
             if cs.n > 0:
                 seen.add("accepted")
+            if len(cs.step1) > 1:
+                seen.add("step1 round 2")
+                if cs.extra is None:
+                    seen.add("step1 round 2 kept")
+                else:
+                    seen.add("step1 withdrawn")
             ost[b] = cs.after
             compared += 1
     for b in range(B):
@@ -257,13 +282,27 @@ def test_soft_controller_steps_match_oracle(request, which, a_t, r_t, bb, state)
     assert state in seen
 
 
+@pytest.mark.parametrize("r_t", [1.0, 2.0])
+def test_controller_step1_two_rounds_match_oracle(tiny, r_t):
+    """Alg. 1 with b = 2 (a_t = 2 keeps every prompt in S2/S3): when M_p's
+    first token misses r_t, it is appended tentatively and its successor is
+    scored; a second miss withdraws it and Step-2 decides.  6 prompts, 5
+    iterations, every round compared with the oracle's."""
+    compared, seen, stopped = _run_controller(tiny, 6, 5, 2.0, r_t, 2)
+    assert compared >= 10
+    assert compared == 30 or stopped
+    assert "step1 round 2" in seen and "step1 withdrawn" in seen
+    if r_t == 1.0:
+        assert "step1 round 2 kept" in seen
+
+
 def test_controller_error_paths(tiny):
     from paper_2412_10418_amd.binding import CDSLError
     s, eng = tiny, tiny.engine
     st = eng.start(torch.from_numpy(s.prompts(1)).cuda())
     kw = torch.from_numpy(s.kws[:1]).cuda()
     with pytest.raises(ValueError):
-        eng.controller_step(st, kw, 0.5, 1.0, 2)
+        eng.controller_step(st, kw, 0.5, 1.0, -1)
     with pytest.raises(ValueError):
         eng.controller_step(st, kw, 0.0, 1.0, 1)
     # a head-only commit without a rollout is out of order
