@@ -121,9 +121,12 @@ def roofline(stats, workload):
     traffic = tr["bytes_per_launch"] if tr else None
     if best in ("gemm_dense",):
         ach = st["flops"] / sec / 1e12
+        # the executed MFMA work is twice the algorithmic flops (the hi and
+        # lo products of the fp32 activations)
         return best, {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_MFMA_BF16_TFS, "unit": "TFLOP/s",
                       "frac": round(ach / PEAK_MFMA_BF16_TFS, 4), "traffic": traffic,
-                      "alg_flops_per_launch": round(st["flops"] / n), **extra}
+                      "alg_flops_per_launch": round(st["flops"] / n),
+                      "executed_frac": round(2.0 * ach / PEAK_MFMA_BF16_TFS, 4), **extra}
     ach = st["bytes"] / sec / 1e9
     return best, {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                   "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": traffic, **extra}
@@ -253,21 +256,33 @@ def summarize_profile(args):
 def phase_rooflines(wl, B, k, d, ms, sum_prefix):
     """Algorithmic rates of the rollout (HBM-bound: every draft forward
     streams the draft weights and the prefix KV of every prompt once) and of
-    the verification (MFMA-bound: 2 M flops per weight, M = B k d rows)."""
+    the verification (MFMA-bound: 2 M flops per weight, M = B k d rows).
+    The rollout's algorithmic bytes count the KV at bf16 width (2 bytes per
+    element, the layout the scope table prices); the library stores each KV
+    value as a bf16 hi + lo pair, so the bytes it actually streams count 4
+    (``rollout_stored_*``).  The verification's executed MFMA work is twice
+    its algorithmic flops (hi and lo products)."""
     dr, tg = wl.draft, wl.target
-    kv_tok = lambda m: m.n_layers * 2 * m.n_kv_heads * m.head_dim * 4.0   # fp32-equivalent K + V
-    ro_bytes = d * (dr.n_params(with_embeddings=False) * 2.0 + sum_prefix * kv_tok(dr))
+    kv_tok = lambda m, w: m.n_layers * 2 * m.n_kv_heads * m.head_dim * w   # K + V of one token
+    wbytes = dr.n_params(with_embeddings=False) * 2.0
+    ro_bytes = d * (wbytes + sum_prefix * kv_tok(dr, 2.0))
+    ro_stored = d * (wbytes + sum_prefix * kv_tok(dr, 4.0))
     ve_flops = 2.0 * B * k * d * tg.n_params(with_embeddings=False)
     out = {"rollout_ms": round(ms["rollout"], 3), "verify_ms": round(ms["verify"], 3),
            "tail_ms": round(ms["tail"], 3)}
     if ms["rollout"] > 0:
-        gbs = ro_bytes / (ms["rollout"] * 1e-3) / 1e9
+        sec = ms["rollout"] * 1e-3
+        gbs = ro_bytes / sec / 1e9
         out.update({"rollout_GB_per_s": round(gbs, 1), "rollout_hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
-                    "rollout_bytes": round(ro_bytes)})
+                    "rollout_bytes": round(ro_bytes),
+                    "rollout_stored_GB_per_s": round(ro_stored / sec / 1e9, 1),
+                    "rollout_stored_hbm_frac": round(ro_stored / sec / 1e9 / PEAK_HBM_GBS, 4),
+                    "rollout_stored_bytes": round(ro_stored)})
     if ms["verify"] > 0:
         tfs = ve_flops / (ms["verify"] * 1e-3) / 1e12
         out.update({"verify_TFLOP_per_s": round(tfs, 1), "verify_mfma_frac": round(tfs / PEAK_MFMA_BF16_TFS, 4),
-                    "verify_gemm_flops": round(ve_flops)})
+                    "verify_gemm_flops": round(ve_flops),
+                    "verify_executed_mfma_frac": round(2.0 * tfs / PEAK_MFMA_BF16_TFS, 4)})
     return out
 
 

@@ -86,7 +86,7 @@ enum { CDSL_F32 = 0, CDSL_BF16 = 1 };
 /* Shape of one Llama-style decoder: pre-norm RMSNorm, rotary embedding
  * (rotate-half pairing, 0-based positions), grouped-query attention,
  * SwiGLU MLP, no biases, untied LM head.  head_dim = d_model / n_heads and
- * must be 32, 64 or 128 (64 or 128 for CDSL_BF16). */
+ * must be 32, 64 or 128 (64 or 128 for CDSL_BF16); d_model <= 8192. */
 typedef struct cdsl_model_config {
   int32_t n_layers;
   int32_t d_model;

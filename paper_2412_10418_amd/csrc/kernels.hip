@@ -62,6 +62,10 @@ __global__ __launch_bounds__(256) void embed_rows(PassDesc p, const T* __restric
 // row is first completed: x[r] += sum of the planes in split order (the
 // same arithmetic as the split-K reduce), written back to x.  g == null
 // then only folds.
+// The row stays in registers between the two phases: float4 column groups
+// threadIdx.x + NT * u, u < kNormU (D <= 4 * NT * kNormU).
+constexpr int kNormU = 8;
+
 template <int NT>
 __global__ __launch_bounds__(NT) void rmsnorm_rows(float* __restrict__ x, const float* __restrict__ g,
                                                     float* __restrict__ out32, bf16* __restrict__ ohi,
@@ -72,41 +76,47 @@ __global__ __launch_bounds__(NT) void rmsnorm_rows(float* __restrict__ x, const 
   const int r = blockIdx.x;
   const int src = last_only ? r * R + (R - 1) : r;
   float* xr = x + (long long)src * D;
+  float4 v[kNormU];
   float ss = 0.f;
-  if (S > 0) {
-    // float4 columns; the planes are loaded eight at a time (independent
-    // loads in flight) and added in split order
-    const long long plane = (long long)rows * D;
-    const float* pr = part + (long long)src * D;
-    for (int c = threadIdx.x * 4; c < D; c += 4 * NT) {
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  const long long plane = (long long)rows * D;
+  const float* pr = part + (long long)src * D;
+#pragma unroll
+  for (int u = 0; u < kNormU; ++u) {
+    const int c = (threadIdx.x + NT * u) * 4;
+    v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (c >= D) continue;
+    if (S > 0) {
+      // the planes are loaded eight at a time (independent loads in flight)
+      // and added in split order
+      float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
       for (int z0 = 0; z0 < S; z0 += 8) {
         float4 t[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
-          t[u] = z0 + u < S ? *(const float4*)(pr + (z0 + u) * plane + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int e = 0; e < 8; ++e)
+          t[e] = z0 + e < S ? *(const float4*)(pr + (z0 + e) * plane + c) : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
-          if (z0 + u < S) {
-            v.x += t[u].x;
-            v.y += t[u].y;
-            v.z += t[u].z;
-            v.w += t[u].w;
+        for (int e = 0; e < 8; ++e)
+          if (z0 + e < S) {
+            a.x += t[e].x;
+            a.y += t[e].y;
+            a.z += t[e].z;
+            a.w += t[e].w;
           }
       }
       const float4 h = *(const float4*)(xr + c);
-      v.x += h.x;
-      v.y += h.y;
-      v.z += h.z;
-      v.w += h.w;
-      *(float4*)(xr + c) = v;
-      ss = fmaf(v.x, v.x, ss);
-      ss = fmaf(v.y, v.y, ss);
-      ss = fmaf(v.z, v.z, ss);
-      ss = fmaf(v.w, v.w, ss);
+      a.x += h.x;
+      a.y += h.y;
+      a.z += h.z;
+      a.w += h.w;
+      *(float4*)(xr + c) = a;
+      v[u] = a;
+    } else {
+      v[u] = *(const float4*)(xr + c);
     }
-  } else {
-    for (int c = threadIdx.x; c < D; c += NT) ss = fmaf(xr[c], xr[c], ss);
+    ss = fmaf(v[u].x, v[u].x, ss);
+    ss = fmaf(v[u].y, v[u].y, ss);
+    ss = fmaf(v[u].z, v[u].z, ss);
+    ss = fmaf(v[u].w, v[u].w, ss);
   }
   if (!g) return;
   ss = block_sum<NT / 64>(ss, sh);
@@ -114,17 +124,28 @@ __global__ __launch_bounds__(NT) void rmsnorm_rows(float* __restrict__ x, const 
   const long long o = (long long)r * D;
   const bool want_hid = hid && (last_only || (r % R) == R - 1);
   float* hr = want_hid ? hid + (long long)(last_only ? r : r / R) * D : nullptr;
-  for (int c = threadIdx.x; c < D; c += NT) {
-    const float v = xr[c] * inv * g[c];
+#pragma unroll
+  for (int u = 0; u < kNormU; ++u) {
+    const int c = (threadIdx.x + NT * u) * 4;
+    if (c >= D) continue;
+    const float4 gg = *(const float4*)(g + c);
+    const float4 y = make_float4(v[u].x * inv * gg.x, v[u].y * inv * gg.y, v[u].z * inv * gg.z, v[u].w * inv * gg.w);
     if (out32) {
-      out32[o + c] = v;
+      *(float4*)(out32 + o + c) = y;
     } else {
-      bf16 h, l;
-      split_bf16(v, h, l);
-      ohi[o + c] = h;
-      olo[o + c] = l;
+      bf16x4 h4, l4;
+      const float yy[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        bf16 h, l;
+        split_bf16(yy[e], h, l);
+        h4[e] = h;
+        l4[e] = l;
+      }
+      *(bf16x4*)(ohi + o + c) = h4;
+      *(bf16x4*)(olo + o + c) = l4;
     }
-    if (hr) hr[c] = v;
+    if (hr) *(float4*)(hr + c) = y;
   }
 }
 
@@ -316,17 +337,19 @@ __global__ __launch_bounds__(NT) void rope_kv_write_split(PassDesc p, const floa
     int blk, slot, pos;
     kv_slot(p, b, i, j, Lp, blk, slot, pos);
     const int n = min(p.R - j, kBlock - slot);   // rows of this block: slots [slot, slot + n)
+    // every row's load is issued before any is used (the rows are
+    // independent; one latency per block instead of one per row)
+    float vv[kBlock];
+#pragma unroll
+    for (int t = 0; t < kBlock; ++t) vv[t] = (t >= slot && t < slot + n) ? src.val(m0 + j + (t - slot), W, voff) : 0.f;
     bf16 vh[kBlock], vlo[kBlock];
 #pragma unroll
     for (int t = 0; t < kBlock; ++t) {
-      vh[t] = (bf16)0.f;
-      vlo[t] = (bf16)0.f;
-      if (t >= slot && t < slot + n) {
-        bf16 h, l;
-        split_bf16(src.val(m0 + j + (t - slot), W, voff), h, l);
-        vh[t] = h;
-        vlo[t] = l;
-      }
+      bf16 h, l;
+      split_bf16(vv[t], h, l);
+      const bool in = t >= slot && t < slot + n;
+      vh[t] = in ? h : (bf16)0.f;
+      vlo[t] = in ? l : (bf16)0.f;
     }
     bf16* row = vl + ((long long)blk * Hkv + hh) * unit + (long long)d * kBlock;
     // widest stores inside [slot, slot + n): whole 8-slot halves as 16 bytes,
@@ -1104,6 +1127,7 @@ hipError_t rmsnorm_launch(float* x, const float* g, float* out32, bf16* ohi, bf1
                           float eps, int last_only, int R, float* hid, hipStream_t st, const float* part, int S) {
   if (rows == 0) return hipSuccess;
   if (S > 0 && last_only) return hipErrorInvalidValue;
+  if (D % 4 != 0 || D > 4 * 256 * kNormU) return hipErrorInvalidValue;
   // few rows (the rollout): more threads per row keep more split planes'
   // loads in flight
   if (rows < 256)

@@ -269,6 +269,10 @@ bool cfg_ok(const cdsl_model_config& c, std::string& why) {
     why = "dtype must be CDSL_F32 or CDSL_BF16";
     return false;
   }
+  if (c.d_model > 8192) {
+    why = "d_model must be at most 8192";
+    return false;
+  }
   if (c.ffn_dim % 16 != 0) {
     why = "ffn_dim must be a multiple of 16";
     return false;
