@@ -50,6 +50,9 @@ def parse():
                     help="write a markdown summary of rocprofv3 runs of this script (kernel trace, FETCH_SIZE and "
                          "WRITE_SIZE passes with --calibrate-copy, optionally a MfmaUtil/LdsUtil pass) and exit; "
                          "no GPU needed")
+    ap.add_argument("--grid", default=None, metavar="K1,K2,..:D1,D2,..",
+                    help="measure every (k, d) point of the grid on one engine (a fresh prefill per point) and "
+                         "print one JSON line with a row per point instead of the bench line")
     ap.add_argument("--summary-out", default=None)
     ap.add_argument("--commands", default=None, help="text file with the exact profiling commands (for the summary)")
     return ap.parse_args()
@@ -405,6 +408,42 @@ def measure_methods(eng, wl, prompts, k, d, steps):
     return out
 
 
+def measure_grid(eng, wl, prompts, kw_t, rw_t, points, steps, warmup):
+    """Steps per second and lookahead tokens verified per second at each
+    (k, d) point, with the rollout / verification split (median over the
+    timed steps) and their algorithmic rates."""
+    import numpy as np
+    import torch
+    B = prompts.shape[0]
+    rows = []
+    for k, d in points:
+        st = eng.start(torch.from_numpy(prompts).cuda(), k=k)
+        for _ in range(warmup):
+            eng.step(st, keywords=kw_t, reward_w=rw_t, k=k, d=d)
+        torch.cuda.synchronize()
+        ph = {"rollout": [], "verify": [], "tail": []}
+        lens = []
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            lens.append(float(np.sum(st.prefix.lengths())))
+            marks = []
+            eng.step(st, keywords=kw_t, reward_w=rw_t, k=k, d=d, marks=marks)
+            ph["rollout"].append(marks)
+        torch.cuda.synchronize()
+        sec = time.perf_counter() - t0
+        med = {"rollout": float(np.median([m[0].elapsed_time(m[1]) for m in ph["rollout"]])),
+               "verify": float(np.median([m[1].elapsed_time(m[2]) for m in ph["rollout"]])),
+               "tail": float(np.median([m[2].elapsed_time(m[3]) for m in ph["rollout"]]))}
+        row = {"k": k, "d": d, "ms_per_step": round(sec * 1e3 / steps, 3),
+               "lookahead_tokens_per_s": round(B * k * d * steps / sec, 1),
+               "cdsl_steps_per_s": round(steps / sec, 2)}
+        row.update(phase_rooflines(wl, B, k, d, med, float(np.mean(lens))))
+        log(json.dumps(row))
+        rows.append(row)
+        st.prefix.free()
+    return rows
+
+
 def main():
     args = parse()
     if args.summarize_profile:
@@ -424,6 +463,11 @@ def main():
         wl = wl.with_(batch=args.batch)
     k = args.k or wl.k
     d = args.d or wl.d
+    points = None
+    if args.grid:
+        ks, ds = args.grid.split(":")
+        points = [(int(a), int(b)) for a in ks.split(",") for b in ds.split(",")]
+        k, d = max(p[0] for p in points), max(p[1] for p in points)
     B, L = wl.batch, wl.prompt_len
     torch.cuda.set_device(0)
     t0 = time.perf_counter()
@@ -446,6 +490,11 @@ def main():
     kw_t = torch.from_numpy(kws).cuda() if kws is not None else None
     rw_t = torch.from_numpy(rw).cuda() if rw is not None else None
 
+    if points:
+        grid = measure_grid(eng, wl, prompts, kw_t, rw_t, points, args.steps, args.warmup)
+        eng.close()
+        print(json.dumps({"workload": wl.name, "batch": B, "prompt_len": L, "grid": grid}), flush=True)
+        return
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     st = eng.start(torch.from_numpy(prompts).cuda(), k=k)
