@@ -832,18 +832,22 @@ Plan make_plan(int M, int N, int K, int dtype, bool no_split = false) {
     const int kc = d.kc;
     const int nk = K / kc;
     // One workgroup fits per CU.  Pick the K split s that minimises
-    // rounds(s) x stages(s) -- whole rounds of 256 workgroups, so a split
-    // that leaves the last round half empty is avoided -- plus the traffic
-    // of the s fp32 planes (written, then read by the fold), expressed in
-    // stage times (about 2 us per stage of this tile, ~5 TB/s for planes).
+    // rounds(s) x (stages(s) + 2) -- whole rounds of 256 workgroups, so a
+    // split that leaves the last round half empty is avoided, and each
+    // workgroup pays about two stages of prologue and epilogue -- plus the
+    // traffic of the s fp32 planes (written, then read by the fold),
+    // expressed in stage times (about 2 us per stage of this tile, ~5 TB/s
+    // for planes).  Splits keep at least two stages each: few row blocks
+    // (the draft rollout of more than 128 rows) would otherwise leave most
+    // CUs idle (the o projection at 160 rows: 8 tiles).
     int s = 1;
     double best = 1e300;
-    for (int c = 1; c <= 8 && c <= max(1, nk / 8); ++c) {
+    for (int c = 1; c <= 32 && c <= max(1, nk / 2); ++c) {
       const int per = (nk + c - 1) / c;
       const double rounds = (double)((tiles * c + 255) / 256);
       const double planes = c > 1 ? (c + 1.0) * M * N * 4.0 / 5e12 / 2e-6 : 0.0;
       // a split must gain more than 5% over the unsplit launch
-      const double t = (rounds * per + planes) * (c > 1 ? 1.05 : 1.0);
+      const double t = (rounds * (per + 2.0) + planes) * (c > 1 ? 1.05 : 1.0);
       if (t < best - 1e-9) {
         best = t;
         s = c;
