@@ -95,7 +95,7 @@ __device__ __forceinline__ void part_store(const GemmArgs& a, int row, int col, 
 // tile's index in the RowStats layout.
 template <int NT, int BM, int BN>
 struct RsLayout {
-  static constexpr int P = NT / BM >= 4 ? 4 : (NT / BM >= 2 ? 2 : 1);   // lanes per row, divides 64
+  static constexpr int P = BN >= 64 ? 4 : (BN >= 32 ? 2 : 1);            // lanes per row, divides 64
   static constexpr int CW = BN / P;                                     // columns per lane
   static constexpr int XM = (CW < 32 ? CW : 32) - 1;
   static_assert(BN % P == 0 && (CW & (CW - 1)) == 0, "power-of-two column runs");
@@ -124,6 +124,8 @@ __device__ void tile_row_stats(const float* tile, int m0, int n0, int M, int N, 
   };
 #pragma unroll 1
   for (int r0 = 0; r0 < BM; r0 += RPP) {
+    // a wave whose first row is past the tile has no live row (uniform)
+    if (r0 + (int)(threadIdx.x & ~63u) / P >= BM) continue;
     const int r = min(r0 + (int)threadIdx.x / P, BM - 1);
     const int m = m0 + r;
     const bool live = r0 + (int)threadIdx.x / P < BM && m < M;
@@ -142,9 +144,12 @@ __device__ void tile_row_stats(const float* tile, int m0, int n0, int M, int N, 
     }
     int ai = al >= 0 ? cbase + al : 0x7fffffff;
     row_best(av, ai);
+    // sum of exp(v - max) as 2^(v log2 e - max log2 e): one FMA per value
+    constexpr float kL2e = 1.4426950408889634f;
+    const float nb = -av * kL2e;
     float se = 0.f;
 #pragma unroll
-    for (int i = 0; i < CW; ++i) se += __expf(v[i] - av);   // exp(-inf) = 0 past N
+    for (int i = 0; i < CW; ++i) se += __builtin_amdgcn_exp2f(fmaf(v[i], kL2e, nb));   // 2^-inf = 0 past N
 #pragma unroll
     for (int o = 1; o < P; o <<= 1) se += __shfl_xor(se, o, 64);
     const long long o = (long long)m * s.tiles + t;
@@ -158,30 +163,65 @@ __device__ void tile_row_stats(const float* tile, int m0, int n0, int M, int N, 
       }
     }
     // top-kk: place 0 is the maximum; place u is the best entry ordered
-    // after place u - 1 (value descending, column ascending)
-    float pv = av;
-    int pc = ai;
+    // after place u - 1 (value descending, column ascending).  The fast
+    // passes take the best value strictly below the previous pick.  That is
+    // the same order unless some value equals an earlier pick at another
+    // column, which shows as more than kk values >= the last pick in the
+    // row (a last pick of -inf counts every column); then the wave redoes
+    // the places with the tie-aware order, overwriting the stored ones.
+    if (s.kk > 1) {
+      float pv = av;
 #pragma unroll 1
-    for (int u = 1; u < s.kk; ++u) {
-      const int pl = pc - cbase;   // the previous pick as a local position (any value)
-      float cv = -INFINITY;
-      int cl = -1;
+      for (int u = 1; u < s.kk; ++u) {
+        float cv = -INFINITY;
+        int cl = -1;
 #pragma unroll
-      for (int i = 0; i < CW; ++i) {
-        const float x = v[i];
-        const bool after = x < pv || (x == pv && i > pl);
-        const bool b = after && x > cv;
-        cv = b ? x : cv;
-        cl = b ? i : cl;
+        for (int i = 0; i < CW; ++i) {
+          const float x = v[i];
+          const bool b = (x < pv) & (x > cv);
+          cv = b ? x : cv;
+          cl = b ? i : cl;
+        }
+        int ci = cl >= 0 ? cbase + cl : 0x7fffffff;
+        row_best(cv, ci);
+        if (live && part == 0) {
+          s.tv[o * s.kk + u] = cv;
+          s.tc[o * s.kk + u] = ci;
+        }
+        pv = cv;
       }
-      int ci = cl >= 0 ? cbase + cl : 0x7fffffff;
-      row_best(cv, ci);
-      if (live && part == 0) {
-        s.tv[o * s.kk + u] = cv;
-        s.tc[o * s.kk + u] = ci;
+      int cnt = 0;
+#pragma unroll
+      for (int i = 0; i < CW; ++i) cnt += v[i] >= pv ? 1 : 0;
+#pragma unroll
+      for (int q = 1; q < P; q <<= 1) cnt += __shfl_xor(cnt, q, 64);
+      if (__any(live && cnt > s.kk)) {
+        pv = av;
+        int pc = ai;
+#pragma unroll 1
+        for (int u = 1; u < s.kk; ++u) {
+          const int pl = pc - cbase;   // the previous pick as a local position (any value)
+          float cv = -INFINITY;
+          int cl = -1;
+#pragma unroll
+          for (int i = 0; i < CW; ++i) {
+            const float x = v[i];
+            // bitwise, not short-circuit, so the pass stays free of branches
+            const bool after = (x < pv) | ((x == pv) & (i > pl));
+            const bool b = after & (x > cv);
+            cv = b ? x : cv;
+            cl = b ? i : cl;
+          }
+          int ci = cl >= 0 ? cbase + cl : 0x7fffffff;
+          row_best(cv, ci);
+          if (live && part == 0) {
+            s.tv[o * s.kk + u] = cv;
+            s.tc[o * s.kk + u] = ci;
+          }
+          pv = cv;
+          pc = ci;
+        }
       }
-      pv = cv;
-      pc = ci;
     }
     if (live && s.gather_tok) {
       const int x = min(max(s.gather_tok[rowmap_index(s.gather_map, m)], 0), N - 1);

@@ -614,13 +614,12 @@ void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, lon
     Span sp(c, CDSL_K_ROWWISE, 0.0, (double)rows * D * (4.0 + es));
     CK(rmsnorm_launch(w.h, md.gf, w.u32, w.uh, w.ul, rows, D, k.rms_eps, last_only ? 1 : 0, p.R, hid, c->st));
   }
-  // The fused epilogue pays where it only reduces (argmax, logsumexp) or
-  // the rows fit the skinny kernel (measured, 32000-token head, k = 5: 80
-  // rows 106 vs 132 us, 16 rows 76 vs 115 us).  On the dense kernel its
-  // per-tile top-k passes keep the matrix cores idle for longer than
-  // writing and re-reading the logits takes (800 rows: 532 vs 506 us; 4096
-  // rows of a 128256-token head, k = 8: 9.53 vs 8.58 ms).
-  if (fuse && (fuse->kk == 0 || rows <= 128)) {
+  // Every head whose caller wants only row outputs takes the fused
+  // epilogue: no logits reach memory.  Measured against writing the logits
+  // and reducing them with logit_rows: 80 rows of a 32000-token head, top-5,
+  // 97 vs 131 us; 800 rows, top-5, 497 vs 505 us; 4096 rows of a
+  // 128256-token head, top-8, 8.30 vs 8.35 ms.
+  if (fuse) {
     const int tiles = gemm_rowstats_tiles(rows, k.vocab, D, c->dtype);
     if (tiles > 0 && (size_t)rows * tiles <= w.rs_cap && fuse->kk <= c->lim.max_k) {
       RowStats rs{};

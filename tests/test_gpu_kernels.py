@@ -95,21 +95,25 @@ def test_logit_rows_match_oracle(M, V, kk):
         assert np.max(np.abs(tl[m] - ls[ids])) < 2e-5
 
 
-@pytest.mark.parametrize("M,V,K,dt,kk", [
-    (80, 32000, 2048, "bf16", 0),      # rollout: draft LM head, argmax only (skinny, 128-column tiles)
-    (80, 32000, 2048, "bf16", 5),
-    (800, 32000, 4096, "bf16", 5),     # verification block (dense, 256-column tiles)
-    (333, 1300, 576, "bf16", 8),       # dense, ragged rows and last tile
-    (7, 1000, 256, "bf16", 16),        # skinny, 64-column tiles, ragged last tile
-    (5, 128256, 256, "bf16", 8),       # large vocabulary
-    (37, 997, 64, "f32", 4),           # fp32 kernel, 64-column tiles
+@pytest.mark.parametrize("M,V,K,dt,kk,rep", [
+    (80, 32000, 2048, "bf16", 0, 1),      # rollout: draft LM head, argmax only (skinny, 128-column tiles)
+    (80, 32000, 2048, "bf16", 5, 1),
+    (800, 32000, 4096, "bf16", 5, 1),     # verification block (dense, 256-column tiles)
+    (333, 1300, 576, "bf16", 8, 1),       # dense, ragged rows and last tile
+    (7, 1000, 256, "bf16", 16, 1),        # skinny, 64-column tiles, ragged last tile
+    (5, 128256, 256, "bf16", 8, 1),       # large vocabulary
+    (37, 997, 64, "f32", 4, 1),           # fp32 kernel, 64-column tiles
+    (200, 1300, 256, "bf16", 8, 4),    # dense; every logit four times in a row
+    (64, 1000, 128, "bf16", 6, 3),     # skinny; runs of three equal logits
+    (40, 997, 64, "f32", 5, 2),        # fp32 kernel; equal pairs
 ])
-def test_fused_lm_head_rows_match_reference(M, V, K, dt, kk):
+def test_fused_lm_head_rows_match_reference(M, V, K, dt, kk, rep):
     """The LM head with its row statistics fused into the GEMM epilogue,
     against float64 logits: argmax and top-k ids exact wherever the
     reference's deciding gap exceeds 1e-3 (the fp32 product is accurate to
     ~1e-5 here), log-probs within 1e-4.  Planted exact ties (identical weight
-    rows) must resolve to the lowest id."""
+    rows) must resolve to the lowest id; with rep > 1 every weight row is
+    repeated rep times, so every top-k place of every row is a tie."""
     from paper_2412_10418_amd.binding import cdsl_op_lm_head_rows
     rng = np.random.default_rng([M, V, K, kk])
     A = rng.standard_normal((M, K)).astype(np.float32)
@@ -123,6 +127,10 @@ def test_fused_lm_head_rows_match_reference(M, V, K, dt, kk):
     for a, b in ((3, 700 % V), (V - 2, V - 1)):
         Bd[b] = Bd[a]
     Bt[[700 % V, V - 1]] = Bt[[3, V - 2]]
+    if rep > 1:
+        src = np.arange(V) // rep * rep
+        Bd = Bd[src]
+        Bt = Bt[torch.from_numpy(src).cuda()].contiguous()
     g = rng.integers(0, V, M).astype(np.int32)
     lp, amax, tk, tl = cdsl_op_lm_head_rows(torch.from_numpy(A).cuda(), Bt, torch.from_numpy(g).cuda(), kk)
     lp, amax, tk, tl = (t.cpu().numpy() for t in (lp, amax, tk, tl))
@@ -131,8 +139,9 @@ def test_fused_lm_head_rows_match_reference(M, V, K, dt, kk):
     for m in range(M):
         ls = oracle.log_softmax(z[m])
         assert abs(lp[m] - ls[g[m]]) < 1e-4
-        srt = np.sort(z[m])[::-1]
-        if srt[0] - srt[1] > 1e-3 or oracle.argmax_lowest(z[m]) in (3, V - 2):
+        top = z[m].max()
+        below = z[m][z[m] < top]     # exact ties of the maximum order by id
+        if below.size == 0 or top - below.max() > 1e-3:
             assert amax[m] == oracle.argmax_lowest(z[m])
             checked += 1
         if kk:
