@@ -116,17 +116,19 @@ __device__ __forceinline__ bool window_sees(const Window& w, int owner, int base
   return owner >= w.i_lo && owner <= w.i_hi && base <= w.slot_lim;
 }
 
-// KW = key groups: the 4 waves are (4 / KW) row tiles x KW key groups,
+// KW = key groups: the NW waves are (NW / KW) row tiles x KW key groups,
 // and one iteration stages KW pairs of key blocks: wave (rt, kw) computes
 // pair kw of it for row tile rt, and the key groups of a row tile merge
 // their (m, l, O) states at the end.  KW > 1 keeps every wave busy, and
 // the grid full, when a (prompt, KV head) has few row tiles (the rollout:
 // k beams x G heads); the chain of dependent memory round trips (block
-// table, then one per iteration) is then short.
-template <int HD, int KW>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_split(AttnArgs a) {
-  constexpr int NT = 256;                      // 4 waves
-  constexpr int RTW = 4 / KW;                  // row tiles per workgroup
+// table, then one per iteration) is then short.  Eight waves put up to
+// four row tiles of a (prompt, KV head) in one workgroup, so its keys are
+// read from memory once for all of them.
+template <int HD, int KW, int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) void attn_split(AttnArgs a) {
+  constexpr int NT = 64 * NW;
+  constexpr int RTW = NW / KW;                 // row tiles per workgroup
   constexpr int NPI = KW;                      // pairs per iteration
   constexpr int KCH = HD / 8;                  // 16-byte chunks per K row
   constexpr int KPL = 2 * kBlock * HD;         // LDS K plane: 2 blocks x 16 keys x HD
@@ -134,10 +136,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   constexpr int BUF = 2 * KPL + 2 * VPL;       // K hi, K lo, V hi, V lo
   constexpr int UNIT = 2 * kBlock * HD;        // pool unit (both planes), bf16
   constexpr int UCH = UNIT / 8;                // 16-byte chunks per unit
-  constexpr int PER = 4 * UCH / NT;            // chunks per thread per pair
+  constexpr int PER = 4 * UCH / NT;            // chunks per thread per pair (UCH is a multiple of 64)
   constexpr int KS = HD / 32;                  // k-steps of the score product
   constexpr int DT = HD / 16;                  // 16-dim output tiles
-  static_assert(UCH % NT == 0, "static chunk regions");
+  static_assert((4 * UCH) % NT == 0 && UCH % 64 == 0, "whole chunks per thread, one region per wave");
   __shared__ __attribute__((aligned(16))) bf16 lds[2][NPI][BUF];
   __shared__ int lblk[kAttnMaxList];
   __shared__ int lmeta[kAttnMaxList];   // base * 32 + owner + 1
@@ -222,7 +224,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   const bf16* kpool = (const bf16*)a.pool.k + (long long)a.layer * 2 * a.pool.layer_elems;
   const bf16* vpool = (const bf16*)a.pool.v + (long long)a.layer * 2 * a.pool.layer_elems;
   auto dst_of = [&](int u) __attribute__((always_inline)) {
-    const int region = (NT * u) / UCH, w = (tid + NT * u) % UCH;
+    const int region = (tid + NT * u) / UCH, w = (tid + NT * u) % UCH;
     const int plane = w / (UCH / 2), wp = w % (UCH / 2);
     if (region < 2) {
       const int row = region * kBlock + wp / KCH, c = wp % KCH;
@@ -246,7 +248,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
       const long long ub = ((long long)lblk[eB] * a.Hkv + kvh) * UNIT;
 #pragma unroll
       for (int u = 0; u < PER; ++u) {
-        const int region = (NT * u) / UCH;   // exact: tid < NT <= UCH
+        const int region = (tid + NT * u) / UCH;   // uniform over a wave
         const bf16* base = (region < 2 ? kpool : vpool) + ((region & 1) ? ub : ua);
         stg[q][u] = *(const u32x4*)(base + ((tid + NT * u) % UCH) * 8);
       }
@@ -257,7 +259,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     for (int q = 0; q < NPI; ++q)
 #pragma unroll
       for (int u = 0; u < PER; ++u) {
-        const int region = (NT * u) / UCH;
+        const int region = (tid + NT * u) / UCH;
         bf16* d = &lds[buf][q][dst_of(u)];
         if (region < 2) {
           *(u32x4*)d = stg[q][u];
@@ -585,15 +587,29 @@ AttnPlan attn_plan(const PassDesc& p, int H, int Hkv, int hd, int dtype, int max
     pl.blocks_per_split = nK;
     return pl;
   }
-  // 16-row tiles, 4 waves per workgroup (a wave without rows still stages
-  // its share of the key blocks).  At most 2 row tiles: the waves become
-  // key groups instead -- 4 of them and one row tile per workgroup at
-  // hd = 64; 2, with both row tiles in one workgroup, at hd = 128 (LDS:
-  // 2 x 32 KB per key group).
+  // 16-row tiles, 4 or 8 waves per workgroup (a wave without rows still
+  // stages its share of the key blocks).  At most 2 row tiles: the waves
+  // become key groups instead -- 4 of them per row tile at hd = 64; 2, with
+  // both row tiles in one workgroup, at hd = 128 (LDS: 2 x 32 KB per key
+  // group).
   pl.row_tiles = (nrows + 15) / 16;
   pl.threads = 256;
   pl.kw = pl.row_tiles <= 2 ? (hd == 64 ? 4 : 2) : 1;
-  const int rtw = 4 / pl.kw;
+  if (hd == 64 && pl.row_tiles >= 2 && pl.row_tiles <= 4 && p.nb * Hkv >= 256) {
+    // eight waves: 2 row tiles x 4 key groups, or 4 x 2; the keys are read
+    // once per (prompt, KV head) instead of once per row tile.  With fewer
+    // than 256 (prompt, KV head) pairs the pass is latency-bound and twice
+    // the workgroups (one per row tile) finish sooner (measured at 16
+    // prompts x 8 KV heads: the eight-wave form cost 0.1 ms more per step)
+    pl.threads = 512;
+    pl.kw = pl.row_tiles == 2 ? 4 : 2;
+  } else if (pl.row_tiles > 4) {
+    // eight row tiles per workgroup: each key block is read once per 128
+    // rows (the verification of long prefixes) instead of once per 64
+    pl.threads = 512;
+    pl.kw = 1;
+  }
+  const int rtw = pl.threads / 64 / pl.kw;
   pl.row_groups = (pl.row_tiles + rtw - 1) / rtw;
   // enough workgroups for two per CU, >= 1 key-block pair per split, and at
   // most kAttnMaxList key blocks per split; no split (and no combine
@@ -632,11 +648,19 @@ hipError_t attn_launch(const AttnArgs& args, const AttnPlan& pl, int hd, int dty
   dim3 grid(pl.nsplit, a.p.nb * a.Hkv, pl.row_groups);
   // LDS: 2 buffers x KW pairs of 16 KB (hd 64) or 32 KB (hd 128)
   if (hd == 64) {
-    if (pl.kw == 4) attn_split<64, 4><<<grid, 256, 0, st>>>(a);
-    else attn_split<64, 1><<<grid, 256, 0, st>>>(a);
+    if (pl.threads == 512) {
+      if (pl.kw == 4) attn_split<64, 4, 8><<<grid, 512, 0, st>>>(a);
+      else if (pl.kw == 2) attn_split<64, 2, 8><<<grid, 512, 0, st>>>(a);
+      else attn_split<64, 1, 8><<<grid, 512, 0, st>>>(a);
+    } else if (pl.kw == 4) {
+      attn_split<64, 4, 4><<<grid, 256, 0, st>>>(a);
+    } else {
+      attn_split<64, 1, 4><<<grid, 256, 0, st>>>(a);
+    }
   } else if (hd == 128) {
-    if (pl.kw == 2) attn_split<128, 2><<<grid, 256, 0, st>>>(a);
-    else attn_split<128, 1><<<grid, 256, 0, st>>>(a);
+    if (pl.threads == 512) attn_split<128, 1, 8><<<grid, 512, 0, st>>>(a);
+    else if (pl.kw == 2) attn_split<128, 2, 4><<<grid, 256, 0, st>>>(a);
+    else attn_split<128, 1, 4><<<grid, 256, 0, st>>>(a);
   } else {
     return hipErrorInvalidValue;
   }
