@@ -1,6 +1,6 @@
 // Attention of one decoder layer over the paged KV cache.
 //
-// Workgroup = (key split, prompt x KV head, group of 32-row tiles).  The
+// Workgroup = (key split, prompt x KV head, group of 16-row tiles).  The
 // query rows of one prompt and one KV head are ALL beams x all rows of the
 // beam x the G query heads sharing that KV head, so every shared-prefix KV
 // block is read once for all k beams (speculative lookaheads of every beam
@@ -13,13 +13,14 @@
 // (hi, lo) planes.  The workgroup first lists the key blocks its rows can
 // see, then streams them in pairs (32 keys) through double-buffered LDS,
 // the next pair's global loads in flight while the current pair is
-// computed.  Per wave: 32 query rows.  Scores are computed transposed,
-//   S^T[32 keys, 32 rows] = K[32, hd] . Q^T[hd, 32]      (MFMA 32x32x16)
-// so that lane (row c, half g) holds P[c][keys 8q + 4g + e] -- exactly the
-// B fragment of
-//   O^T[hd, 32 rows] += V^T[hd, 32 keys] . P^T[32 keys, 32 rows]
-// once V's slots within a block are stored in that key order: no shuffles
-// or LDS round trip between the two products.  Every product takes three
+// computed.  Per wave: 16 query rows.  Scores are computed transposed, per
+// block of 16 keys,
+//   S^T[16 keys, 16 rows] = K[16, hd] . Q^T[hd, 16]      (MFMA 16x16x32)
+// so that lane (row r, group g) holds keys 4g..4g+3 of both blocks of the
+// pair -- exactly its B fragment of
+//   O^T[16 dims, 16 rows] += V^T[16 dims, 32 keys] . P^T[32 keys, 16 rows]
+// once V's slots are stored in that key order: no shuffles or LDS round
+// trip between the two products.  Every product takes three
 // MFMAs (hi*hi + hi*lo + lo*hi), keeping fp32-level accuracy.  Online
 // softmax in the log2 domain; the row max / sum combine the two lanes of a
 // row with one xor shuffle.  Key splits write (m, l, unnormalised O)

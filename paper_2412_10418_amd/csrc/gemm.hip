@@ -10,19 +10,21 @@
 // CDNA4 MFMA fragments want: lane (r, g) of v_mfma_f32_16x16x32_bf16 holds 8
 // consecutive K elements of row r, so every fragment is one 16-byte load.
 //
-//   dense  (M > 128): 128 x 128 tiles, 4 waves (2 x 2) of 64 x 64, K step
-//          32, double-buffered LDS fed from registers two K steps ahead.
-//          Arithmetic intensity ~M flop/B: the verification block, prefill.
+//   dense  (M > 128): 160 x 256 block tiles, 8 waves (2 x 4) of 80 x 64,
+//          64-deep K stages, double-buffered LDS fed from registers two
+//          stages ahead, XCD-aware tile order.  The verification block, the
+//          prefill, and draft passes of more than 128 rows.
 //   skinny (M <= 128): the decode rows of the draft rollout.  Weight
-//          streaming bound: each wave owns 16 columns and keeps four K
-//          stages of weight fragments in flight in registers, straight from
-//          HBM; the small activation block is staged once per K stage in
-//          LDS and shared by the 4 waves.  Loads are issued in the order they
-//          are consumed so the in-order vmcnt waits never stall on a later
-//          prefetch.
+//          streaming bound: each wave owns 16 or 32 columns and keeps a ring
+//          of 4 or 8 K stages of weight fragments in flight in registers,
+//          straight from HBM; the small activation block is staged once per
+//          K stage in LDS and shared by the 4 waves.  Loads are issued in the
+//          order they are consumed so the in-order vmcnt waits never stall on
+//          a later prefetch.
 // When the tile grid cannot fill the 256 CUs, K is split across workgroups;
-// each split writes its own fp32 plane and a reduce kernel sums the planes
-// in split order and applies the epilogue (bitwise deterministic).
+// each split writes its own fp32 plane, summed in split order (bitwise
+// deterministic) by a reduce kernel or by the kernel that consumes the
+// result.
 #include <stdlib.h>
 
 #include <type_traits>
@@ -316,7 +318,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dense(GemmArgs a) {
   // XCD a contiguous range of logical tiles, ordered with the row block
   // fastest: the tiles an XCD runs together then share weight column blocks
   // (and the few activation row blocks) through its L2 instead of fetching
-  // them once per tile (measured: 894 MB -> 224 MB of HBM reads for the
+  // them once per tile (measured: 894 MB -> about 420 MB of HBM reads for the
   // 800 x 22016 x 4096 projection).
   const int T = a.tiles_m * a.tiles_n;
   const int p = blockIdx.x, xcd = p & 7, slot = p >> 3;
