@@ -107,11 +107,14 @@ typedef struct cdsl_model_config {
  * layer in this order:
  *   attn_norm[D], wq[H*hd, D], wk[Hkv*hd, D], wv[Hkv*hd, D], wo[D, H*hd],
  *   mlp_norm[D], w_gate[F, D], w_up[F, D], w_down[D, F]
- * cdsl_init copies (and re-packs) everything into library-owned memory; the
- * caller's buffers are not referenced after cdsl_init returns.  The copy is
- * the packing the kernels want: q/k/v concatenated into one matrix and
- * gate/up interleaved in groups of 16 rows, so each layer's fused
- * projections read one contiguous weight. */
+ * Ownership: tok_emb, lm_head, the norm gains, wo and w_down are BORROWED --
+ * the kernels read them in place, so the caller keeps them alive and
+ * unchanged until cdsl_destroy; every weight pointer must be 16-byte aligned
+ * (CDSL_EINVAL otherwise).  wq/wk/wv and w_gate/w_up are re-packed at
+ * cdsl_init into library-owned copies (q/k/v concatenated into one matrix,
+ * gate/up interleaved in groups of 16 rows, so each fused projection reads
+ * one contiguous weight); the caller's wq, wk, wv, w_gate and w_up are not
+ * referenced after cdsl_init returns. */
 typedef struct cdsl_model {
   cdsl_model_config cfg;
   const void* tok_emb;              /* [V, D]   */

@@ -301,12 +301,15 @@ class Context:
         self.dtype = dtype
         self.limits = {"max_batch": lim.max_batch, "max_ctx": lim.max_ctx, "max_k": lim.max_k,
                        "max_d": lim.max_d, "max_prompt": lim.max_prompt, "max_prefixes": lim.max_prefixes}
-        del dkeep, tkeep
+        # the library borrows the embedding, LM head, norm gains, wo and
+        # w_down: their tensors live as long as the context
+        self._borrowed = (draft_w, target_w, dkeep, tkeep)
 
     def close(self):
         if self.handle:
             lib().cdsl_destroy(self.handle)
             self.handle = None
+        self._borrowed = None
 
     def __del__(self):
         try:

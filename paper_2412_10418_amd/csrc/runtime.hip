@@ -2,6 +2,7 @@
 // pool and its block allocator, the per-pass model runner, and the entry
 // points declared in include/cdsl.h and include/cdsl_ops.h.
 #include <math.h>
+#include <stdint.h>
 #include <stdio.h>
 #include <string.h>
 
@@ -308,12 +309,19 @@ void load_model(cdsl_ctx* c, Model& md, const cdsl_model& src, int max_pos) {
     g_err = "null weight pointer";
     throw Fail{CDSL_EINVAL};
   }
-  md.emb = dev_alloc_bytes(c, V * D * es);
-  CK(hipMemcpyAsync(md.emb, src.tok_emb, V * D * es, hipMemcpyDeviceToDevice, st));
-  md.lm = dev_alloc_bytes(c, V * D * es);
-  CK(hipMemcpyAsync(md.lm, src.lm_head, V * D * es, hipMemcpyDeviceToDevice, st));
-  md.gf = dev_alloc<float>(c, D);
-  CK(hipMemcpyAsync(md.gf, src.final_norm, D * 4, hipMemcpyDeviceToDevice, st));
+  // Matrices the kernels read as given are borrowed (used in place; the
+  // caller keeps them alive until cdsl_destroy).  Their rows are read with
+  // 16-byte vector loads, so every pointer must be 16-byte aligned.
+  auto borrow = [&](const void* p) {
+    if (((uintptr_t)p & 15) != 0) {
+      g_err = "weight pointers must be 16-byte aligned";
+      throw Fail{CDSL_EINVAL};
+    }
+    return const_cast<void*>(p);
+  };
+  md.emb = borrow(src.tok_emb);
+  md.lm = borrow(src.lm_head);
+  md.gf = (float*)borrow(src.final_norm);
   for (int l = 0; l < k.n_layers; ++l) {
     const void* const* lp = src.layer_ptrs + 9 * l;
     for (int u = 0; u < 9; ++u)
@@ -321,29 +329,21 @@ void load_model(cdsl_ctx* c, Model& md, const cdsl_model& src, int max_pos) {
         g_err = "null layer weight pointer";
         throw Fail{CDSL_EINVAL};
       }
-    float* g1 = dev_alloc<float>(c, D);
-    float* g2 = dev_alloc<float>(c, D);
-    CK(hipMemcpyAsync(g1, lp[0], D * 4, hipMemcpyDeviceToDevice, st));
-    CK(hipMemcpyAsync(g2, lp[5], D * 4, hipMemcpyDeviceToDevice, st));
-    md.g1.push_back(g1);
-    md.g2.push_back(g2);
+    md.g1.push_back((float*)borrow(lp[0]));
+    md.g2.push_back((float*)borrow(lp[5]));
     char* qkv = (char*)dev_alloc_bytes(c, (Hq + 2 * Hk) * D * es);
     CK(hipMemcpyAsync(qkv, lp[1], Hq * D * es, hipMemcpyDeviceToDevice, st));
     CK(hipMemcpyAsync(qkv + Hq * D * es, lp[2], Hk * D * es, hipMemcpyDeviceToDevice, st));
     CK(hipMemcpyAsync(qkv + (Hq + Hk) * D * es, lp[3], Hk * D * es, hipMemcpyDeviceToDevice, st));
     md.wqkv.push_back(qkv);
-    void* wo = dev_alloc_bytes(c, D * Hq * es);
-    CK(hipMemcpyAsync(wo, lp[4], D * Hq * es, hipMemcpyDeviceToDevice, st));
-    md.wo.push_back(wo);
+    md.wo.push_back(borrow(lp[4]));
     // gate/up interleaved in groups of 16 rows: [g0..g15, u0..u15, g16..]
     char* gu = (char*)dev_alloc_bytes(c, 2 * F * D * es);
     CK(hipMemcpy2DAsync(gu, 32 * D * es, lp[6], 16 * D * es, 16 * D * es, F / 16, hipMemcpyDeviceToDevice, st));
     CK(hipMemcpy2DAsync(gu + 16 * D * es, 32 * D * es, lp[7], 16 * D * es, 16 * D * es, F / 16,
                         hipMemcpyDeviceToDevice, st));
     md.wgu.push_back(gu);
-    void* wd = dev_alloc_bytes(c, D * F * es);
-    CK(hipMemcpyAsync(wd, lp[8], D * F * es, hipMemcpyDeviceToDevice, st));
-    md.wd.push_back(wd);
+    md.wd.push_back(borrow(lp[8]));
   }
   // rotary tables in double precision, stored fp32: [max_pos][hd/2]
   const int half = md.hd / 2;

@@ -1,8 +1,8 @@
 """Failure handling and resume on the GPU, through the C ABI: token ids
 outside the vocabulary, a commit that fails validation (the prefix and its
 generated tokens stay as they were), destroyed contexts and freed prefix
-handles, limits beyond device memory, and a run resumed by re-prefilling
-its tokens.  Every error is forced from the host; no kernel faults."""
+handles, limits beyond device memory, misaligned borrowed weights, and a
+run resumed by re-prefilling its tokens.  Every error is forced from the host; no kernel faults."""
 import math
 
 import numpy as np
@@ -144,6 +144,24 @@ def test_limits_beyond_device_memory(tiny):
         Engine(tiny.wl, dwd, twd, max_steps=2, max_batch=4096, max_prompt=65536)
     assert e.value.code == bd.CDSL_ENOMEM
     assert "exceeds free device memory" in str(e.value)
+
+
+def test_borrowed_weights_must_be_aligned(tiny):
+    """The embedding, LM head, norm gains, wo and w_down are read in place
+    with 16-byte loads: a pointer off that alignment is refused at init
+    (EINVAL) before any kernel reads it."""
+    from paper_2412_10418_amd import binding as bd
+    from paper_2412_10418_amd.engine import Engine
+    dwd, twd = Engine.upload(tiny.wl, tiny.draft_np, tiny.target_np)
+    emb = twd["tok_emb"]
+    shifted = torch.empty(emb.numel() + 1, dtype=emb.dtype, device=emb.device)[1:].view(emb.shape)
+    shifted.copy_(emb)
+    assert shifted.data_ptr() % 16 != 0
+    twd = dict(twd, tok_emb=shifted)
+    with pytest.raises(bd.CDSLError) as e:
+        Engine(tiny.wl, dwd, twd, max_steps=2, max_batch=2)
+    assert e.value.code == bd.CDSL_EINVAL
+    assert "aligned" in str(e.value)
 
 
 def test_resume_by_reprefill_matches_uninterrupted(tiny):
