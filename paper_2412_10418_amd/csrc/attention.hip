@@ -150,12 +150,39 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
-  const int split = blockIdx.x;
-  const int bi = blockIdx.y / a.Hkv, kvh = blockIdx.y % a.Hkv;
+  // (key split, prompt x KV head, row group) of this workgroup.  With key
+  // splits the grid is (split, pair, row group).  Without, it is one
+  // dimension of pairs x row groups: the row groups of one (prompt, KV head)
+  // read the same keys, and workgroup p runs on XCD p % 8, so the row groups
+  // of a pair take consecutive slots of one XCD (ids xcd + 8 t) and the
+  // second read of each key block finds it in that XCD's L2; the pairs past
+  // the last multiple of 8 follow in order.
+  int split, pq, rg;
+  if (a.nsplit > 1) {
+    split = blockIdx.x;
+    pq = blockIdx.y;
+    rg = blockIdx.z;
+  } else {
+    split = 0;
+    const int NQ = p.nb * a.Hkv;
+    const int NR = gridDim.x / NQ;   // row groups per pair
+    const int full = NQ & ~7;
+    const int L = blockIdx.x;
+    if (L < full * NR) {
+      const int t = L >> 3;
+      pq = (L & 7) + 8 * (t / NR);
+      rg = t % NR;
+    } else {
+      const int l2 = L - full * NR;
+      pq = full + l2 / NR;
+      rg = l2 % NR;
+    }
+  }
+  const int bi = pq / a.Hkv, kvh = pq % a.Hkv;
   const int b = pass_batch(p, bi);
   const int G = a.G;
   const int nrows = p.kp * p.R * G;
-  const int wg_r0 = blockIdx.z * 16 * RTW;
+  const int wg_r0 = rg * 16 * RTW;
   if (wg_r0 >= nrows) return;   // uniform over the workgroup
   const int Lp = p.Lp[b];
 
@@ -646,7 +673,8 @@ hipError_t attn_launch(const AttnArgs& args, const AttnPlan& pl, int hd, int dty
     return hipGetLastError();
   }
   if (pl.blocks_per_split > kAttnMaxList) return hipErrorInvalidValue;
-  dim3 grid(pl.nsplit, a.p.nb * a.Hkv, pl.row_groups);
+  const dim3 grid = pl.nsplit > 1 ? dim3(pl.nsplit, a.p.nb * a.Hkv, pl.row_groups)
+                                   : dim3(a.p.nb * a.Hkv * pl.row_groups);
   // LDS: 2 buffers x KW pairs of 16 KB (hd 64) or 32 KB (hd 128)
   if (hd == 64) {
     if (pl.threads == 512) {
