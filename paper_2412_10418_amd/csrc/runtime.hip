@@ -692,6 +692,8 @@ void ensure_blocks(cdsl_ctx* c, cdsl_prefix* px, int b, int new_len) {
   }
 }
 
+// Callers synchronise the stream first: the staging buffer is shared by
+// every prefix handle, and the previous copy from it may still be queued.
 void upload_table(cdsl_ctx* c, cdsl_prefix* px) {
   const size_t n = (size_t)px->B * c->pstride;
   for (size_t u = 0; u < n; ++u) c->table_host[u] = px->table[u] < 0 ? 0 : px->table[u];
@@ -874,6 +876,10 @@ int cdsl_prefill(cdsl_ctx* c, const int32_t* tokens, int32_t B, int32_t L, int32
   cdsl_prefix* px = new (std::nothrow) cdsl_prefix();
   if (!px) return fail(c, CDSL_ENOMEM, "host allocation failed");
   int rc = guarded(c, [&]() {
+    // the pinned block-table staging buffer may still feed the table copy
+    // a commit queued for another prefix: let the stream drain before
+    // upload_table refills it
+    CK(hipStreamSynchronize(c->st));
     px->B = B;
     px->L0 = L;
     px->len.assign(B, 0);
