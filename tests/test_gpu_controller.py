@@ -352,6 +352,17 @@ def test_small_bf16_controller_matches_oracle(small):
 
 
 @pytest.mark.timeout(900)
+def test_small_bf16_controller_step1_two_rounds_match_oracle(small):
+    """b = 2 on the bf16 pair (a_t = 2 keeps every prompt in S2/S3): the
+    tentative append of M_p's token into the hi/lo KV pool, the second
+    round's rollout and reward, and the withdrawal; 2 iterations for 2
+    prompts."""
+    compared, seen, stopped = _run_controller(small, 2, 2, 2.0, 1.0, 2)
+    assert compared == 4 or stopped
+    assert "step1 round 2" in seen or stopped
+
+
+@pytest.mark.timeout(900)
 def test_small_bf16_soft_controller_matches_oracle(small):
     """Alg. 1 with speculative sampling's test on the bf16 pair: 2
     iterations for 2 prompts."""

@@ -1,8 +1,8 @@
 """Failure handling and resume on the GPU, through the C ABI: token ids
 outside the vocabulary, a commit that fails validation (the prefix and its
 generated tokens stay as they were), destroyed contexts and freed prefix
-handles, limits beyond device memory, misaligned borrowed weights, and a
-run resumed by re-prefilling its tokens.  Every error is forced from the host; no kernel faults."""
+handles, limits beyond device memory, misaligned borrowed weights, a run
+resumed by re-prefilling its tokens, and two live prefix handles.  Every error is forced from the host; no kernel faults."""
 import math
 
 import numpy as np
@@ -192,4 +192,49 @@ def test_resume_by_reprefill_matches_uninterrupted(tiny):
         print(f"prompt {b}: {len(runs[4][b])} + {len(st.emitted[0])} tokens resumed, {len(runs[8][b])} straight")
         assert runs[4][b] + st.emitted[0] == runs[8][b]
         st.prefix.free()
+    eng.close()
+
+
+def test_second_prefix_leaves_the_first_unchanged(tiny):
+    """Two live prefix handles on one context: prompt set A steps, set B is
+    prefilled right after A's commit (the shared pinned block-table buffer
+    is refilled for B while A's table upload was queued), then both step in
+    turn.  A's tokens and log-probs equal a run of A alone, bitwise, and B's
+    equal a run of B alone."""
+    from paper_2412_10418_amd.engine import Engine
+    wl = tiny.wl
+    B = 2
+    dwd, twd = Engine.upload(wl, tiny.draft_np, tiny.target_np)
+    eng = Engine(wl, dwd, twd, max_steps=8, max_batch=B, max_prefixes=2)
+    kw = torch.from_numpy(tiny.kws[:B]).cuda()
+    pa = torch.from_numpy(tiny.prompts(B)).cuda()
+    pb = torch.from_numpy(tiny.prompts(B, first=B)).cuda()
+
+    def run(prompts, n):
+        st = eng.start(prompts)
+        lps = []
+        for _ in range(n):
+            bf = eng.step(st, keywords=kw)
+            lps.append(bf.verify["logprobs"].cpu().clone())
+        out = ([list(e) for e in st.emitted], lps)
+        st.prefix.free()
+        return out
+
+    alone_a, alone_b = run(pa, 4), run(pb, 3)
+    sa = eng.start(pa)
+    lpa, lpb = [], []
+    bf = eng.step(sa, keywords=kw)
+    lpa.append(bf.verify["logprobs"].cpu().clone())
+    sb = eng.start(pb)
+    for t in range(3):
+        bf = eng.step(sa, keywords=kw)
+        lpa.append(bf.verify["logprobs"].cpu().clone())
+        bf = eng.step(sb, keywords=kw)
+        lpb.append(bf.verify["logprobs"].cpu().clone())
+    assert [list(e) for e in sa.emitted] == alone_a[0]
+    assert [list(e) for e in sb.emitted] == alone_b[0]
+    assert all(torch.equal(x, y) for x, y in zip(lpa, alone_a[1]))
+    assert all(torch.equal(x, y) for x, y in zip(lpb, alone_b[1]))
+    sa.prefix.free()
+    sb.prefix.free()
     eng.close()
