@@ -182,7 +182,32 @@ def summarize_profile(args):
         out.append(f"| `{nm[:80]}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.2f} | "
                    f"{float(r['AverageNs']) / 1e3:.2f} | {100 * float(r['TotalDurationNs']) / total:.1f}% |")
     out += ["", "Calls include the prompt prefill (separately named `gemm_bf16_dense<..., 1>`) and the warmup, "
-            "timed and instrumented steps.", "",
+            "timed and instrumented steps.", ""]
+    trace_csv = os.path.join(trace_dir, "bench_kernel_trace.csv")
+    if os.path.exists(trace_csv):
+        # one timed step: the launches between two commits in the middle of
+        # the run (the instrumented steps at the end carry timing events)
+        tr = sorted(csv.DictReader(open(trace_csv)), key=lambda r: int(r["Start_Timestamp"]))
+        cut = [i for i, r in enumerate(tr) if "commit_kernel" in r["Kernel_Name"]]
+        if len(cut) >= 4:
+            u = len(cut) // 2
+            seg = tr[cut[u - 1] + 1:cut[u] + 1]
+            ksum = sum(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in seg) / 1e6
+            wall = (int(seg[-1]["End_Timestamp"]) - int(seg[0]["Start_Timestamp"])) / 1e6
+            gaps = sorted(int(seg[i + 1]["Start_Timestamp"]) - int(seg[i]["End_Timestamp"])
+                          for i in range(len(seg) - 1))
+            fam = {}
+            for r in seg:
+                nm = r["Kernel_Name"].replace("cdsl::(anonymous namespace)::", "").replace("cdsl::", "")
+                nm = "embed_rows" if "embed_rows" in nm else re.sub(r"[<(].*$", "", nm.replace("void ", ""))
+                fam[nm] = fam.get(nm, 0) + 1
+            top = ", ".join(f"{k} {v}" for k, v in sorted(fam.items(), key=lambda kv: -kv[1])[:8])
+            out += ["## Launches per step", "",
+                    f"One timed step of the traced run (between two commits): {len(seg)} launches, "
+                    f"{ksum:.2f} ms of kernel time in {wall:.2f} ms; median gap between kernels "
+                    f"{gaps[len(gaps) // 2] / 1e3:.2f} us. By kernel: {top}.", ""]
+    out += [
+            "## HBM traffic (FETCH_SIZE and WRITE_SIZE passes)", "",
             "## HBM traffic (FETCH_SIZE and WRITE_SIZE passes)", "",
             f"Calibration: a plain 256 MiB device copy (262144 KiB read, 262144 KiB written) reads "
             f"FETCH_SIZE = {fcal:.1f} KiB and WRITE_SIZE = {wcal:.1f} KiB per dispatch, so the counters are "
