@@ -1,0 +1,130 @@
+"""Host logic of the benchmark, without a GPU: the one-GPU contract, the
+roofline arithmetic, the phase rates, and the rocprofv3 summary (counter
+calibration, bytes per launch, the source-digest gate on stored traffic)."""
+import csv
+import json
+import os
+import subprocess
+import sys
+import types
+
+import pytest
+
+import cdsl_inputs as ci
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 2
+    assert "one GPU" in r.stdout + r.stderr
+
+
+def test_roofline_of_the_dominant_class(monkeypatch):
+    """frac = algorithmic flops (or bytes) per second over the peak; the
+    dense projection's executed fraction is twice the algorithmic one."""
+    monkeypatch.setattr(bench, "stored_traffic", lambda cls, wl: None)
+    stats = {"gemm_dense": {"ms": 10.0, "launches": 4, "flops": 5e12, "bytes": 4e9},
+             "attention": {"ms": 2.0, "launches": 8, "flops": 0.0, "bytes": 8e9}}
+    cls, r = bench.roofline(stats, "7b1b")
+    assert cls == "gemm_dense" and r["bound"] == "mfma"
+    assert r["achieved"] == pytest.approx(500.0)                 # 5e12 flop / 10 ms
+    assert r["frac"] == pytest.approx(0.2)
+    assert r["executed_frac"] == pytest.approx(0.4)
+    assert r["alg_flops_per_launch"] == pytest.approx(1.25e12)
+    assert r["avg_launch_us"] == pytest.approx(2500.0)
+    assert r["traffic"] is None
+    stats["attention"]["ms"] = 20.0
+    cls, r = bench.roofline(stats, "7b1b")
+    assert cls == "attention" and r["bound"] == "hbm"
+    assert r["achieved"] == pytest.approx(400.0)                 # 8e9 B / 20 ms
+    assert r["frac"] == pytest.approx(0.05)
+
+
+def test_phase_rates_count_weights_and_prefix_kv():
+    """Rollout bytes: d passes, each streaming the draft weights (bf16, no
+    embedding) and every prompt's prefix KV once (bf16; the stored figure
+    at 4 bytes for the hi + lo pair).  Verify flops: 2 per target weight
+    (no embedding) per fed row."""
+    wl = ci.workload("7b1b")
+    B, k, d, L = wl.batch, wl.k, wl.d, wl.prompt_len
+    dr, tg = wl.draft, wl.target
+
+    def params(m):   # per layer: q, k, v, o, gate, up, down; plus the LM head
+        hd = m.d_model // m.n_heads
+        per = m.d_model * (m.n_heads * hd + 2 * m.n_kv_heads * hd) + m.n_heads * hd * m.d_model \
+            + 3 * m.d_model * m.ffn_dim
+        return m.n_layers * per + m.vocab * m.d_model
+
+    hd = dr.d_model // dr.n_heads
+    kv_tok = dr.n_layers * 2 * dr.n_kv_heads * hd
+    out = bench.phase_rooflines(wl, B, k, d, {"rollout": 10.0, "verify": 20.0, "tail": 1.0}, B * L)
+    assert out["rollout_bytes"] == pytest.approx(d * (2.0 * params(dr) + B * L * kv_tok * 2.0), rel=1e-3)
+    assert out["rollout_stored_bytes"] == pytest.approx(d * (2.0 * params(dr) + B * L * kv_tok * 4.0), rel=1e-3)
+    assert out["verify_gemm_flops"] == pytest.approx(2.0 * B * k * d * params(tg), rel=1e-3)
+    assert out["rollout_GB_per_s"] == pytest.approx(out["rollout_bytes"] / 10e-3 / 1e9, rel=1e-3)
+    assert out["verify_executed_mfma_frac"] == pytest.approx(2 * out["verify_mfma_frac"], rel=1e-3)
+
+
+def _write_csv(path, rows):
+    with open(path, "w", newline="") as fh:
+        w = csv.DictWriter(fh, fieldnames=list(rows[0].keys()))
+        w.writeheader()
+        w.writerows(rows)
+
+
+def test_profile_summary_scales_counters_by_the_copy_calibration(tmp_path, monkeypatch):
+    """A synthetic run: the calibration copies read FETCH_SIZE = 131072 KiB
+    for 262144 KiB moved (scale 2) and WRITE_SIZE = 262144 KiB (scale 1);
+    the dense class reads 1000 KiB and writes 500 KiB per dispatch, so
+    (1000 * 2 + 500) KiB per launch.  The summary's traffic record carries
+    that figure and the digest of the kernel's sources, and the bench only
+    uses a record whose digest matches."""
+    trace, fetch, write = (tmp_path / n for n in ("trace", "fetch", "write"))
+    for p in (trace, fetch, write):
+        p.mkdir()
+    dense = "void cdsl::(anonymous namespace)::gemm_bf16_dense<2, 4, 5, 4, 64, 0>(GemmArgs)"
+    _write_csv(trace / "bench_kernel_stats.csv",
+               [{"Name": dense, "Calls": "10", "TotalDurationNs": "1500000", "AverageNs": "150000"}])
+    copy = "__amd_rocclr_copyBuffer"
+
+    def counters(val, cal):
+        rows = [{"Kernel_Name": dense, "Counter_Value": str(val)} for _ in range(3)]
+        rows += [{"Kernel_Name": copy, "Counter_Value": str(cal)} for _ in range(3)]
+        return rows
+
+    _write_csv(fetch / "bench_counter_collection.csv", counters(1000.0, 131072.0))
+    _write_csv(write / "bench_counter_collection.csv", counters(500.0, 262144.0))
+    line = {"ms_per_step": 37.0, "value": 21600.0, "unit": "lookahead tokens verified/s",
+            "config": {"workload": "7b1b", "batch": 16, "k": 5, "d": 10},
+            "roofline": {"kernel": "gemm_dense", "alg_bytes_per_launch": 1.5e8},
+            "kernels": {"gemm_dense": {"avg_launch_us": 151.0}}}
+    bj = tmp_path / "bench.json"
+    bj.write_text(json.dumps(line) + "\n")
+    out = tmp_path / "summary.md"
+    args = types.SimpleNamespace(summarize_profile=[str(bj), str(trace), str(fetch), str(write)],
+                                 summary_out=str(out), commands=None)
+    bench.summarize_profile(args)
+    text = out.read_text()
+    assert "scaled by 2.0000 (fetch) and 1.0000 (write)" in text
+    recs = [json.loads(ln[len(bench.TRAFFIC_TAG):-len(" -->")]) for ln in text.splitlines()
+            if ln.startswith(bench.TRAFFIC_TAG)]
+    rec = [r for r in recs if r["class"] == "gemm_dense"][0]
+    assert rec["bytes_per_launch"] == round((1000.0 * 2 + 500.0) * 1024)
+    assert rec["source"] == bench.source_digest(bench.CLASS_KERNEL["gemm_dense"][1])
+    # the gate: a matching digest is used, a stale one is not
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    (prof / "summary.md").write_text(text)
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    real = bench.source_digest
+    monkeypatch.setattr(bench, "source_digest", lambda files: rec["source"])
+    assert bench.stored_traffic("gemm_dense", "7b1b")["bytes_per_launch"] == rec["bytes_per_launch"]
+    assert bench.stored_traffic("gemm_dense", "long") is None
+    monkeypatch.setattr(bench, "source_digest", lambda files: "0" * 16)
+    assert bench.stored_traffic("gemm_dense", "7b1b") is None
+    monkeypatch.setattr(bench, "source_digest", real)
