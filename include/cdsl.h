@@ -138,9 +138,12 @@ typedef struct cdsl_prefix cdsl_prefix;
 
 /* Create a context for a draft/target pair (same vocabulary and dtype, as
  * speculative decoding requires models of one family, Sec. 4.2).  stream is
- * a hipStream_t (NULL = the default stream).  Allocates the weights copy,
- * the paged KV pools of both models, the rotary tables and all workspaces.
- * Errors: EINVAL (shapes, vocab or dtype mismatch), ENOMEM, EDEVICE. */
+ * a hipStream_t (NULL = the default stream).  Allocates the re-packed
+ * q/k/v and gate/up weights, the paged KV pools of both models, the rotary
+ * tables and all workspaces; the other weights are borrowed (see
+ * cdsl_model).  Errors: EINVAL (shapes, vocab or dtype mismatch, a weight
+ * pointer not 16-byte aligned), ENOMEM (also a KV pool beyond the free
+ * device memory, refused before it is allocated), EDEVICE. */
 int cdsl_init(const cdsl_model* draft, const cdsl_model* target,
               const cdsl_limits* limits, void* stream, cdsl_ctx** out);
 
