@@ -623,6 +623,8 @@ def main():
         "phases": phases,
         "methods": methods,
         "kernels": table,
+        "launches_per_step": (round(sum(v["launches"] for v in stats.values()) / args.profile_steps)
+                              if args.profile_steps > 0 else None),
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
