@@ -115,14 +115,14 @@ def _whole_steps(s, eng, st, ost, check, k, d, steps):
     assert_full_or_tie(reps, steps)
 
 
-def _full_size(name, points, check, roll_beams=2, step_at=None, steps=1, **over):
+def _full_size(name, points, check, roll_beams=2, step_at=(), steps=1, **over):
     """points: the (k, d) grid checked on one prefill with the largest k;
-    step_at: the (k, d) of the whole steps (from a fresh prefill)."""
+    step_at: the (k, d) points of whole steps, each from a fresh prefill."""
     s = make_setup(name, **over)
     wl = s.wl
     B = wl.batch
-    kmax = max(k for k, _ in points + ([step_at] if step_at else []))
-    dmax = max(d for _, d in points + ([step_at] if step_at else []))
+    kmax = max(k for k, _ in list(points) + list(step_at))
+    dmax = max(d for _, d in list(points) + list(step_at))
     eng = make_engine(s, B=B, max_steps=steps + 1, k=kmax, d=dmax)
     try:
         prompts = s.prompts(B)
@@ -131,8 +131,7 @@ def _full_size(name, points, check, roll_beams=2, step_at=None, steps=1, **over)
         for k, d in points:
             _block_checks(s, eng, st, ost, check, k, d, roll_beams, seed=11)
         st.prefix.free()
-        if step_at:
-            k, d = step_at
+        for k, d in step_at:
             st = eng.start(torch.from_numpy(prompts).cuda(), k=k)
             _whole_steps(s, eng, st, ost, check, k, d, steps)
             st.prefix.free()
@@ -144,15 +143,16 @@ def _full_size(name, points, check, roll_beams=2, step_at=None, steps=1, **over)
 def test_sweep_full_size_every_point():
     """7B/1B pair at batch 32 with 512-token prompts: every point of the
     k in {2, 5, 10} x d in {2, 5, 10, 20} grid (the widest, k=10 x d=20, has
-    two suffix blocks per beam and 6400 verify rows), and a whole step at
-    k=5, d=10."""
+    two suffix blocks per beam and 6400 verify rows), and whole steps at
+    k=2 d=20 (two suffix blocks per beam, 64 draft rows on the skinny
+    kernel), k=5 d=10 and k=10 d=2 (320 draft rows on the dense kernel)."""
     points = [(k, d) for k in SWEEP_K for d in SWEEP_D]
-    _full_size("sweep", points, check=[0, 31], roll_beams=1, step_at=(5, 10), steps=1)
+    _full_size("sweep", points, check=[0, 31], roll_beams=1, step_at=[(2, 20), (5, 10), (10, 2)], steps=1)
 
 
 @pytest.mark.timeout(1000)
 def test_long_context_full_size():
     """7B GQA-8 target, V=128256, batch 64 with 2048-token prompts, k=8,
     d=8: the block checks and one whole step (linear reward, selection,
-    commit, next heads over the 128256-token vocabulary)."""
-    _full_size("long", [(8, 8)], check=[0], step_at=(8, 8), steps=1)
+    commit, next heads over the 128256-token vocabulary), two of them."""
+    _full_size("long", [(8, 8)], check=[0], step_at=[(8, 8)], steps=2)
