@@ -240,6 +240,29 @@ def test_small_bf16_k1_matches_oracle():
         s.engine.close()
 
 
+@pytest.mark.parametrize("same", [False, True])
+def test_one_lookahead_token_matches_oracle(same):
+    """d = 1, the smallest lookahead: one draft pass per beam, one verified
+    row per beam, with k = 4 beams and with a single beam, hard and soft
+    rejection.  With draft = target every token is accepted, so n = d = 1
+    and every step feeds the catch-up row."""
+    s = make_setup("tiny", draft_is_target=same)
+    make_engine(s, B=3, max_steps=10, k=4, d=1)
+    try:
+        for k in (4, 1):
+            for soft in (False, True):
+                st, reps = run_and_compare(s, B=3, steps=6, check_prompts=[0, 1, 2], k=k, d=1, soft=soft)
+                for b, r in reps.items():
+                    print(f"same={same} k={k} soft={soft} prompt {b}: {r.steps_compared} steps, "
+                          f"max |dlp| {r.max_lp_err:.2e}, stop: {r.stopped or '-'}")
+                assert_full_or_tie(reps, 6)
+                if same:
+                    assert all(len(e) == 6 * 2 for e in st.emitted)   # c + x_1 every step
+                st.prefix.free()
+    finally:
+        s.engine.close()
+
+
 def test_largest_k_and_d_match_oracle():
     """The largest beam count and lookahead depth the library takes (k = 16,
     d = 32: two suffix blocks per beam, 512 verified rows per prompt, top-16
