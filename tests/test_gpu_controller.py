@@ -15,7 +15,8 @@ import torch
 
 import cdsl_inputs as ci
 import oracle
-from cdsl_harness import TOK_MARGIN, lp_tol, make_engine, make_setup, soft_margins
+from cdsl_harness import (TOK_MARGIN, assert_full_or_tie, lp_tol, make_engine, make_setup, run_and_compare,
+                          soft_margins)
 
 pytestmark = pytest.mark.gpu
 
@@ -294,6 +295,23 @@ def test_controller_step1_two_rounds_match_oracle(tiny, r_t):
     assert "step1 round 2" in seen and "step1 withdrawn" in seen
     if r_t == 1.0:
         assert "step1 round 2 kept" in seen
+
+
+def test_one_token_prompts():
+    """Prompts of a single token: the beam step, and Alg. 1 drafting from
+    the prefix, whose first pass re-feeds that token at position 0 over an
+    empty prefix; 4 iterations for 3 prompts each, against the oracle."""
+    s = make_setup("tiny", prompt_len=1)
+    make_engine(s, B=3, max_steps=12)
+    try:
+        st, reps = run_and_compare(s, B=3, steps=4, check_prompts=[0, 1, 2])
+        assert_full_or_tie(reps, 4)
+        st.prefix.free()
+        compared, seen, stopped = _run_controller(s, 3, 4, 0.5, 1.0, 1)
+        assert compared == 12 or stopped
+        assert "S2/S3" in seen
+    finally:
+        s.engine.close()
 
 
 def test_controller_error_paths(tiny):
