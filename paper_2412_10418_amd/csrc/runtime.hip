@@ -503,10 +503,10 @@ void logit_rows(cdsl_ctx* c, const LogitArgs& la, int M);
 // through the LM head into ws.logits (or logits_out at row stride
 // logits_ld); hid receives fp32 final-normed rows of every beam's last row
 // when non-null.  fuse names the row outputs wanted from the logits
-// (argmax, gathered log-prob, top-k).  For argmax-only heads and heads of
-// few rows the LM head leaves per-tile row statistics and a merge kernel
-// writes those outputs, so no logits reach memory; other heads write the
-// logits and logit_rows reduces them.
+// (argmax, gathered log-prob, top-k): the LM head then leaves per-tile row
+// statistics and a merge kernel writes those outputs, so no logits reach
+// memory.  Without fuse (speculative sampling, which reads whole rows) the
+// head writes the logits.
 void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, long long sum_prefix_len,
               bool want_logits, bool last_only, float* hid, bool prefill = false, float* logits_out = nullptr,
               int logits_ld = 0, const LogitArgs* fuse = nullptr) {
