@@ -53,6 +53,10 @@ def parse():
     ap.add_argument("--grid", default=None, metavar="K1,K2,..:D1,D2,..",
                     help="measure every (k, d) point of the grid on one engine (a fresh prefill per point) and "
                          "print one JSON line with a row per point instead of the bench line")
+    ap.add_argument("--summarize-ranges", default=None, metavar="TRACE_DIR",
+                    help="markdown summary of a rocprofv3 --kernel-trace --marker-trace --hip-runtime-trace run "
+                         "of this script: per library call (roctx range), its calls, host time, kernels launched "
+                         "and their GPU time; no GPU needed")
     ap.add_argument("--summary-out", default=None)
     ap.add_argument("--commands", default=None, help="text file with the exact profiling commands (for the summary)")
     return ap.parse_args()
@@ -281,6 +285,48 @@ def summarize_profile(args):
         sys.stdout.write(text)
 
 
+def summarize_ranges(args):
+    """Per roctx range (one library call): calls, host time, and the kernels
+    whose launch API call started inside the range on the same thread, with
+    their GPU time (from the kernel trace, matched by correlation id)."""
+    import csv
+    import glob
+    d = args.summarize_ranges
+
+    def one(pattern):
+        fs = glob.glob(os.path.join(d, pattern))
+        if not fs:
+            raise SystemExit(f"no {pattern} in {d}")
+        return list(csv.DictReader(open(fs[0])))
+
+    marks, hip, kern = one("*_marker_api_trace.csv"), one("*_hip_api_trace.csv"), one("*_kernel_trace.csv")
+    gpu_ns = {r["Correlation_Id"]: int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in kern}
+    launches = sorted((int(r["Start_Timestamp"]), r["Thread_Id"], r["Correlation_Id"]) for r in hip
+                      if r["Correlation_Id"] in gpu_ns)
+    starts = [t for t, _, _ in launches]
+    import bisect
+    agg = {}
+    for m in marks:
+        t0, t1, th = int(m["Start_Timestamp"]), int(m["End_Timestamp"]), m["Thread_Id"]
+        lo, hi = bisect.bisect_left(starts, t0), bisect.bisect_right(starts, t1)
+        ks = [cid for t, tid, cid in launches[lo:hi] if tid == th]
+        a = agg.setdefault(m["Function"], [0, 0, 0, 0])
+        a[0] += 1
+        a[1] += t1 - t0
+        a[2] += len(ks)
+        a[3] += sum(gpu_ns[c] for c in ks)
+    out = ["| library call | calls | host ms per call | kernels per call | GPU ms per call |",
+           "|---|---:|---:|---:|---:|"]
+    for nm, (n, host, nk, g) in sorted(agg.items(), key=lambda kv: -kv[1][3]):
+        out.append(f"| `{nm}` | {n} | {host / n / 1e6:.3f} | {nk / n:.1f} | {g / n / 1e6:.3f} |")
+    text = "\n".join(out) + "\n"
+    if args.summary_out:
+        with open(args.summary_out, "w") as fh:
+            fh.write(text)
+    else:
+        sys.stdout.write(text)
+
+
 def phase_rooflines(wl, B, k, d, ms, sum_prefix):
     """Algorithmic rates of the rollout (HBM-bound: every draft forward
     streams the draft weights and the prefix KV of every prompt once) and of
@@ -473,6 +519,9 @@ def main():
     args = parse()
     if args.summarize_profile:
         summarize_profile(args)
+        return
+    if args.summarize_ranges:
+        summarize_ranges(args)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path shards by prompt "

@@ -13,6 +13,8 @@
 #include <unordered_set>
 #include <vector>
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include "../../include/cdsl.h"
 #include "../../include/cdsl_ops.h"
 #include "attention.h"
@@ -26,6 +28,15 @@ using namespace cdsl;
 static_assert(kBlock == kPoolBlock, "KV blocks and the pool bookkeeping agree on the block size");
 
 namespace {
+
+// A roctx range around each library call (shown by rocprofv3 --marker-trace
+// and correlated with the kernels it launches); a no-op without a tool.
+struct Range {
+  explicit Range(const char* name) { roctxRangePushA(name); }
+  ~Range() { roctxRangePop(); }
+  Range(const Range&) = delete;
+  Range& operator=(const Range&) = delete;
+};
 
 constexpr int kMaxSplits = kAttnMaxSplits;
 
@@ -865,6 +876,7 @@ const char* cdsl_last_error(const cdsl_ctx* c) {
 
 int cdsl_prefill(cdsl_ctx* c, const int32_t* tokens, int32_t B, int32_t L, int32_t k, cdsl_prefix** out,
                  int32_t* beams, float* head_lp) {
+  Range range_("cdsl_prefill");
   CTX_CHECK(c);
   if (!tokens || !out || !beams || !head_lp) return fail(c, CDSL_EINVAL, "null argument");
   if (B <= 0 || L <= 0 || k <= 0) return fail(c, CDSL_EINVAL, "B, L and k must be positive");
@@ -954,6 +966,7 @@ namespace {
 // greedy token at the end of the prefix.
 int rollout_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* beams, int32_t k, int32_t d, int32_t roller,
                  int32_t* lookaheads, float* keep, bool pfx = false) {
+  Range range_("cdsl_rollout");
   CTX_CHECK(c);
   PX_CHECK(c, px);
   if (roller != 0 && roller != 1) return fail(c, CDSL_EINVAL, "roller must be 0 (draft) or 1 (target)");
@@ -1055,6 +1068,7 @@ struct SoftArgs {
 int verify_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d, int32_t kk,
                 const float* head_lp, float* logprobs, int32_t* target_argmax, int32_t* n_accept, float* scores,
                 int32_t* row_topk_ids, float* row_topk_lp, float* hidden, const SoftArgs* soft, bool pfx = false) {
+  Range range_("cdsl_verify");
   CTX_CHECK(c);
   PX_CHECK(c, px);
   if (kk <= 0 || kk > c->lim.max_k) return fail(c, CDSL_ERANGE, "top-k width beyond the limits");
@@ -1168,6 +1182,7 @@ int cdsl_reward_keywords(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int3
 namespace {
 int reward_kw_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, int32_t k, int32_t d, const int32_t* upto,
                    int head, const int32_t* keywords, int32_t n_kw, int32_t normalize, float* reward) {
+  Range range_("cdsl_reward_keywords");
   CTX_CHECK(c);
   PX_CHECK(c, px);
   if (!px || !look || !keywords || !reward) return fail(c, CDSL_EINVAL, "null argument");
@@ -1194,6 +1209,7 @@ int cdsl_reward_keywords_prefix(cdsl_ctx* c, cdsl_prefix* px, const int32_t* loo
 
 int cdsl_reward_linear(cdsl_ctx* c, const float* hidden, const float* w, int32_t B, int32_t k, int32_t D,
                        float* reward) {
+  Range range_("cdsl_reward_linear");
   CTX_CHECK(c);
   if (!hidden || !w || !reward || B <= 0 || k <= 0 || D <= 0) return fail(c, CDSL_EINVAL, "bad argument");
   return guarded(c, [&]() {
@@ -1205,6 +1221,7 @@ int cdsl_reward_linear(cdsl_ctx* c, const float* hidden, const float* w, int32_t
 
 int cdsl_select(cdsl_ctx* c, const float* scores, const float* reward, float alpha, int32_t B, int32_t k,
                 int32_t* beam) {
+  Range range_("cdsl_select");
   CTX_CHECK(c);
   if (!scores || !reward || !beam || B <= 0 || k <= 0) return fail(c, CDSL_EINVAL, "bad argument");
   if (isnan(alpha) || (isinf(alpha) && alpha < 0)) return fail(c, CDSL_EINVAL, "alpha must be finite or +inf");
@@ -1218,6 +1235,7 @@ int cdsl_select(cdsl_ctx* c, const float* scores, const float* reward, float alp
 
 int cdsl_select_first(cdsl_ctx* c, const float* reward, const float* first_at, int32_t B, int32_t k,
                       int32_t* beam) {
+  Range range_("cdsl_select_first");
   CTX_CHECK(c);
   if (!reward || !first_at || !beam || B <= 0 || k <= 0) return fail(c, CDSL_EINVAL, "bad argument");
   return guarded(c, [&]() {
@@ -1229,6 +1247,7 @@ int cdsl_select_first(cdsl_ctx* c, const float* reward, const float* first_at, i
 
 int cdsl_controller_states(cdsl_ctx* c, const int32_t* n_accept, const float* reward, int32_t B, int32_t d,
                            double a_t, double r_t, int32_t b, int32_t* state, float* first_at) {
+  Range range_("cdsl_controller_states");
   CTX_CHECK(c);
   if (!n_accept || !reward || !state || !first_at || B <= 0 || d <= 0) return fail(c, CDSL_EINVAL, "bad argument");
   if (b != 0 && b != 1) return fail(c, CDSL_EINVAL, "b must be 0 or 1");
@@ -1298,6 +1317,7 @@ int commit_impl(cdsl_ctx* c, cdsl_prefix* px, const int32_t* look, const int32_t
                 const int32_t* rtk_ids, const float* rtk_lp, const int32_t* res_ids, const float* res_lp, int32_t k,
                 int32_t d, int32_t kk, int32_t* emitted_host, int32_t* n_emit_host, int32_t* next_beams,
                 float* next_head_lp, bool pfx) {
+  Range range_("cdsl_commit");
   if (!px || !look || (!beam && !pfx) || !n_accept || !rtk_ids || !rtk_lp || !emitted_host || !n_emit_host ||
       !next_beams || !next_head_lp)
     return fail(c, CDSL_EINVAL, "null argument");
@@ -1414,6 +1434,7 @@ namespace {
 template <typename StageFn>
 int append_impl(cdsl_ctx* c, cdsl_prefix* px, int32_t kk, const int32_t* mask_host, int32_t* emitted_host,
                 int32_t* next_beams, float* next_head_lp, const char* bad_msg_c, StageFn&& stage_launch) {
+  Range range_("cdsl_append");
   const std::string bad_msg = bad_msg_c;
   return guarded(c, [&]() {
     const int B = px->B;
@@ -1526,6 +1547,7 @@ int cdsl_append(cdsl_ctx* c, cdsl_prefix* px, const int32_t* tokens, const int32
 }
 
 int cdsl_withdraw(cdsl_ctx* c, cdsl_prefix* px, const int32_t* count_host) {
+  Range range_("cdsl_withdraw");
   CTX_CHECK(c);
   PX_CHECK(c, px);
   if (!px || !count_host) return fail(c, CDSL_EINVAL, "null argument");
@@ -1588,6 +1610,7 @@ int cdsl_profile_read(cdsl_ctx* c, cdsl_kernel_stats* out) {
 }
 
 int cdsl_free_prefix(cdsl_ctx* c, cdsl_prefix* px) {
+  Range range_("cdsl_free_prefix");
   CTX_CHECK(c);
   if (!px) return CDSL_OK;
   PX_CHECK(c, px);

@@ -1,6 +1,7 @@
 """Host logic of the benchmark, without a GPU: the one-GPU contract, the
 roofline arithmetic, the phase rates, and the rocprofv3 summary (counter
-calibration, bytes per launch, the source-digest gate on stored traffic)."""
+calibration, bytes per launch, the source-digest gate on stored traffic), and
+the per-call summary of a marker trace."""
 import csv
 import json
 import os
@@ -128,3 +129,33 @@ def test_profile_summary_scales_counters_by_the_copy_calibration(tmp_path, monke
     monkeypatch.setattr(bench, "source_digest", lambda files: "0" * 16)
     assert bench.stored_traffic("gemm_dense", "7b1b") is None
     monkeypatch.setattr(bench, "source_digest", real)
+
+
+def test_range_summary_attributes_kernels_by_launch_time(tmp_path):
+    """A kernel counts for the roctx range (library call) in which its launch
+    call started on the same thread; its GPU time is its own duration."""
+    def w(name, rows):
+        _write_csv(tmp_path / name, rows)
+
+    w("x_marker_api_trace.csv", [
+        {"Function": "cdsl_rollout", "Thread_Id": "1", "Start_Timestamp": "100", "End_Timestamp": "200"},
+        {"Function": "cdsl_verify", "Thread_Id": "1", "Start_Timestamp": "300", "End_Timestamp": "400"},
+        {"Function": "cdsl_rollout", "Thread_Id": "1", "Start_Timestamp": "500", "End_Timestamp": "600"}])
+    w("x_hip_api_trace.csv", [
+        {"Correlation_Id": "1", "Thread_Id": "1", "Start_Timestamp": "110"},
+        {"Correlation_Id": "2", "Thread_Id": "1", "Start_Timestamp": "150"},
+        {"Correlation_Id": "3", "Thread_Id": "2", "Start_Timestamp": "160"},   # another thread
+        {"Correlation_Id": "4", "Thread_Id": "1", "Start_Timestamp": "350"},
+        {"Correlation_Id": "5", "Thread_Id": "1", "Start_Timestamp": "550"},
+        {"Correlation_Id": "6", "Thread_Id": "1", "Start_Timestamp": "450"}])  # outside every range
+    w("x_kernel_trace.csv", [
+        {"Correlation_Id": c, "Start_Timestamp": "0", "End_Timestamp": str(ns)}
+        for c, ns in (("1", 1_000_000), ("2", 3_000_000), ("3", 9_000_000), ("4", 5_000_000),
+                      ("5", 2_000_000), ("6", 7_000_000))])
+    out = tmp_path / "r.md"
+    bench.summarize_ranges(types.SimpleNamespace(summarize_ranges=str(tmp_path), summary_out=str(out)))
+    rows = {ln.split("|")[1].strip(" `"): [x.strip() for x in ln.split("|")[2:6]]
+            for ln in out.read_text().splitlines()[2:]}
+    # rollout: 2 calls, kernels 1, 2 (first) and 5 (second): 3 / 2 per call, 6 ms / 2
+    assert rows["cdsl_rollout"] == ["2", f"{100 / 1e6:.3f}", "1.5", "3.000"]
+    assert rows["cdsl_verify"] == ["1", f"{100 / 1e6:.3f}", "1.0", "5.000"]
