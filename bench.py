@@ -139,6 +139,19 @@ def roofline(stats, workload):
                   "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": traffic, **extra}
 
 
+def mangled_short(nm):
+    """The function name of an Itanium-mangled kernel name the tracer left
+    mangled ("_ZN4cdsl12_GLOBAL__N_110embed_rowsI..." -> "embed_rows<...>")."""
+    i, last = (3 if nm.startswith("_ZN") else 2), nm
+    while i < len(nm) and nm[i].isdigit():
+        j = i
+        while j < len(nm) and nm[j].isdigit():
+            j += 1
+        n = int(nm[i:j])
+        last, i = nm[j:j + n], j + n
+    return last + ("<...>" if i < len(nm) and nm[i] == "I" else "")
+
+
 def summarize_profile(args):
     """Markdown summary of the three rocprofv3 runs of this script."""
     import csv
@@ -182,7 +195,7 @@ def summarize_profile(args):
     for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"]))[:16]:
         nm = r["Name"]
         nm = nm.replace("cdsl::(anonymous namespace)::", "").replace("cdsl::", "")
-        nm = nm.split("(")[0] if not nm.startswith("_Z") else nm
+        nm = nm.split("(")[0] if not nm.startswith("_Z") else mangled_short(nm)
         out.append(f"| `{nm[:80]}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.2f} | "
                    f"{float(r['AverageNs']) / 1e3:.2f} | {100 * float(r['TotalDurationNs']) / total:.1f}% |")
     out += ["", "Calls include the prompt prefill (separately named `gemm_bf16_dense<..., 1>`) and the warmup, "
@@ -211,7 +224,6 @@ def summarize_profile(args):
                     f"{ksum:.2f} ms of kernel time in {wall:.2f} ms; median gap between kernels "
                     f"{gaps[len(gaps) // 2] / 1e3:.2f} us. By kernel: {top}.", ""]
     out += [
-            "## HBM traffic (FETCH_SIZE and WRITE_SIZE passes)", "",
             "## HBM traffic (FETCH_SIZE and WRITE_SIZE passes)", "",
             f"Calibration: a plain 256 MiB device copy (262144 KiB read, 262144 KiB written) reads "
             f"FETCH_SIZE = {fcal:.1f} KiB and WRITE_SIZE = {wcal:.1f} KiB per dispatch, so the counters are "

@@ -56,6 +56,41 @@ __host__ __device__ inline int pass_batch(const PassDesc& p, int bi) {
   return p.prompt_ids ? p.prompt_ids[bi] : bi;
 }
 
+// Row m of a pass as (prompt slot bi, batch index b, beam i, row j).
+__device__ __forceinline__ void row_decode(const PassDesc& p, int m, int& bi, int& b, int& i, int& j) {
+  j = m % p.R;
+  const int t = m / p.R;
+  i = t % p.kp;
+  bi = t / p.kp;
+  b = pass_batch(p, bi);
+}
+
+// KV block, slot in the block, and position of row (b, i, j) of a pass whose
+// prompt b has Lp prefix tokens: a suffix slot j0 + j of beam i, or prefix
+// position Lp + j.
+__device__ __forceinline__ void kv_slot(const PassDesc& p, int b, int i, int j, int Lp, int& blk, int& slot,
+                                        int& pos) {
+  if (p.mode == kSuffix) {
+    const int s = p.j0 + j;
+    pos = Lp + s;
+    blk = p.stable[(long long)b * p.s_stride_b + i * p.s_stride_i + s / kBlock];
+    slot = s % kBlock;
+  } else {
+    pos = Lp + j;
+    blk = p.ptable[(long long)b * p.ptable_stride + pos / kBlock];
+    slot = pos % kBlock;
+  }
+}
+
+// Rotary embedding of the pair (x1, x2) = (x[d], x[d + hd/2]) at angle
+// theta with c = cos(theta), s = sin(theta):
+//   y1 = x1 c - x2 s,  y2 = x2 c + x1 s.
+// Written with explicit fused multiply-adds so that every kernel that
+// rotates (the rotary kernels and the q/k/v projection's epilogue) rounds
+// the same way.
+__device__ __forceinline__ float rope_first(float x1, float x2, float c, float s) { return fmaf(x1, c, -(x2 * s)); }
+__device__ __forceinline__ float rope_second(float x1, float x2, float c, float s) { return fmaf(x2, c, x1 * s); }
+
 // Index of row m of a pass into a [B][kp][stride] token array:
 // (b * kp + i) * stride + off + j.  Disabled: index = m.
 struct RowMap {
@@ -147,6 +182,53 @@ __device__ __forceinline__ float wave_sum(float v) {
 __device__ __forceinline__ void split_bf16(float x, bf16& hi, bf16& lo) {
   hi = (bf16)x;
   lo = (bf16)(x - (float)hi);
+}
+
+// Slots [slot, slot + n) of one dim row of a V unit in the split KV format
+// (hi plane at row[0..16), lo plane at row[plane..plane + 16)), from vv[t]
+// for slot t; entries outside the run are ignored.  The widest stores that
+// stay inside the run: whole 8-slot halves as 16 bytes, else slot pairs as
+// 4 bytes, else single slots.
+__device__ __forceinline__ void store_v_run(bf16* row, long long plane, const float (&vv)[kBlock], int slot, int n) {
+  bf16 vh[kBlock], vlo[kBlock];
+#pragma unroll
+  for (int t = 0; t < kBlock; ++t) {
+    bf16 h, l;
+    split_bf16(vv[t], h, l);
+    const bool in = t >= slot && t < slot + n;
+    vh[t] = in ? h : (bf16)0.f;
+    vlo[t] = in ? l : (bf16)0.f;
+  }
+#pragma unroll
+  for (int h8 = 0; h8 < 2; ++h8) {
+    const int t0 = h8 * 8;
+    if (t0 >= slot && t0 + 8 <= slot + n) {
+      bf16x8 a, c;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        a[e] = vh[t0 + e];
+        c[e] = vlo[t0 + e];
+      }
+      *(bf16x8*)(row + t0) = a;
+      *(bf16x8*)(row + plane + t0) = c;
+    } else {
+#pragma unroll
+      for (int t = t0; t < t0 + 8; t += 2) {
+        const bool in0 = t >= slot && t < slot + n, in1 = t + 1 >= slot && t + 1 < slot + n;
+        if (in0 && in1) {
+          bf16x2v a = {vh[t], vh[t + 1]}, c = {vlo[t], vlo[t + 1]};
+          *(bf16x2v*)(row + t) = a;
+          *(bf16x2v*)(row + plane + t) = c;
+        } else if (in0) {
+          row[t] = vh[t];
+          row[plane + t] = vlo[t];
+        } else if (in1) {
+          row[t + 1] = vh[t + 1];
+          row[plane + t + 1] = vlo[t + 1];
+        }
+      }
+    }
+  }
 }
 
 // (value, id) ordering used by every argmax / top-k: larger value first,

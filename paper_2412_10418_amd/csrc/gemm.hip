@@ -53,6 +53,7 @@ struct GemmArgs {
   float* partial;   // split planes [ksplit][M][N]
   int tiles_m, tiles_n;
   RowStats rs;      // kEpiRowStats: per-tile row statistics instead of C
+  RopeEpi re;       // kEpiRope: rotary + KV write instead of C
 };
 
 __device__ __forceinline__ float silu(float x) { return x / (1.f + __expf(-x)); }
@@ -265,6 +266,175 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
 template <int I>
 using ic = std::integral_constant<int, I>;
 
+// kEpiRope.  The tile holds whole heads.  For its rotary heads the fp32
+// output tile [BM][BN] is staged in LDS (rope_at: 16-column groups
+// XOR-permuted by (row / 4) % 4, so that the four row groups of an MFMA
+// fragment write different banks; float4 runs stay whole), and:
+//  - rotary heads (q, then k): unit = (row, head, 8 dims of the first half)
+//    with its 8 partners; BM * BN / 16 units, a fixed number per thread, so
+//    every row record and cos / sin load of a thread is issued before the
+//    tile is staged.  q goes out as 16-byte fp32 runs, K as 16-byte runs of
+//    each bf16 plane.
+//  - value heads: straight from the accumulators, which hold four
+//    consecutive rows (slots) of one dim per lane; a tile without rotary
+//    heads is not staged.
+template <int BN>
+__device__ __forceinline__ int rope_at(int r, int c) {
+  return r * BN + (c ^ (((r >> 2) & 3) << 4));
+}
+
+template <int NT, int BM, int BN, int HD, int TM, int TN>
+__device__ __forceinline__ void rope_epilogue(const GemmArgs& a, const f32x4 (&acc)[TM * TN], float* tile, int m0,
+                                              int n0, int wm, int wn, int lr, int lg) {
+  constexpr int HALF = HD / 2, C8 = HALF / 8, UPT = BM * BN / 16 / NT;
+  static_assert(BN % HD == 0 && HALF % 8 == 0 && BM * BN % (16 * NT) == 0, "rotary units per thread");
+  const RopeEpi& re = a.re;
+  const int H = re.H, Hkv = re.Hkv, Hqk = H + Hkv;
+  const long long unit = split_unit_elems(HD), plane = (long long)kBlock * HD;
+  bf16* kl = (bf16*)re.pool.k + (long long)re.layer * 2 * re.pool.layer_elems;
+  bf16* vl = (bf16*)re.pool.v + (long long)re.layer * 2 * re.pool.layer_elems;
+  const int2* __restrict__ rinfo = re.rowinfo;
+  const int rows = min(BM, a.M - m0);
+  const int h0 = n0 / HD, nh = min(BN, a.N - n0) / HD;
+  const int nrot = max(0, min(nh, Hqk - h0));
+  auto tile4 = [&](int r, int c) { return *(const float4*)&tile[rope_at<BN>(r, c)]; };
+
+  // value columns (below) come straight from the accumulators: this lane's
+  // rows' KV places are loaded up front
+  const int nv = nh - nrot;
+  const int rw = wm * TM * 16 + lg * 4;   // first local row of this lane
+  int kvr[TM][4];
+#pragma unroll
+  for (int t = 0; t < TM; ++t)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) kvr[t][e] = nv > 0 ? rinfo[m0 + min(rw + t * 16 + e, rows - 1)].x : 0;
+
+  // rotary units u = tid + NT * w: chunk fastest, then head, then row
+  if (nrot > 0) {
+    int2 ri[UPT];
+    float4 cs[UPT][4];
+    bool live[UPT];
+#pragma unroll
+    for (int w = 0; w < UPT; ++w) {
+      const int u = threadIdx.x + NT * w;
+      const int r = u / (C8 * (BN / HD)), hh = u / C8 % (BN / HD);
+      live[w] = r < rows && hh < nrot;
+      ri[w] = rinfo[m0 + min(r, rows - 1)];
+    }
+#pragma unroll
+    for (int w = 0; w < UPT; ++w) {
+      const int d = (threadIdx.x + NT * w) % C8 * 8;
+      const float* ct = re.cos_t + (long long)ri[w].y * HALF + d;
+      const float* st = re.sin_t + (long long)ri[w].y * HALF + d;
+      cs[w][0] = *(const float4*)ct;
+      cs[w][1] = *(const float4*)(ct + 4);
+      cs[w][2] = *(const float4*)st;
+      cs[w][3] = *(const float4*)(st + 4);
+    }
+    // the loads above are in flight while the tile goes to LDS (the K
+    // stages' buffers are free once every wave has left the K loop)
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < TM; ++t)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          tile[rope_at<BN>(wm * TM * 16 + t * 16 + lg * 4 + e, wn * TN * 16 + j * 16 + lr)] = acc[t * TN + j][e];
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < UPT; ++w) {
+      if (!live[w]) continue;
+      const int u = threadIdx.x + NT * w;
+      const int r = u / (C8 * (BN / HD)), hh = u / C8 % (BN / HD), d = u % C8 * 8;
+      const int m = m0 + r, head = h0 + hh, lc = hh * HD + d;
+      const float4 x1a = tile4(r, lc), x1b = tile4(r, lc + 4), x2a = tile4(r, lc + HALF), x2b = tile4(r, lc + HALF + 4);
+      const float x1[8] = {x1a.x, x1a.y, x1a.z, x1a.w, x1b.x, x1b.y, x1b.z, x1b.w};
+      const float x2[8] = {x2a.x, x2a.y, x2a.z, x2a.w, x2b.x, x2b.y, x2b.z, x2b.w};
+      const float c[8] = {cs[w][0].x, cs[w][0].y, cs[w][0].z, cs[w][0].w, cs[w][1].x, cs[w][1].y, cs[w][1].z, cs[w][1].w};
+      const float sn[8] = {cs[w][2].x, cs[w][2].y, cs[w][2].z, cs[w][2].w, cs[w][3].x, cs[w][3].y, cs[w][3].z, cs[w][3].w};
+      float y1[8], y2[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        y1[e] = rope_first(x1[e], x2[e], c[e], sn[e]);
+        y2[e] = rope_second(x1[e], x2[e], c[e], sn[e]);
+      }
+      if (head < H) {
+        float* q = re.qout + ((long long)m * H + head) * HD + d;
+        *(float4*)q = make_float4(y1[0], y1[1], y1[2], y1[3]);
+        *(float4*)(q + 4) = make_float4(y1[4], y1[5], y1[6], y1[7]);
+        *(float4*)(q + HALF) = make_float4(y2[0], y2[1], y2[2], y2[3]);
+        *(float4*)(q + HALF + 4) = make_float4(y2[4], y2[5], y2[6], y2[7]);
+      } else {
+        bf16x8 h1, l1, h2, l2;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          bf16 h, l;
+          split_bf16(y1[e], h, l);
+          h1[e] = h;
+          l1[e] = l;
+          split_bf16(y2[e], h, l);
+          h2[e] = h;
+          l2[e] = l;
+        }
+        bf16* kr = kl + ((long long)(ri[w].x / kBlock) * Hkv + (head - H)) * unit + (long long)(ri[w].x % kBlock) * HD + d;
+        *(bf16x8*)kr = h1;
+        *(bf16x8*)(kr + plane) = l1;
+        *(bf16x8*)(kr + HALF) = h2;
+        *(bf16x8*)(kr + plane + HALF) = l2;
+      }
+    }
+  }
+
+  // value heads: unit = (segment, head, dim), dim fastest.  A segment is
+  // the part of one beam's R rows that lies in the tile; its rows sit at
+  // consecutive slots, a new block where the slot wraps to 0.  The first
+  // row record of the next unit is loaded while the current one is stored.
+  if (nv <= 0) return;
+  // V is stored [hd][16 slots] per block and KV head, so a lane's four
+  // consecutive rows of one dim are four consecutive slots of its dim row
+  // when they lie in one block from a slot that is a multiple of 4: one
+  // 8-byte store per plane; otherwise slot by slot
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int col = n0 + wn * TN * 16 + j * 16 + lr;
+    const int head = col / HD;
+    if (col >= a.N || head < Hqk) continue;
+    const int d = col - head * HD;
+    bf16* vh0 = vl + (long long)(head - Hqk) * unit + (long long)d * kBlock;
+#pragma unroll
+    for (int t = 0; t < TM; ++t) {
+      const int k0 = kvr[t][0];
+      const bool live0 = rw + t * 16 < rows;
+      const bool run = rw + t * 16 + 3 < rows && (k0 & 3) == 0 && kvr[t][1] == k0 + 1 && kvr[t][2] == k0 + 2 &&
+                       kvr[t][3] == k0 + 3;
+      if (run) {
+        bf16x4 hv, lv;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          bf16 h, l;
+          split_bf16(acc[t * TN + j][e], h, l);
+          hv[e] = h;
+          lv[e] = l;
+        }
+        bf16* vr = vh0 + (long long)(k0 / kBlock) * Hkv * unit + k0 % kBlock;
+        *(bf16x4*)vr = hv;
+        *(bf16x4*)(vr + plane) = lv;
+      } else if (live0) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (rw + t * 16 + e >= rows) continue;
+          bf16 h, l;
+          split_bf16(acc[t * TN + j][e], h, l);
+          bf16* vr = vh0 + (long long)(kvr[t][e] / kBlock) * Hkv * unit + kvr[t][e] % kBlock;
+          vr[0] = h;
+          vr[plane] = l;
+        }
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // dense kernel: WM x WN waves, each owning TM x TN tiles of 16 x 16; K step 32
 //
@@ -449,6 +619,12 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dense(GemmArgs a) {
                 acc[t * TN + j][e];
       __syncthreads();
       tile_row_stats<C::NT, BM, BN>(tile, m0, n0, a.M, a.N, tn_blk, a.rs);
+      return;
+    }
+    if (a.epi == kEpiRope) {
+      float* tile = reinterpret_cast<float*>(&lds[0][0]);
+      if (a.re.hd == 128) rope_epilogue<C::NT, BM, BN, 128, TM, TN>(a, acc, tile, m0, n0, wm, wn, lr, lg);
+      else rope_epilogue<C::NT, BM, BN, 64, TM, TN>(a, acc, tile, m0, n0, wm, wn, lr, lg);
       return;
     }
   }
@@ -908,14 +1084,25 @@ Plan make_plan(int M, int N, int K, int dtype, bool no_split = false) {
   return p;
 }
 
+// Whether a dense configuration's fp32 output tile fits the LDS of its K
+// stages (the row-statistics and rotary epilogues stage it there).
+bool tile_fits_lds(const DenseShape& d) {
+  const size_t lds = 2 * 2 * ((size_t)(2 * d.bm + d.bn) * d.kc + 64 * d.wm * d.wn * 8);
+  return (size_t)d.bm * d.bn * sizeof(float) <= lds;
+}
+
 // Column tiles of a row-statistics launch (0: the shape's kernel cannot
 // stage its output tile through LDS).
 int rowstats_tiles(const Plan& p, int N) {
   if (p.kind == 2) return (N + 63) / 64;
   if (p.kind == 1) return p.tiles_n;
+  return tile_fits_lds(kDense[p.cfg]) ? p.tiles_n : 0;
+}
+
+bool rope_fusable(const Plan& p, int N, int hd) {
+  if (p.kind != 0 || p.ksplit != 1 || (hd != 64 && hd != 128) || N % hd != 0) return false;
   const DenseShape& d = kDense[p.cfg];
-  const size_t lds = 2 * 2 * ((size_t)(2 * d.bm + d.bn) * d.kc + 64 * d.wm * d.wn * 8);
-  return (size_t)d.bm * d.bn * sizeof(float) <= lds ? p.tiles_n : 0;
+  return d.bn % hd == 0 && tile_fits_lds(d);
 }
 
 }  // namespace
@@ -933,6 +1120,11 @@ int gemm_rowstats_tiles(int M, int N, int K, int dtype) {
   return rowstats_tiles(make_plan(M, N, K, dtype, true), N);
 }
 
+bool gemm_rope_fusable(int M, int N, int K, int dtype, int hd) {
+  if (M <= 0 || dtype != 1) return false;
+  return rope_fusable(make_plan(M, N, K, dtype), N, hd);
+}
+
 int gemm_check(int M, int N, int K, int dtype) {
   if (M < 0 || N <= 0 || K <= 0) return -1;
   if (dtype == 1 && K % DBK != 0) return -1;
@@ -942,12 +1134,14 @@ int gemm_check(int M, int N, int K, int dtype) {
 
 hipError_t gemm_launch(const GemmOperand& A, const void* B, const GemmOut& out, int M, int N, int K, int dtype,
                        int epi, void* ws, size_t ws_bytes, hipStream_t st, bool prefill, GemmHook* hook,
-                       int* deferred, RowStats* rs) {
+                       int* deferred, RowStats* rs, const RopeEpi* rope) {
   if (deferred) *deferred = 1;
   if (M == 0) return hipSuccess;
   const bool stats = epi == kEpiRowStats;
   if (stats != (rs != nullptr)) return hipErrorInvalidValue;
+  if ((epi == kEpiRope) != (rope != nullptr)) return hipErrorInvalidValue;
   Plan p = make_plan(M, N, K, dtype, stats);
+  if (rope && !rope_fusable(p, N, rope->hd)) return hipErrorInvalidValue;
   if (stats) {
     rs->tiles = rowstats_tiles(p, N);
     if (rs->tiles == 0 || rs->kk < 0 || rs->kk > 16) return hipErrorInvalidValue;
@@ -978,6 +1172,7 @@ hipError_t gemm_launch(const GemmOperand& A, const void* B, const GemmOut& out, 
   a.tiles_n = p.tiles_n;
   a.partial = (float*)ws;
   a.rs = stats ? *rs : RowStats{};
+  a.re = rope ? *rope : RopeEpi{};
   if (p.kind == 0) {
     dim3 grid(p.tiles_m * p.tiles_n, 1, p.ksplit);
     const DenseShape& d = kDense[p.cfg];

@@ -30,7 +30,9 @@ struct LogitArgs {
 //   [kStageHdr + tcap + kk, + kk)                next head log-probs (float bits)
 constexpr int kStageHdr = 4;
 
-hipError_t embed_launch(const PassDesc& p, const void* emb, float* h, int D, int V, int dtype, hipStream_t st);
+// rowinfo (may be null): [M] (block * 16 + slot, position) of each row.
+hipError_t embed_launch(const PassDesc& p, const void* emb, float* h, int D, int V, int dtype, hipStream_t st,
+                        int2* rowinfo = nullptr);
 // S > 0: fold S split planes part[S][rows][D] into x first (written back);
 // g == null then only folds.
 hipError_t rmsnorm_launch(float* x, const float* g, float* out32, bf16* ohi, bf16* olo, int rows, int D,

@@ -12,14 +12,6 @@ namespace cdsl {
 
 namespace {
 
-__device__ __forceinline__ void row_decode(const PassDesc& p, int m, int& bi, int& b, int& i, int& j) {
-  j = m % p.R;
-  int t = m / p.R;
-  i = t % p.kp;
-  bi = t / p.kp;
-  b = pass_batch(p, bi);
-}
-
 template <int NW>
 __device__ __forceinline__ float block_sum(float v, float* sh) {
   v = wave_sum(v);
@@ -37,12 +29,19 @@ __device__ __forceinline__ float block_sum(float v, float* sh) {
 // A token id outside [0, V) sets *bad (the library reports it as an invalid
 // argument at its next synchronisation) and is clamped for the read, so it
 // never reads out of bounds.
+// With rowinfo, row m's KV place is also recorded for the pass's layers:
+// rowinfo[m] = (block * 16 + slot, position).
 template <typename T>
 __global__ __launch_bounds__(256) void embed_rows(PassDesc p, const T* __restrict__ emb, float* __restrict__ h,
-                                                  int D, int V, int* __restrict__ bad) {
+                                                  int D, int V, int* __restrict__ bad, int2* __restrict__ rowinfo) {
   const int m = blockIdx.x;
   int bi, b, i, j;
   row_decode(p, m, bi, b, i, j);
+  if (rowinfo && threadIdx.x == 0) {
+    int blk, slot, pos;
+    kv_slot(p, b, i, j, p.Lp[b], blk, slot, pos);
+    rowinfo[m] = make_int2(blk * kBlock + slot, pos);
+  }
   const int raw = p.tok[(long long)(b * p.kp + i) * p.tok_stride + p.tok_off + j];
   if ((raw < 0 || raw >= V) && threadIdx.x == 0 && bad) *bad = 1;
   const int tok = min(max(raw, 0), V - 1);
@@ -160,18 +159,8 @@ __global__ __launch_bounds__(256) void rope_kv_write(PassDesc p, const float* __
   const int m = blockIdx.x;
   int bi, b, i, j;
   row_decode(p, m, bi, b, i, j);
-  const int Lp = p.Lp[b];
   int pos, blk, slot;
-  if (p.mode == kSuffix) {
-    const int s = p.j0 + j;
-    pos = Lp + s;
-    blk = p.stable[(long long)b * p.s_stride_b + i * p.s_stride_i + s / kBlock];
-    slot = s % kBlock;
-  } else {
-    pos = Lp + j;
-    blk = p.ptable[(long long)b * p.ptable_stride + pos / kBlock];
-    slot = pos % kBlock;
-  }
+  kv_slot(p, b, i, j, p.Lp[b], blk, slot, pos);
   const int half = hd / 2;
   const float* row = qkv + (long long)m * (H + 2 * Hkv) * hd;
   const float* ct = cos_t + (long long)pos * half;
@@ -184,7 +173,7 @@ __global__ __launch_bounds__(256) void rope_kv_write(PassDesc p, const float* __
     const int hh = u / half, d = u % half;
     const float x1 = row[hh * hd + d], x2 = row[hh * hd + d + half];
     const float c = ct[d], s = stt[d];
-    const float y1 = x1 * c - x2 * s, y2 = x2 * c + x1 * s;
+    const float y1 = rope_first(x1, x2, c, s), y2 = rope_second(x1, x2, c, s);
     if (hh < H) {
       T* q = qout + ((long long)m * H + hh) * hd;
       q[d] = from_f32<T>(y1);
@@ -248,20 +237,6 @@ struct QkvRow {
   }
 };
 
-__device__ __forceinline__ void kv_slot(const PassDesc& p, int b, int i, int j, int Lp, int& blk, int& slot,
-                                        int& pos) {
-  if (p.mode == kSuffix) {
-    const int s = p.j0 + j;
-    pos = Lp + s;
-    blk = p.stable[(long long)b * p.s_stride_b + i * p.s_stride_i + s / kBlock];
-    slot = s % kBlock;
-  } else {
-    pos = Lp + j;
-    blk = p.ptable[(long long)b * p.ptable_stride + pos / kBlock];
-    slot = pos % kBlock;
-  }
-}
-
 template <int NT>
 __global__ __launch_bounds__(NT) void rope_kv_write_split(PassDesc p, const float* __restrict__ qkv,
                                                            float* __restrict__ qout, KVPool pool, int layer,
@@ -291,10 +266,10 @@ __global__ __launch_bounds__(NT) void rope_kv_write_split(PassDesc p, const floa
       const int hh = u / q4, d = (u % q4) * 4;
       const float4 x1 = src.val4(m, W, hh * hd + d), x2 = src.val4(m, W, hh * hd + d + half);
       const float4 c = *(const float4*)(ct + d), sn = *(const float4*)(stt + d);
-      const float y1[4] = {x1.x * c.x - x2.x * sn.x, x1.y * c.y - x2.y * sn.y, x1.z * c.z - x2.z * sn.z,
-                           x1.w * c.w - x2.w * sn.w};
-      const float y2[4] = {x2.x * c.x + x1.x * sn.x, x2.y * c.y + x1.y * sn.y, x2.z * c.z + x1.z * sn.z,
-                           x2.w * c.w + x1.w * sn.w};
+      const float y1[4] = {rope_first(x1.x, x2.x, c.x, sn.x), rope_first(x1.y, x2.y, c.y, sn.y),
+                           rope_first(x1.z, x2.z, c.z, sn.z), rope_first(x1.w, x2.w, c.w, sn.w)};
+      const float y2[4] = {rope_second(x1.x, x2.x, c.x, sn.x), rope_second(x1.y, x2.y, c.y, sn.y),
+                           rope_second(x1.z, x2.z, c.z, sn.z), rope_second(x1.w, x2.w, c.w, sn.w)};
       if (hh < H) {
         float* q = qout + ((long long)m * H + hh) * hd + d;
         *(float4*)q = make_float4(y1[0], y1[1], y1[2], y1[3]);
@@ -342,48 +317,7 @@ __global__ __launch_bounds__(NT) void rope_kv_write_split(PassDesc p, const floa
     float vv[kBlock];
 #pragma unroll
     for (int t = 0; t < kBlock; ++t) vv[t] = (t >= slot && t < slot + n) ? src.val(m0 + j + (t - slot), W, voff) : 0.f;
-    bf16 vh[kBlock], vlo[kBlock];
-#pragma unroll
-    for (int t = 0; t < kBlock; ++t) {
-      bf16 h, l;
-      split_bf16(vv[t], h, l);
-      const bool in = t >= slot && t < slot + n;
-      vh[t] = in ? h : (bf16)0.f;
-      vlo[t] = in ? l : (bf16)0.f;
-    }
-    bf16* row = vl + ((long long)blk * Hkv + hh) * unit + (long long)d * kBlock;
-    // widest stores inside [slot, slot + n): whole 8-slot halves as 16 bytes,
-    // else slot pairs as 4 bytes, else single slots
-#pragma unroll
-    for (int h8 = 0; h8 < 2; ++h8) {
-      const int t0 = h8 * 8;
-      if (t0 >= slot && t0 + 8 <= slot + n) {
-        bf16x8 a, c;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          a[e] = vh[t0 + e];
-          c[e] = vlo[t0 + e];
-        }
-        *(bf16x8*)(row + t0) = a;
-        *(bf16x8*)(row + plane + t0) = c;
-      } else {
-#pragma unroll
-        for (int t = t0; t < t0 + 8; t += 2) {
-          const bool in0 = t >= slot && t < slot + n, in1 = t + 1 >= slot && t + 1 < slot + n;
-          if (in0 && in1) {
-            bf16x2v a = {vh[t], vh[t + 1]}, c = {vlo[t], vlo[t + 1]};
-            *(bf16x2v*)(row + t) = a;
-            *(bf16x2v*)(row + plane + t) = c;
-          } else if (in0) {
-            row[t] = vh[t];
-            row[plane + t] = vlo[t];
-          } else if (in1) {
-            row[t + 1] = vh[t + 1];
-            row[plane + t + 1] = vlo[t + 1];
-          }
-        }
-      }
-    }
+    store_v_run(vl + ((long long)blk * Hkv + hh) * unit + (long long)d * kBlock, plane, vv, slot, n);
     j += n;
   }
 }
@@ -1115,11 +1049,12 @@ __global__ void heads_to_lookaheads(int BK, int d, const int* __restrict__ beams
 }  // namespace
 
 // ---------------------------------------------------------------------------
-hipError_t embed_launch(const PassDesc& p, const void* emb, float* h, int D, int V, int dtype, hipStream_t st) {
+hipError_t embed_launch(const PassDesc& p, const void* emb, float* h, int D, int V, int dtype, hipStream_t st,
+                        int2* rowinfo) {
   const int M = p.M();
   if (M == 0) return hipSuccess;
-  if (dtype == 1) embed_rows<bf16><<<M, 256, 0, st>>>(p, (const bf16*)emb, h, D, V, p.bad);
-  else embed_rows<float><<<M, 256, 0, st>>>(p, (const float*)emb, h, D, V, p.bad);
+  if (dtype == 1) embed_rows<bf16><<<M, 256, 0, st>>>(p, (const bf16*)emb, h, D, V, p.bad, rowinfo);
+  else embed_rows<float><<<M, 256, 0, st>>>(p, (const float*)emb, h, D, V, p.bad, rowinfo);
   return hipGetLastError();
 }
 

@@ -63,6 +63,7 @@ struct Workspace {
   float* h = nullptr;        // residual stream [M, D]
   float* qkv = nullptr;      // [M, (H + 2 Hkv) hd]
   float* q = nullptr;        // [M, H, hd] after rotary
+  int2* rowinfo = nullptr;   // [M] (block * 16 + slot, position) of each row of the pass
   // projection inputs: hi / lo bf16 planes (bf16 weights) or fp32
   bf16 *uh = nullptr, *ul = nullptr, *oh = nullptr, *ol = nullptr, *ah = nullptr, *al = nullptr;
   float *u32 = nullptr, *o32 = nullptr, *act32 = nullptr;
@@ -419,6 +420,7 @@ void alloc_workspace(cdsl_ctx* c) {
   w.h = dev_alloc<float>(c, M * Dm);
   w.qkv = dev_alloc<float>(c, M * QKVm);
   w.q = dev_alloc<float>(c, M * HQm);
+  w.rowinfo = dev_alloc<int2>(c, M);
   if (c->dtype == CDSL_BF16) {
     w.uh = dev_alloc<bf16>(c, M * Dm);
     w.ul = dev_alloc<bf16>(c, M * Dm);
@@ -469,10 +471,11 @@ void alloc_workspace(cdsl_ctx* c) {
 // Returns the number of split planes left in the GEMM workspace for the
 // caller to fold (1: none) when defer is set.
 int gemm(cdsl_ctx* c, const GemmOperand& A, const void* W, const GemmOut& out, int M, int N, int K, int epi,
-         bool prefill, bool defer = false, RowStats* rs = nullptr) {
+         bool prefill, bool defer = false, RowStats* rs = nullptr, const RopeEpi* rope = nullptr) {
   const double wes = c->dtype == CDSL_BF16 ? 2.0 : 4.0;   // weight element size
-  // output bytes: fp32 store, fp32 read-modify-write, the two bf16 planes
-  // of the half-width SwiGLU output, or the per-tile row statistics
+  // output bytes: fp32 store (also the rotary epilogue's fp32 q and hi / lo
+  // K, V), fp32 read-modify-write, the two bf16 planes of the half-width
+  // SwiGLU output, or the per-tile row statistics
   const double outb =
       epi == kEpiSwiGLU     ? (double)M * (N / 2) * 4.0
       : epi == kEpiRowStats ? (double)M * gemm_rowstats_tiles(M, N, K, c->dtype) * (3.0 + 2.0 * rs->kk) * 4.0
@@ -503,7 +506,7 @@ int gemm(cdsl_ctx* c, const GemmOperand& A, const void* W, const GemmOut& out, i
   hk.plane = (double)M * N * 4.0;
   int planes = 1;
   CK(gemm_launch(A, W, out, M, N, K, c->dtype, epi, c->ws.gemm_ws, c->ws.gemm_ws_bytes, c->st, prefill,
-                 c->prof ? &hk : nullptr, defer ? &planes : nullptr, rs));
+                 c->prof ? &hk : nullptr, defer ? &planes : nullptr, rs, rope));
   return planes;
 }
 
@@ -533,7 +536,7 @@ void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, lon
   const double es = 4.0;   // fp32 activations and KV
   {
     Span sp(c, CDSL_K_ROWWISE, 0.0, (double)M * D * ((dt == CDSL_BF16 ? 2.0 : 4.0) + 4.0));
-    CK(embed_launch(p, md.emb, w.h, D, k.vocab, dt, c->st));
+    CK(embed_launch(p, md.emb, w.h, D, k.vocab, dt, c->st, w.rowinfo));
   }
   // algorithmic attention work of this pass: the prefix KV of a prompt is
   // read once for all its rows; every query head sees its visible keys
@@ -576,13 +579,25 @@ void run_pass(cdsl_ctx* c, Model& md, const PassDesc& p, int max_prefix_len, lon
   // consumes the result (RMSNorm of the residual stream, rotary + KV
   // write), which saves a reduce launch per projection.
   const float* planes_ws = (const float*)w.gemm_ws;
+  // Where the q/k/v projection is not split (the dense kernel at the
+  // verification and prefill row counts), its epilogue applies the rotary
+  // embedding and writes q and the KV pool itself: no q/k/v product in
+  // memory and no rotary launch.  CDSL_UNFUSED_ROPE=1 keeps the separate
+  // kernel (same arithmetic, for comparison).
+  const char* unfused_env = getenv("CDSL_UNFUSED_ROPE");
+  const bool fuse_rope = bf && !(unfused_env && unfused_env[0] == '1') &&
+                         gemm_rope_fusable(M, md.qkv_n, D, c->dtype, hd);
+  RopeEpi rope{p, w.rowinfo, w.q, md.pool, 0, md.cos_t, md.sin_t, H, Hkv, hd};
   {
     Span sp(c, CDSL_K_ROWWISE, 0.0, norm_bytes);
     CK(rmsnorm_launch(w.h, md.g1[0], w.u32, w.uh, w.ul, M, D, k.rms_eps, 0, 1, nullptr, c->st));
   }
   for (int l = 0; l < k.n_layers; ++l) {
-    const int sq = gemm(c, Au, md.wqkv[l], to_qkv, M, md.qkv_n, D, kEpiStore, prefill, bf);
-    {
+    if (fuse_rope) {
+      rope.layer = l;
+      gemm(c, Au, md.wqkv[l], GemmOut{}, M, md.qkv_n, D, kEpiRope, prefill, false, nullptr, &rope);
+    } else {
+      const int sq = gemm(c, Au, md.wqkv[l], to_qkv, M, md.qkv_n, D, kEpiStore, prefill, bf);
       Span sp(c, CDSL_K_ROWWISE, 0.0, rope_bytes + (sq > 1 ? (double)sq * M * md.qkv_n * 4.0 : 0.0));
       CK(rope_kv_launch(p, sq > 1 ? planes_ws : w.qkv, w.q, md.pool, l, md.cos_t, md.sin_t, H, Hkv, hd, dt, c->st,
                         sq > 1 ? sq : 0));
