@@ -57,6 +57,9 @@ def parse():
                     help="markdown summary of a rocprofv3 --kernel-trace --marker-trace --hip-runtime-trace run "
                          "of this script: per library call (roctx range), its calls, host time, kernels launched "
                          "and their GPU time; no GPU needed")
+    ap.add_argument("--summarize-trace", nargs=2, default=None, metavar=("BENCH_JSON", "TRACE_DIR"),
+                    help="markdown summary of a rocprofv3 --kernel-trace --stats run of this script on any "
+                         "workload: top kernels, and one step's launches by kernel and grid; no GPU needed")
     ap.add_argument("--summary-out", default=None)
     ap.add_argument("--commands", default=None, help="text file with the exact profiling commands (for the summary)")
     return ap.parse_args()
@@ -289,6 +292,67 @@ def summarize_profile(args):
                            f"{sum(lv) / len(lv) if lv else float('nan'):.1f} |")
         out.append("")
     out += [TRAFFIC_TAG + json.dumps(r) + " -->" for r in recs]
+    text = "\n".join(out) + "\n"
+    if args.summary_out:
+        with open(args.summary_out, "w") as fh:
+            fh.write(text)
+    else:
+        sys.stdout.write(text)
+
+
+def summarize_trace(args):
+    """Top kernels of a traced bench run, and the launches of one step (the
+    last step between two commits before the instrumented steps) grouped by
+    kernel and grid."""
+    import csv
+    import glob
+    import re
+    bench_json, d = args.summarize_trace
+
+    def one(pattern):
+        fs = glob.glob(os.path.join(d, pattern))
+        if not fs:
+            raise SystemExit(f"no {pattern} in {d}")
+        return list(csv.DictReader(open(fs[0])))
+
+    def short(nm):
+        nm = nm.replace("cdsl::(anonymous namespace)::", "").replace("cdsl::", "")
+        return mangled_short(nm) if nm.startswith("_Z") else re.sub(r"\(.*$", "", nm)
+
+    with open(bench_json) as fh:
+        b = json.loads([ln for ln in fh.read().splitlines() if ln.startswith("{")][-1])
+    cfg = b["config"]
+    stats = sorted(one("*_kernel_stats.csv"), key=lambda r: -float(r["TotalDurationNs"]))
+    tot = sum(float(r["TotalDurationNs"]) for r in stats)
+    out = [f"# rocprofv3 summary: CDSL step, workload {cfg['workload']} (batch {cfg['batch']}, k = {cfg['k']}, "
+           f"d = {cfg['d']})", ""]
+    if args.commands:
+        out += ["Commands (run from /tmp with TMPDIR=/tmp on one MI355X; R = repository root):", "", "```"]
+        out += [ln.rstrip() for ln in open(args.commands) if ln.strip()]
+        out += ["```", ""]
+    out += [f"Bench line of the traced run: {b['ms_per_step']} ms/step, {b['value']:.0f} {b['unit']}.", "",
+            "| kernel | calls | total ms | avg us | share |", "|---|---:|---:|---:|---:|"]
+    for r in stats[:16]:
+        out.append(f"| `{short(r['Name'])}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.2f} | "
+                   f"{float(r['AverageNs']) / 1e3:.2f} | {100 * float(r['TotalDurationNs']) / tot:.1f}% |")
+    out += ["", "Calls cover the prompt prefill and every warmup, timed, phase-timed and instrumented step.", ""]
+    tr = sorted(one("*_kernel_trace.csv"), key=lambda r: int(r["Start_Timestamp"]))
+    idx = [i for i, r in enumerate(tr) if "commit_kernel" in r["Kernel_Name"]]
+    if len(idx) >= 3:
+        a, z = idx[-3] + 1, idx[-2] + 1
+        agg = {}
+        for r in tr[a:z]:
+            g = (f"{int(r['Grid_Size_X']) // int(r['Workgroup_Size_X'])}x{r['Grid_Size_Y']}x{r['Grid_Size_Z']}")
+            v = agg.setdefault((short(r["Kernel_Name"]), g), [0, 0.0])
+            v[0] += 1
+            v[1] += (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        ks = sum(v[1] for v in agg.values()) / 1e3
+        wall = (int(tr[z - 1]["End_Timestamp"]) - int(tr[a]["Start_Timestamp"])) / 1e6
+        out += [f"One step of the traced run (between two commits): {z - a} launches, {ks:.1f} ms of kernel time "
+                f"in {wall:.1f} ms. By kernel and grid (workgroups x y x z):", "",
+                "| kernel | grid | launches | ms | avg us |", "|---|---|---:|---:|---:|"]
+        for (nm, g), (c, t) in sorted(agg.items(), key=lambda kv: -kv[1][1])[:16]:
+            out.append(f"| `{nm}` | {g} | {c} | {t / 1e3:.2f} | {t / c:.1f} |")
     text = "\n".join(out) + "\n"
     if args.summary_out:
         with open(args.summary_out, "w") as fh:
@@ -534,6 +598,9 @@ def main():
         return
     if args.summarize_ranges:
         summarize_ranges(args)
+        return
+    if args.summarize_trace:
+        summarize_trace(args)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path shards by prompt "

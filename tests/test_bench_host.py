@@ -159,3 +159,35 @@ def test_range_summary_attributes_kernels_by_launch_time(tmp_path):
     # rollout: 2 calls, kernels 1, 2 (first) and 5 (second): 3 / 2 per call, 6 ms / 2
     assert rows["cdsl_rollout"] == ["2", f"{100 / 1e6:.3f}", "1.5", "3.000"]
     assert rows["cdsl_verify"] == ["1", f"{100 / 1e6:.3f}", "1.0", "5.000"]
+
+
+def test_trace_summary_groups_one_step_by_kernel_and_grid(tmp_path):
+    """The step summarised is the last one between two commits before the
+    instrumented step; launches are grouped by kernel and grid, and a name
+    the tracer left mangled is shortened."""
+    bj = tmp_path / "b.json"
+    bj.write_text(json.dumps({"ms_per_step": 5.0, "value": 100.0, "unit": "lookahead tokens verified/s",
+                              "config": {"workload": "long", "batch": 64, "k": 8, "d": 8}}) + "\n")
+    _write_csv(tmp_path / "x_kernel_stats.csv", [
+        {"Name": "void cdsl::(anonymous namespace)::gemm_bf16_dense<2, 4, 5, 4, 64, 0>(GemmArgs)", "Calls": "4",
+         "TotalDurationNs": "4000", "AverageNs": "1000"},
+        {"Name": "_ZN4cdsl12_GLOBAL__N_110embed_rowsIDF16bEEvNS_8PassDescE", "Calls": "2",
+         "TotalDurationNs": "1000", "AverageNs": "500"}])
+    seq = ["commit_kernel", "gemm", "gemm", "emb", "commit_kernel", "gemm", "emb", "commit_kernel", "gemm",
+           "commit_kernel"]
+    names = {"gemm": "void cdsl::(anonymous namespace)::gemm_bf16_dense<2, 4, 5, 4, 64, 0>(GemmArgs)",
+             "emb": "_ZN4cdsl12_GLOBAL__N_110embed_rowsIDF16bEEvNS_8PassDescE",
+             "commit_kernel": "cdsl::commit_kernel(CommitArgs)"}
+    _write_csv(tmp_path / "x_kernel_trace.csv", [
+        {"Kernel_Name": names[n], "Start_Timestamp": str(1000 * t), "End_Timestamp": str(1000 * t + 500),
+         "Grid_Size_X": "512", "Workgroup_Size_X": "256", "Grid_Size_Y": "1", "Grid_Size_Z": "3" if n == "gemm" else "1"}
+        for t, n in enumerate(seq)])
+    out = tmp_path / "s.md"
+    bench.summarize_trace(types.SimpleNamespace(summarize_trace=[str(bj), str(tmp_path)], summary_out=str(out),
+                                                commands=None))
+    text = out.read_text()
+    assert "workload long (batch 64, k = 8, d = 8)" in text
+    assert "| `embed_rows<...>` | 2 |" in text
+    # the step between the second and third commits: gemm, emb, commit
+    assert "One step of the traced run (between two commits): 3 launches" in text
+    assert "| `void gemm_bf16_dense<2, 4, 5, 4, 64, 0>` | 2x1x3 | 1 |" in text
