@@ -87,11 +87,19 @@ HBM_RATE_KERNELS = [
 
 
 def source_digest(files):
+    """Digest of a kernel's source files with comments, blank lines and
+    indentation left out, so that an edit of the comments alone keeps the
+    counters taken for the code."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for f in files:
-        with open(os.path.join(ROOT, "paper_2412_10418_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2412_10418_amd", "csrc", f)) as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        code = "\n".join(ln.strip() for ln in text.splitlines() if ln.strip())
+        h.update(code.encode())
     return h.hexdigest()[:16]
 
 

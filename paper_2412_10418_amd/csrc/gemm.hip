@@ -386,12 +386,8 @@ __device__ __forceinline__ void rope_epilogue(const GemmArgs& a, const f32x4 (&a
     }
   }
 
-  // value heads: unit = (segment, head, dim), dim fastest.  A segment is
-  // the part of one beam's R rows that lies in the tile; its rows sit at
-  // consecutive slots, a new block where the slot wraps to 0.  The first
-  // row record of the next unit is loaded while the current one is stored.
   if (nv <= 0) return;
-  // V is stored [hd][16 slots] per block and KV head, so a lane's four
+  // value heads.  V is stored [hd][16 slots] per block and KV head, so a lane's four
   // consecutive rows of one dim are four consecutive slots of its dim row
   // when they lie in one block from a slot that is a multiple of 4: one
   // 8-byte store per plane; otherwise slot by slot

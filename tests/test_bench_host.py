@@ -191,3 +191,16 @@ def test_trace_summary_groups_one_step_by_kernel_and_grid(tmp_path):
     # the step between the second and third commits: gemm, emb, commit
     assert "One step of the traced run (between two commits): 3 launches" in text
     assert "| `void gemm_bf16_dense<2, 4, 5, 4, 64, 0>` | 2x1x3 | 1 |" in text
+
+
+def test_source_digest_ignores_comments_but_not_code(tmp_path, monkeypatch):
+    src = tmp_path / "paper_2412_10418_amd" / "csrc"
+    src.mkdir(parents=True)
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    f = src / "k.hip"
+    f.write_text("// header\n__global__ void k(float* x) {\n  x[0] = 1.f;  // one\n}\n")
+    d0 = bench.source_digest(["k.hip"])
+    f.write_text("/* a block\n comment */\n__global__ void k(float* x) {\n\n    x[0] = 1.f;\n}\n")
+    assert bench.source_digest(["k.hip"]) == d0
+    f.write_text("__global__ void k(float* x) {\n  x[0] = 2.f;\n}\n")
+    assert bench.source_digest(["k.hip"]) != d0
